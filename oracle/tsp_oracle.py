@@ -1,0 +1,264 @@
+"""fp64 oracle for the per-rank forward of a folded TSP transformer layer.
+
+TEST INFRASTRUCTURE ONLY -- imported by tests/, the smoke check and the benchmark's
+CPU-baseline leg; never by the product path.  Shares no code with the HIP library.
+
+Every array argument holds float64 values (the caller converts bf16 bit patterns
+with the input generator).  Nothing here rounds to bf16: the GPU path rounds some
+intermediates (Q, K, V, P, A, the gated product, the layer's MLP input) and the
+tests absorb that in their tolerance.
+
+Conventions (paper, Sections 3-4):
+  x        [B, S, h]  layer input;  rank p holds the contiguous chunk
+           x[:, p*S_loc:(p+1)*S_loc], S_loc = S/D.
+  W_Q      [n_h d, h], W_K / W_V [n_kv d, h]; Q = X W_Q^T etc.
+  W_O      [h, n_h d]; the attention block returns Flatten(A) W_O^T.
+  W1 (gate), W3 (up), W2 (down)  [F, h]; MLP(u) = (SiLU(u W1^T) * (u W3^T)) W2.
+  Query head i reads key/value head floor(i / g), g = n_h / n_kv (GQA).
+  Softmax scale defaults to 1/sqrt(d).
+  Causal rule: a query at global position t sees keys at positions j <= t.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+_Q_CHUNK = 512
+
+
+# ---------------------------------------------------------------------------
+# Shared definitions of the two nonlinear pieces.
+# ---------------------------------------------------------------------------
+
+def silu(z: np.ndarray) -> np.ndarray:
+    """SiLU(z) = z * sigmoid(z): the gate activation of a SwiGLU MLP (Section 4 model)."""
+    with np.errstate(over="ignore"):
+        return z / (1.0 + np.exp(-z))
+
+
+def causal_probs(q: np.ndarray, k: np.ndarray, q_offset: int, scale: float) -> np.ndarray:
+    """Softmax probabilities P[i, j] of query row i (global position q_offset + i)
+    over keys j, with keys j > q_offset + i masked out.  q [Lq, d], k [Lk, d]."""
+    s = (q @ k.T) * scale
+    lq, lk = s.shape
+    allowed = np.arange(lk)[None, :] <= (q_offset + np.arange(lq))[:, None]
+    s = np.where(allowed, s, -np.inf)
+    s = s - s.max(axis=1, keepdims=True)
+    e = np.exp(s)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def causal_attention_core(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_offset: int,
+                          scale: float) -> np.ndarray:
+    """o_i = sum_j P[i, j] v_j for one head; q [Lq, d], k/v [Lk, d] -> [Lq, d].
+
+    The query block starts at global position q_offset, so this is the
+    bottom-right-aligned causal attention a rank runs for its chunk against the
+    gathered prefix (Algorithm 1, the CausalAttn call).  Queries are processed in
+    chunks only to bound memory.
+    """
+    lq = q.shape[0]
+    out = np.empty((lq, v.shape[1]), dtype=np.float64)
+    for lo in range(0, lq, _Q_CHUNK):
+        hi = min(lq, lo + _Q_CHUNK)
+        kmax = min(k.shape[0], q_offset + hi)  # later keys are all masked for this chunk
+        p = causal_probs(q[lo:hi], k[:kmax], q_offset + lo, scale)
+        out[lo:hi] = p @ v[:kmax]
+    return out
+
+
+def default_scale(head_dim: int, scale: float | None) -> float:
+    return 1.0 / math.sqrt(head_dim) if scale is None or scale <= 0 else float(scale)
+
+
+# ---------------------------------------------------------------------------
+# O1 -- the unsharded layer (what the folded schedule must reproduce).
+# ---------------------------------------------------------------------------
+
+def attention_full(x, wq, wk, wv, wo, n_heads, n_kv_heads, scale=None):
+    """Causal multi-head / grouped-query attention block on the whole sequence.
+
+    Section 4 model: learned Q, K, V, O projections, no biases, no positional
+    encoding, no normalisation.  x [B, S, h] -> [B, S, h].
+    """
+    b_, s_, _ = x.shape
+    d = wq.shape[0] // n_heads
+    g = n_heads // n_kv_heads
+    sc = default_scale(d, scale)
+    q = (x @ wq.T).reshape(b_, s_, n_heads, d)
+    k = (x @ wk.T).reshape(b_, s_, n_kv_heads, d)
+    v = (x @ wv.T).reshape(b_, s_, n_kv_heads, d)
+    a = np.empty((b_, s_, n_heads, d), dtype=np.float64)
+    for b in range(b_):
+        for i in range(n_heads):
+            a[b, :, i] = causal_attention_core(q[b, :, i], k[b, :, i // g], v[b, :, i // g], 0, sc)
+    return a.reshape(b_, s_, n_heads * d) @ wo.T
+
+
+def mlp_full(u, w1, w3, w2):
+    """Gated MLP: (SiLU(u W1^T) * (u W3^T)) W2, Algorithm 2's three projections unsharded."""
+    return (silu(u @ w1.T) * (u @ w3.T)) @ w2
+
+
+def layer_full(x, w, n_heads, n_kv_heads, scale=None):
+    """Pre-norm residual layer with the norms left out (Section 4 model):
+    u = x + Attn(x);  y = u + MLP(u).  Returns every block output."""
+    attn = attention_full(x, w["wq"], w["wk"], w["wv"], w["wo"], n_heads, n_kv_heads, scale)
+    u = x + attn
+    mlp = mlp_full(u, w["w1"], w["w3"], w["w2"])
+    return {"attn": attn, "u": u, "mlp": mlp, "y": u + mlp}
+
+
+# ---------------------------------------------------------------------------
+# O2 -- the folded per-rank schedule, following Algorithms 1 and 2 step by step.
+# ---------------------------------------------------------------------------
+
+def mlp_rank(x_loc, w1_shards, w3_shards, w2_shards, p):
+    """TSP gated ring MLP on rank p (Algorithm 2).
+
+    Y starts at zero; at ring step t the rank holds the shard that started on
+    rank (p - t) mod D (each step receives from the left neighbour) and adds
+    (SiLU(X W1_j^T) * (X W3_j^T)) W2_j for its own tokens.  x_loc [B, S_loc, h].
+    """
+    degree = len(w1_shards)
+    y = np.zeros_like(x_loc, dtype=np.float64)
+    for t in range(degree):
+        j = (p - t) % degree
+        g = silu(x_loc @ w1_shards[j].T)
+        hh = x_loc @ w3_shards[j].T
+        y += (g * hh) @ w2_shards[j]
+    return y
+
+
+def unpack_attn_shard(packed, heads_per_shard, kv_heads_per_shard, head_dim):
+    """Split a packed shard [W_Q^(r); W_K^(r); W_V^(r); W_O^(r)^T] (Algorithm 1's
+    packed broadcast buffer) into its four row blocks."""
+    hs = heads_per_shard * head_dim
+    ks = kv_heads_per_shard * head_dim
+    wq = packed[:hs]
+    wk = packed[hs:hs + ks]
+    wv = packed[hs + ks:hs + 2 * ks]
+    wo_t = packed[hs + 2 * ks:hs + 2 * ks + hs]
+    assert wo_t.shape[0] == hs, "packed shard has the wrong number of rows"
+    return wq, wk, wv, wo_t
+
+
+def kv_project(x_chunk, packed, heads_per_shard, kv_heads_per_shard, head_dim):
+    """One rank's K, V for shard r on its own tokens: [B, S_loc, K_s, d] each.
+    This is what the rank contributes to the sequence-wise all-gather."""
+    _, wk, wv, _ = unpack_attn_shard(packed, heads_per_shard, kv_heads_per_shard, head_dim)
+    b_, s_loc, _ = x_chunk.shape
+    k = (x_chunk @ wk.T).reshape(b_, s_loc, kv_heads_per_shard, head_dim)
+    v = (x_chunk @ wv.T).reshape(b_, s_loc, kv_heads_per_shard, head_dim)
+    return k, v
+
+
+def gather_kv(x_chunks, packed, heads_per_shard, kv_heads_per_shard, head_dim):
+    """The sequence-wise all-gather of shard r's K and V over all ranks, in
+    sequence order (contiguous chunks need no reordering): [B, S, K_s, d]."""
+    parts = [kv_project(xc, packed, heads_per_shard, kv_heads_per_shard, head_dim)
+             for xc in x_chunks]
+    return (np.concatenate([k for k, _ in parts], axis=1),
+            np.concatenate([v for _, v in parts], axis=1))
+
+
+def attn_rank(x_loc, shards, kv_gathered, p, n_heads, n_kv_heads, head_dim, scale=None,
+              rows=None):
+    """TSP attention on rank p (Algorithm 1) with contiguous sequence chunks.
+
+    For r = 0 .. D-1: unpack shard r, project the local Q, take the gathered
+    full-sequence K, V of shard r (``kv_gathered[r]``, from :func:`gather_kv`),
+    attend causally from the local chunk against the prefix of length (p+1) S_loc
+    -- bottom-right aligned, so local row i sits at global position p S_loc + i --
+    and accumulate Flatten(A) W_O^(r)^T into Y, which starts at zero.
+
+    ``rows`` optionally restricts the computation to some local query rows
+    (every row of the output depends only on its own query).
+    """
+    degree = len(shards)
+    hs_heads = n_heads // degree
+    ks_heads = n_kv_heads // degree
+    g = n_heads // n_kv_heads
+    d = head_dim
+    sc = default_scale(d, scale)
+    b_, s_loc, h = x_loc.shape
+    xq = x_loc if rows is None else x_loc[:, rows]
+    lq = xq.shape[1]
+    row_pos = np.arange(s_loc) if rows is None else np.asarray(rows)
+    s1 = (p + 1) * s_loc
+    y = np.zeros((b_, lq, h), dtype=np.float64)
+    for r in range(degree):
+        wq, _, _, wo_t = unpack_attn_shard(shards[r], hs_heads, ks_heads, d)
+        q = (xq @ wq.T).reshape(b_, lq, hs_heads, d)
+        k_hat, v_hat = kv_gathered[r]
+        a = np.empty((b_, lq, hs_heads, d), dtype=np.float64)
+        for b in range(b_):
+            for i in range(hs_heads):
+                kh = i // g
+                if rows is None:
+                    a[b, :, i] = causal_attention_core(q[b, :, i], k_hat[b, :s1, kh],
+                                                       v_hat[b, :s1, kh], p * s_loc, sc)
+                else:
+                    for n, t in enumerate(row_pos):
+                        a[b, n:n + 1, i] = causal_attention_core(
+                            q[b, n:n + 1, i], k_hat[b, :s1, kh], v_hat[b, :s1, kh],
+                            p * s_loc + int(t), sc)
+        y += a.reshape(b_, lq, hs_heads * d) @ wo_t
+    return y
+
+
+def layer_rank(x_chunks, attn_shards, w1_shards, w3_shards, w2_shards, p, n_heads,
+               n_kv_heads, head_dim, scale=None):
+    """One rank's layer forward: u = x_loc + TSP-Attn(x), y = u + TSP-MLP(u).
+
+    The K/V all-gather is built from every rank's chunk of the layer input.
+    Returns the block outputs and the layer output for rank p's tokens.
+    """
+    degree = len(attn_shards)
+    hsh, ksh = n_heads // degree, n_kv_heads // degree
+    kv = [gather_kv(x_chunks, attn_shards[r], hsh, ksh, head_dim) for r in range(degree)]
+    x_loc = x_chunks[p]
+    attn = attn_rank(x_loc, attn_shards, kv, p, n_heads, n_kv_heads, head_dim, scale)
+    u = x_loc + attn
+    mlp = mlp_rank(u, w1_shards, w3_shards, w2_shards, p)
+    return {"attn": attn, "u": u, "mlp": mlp, "y": u + mlp}
+
+
+# ---------------------------------------------------------------------------
+# Sampled rows of the unsharded attention block, for full-size checks.
+# ---------------------------------------------------------------------------
+
+def attention_rows(x_b, wq, wk, wv, wo, n_heads, n_kv_heads, positions, scale=None):
+    """Attention-block output rows at the given global positions of one sequence.
+
+    x_b [S, h] is one batch entry of the layer input.  Uses only associativity of
+    the matrix products: the score of key j is (W_K,i^T q_t) . x_j and the context
+    is W_V,i (sum_j P_tj x_j), so no K or V for the whole prefix is ever formed.
+    Returns [len(positions), h].
+    """
+    positions = np.asarray(positions, dtype=np.int64)
+    d = wq.shape[0] // n_heads
+    g = n_heads // n_kv_heads
+    sc = default_scale(d, scale)
+    t_max = int(positions.max()) + 1
+    x_pre = x_b[:t_max]
+    n_r = positions.shape[0]
+    q = (x_b[positions] @ wq.T).reshape(n_r, n_heads, d)
+    wk_h = wk.reshape(n_kv_heads, d, -1)
+    wv_h = wv.reshape(n_kv_heads, d, -1)
+    u = np.empty((n_r, n_heads, x_b.shape[1]), dtype=np.float64)
+    for i in range(n_heads):
+        u[:, i] = q[:, i] @ wk_h[i // g]
+    s = (u.reshape(n_r * n_heads, -1) @ x_pre.T) * sc
+    pos_rows = np.repeat(positions, n_heads)
+    allowed = np.arange(t_max)[None, :] <= pos_rows[:, None]
+    s = np.where(allowed, s, -np.inf)
+    s -= s.max(axis=1, keepdims=True)
+    e = np.exp(s)
+    pmat = e / e.sum(axis=1, keepdims=True)
+    z = (pmat @ x_pre).reshape(n_r, n_heads, -1)
+    a = np.empty((n_r, n_heads, d), dtype=np.float64)
+    for i in range(n_heads):
+        a[:, i] = z[:, i] @ wv_h[i // g].T
+    return a.reshape(n_r, n_heads * d) @ wo.T

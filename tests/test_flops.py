@@ -1,0 +1,54 @@
+"""FLOP accounting of one rank's layer forward against the paper's closed forms
+(Section 4, FLOPs and parameter count; Appendix C reference model)."""
+import json
+import os
+
+import pytest
+
+from paper_2604_26294_amd import flops as F
+from paper_2604_26294_amd.workloads import ALL, L7B_64K, Workload
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paper_constants.json")
+
+
+def test_reference_7b_parameter_count():
+    ref = json.load(open(GOLDEN))["reference_7b_model"]
+    g = ref["n_heads"] / ref["n_kv_heads"]
+    total = ref["layers"] * F.params_per_layer(ref["hidden"], ref["ffn_factor"], g)
+    assert abs(total - ref["total_params_approx"]) <= ref["rounding"]
+    # P_attn + P_mlp with MHA is (4 + 3F) h^2 as the appendix states
+    assert F.params_per_layer(4096, 4, 1.0) == (4 + 3 * 4) * 4096 ** 2
+
+
+@pytest.mark.parametrize("wl", ALL, ids=lambda w: w.name)
+def test_rank_sum_reproduces_paper_layer_flops(wl):
+    """Summed over ranks: MLP + projections equal (4(1+1/g) + 6F) B S h^2 exactly, and
+    the attention core equals the causal half (with diagonal) of 4 B S^2 h."""
+    per = [F.rank_flops(wl, p) for p in range(wl.degree)]
+    g = wl.n_heads / wl.n_kv_heads
+    f = wl.ffn / wl.hidden
+    b, s, h = wl.batch, wl.seq, wl.hidden
+    dense = sum(r.mlp + r.proj for r in per)
+    assert dense == pytest.approx((4 * (1 + 1 / g) + 6 * f) * b * s * h * h, rel=1e-12)
+    core = sum(r.attn_core for r in per)
+    assert core == pytest.approx(4 * b * h * s * (s + 1) / 2, rel=1e-12)
+    # the paper's non-causal F_layer counts the full S^2 square
+    full_sq = F.paper_layer_flops(wl) - (4 * (1 + 1 / g) + 6 * f) * b * s * h * h
+    assert full_sq == pytest.approx(4 * b * s * s * h, rel=1e-12)
+
+
+def test_rank_imbalance_and_target_config():
+    per = [F.rank_flops(L7B_64K, p).total for p in range(8)]
+    assert all(a < b for a, b in zip(per, per[1:]))          # later ranks see longer prefixes
+    r7 = F.rank_flops(L7B_64K, 7)
+    assert r7.total == pytest.approx(11562.1e9, rel=1e-4)
+    assert r7.attn_core / r7.total == pytest.approx(0.713, abs=0.002)
+    assert F.step_attn_core_flops(L7B_64K) * 8 == pytest.approx(r7.attn_core, rel=1e-12)
+
+
+def test_causal_pairs_brute_force():
+    for s_loc in (1, 3, 8):
+        for p in range(4):
+            brute = sum(1 for i in range(s_loc) for j in range((p + 1) * s_loc)
+                        if j <= p * s_loc + i)
+            assert F.causal_pairs(s_loc, p) == brute

@@ -1,0 +1,103 @@
+"""Each plausible mistake planted in the oracle must make at least one pin fail.
+
+The mistakes are planted on the CPU by patching oracle functions for the duration
+of one test; the pins are the functions of test_oracle_pins.
+"""
+import numpy as np
+import pytest
+
+import oracle.tsp_oracle as O
+from tests import test_oracle_pins as P
+
+_orig_probs = O.causal_probs
+_orig_unpack = O.unpack_attn_shard
+_orig_silu = O.silu
+
+
+def _probs_strict_mask(q, k, q_offset, scale):          # j < t instead of j <= t
+    return _orig_probs(q, k, q_offset - 1, scale) if q_offset > 0 else _orig_probs(q, k, 0, scale)
+
+
+def _probs_no_mask(q, k, q_offset, scale):              # causal mask dropped
+    return _orig_probs(q, k, 10 ** 9, scale)
+
+
+def _probs_no_scale(q, k, q_offset, scale):             # softmax scale dropped
+    return _orig_probs(q, k, q_offset, 1.0)
+
+
+def _unpack_swap_kv(packed, hs, ks, d):                 # W_K / W_V blocks swapped
+    wq, wk, wv, wo = _orig_unpack(packed, hs, ks, d)
+    return wq, wv, wk, wo
+
+
+def _silu_sigmoid_only(z):                              # z * sigmoid(z) -> sigmoid(z)
+    return _orig_silu(z) / np.where(z == 0, 1.0, z)
+
+
+def _attention_full_wo_untransposed(x, wq, wk, wv, wo, n_heads, n_kv_heads, scale=None):
+    return _orig_attention_full(x, wq, wk, wv, wo.T, n_heads, n_kv_heads, scale)
+
+
+_orig_attention_full = O.attention_full
+
+
+def _mlp_full_gate_up_swapped(u, w1, w3, w2):
+    return (O.silu(u @ w3.T) * (u @ w1.T)) @ w2
+
+
+def _attn_rank_zero_offset(x_loc, shards, kv, p, n_heads, n_kv, d, scale=None, rows=None):
+    # forgets the rank's query offset: every chunk treated as if it started at 0
+    y = _orig_attn_rank(x_loc, shards, [(k[:, p * x_loc.shape[1]:], v[:, p * x_loc.shape[1]:])
+                                        for k, v in kv], 0, n_heads, n_kv, d, scale, rows)
+    return y
+
+
+_orig_attn_rank = O.attn_rank
+
+
+def _mlp_rank_skips_last_step(x_loc, w1s, w3s, w2s, p):
+    d = len(w1s)
+    y = np.zeros_like(x_loc)
+    for t in range(d - 1):
+        j = (p - t) % d
+        y += (O.silu(x_loc @ w1s[j].T) * (x_loc @ w3s[j].T)) @ w2s[j]
+    return y
+
+
+MUTATIONS = {
+    "mask_excludes_diagonal": ("causal_probs", _probs_strict_mask),
+    "mask_dropped": ("causal_probs", _probs_no_mask),
+    "scale_dropped": ("causal_probs", _probs_no_scale),
+    "kv_blocks_swapped": ("unpack_attn_shard", _unpack_swap_kv),
+    "silu_is_sigmoid": ("silu", _silu_sigmoid_only),
+    "wo_not_transposed": ("attention_full", _attention_full_wo_untransposed),
+    "gate_up_swapped": ("mlp_full", _mlp_full_gate_up_swapped),
+    "rank_offset_dropped": ("attn_rank", _attn_rank_zero_offset),
+    "ring_step_dropped": ("mlp_rank", _mlp_rank_skips_last_step),
+}
+
+PINS = [
+    (P.test_attention_two_token_closed_form, ()),
+    (P.test_gqa_head_mapping_closed_form, ()),
+    (P.test_mlp_closed_form, ()),
+    (P.test_unsharded_layer_matches_brute_force, (2, 1)),
+    (P.test_fold_concat_equals_unsharded, (4, 2, 2)),
+    (P.test_zero_queries_give_prefix_mean, (1,)),
+    (P.test_softmax_rows_sum_to_one_and_first_query_sees_key0, ()),
+    (P.test_linearity_in_output_projections, ()),
+    (P.test_mlp_ring_order_and_row_permutation_invariance, ()),
+]
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(name, monkeypatch):
+    attr, fn = MUTATIONS[name]
+    monkeypatch.setattr(O, attr, fn)
+    failed = []
+    for pin, args in PINS:
+        try:
+            pin(*args)
+        except (AssertionError, ValueError, IndexError):
+            failed.append(pin.__name__)
+    assert failed, f"no pin caught mutation {name}"
