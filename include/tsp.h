@@ -1,0 +1,153 @@
+/*
+ * tsp.h -- C ABI of libtsp: the per-rank forward of a folded Tensor-and-Sequence
+ * Parallel (TSP) transformer layer on one AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "Folding Tensor and Sequence Parallelism for Memory-Efficient Transformer
+ * Training & Inference" (arXiv 2604.26294).  A TSP group of D ranks shards both the
+ * sequence and the layer weights over one device axis: rank p holds the contiguous
+ * token chunk [p*S/D, (p+1)*S/D) and, over D steps, applies every weight shard to it.
+ *
+ *   - Attention (Algorithm 1): for r = 0..D-1 the rank projects Q, K, V of its chunk
+ *     with shard r, attends causally against the full-sequence K/V of shard r (the
+ *     sequence-wise all-gather), and accumulates Flatten(A) W_O^(r)^T.
+ *   - Gated MLP (Algorithm 2): for t = 0..D-1 the rank applies the shard that started
+ *     on rank (p - t) mod D (ring order) and accumulates (SiLU(X W1^T) * X W3^T) W2.
+ *   - Layer (Section 4 model: pre-norm residual block, norms left out):
+ *     u = x + Attn(x), y = u + MLP(u).
+ *
+ * On one GPU the exchanges are modelled by resident buffers: every weight shard is
+ * already in device memory (the broadcast / ring hand-off has happened), and the
+ * K/V buffer holds the full sequence (the all-gather).  Each attention call WRITES
+ * its own chunk's K/V rows for every shard and READS the causal prefix
+ * [0, (p+1)*S/D); rows of earlier ranks are the caller's (see tsp_kv_rank_fwd).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor arguments are DEVICE pointers to dense row-major arrays.  bf16
+ *     values are passed as their 16-bit patterns (uint16_t).  fp32 is float.
+ *   - Arrays of D shard pointers ("w_gate", "w_attn", ...) are HOST arrays whose
+ *     elements are device pointers, one per shard, indexed by shard number.
+ *   - Every device pointer must be 16-byte aligned.
+ *   - The caller owns every buffer.  The library never allocates or frees device
+ *     memory and keeps no state between calls; scratch space is the caller's
+ *     workspace, sized by tsp_workspace_bytes.
+ *   - Calls only enqueue work on `stream` (NULL = the default stream) and never
+ *     synchronise.  Calls on different streams must use different workspaces and
+ *     must not write the same outputs.
+ *   - All validation happens on the host, before anything is enqueued; a call that
+ *     returns an error has enqueued nothing.  TSP_ERR_HIP reports a failed launch
+ *     (work enqueued before the failure may still run).
+ *   - Results are deterministic: no atomics, fixed reduction orders.
+ *   - Supported: head_dim in {64, 128}; hidden, ffn/degree and head_dim multiples
+ *     of 8; layout 0 (contiguous chunks).  Anything else valid returns
+ *     TSP_ERR_UNSUPPORTED.
+ */
+#ifndef TSP_H
+#define TSP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TSP_ABI_VERSION 1
+
+typedef enum tsp_status {
+  TSP_OK = 0,
+  TSP_ERR_NULL = 1,        /* a required pointer (shape, tensor, shard, workspace) is NULL */
+  TSP_ERR_SHAPE = 2,       /* dimensions are non-positive or inconsistent (see below) */
+  TSP_ERR_RANK = 3,        /* rank outside [0, degree) */
+  TSP_ERR_ALIGN = 4,       /* a device pointer is not 16-byte aligned */
+  TSP_ERR_WORKSPACE = 5,   /* ws_bytes is smaller than tsp_workspace_bytes() */
+  TSP_ERR_UNSUPPORTED = 6, /* valid shape the kernels do not implement */
+  TSP_ERR_HIP = 7          /* a kernel launch failed */
+} tsp_status;
+
+/* Problem statement of one rank (paper notation, Section 4 notation table).
+ * Shape rules (TSP_ERR_SHAPE otherwise): batch >= 0, seq >= 0, every other size >= 1;
+ * seq % degree == 0; hidden == n_heads * head_dim; n_heads % n_kv_heads == 0;
+ * n_heads % degree == 0; n_kv_heads % degree == 0; ffn % degree == 0. */
+typedef struct tsp_shape {
+  int32_t batch;        /* B: micro-batch */
+  int32_t seq;          /* S: full sequence length; each rank holds S_loc = S / D tokens */
+  int32_t hidden;       /* h: model width */
+  int32_t ffn;          /* MLP intermediate width (the paper's F*h); shards hold ffn / D rows */
+  int32_t n_heads;      /* n_h: query heads; shard r holds heads [r*n_h/D, (r+1)*n_h/D) */
+  int32_t n_kv_heads;   /* n_kv: key/value heads (GQA ratio g = n_h / n_kv); query head i
+                           reads kv head i / g */
+  int32_t head_dim;     /* d */
+  int32_t degree;       /* D: TSP degree (number of shards) */
+  int32_t rank;         /* p: this rank */
+  int32_t layout;       /* 0 = contiguous chunks (rank p owns [p*S_loc, (p+1)*S_loc)) */
+  float softmax_scale;  /* <= 0 selects 1/sqrt(head_dim) */
+} tsp_shape;
+
+/* Gated ring MLP of rank p (Algorithm 2):
+ *   Y (+)= sum over t = 0..D-1, j = (p - t) mod D, of
+ *          bf16( SiLU(X W_gate[j]^T) * (X W_up[j]^T) ) W_down[j]
+ * with SiLU(z) = z * sigmoid(z), fp32 accumulation across shards in ring order.
+ *   x_loc      [B, S_loc, h] bf16       the rank's tokens
+ *   w_gate[j]  [ffn/D, h]   bf16       W1 shard j
+ *   w_up[j]    [ffn/D, h]   bf16       W3 shard j
+ *   w_down[j]  [ffn/D, h]   bf16       W2 shard j, applied untransposed
+ *   y_loc      [B, S_loc, h] fp32      accumulate == 0: overwritten; != 0: added to
+ *   ws         workspace of at least tsp_workspace_bytes(shape, TSP_OP_MLP) bytes */
+tsp_status tsp_mlp_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
+                            const uint16_t* const* w_gate, const uint16_t* const* w_up,
+                            const uint16_t* const* w_down, float* y_loc, int accumulate,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* This rank's contribution to the sequence-wise K/V all-gather of every shard
+ * (Algorithm 1, the local K and V projections): for r = 0..D-1 writes
+ *   k_buf[b, p*S_loc + t, r*n_kv/D + j, :] = (x_loc[b, t] W_K^(r)^T) head j, bf16
+ * and the same for V.  Used to fill the K/V rows of ranks other than the caller.
+ *   x_loc      [B, S_loc, h] bf16
+ *   w_attn[r]  packed shard r, [(2*n_h/D + 2*n_kv/D) * d, h] bf16: rows
+ *              [W_Q^(r) ; W_K^(r) ; W_V^(r) ; W_O^(r)^T] (the packed broadcast buffer)
+ *   k_buf, v_buf [B, S, n_kv, d] bf16   rows [p*S_loc, (p+1)*S_loc) written */
+tsp_status tsp_kv_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
+                           const uint16_t* const* w_attn, uint16_t* k_buf, uint16_t* v_buf,
+                           hipStream_t stream);
+
+/* TSP attention of rank p (Algorithm 1, contiguous chunks): for r = 0..D-1,
+ *   Q = X W_Q^(r)^T; K, V rows of this rank written into k_buf / v_buf;
+ *   A = causal softmax(Q K^T * scale) V over keys [0, (p+1)*S_loc), where local query
+ *       row t sits at global position p*S_loc + t and sees keys j <= p*S_loc + t;
+ *   Y (+)= Flatten(A) W_O^(r)^T   (fp32, shards accumulated in order r = 0..D-1).
+ * Q, K, V, the softmax probabilities and A are rounded to bf16 for the matrix cores.
+ *   x_loc, w_attn as for tsp_kv_rank_fwd;  k_buf, v_buf [B, S, n_kv, d] bf16: this
+ *   rank's rows are written, rows [0, p*S_loc) must already hold ranks 0..p-1's K/V,
+ *   rows at or beyond (p+1)*S_loc are never read.
+ *   y_loc [B, S_loc, h] fp32, overwritten (accumulate == 0) or added to. */
+tsp_status tsp_attn_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
+                             const uint16_t* const* w_attn, uint16_t* k_buf, uint16_t* v_buf,
+                             float* y_loc, int accumulate, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/* One rank's layer forward: u = x + Attn(x); y = u + MLP(bf16(u)).
+ * Arguments as above; y_loc [B, S_loc, h] fp32 is overwritten with y. */
+tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
+                              const uint16_t* const* w_attn, const uint16_t* const* w_gate,
+                              const uint16_t* const* w_up, const uint16_t* const* w_down,
+                              uint16_t* k_buf, uint16_t* v_buf, float* y_loc, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
+
+enum { TSP_OP_MLP = 0, TSP_OP_ATTN = 1, TSP_OP_LAYER = 2 };
+
+/* Workspace bytes the entry point `op` needs for `shape` (validated as above). */
+tsp_status tsp_workspace_bytes(const tsp_shape* shape, int op, size_t* bytes);
+
+/* Static, human-readable name of a status code. */
+const char* tsp_status_str(tsp_status status);
+
+/* TSP_ABI_VERSION of the built library. */
+int tsp_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TSP_H */

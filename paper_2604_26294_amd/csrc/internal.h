@@ -1,0 +1,79 @@
+// Internal launchers of libtsp's gfx950 kernels (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tsp {
+
+// Parameters of the bf16 MFMA GEMM family: C[M, N] = A[M, K] * B, fp32 accumulation.
+// B is [N, K] row-major ("NT", both operands contraction-contiguous) or [K, N]
+// row-major ("NN").  The epilogue decides what C becomes.
+struct GemmParams {
+  const uint16_t* A;
+  int lda;
+  const uint16_t* B;
+  int ldb;
+  const uint16_t* B2;  // SwiGLU only: the up-projection operand, same layout as B
+  int M, N, K;
+
+  // SwiGLU epilogue: H[m, n] = bf16( SiLU(C_gate) * C_up )
+  uint16_t* H;
+  int ldh;
+
+  // Accumulate epilogue: Y[m, n] = base + C, base = bf16 R[m, n] if R, else Y[m, n]
+  // if accumulate, else 0; optionally U[m, n] = bf16(Y[m, n]).
+  float* Y;
+  int ldy;
+  int accumulate;
+  const uint16_t* R;
+  int ldr;
+  uint16_t* U;
+  int ldu;
+
+  // Q/K/V epilogue: columns [0, nq) -> Q[m, n]; [nq, nq+nkv) -> K buffer;
+  // [nq+nkv, nq+2nkv) -> V buffer.  Row m = b*rows_per_batch + t lands at sequence
+  // position kv_pos0 + t of batch b; column c of the K (or V) block lands at
+  // element kv_col0 + c of that position's row.
+  uint16_t* Q;
+  int ldq;
+  uint16_t* Kb;
+  uint16_t* Vb;
+  int nq, nkv;
+  int rows_per_batch;
+  long long kv_batch_stride;
+  int kv_row_stride;
+  long long kv_pos0;
+  int kv_col0;
+};
+
+hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s);
+hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s);
+hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s);
+
+// Causal flash attention of one rank's query chunk for the heads of one shard.
+//   Q [B, S_loc, H_s, d] bf16;  K/V buffers [B, S, n_kv, d] bf16 (heads
+//   kv_head0 .. kv_head0 + H_s/g - 1 are this shard's);  O [B, S_loc, H_s, d] bf16.
+//   Local query t sits at global position q_pos0 + t and sees keys j <= q_pos0 + t;
+//   keys at or beyond kv_len are never read.
+struct AttnParams {
+  const uint16_t* Q;
+  const uint16_t* Kb;
+  const uint16_t* Vb;
+  uint16_t* O;
+  int batch;
+  int s_loc;
+  int heads;        // H_s
+  int group;        // g = n_h / n_kv
+  int head_dim;     // d
+  long long seq;    // S (K/V buffer rows per batch)
+  int n_kv;         // kv heads in the buffer
+  int kv_head0;     // first kv head of this shard
+  long long q_pos0; // global position of local query 0
+  long long kv_len; // number of readable keys: (p + 1) * S_loc
+  float scale_log2; // softmax scale * log2(e)
+};
+
+hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s);
+
+}  // namespace tsp

@@ -1,0 +1,334 @@
+// Host side of the libtsp C ABI: argument validation, workspace planning and the
+// per-rank shard loops of the paper's two schedules.  Every check runs before the
+// first launch, so a call that returns an error has enqueued nothing.
+#include <math.h>
+#include <stdint.h>
+
+#include "internal.h"
+#include "tsp.h"
+
+namespace {
+
+using tsp::AttnParams;
+using tsp::GemmParams;
+
+constexpr size_t kAlign = 256;
+
+struct Dims {
+  int B, S, h, F, nh, nkv, d, D, p;
+  int s_loc;   // S / D
+  int hs;      // query heads per shard
+  int ks;      // kv heads per shard
+  int g;       // GQA ratio
+  int fs;      // MLP rows per shard
+  long long M; // B * S_loc tokens of this rank
+  float scale;
+};
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+tsp_status check_shape(const tsp_shape* s, Dims* o) {
+  if (!s) return TSP_ERR_NULL;
+  if (s->batch < 0 || s->seq < 0 || s->hidden < 1 || s->ffn < 1 || s->n_heads < 1 ||
+      s->n_kv_heads < 1 || s->head_dim < 1 || s->degree < 1)
+    return TSP_ERR_SHAPE;
+  if (s->rank < 0 || s->rank >= s->degree) return TSP_ERR_RANK;
+  if (s->seq % s->degree != 0 || (long long)s->n_heads * s->head_dim != s->hidden ||
+      s->n_heads % s->n_kv_heads != 0 || s->n_heads % s->degree != 0 ||
+      s->n_kv_heads % s->degree != 0 || s->ffn % s->degree != 0)
+    return TSP_ERR_SHAPE;
+  if (s->layout != 0) return TSP_ERR_UNSUPPORTED;
+  if (s->head_dim != 64 && s->head_dim != 128) return TSP_ERR_UNSUPPORTED;
+  if (s->hidden % 8 != 0 || (s->ffn / s->degree) % 8 != 0) return TSP_ERR_UNSUPPORTED;
+  o->B = s->batch;
+  o->S = s->seq;
+  o->h = s->hidden;
+  o->F = s->ffn;
+  o->nh = s->n_heads;
+  o->nkv = s->n_kv_heads;
+  o->d = s->head_dim;
+  o->D = s->degree;
+  o->p = s->rank;
+  o->s_loc = s->seq / s->degree;
+  o->hs = s->n_heads / s->degree;
+  o->ks = s->n_kv_heads / s->degree;
+  o->g = s->n_heads / s->n_kv_heads;
+  o->fs = s->ffn / s->degree;
+  o->M = (long long)o->B * o->s_loc;
+  if (o->M > INT32_MAX / 2) return TSP_ERR_UNSUPPORTED;
+  o->scale = s->softmax_scale > 0.f ? s->softmax_scale : 1.0f / sqrtf((float)s->head_dim);
+  return TSP_OK;
+}
+
+// Workspace regions (each 256-byte aligned):
+//   MLP:   Hs [M, F/D] bf16
+//   ATTN:  Q [M, H_s d] bf16, A [M, H_s d] bf16
+//   LAYER: u [M, h] bf16, then max(MLP, ATTN)
+size_t ws_mlp(const Dims& d) { return align_up((size_t)d.M * d.fs * 2); }
+size_t ws_attn(const Dims& d) { return 2 * align_up((size_t)d.M * d.hs * d.d * 2); }
+size_t ws_layer(const Dims& d) {
+  const size_t a = ws_mlp(d), b = ws_attn(d);
+  return align_up((size_t)d.M * d.h * 2) + (a > b ? a : b);
+}
+
+bool aligned(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+tsp_status check_ptr(const void* p) {
+  if (!p) return TSP_ERR_NULL;
+  return aligned(p) ? TSP_OK : TSP_ERR_ALIGN;
+}
+
+tsp_status check_shards(const uint16_t* const* arr, int D) {
+  if (!arr) return TSP_ERR_NULL;
+  for (int i = 0; i < D; ++i) {
+    const tsp_status st = check_ptr(arr[i]);
+    if (st != TSP_OK) return st;
+  }
+  return TSP_OK;
+}
+
+#define TSP_TRY(expr)                          \
+  do {                                         \
+    const tsp_status st_ = (expr);             \
+    if (st_ != TSP_OK) return st_;             \
+  } while (0)
+
+#define TSP_HIP(expr)                          \
+  do {                                         \
+    if ((expr) != hipSuccess) return TSP_ERR_HIP; \
+  } while (0)
+
+// ----------------------------------------------------------------- launch sequences
+
+// Algorithm 2 on an already validated problem.  Ring step t uses shard (p - t) mod D.
+tsp_status run_mlp(const Dims& d, const uint16_t* x, const uint16_t* const* wg,
+                   const uint16_t* const* wu, const uint16_t* const* wd, float* y,
+                   int accumulate, uint16_t* hs_ws, hipStream_t st) {
+  for (int t = 0; t < d.D; ++t) {
+    const int j = ((d.p - t) % d.D + d.D) % d.D;
+    GemmParams up = {};
+    up.A = x;
+    up.lda = d.h;
+    up.B = wg[j];
+    up.B2 = wu[j];
+    up.ldb = d.h;
+    up.M = (int)d.M;
+    up.N = d.fs;
+    up.K = d.h;
+    up.H = hs_ws;
+    up.ldh = d.fs;
+    TSP_HIP(tsp::launch_gemm_swiglu(up, st));
+
+    GemmParams dn = {};
+    dn.A = hs_ws;
+    dn.lda = d.fs;
+    dn.B = wd[j];
+    dn.ldb = d.h;
+    dn.M = (int)d.M;
+    dn.N = d.h;
+    dn.K = d.fs;
+    dn.Y = y;
+    dn.ldy = d.h;
+    dn.accumulate = (t > 0 || accumulate) ? 1 : 0;
+    TSP_HIP(tsp::launch_gemm_nn_acc(dn, st));
+  }
+  return TSP_OK;
+}
+
+GemmParams qkv_params(const Dims& d, const uint16_t* x, const uint16_t* shard, int r,
+                      uint16_t* q_ws, uint16_t* kb, uint16_t* vb, bool with_q) {
+  GemmParams g = {};
+  const int qd = d.hs * d.d, kd = d.ks * d.d;
+  g.A = x;
+  g.lda = d.h;
+  g.B = with_q ? shard : shard + (size_t)qd * d.h;
+  g.ldb = d.h;
+  g.M = (int)d.M;
+  g.N = (with_q ? qd : 0) + 2 * kd;
+  g.K = d.h;
+  g.Q = q_ws;
+  g.ldq = qd;
+  g.Kb = kb;
+  g.Vb = vb;
+  g.nq = with_q ? qd : 0;
+  g.nkv = kd;
+  g.rows_per_batch = d.s_loc;
+  g.kv_batch_stride = (long long)d.S * d.nkv * d.d;
+  g.kv_row_stride = d.nkv * d.d;
+  g.kv_pos0 = (long long)d.p * d.s_loc;
+  g.kv_col0 = r * kd;
+  return g;
+}
+
+// Algorithm 1 (contiguous chunks).  `residual` (bf16 [M, h]) initialises Y at the
+// first shard instead of zero / the old Y; `u_out` receives bf16(Y) after the last.
+tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
+                    uint16_t* kb, uint16_t* vb, float* y, int accumulate,
+                    const uint16_t* residual, uint16_t* u_out, uint16_t* q_ws,
+                    uint16_t* a_ws, hipStream_t st) {
+  const int qd = d.hs * d.d, kd = d.ks * d.d;
+  const float log2e = 1.4426950408889634f;
+  for (int r = 0; r < d.D; ++r) {
+    GemmParams g = qkv_params(d, x, wa[r], r, q_ws, kb, vb, true);
+    TSP_HIP(tsp::launch_gemm_qkv(g, st));
+
+    AttnParams ap = {};
+    ap.Q = q_ws;
+    ap.Kb = kb;
+    ap.Vb = vb;
+    ap.O = a_ws;
+    ap.batch = d.B;
+    ap.s_loc = d.s_loc;
+    ap.heads = d.hs;
+    ap.group = d.g;
+    ap.head_dim = d.d;
+    ap.seq = d.S;
+    ap.n_kv = d.nkv;
+    ap.kv_head0 = r * d.ks;
+    ap.q_pos0 = (long long)d.p * d.s_loc;
+    ap.kv_len = (long long)(d.p + 1) * d.s_loc;
+    ap.scale_log2 = d.scale * log2e;
+    TSP_HIP(tsp::launch_flash_attn(ap, st));
+
+    GemmParams o = {};
+    o.A = a_ws;
+    o.lda = qd;
+    o.B = wa[r] + (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T block [H_s d, h]
+    o.ldb = d.h;
+    o.M = (int)d.M;
+    o.N = d.h;
+    o.K = qd;
+    o.Y = y;
+    o.ldy = d.h;
+    o.accumulate = (r > 0 || accumulate) ? 1 : 0;
+    if (r == 0 && residual) {
+      o.R = residual;
+      o.ldr = d.h;
+    }
+    if (r == d.D - 1 && u_out) {
+      o.U = u_out;
+      o.ldu = d.h;
+    }
+    TSP_HIP(tsp::launch_gemm_nn_acc(o, st));
+  }
+  return TSP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tsp_status tsp_workspace_bytes(const tsp_shape* shape, int op, size_t* bytes) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  if (!bytes) return TSP_ERR_NULL;
+  switch (op) {
+    case TSP_OP_MLP: *bytes = ws_mlp(d); return TSP_OK;
+    case TSP_OP_ATTN: *bytes = ws_attn(d); return TSP_OK;
+    case TSP_OP_LAYER: *bytes = ws_layer(d); return TSP_OK;
+    default: return TSP_ERR_SHAPE;
+  }
+}
+
+tsp_status tsp_mlp_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
+                            const uint16_t* const* w_gate, const uint16_t* const* w_up,
+                            const uint16_t* const* w_down, float* y_loc, int accumulate,
+                            void* ws, size_t ws_bytes, hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_ptr(y_loc));
+  TSP_TRY(check_shards(w_gate, d.D));
+  TSP_TRY(check_shards(w_up, d.D));
+  TSP_TRY(check_shards(w_down, d.D));
+  TSP_TRY(check_ptr(ws));
+  if (ws_bytes < ws_mlp(d)) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  return run_mlp(d, x_loc, w_gate, w_up, w_down, y_loc, accumulate,
+                 static_cast<uint16_t*>(ws), stream);
+}
+
+tsp_status tsp_kv_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
+                           const uint16_t* const* w_attn, uint16_t* k_buf, uint16_t* v_buf,
+                           hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_shards(w_attn, d.D));
+  TSP_TRY(check_ptr(k_buf));
+  TSP_TRY(check_ptr(v_buf));
+  if (d.M == 0) return TSP_OK;
+  for (int r = 0; r < d.D; ++r) {
+    GemmParams g = qkv_params(d, x_loc, w_attn[r], r, nullptr, k_buf, v_buf, false);
+    TSP_HIP(tsp::launch_gemm_qkv(g, stream));
+  }
+  return TSP_OK;
+}
+
+tsp_status tsp_attn_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
+                             const uint16_t* const* w_attn, uint16_t* k_buf, uint16_t* v_buf,
+                             float* y_loc, int accumulate, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_shards(w_attn, d.D));
+  TSP_TRY(check_ptr(k_buf));
+  TSP_TRY(check_ptr(v_buf));
+  TSP_TRY(check_ptr(y_loc));
+  TSP_TRY(check_ptr(ws));
+  if (ws_bytes < ws_attn(d)) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  uint16_t* q_ws = static_cast<uint16_t*>(ws);
+  uint16_t* a_ws = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + ws_attn(d) / 2);
+  return run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, accumulate, nullptr, nullptr, q_ws,
+                  a_ws, stream);
+}
+
+tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
+                              const uint16_t* const* w_attn, const uint16_t* const* w_gate,
+                              const uint16_t* const* w_up, const uint16_t* const* w_down,
+                              uint16_t* k_buf, uint16_t* v_buf, float* y_loc, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_shards(w_attn, d.D));
+  TSP_TRY(check_shards(w_gate, d.D));
+  TSP_TRY(check_shards(w_up, d.D));
+  TSP_TRY(check_shards(w_down, d.D));
+  TSP_TRY(check_ptr(k_buf));
+  TSP_TRY(check_ptr(v_buf));
+  TSP_TRY(check_ptr(y_loc));
+  TSP_TRY(check_ptr(ws));
+  if (ws_bytes < ws_layer(d)) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  char* base = static_cast<char*>(ws);
+  uint16_t* u_ws = reinterpret_cast<uint16_t*>(base);
+  char* rest = base + align_up((size_t)d.M * d.h * 2);
+  uint16_t* q_ws = reinterpret_cast<uint16_t*>(rest);
+  uint16_t* a_ws = reinterpret_cast<uint16_t*>(rest + ws_attn(d) / 2);
+  // u = x + Attn(x): Y starts from x at the first shard; the last shard also writes bf16(u).
+  TSP_TRY(run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, 0, x_loc, u_ws, q_ws, a_ws, stream));
+  // y = u + MLP(bf16 u): the MLP accumulates onto Y, which holds u.
+  return run_mlp(d, u_ws, w_gate, w_up, w_down, y_loc, 1, reinterpret_cast<uint16_t*>(rest),
+                 stream);
+}
+
+const char* tsp_status_str(tsp_status status) {
+  switch (status) {
+    case TSP_OK: return "TSP_OK";
+    case TSP_ERR_NULL: return "TSP_ERR_NULL: a required pointer is NULL";
+    case TSP_ERR_SHAPE: return "TSP_ERR_SHAPE: inconsistent or non-divisible dimensions";
+    case TSP_ERR_RANK: return "TSP_ERR_RANK: rank outside [0, degree)";
+    case TSP_ERR_ALIGN: return "TSP_ERR_ALIGN: device pointer not 16-byte aligned";
+    case TSP_ERR_WORKSPACE: return "TSP_ERR_WORKSPACE: workspace too small";
+    case TSP_ERR_UNSUPPORTED: return "TSP_ERR_UNSUPPORTED: shape not implemented";
+    case TSP_ERR_HIP: return "TSP_ERR_HIP: kernel launch failed";
+    default: return "TSP_ERR_UNKNOWN";
+  }
+}
+
+int tsp_abi_version(void) { return TSP_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,81 @@
+"""Device-side setup of one rank's TSP problem from the seeded inputs.
+
+Uploads the bf16 bit patterns drawn by :mod:`paper_2604_26294_amd.inputs`, builds
+the per-shard device buffers the C ABI takes, and allocates outputs, the K/V
+buffer and the workspace.  No arithmetic of the method lives here: everything is
+computed by libtsp through :mod:`paper_2604_26294_amd.tsp`.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import inputs as I
+from . import tsp as T
+from .workloads import Workload
+
+
+def to_device_bf16(bits: np.ndarray, device="cuda") -> torch.Tensor:
+    t = torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16))
+    return t.view(torch.bfloat16).to(device)
+
+
+def bf16_tensor_to_f64(t: torch.Tensor) -> np.ndarray:
+    bits = t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    return I.bf16_bits_to_f64(bits)
+
+
+class RankProblem:
+    """All device buffers of rank ``p`` of workload ``wl``.
+
+    ``x_full`` / ``w`` are the bf16 bit patterns of the whole-sequence input and the
+    full weights (see :func:`inputs.make_x_full`, :func:`inputs.make_weights`).
+    """
+
+    def __init__(self, wl: Workload, x_full: np.ndarray, w: dict, p: int | None = None,
+                 device="cuda", kv_fill: float | None = 0.0):
+        self.wl = wl
+        self.p = wl.rank if p is None else p
+        self.device = device
+        D = wl.degree
+        self.shape = T.shape_of(wl, self.p)
+        self.x_chunks = [to_device_bf16(I.local_chunk(x_full, q, D), device)
+                         for q in range(self.p + 1)]
+        self.x_loc = self.x_chunks[self.p]
+        self.attn = [to_device_bf16(I.attn_shard_packed(w, r, D, wl.n_heads, wl.n_kv_heads,
+                                                        wl.head_dim), device)
+                     for r in range(D)]
+        mlp = [I.mlp_shard(w, j, D) for j in range(D)]
+        self.w1 = [to_device_bf16(m[0], device) for m in mlp]
+        self.w3 = [to_device_bf16(m[1], device) for m in mlp]
+        self.w2 = [to_device_bf16(m[2], device) for m in mlp]
+        kv_shape = (wl.batch, wl.seq, wl.n_kv_heads, wl.head_dim)
+        self.k_buf = torch.empty(kv_shape, dtype=torch.bfloat16, device=device)
+        self.v_buf = torch.empty(kv_shape, dtype=torch.bfloat16, device=device)
+        if kv_fill is not None:
+            self.k_buf.fill_(kv_fill)
+            self.v_buf.fill_(kv_fill)
+        self.y = torch.zeros((wl.batch, wl.s_loc, wl.hidden), dtype=torch.float32, device=device)
+        nbytes = max(T.workspace_bytes(self.shape, op) for op in (T.OP_MLP, T.OP_ATTN, T.OP_LAYER))
+        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+    def prefill_kv(self):
+        """The modelled all-gather: ranks 0 .. p-1 write their K/V rows of every shard."""
+        for q in range(self.p):
+            T.tsp_kv_rank_fwd(T.shape_of(self.wl, q), self.x_chunks[q], self.attn, self.k_buf,
+                              self.v_buf)
+
+    def mlp(self, x=None, accumulate=False):
+        T.tsp_mlp_rank_fwd(self.shape, self.x_loc if x is None else x, self.w1, self.w3,
+                           self.w2, self.y, accumulate, self.ws)
+        return self.y
+
+    def attn_fwd(self, accumulate=False):
+        T.tsp_attn_rank_fwd(self.shape, self.x_loc, self.attn, self.k_buf, self.v_buf, self.y,
+                            accumulate, self.ws)
+        return self.y
+
+    def layer(self):
+        T.tsp_layer_rank_fwd(self.shape, self.x_loc, self.attn, self.w1, self.w3, self.w2,
+                             self.k_buf, self.v_buf, self.y, self.ws)
+        return self.y

@@ -1,0 +1,145 @@
+"""Thin ctypes binding of libtsp (see include/tsp.h).  Argument marshalling only:
+every step of the per-rank forward runs in the library's HIP kernels.
+
+Tensors are torch tensors on the GPU; bf16 operands are ``torch.bfloat16`` (passed
+as their bit patterns), accumulators ``torch.float32``.  Shard lists are Python
+sequences of tensors (one per shard).  Importing this module loads libtsp.so and
+raises ImportError if it has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtsp.so")
+
+TSP_OK = 0
+STATUS_NAMES = {0: "TSP_OK", 1: "TSP_ERR_NULL", 2: "TSP_ERR_SHAPE", 3: "TSP_ERR_RANK",
+                4: "TSP_ERR_ALIGN", 5: "TSP_ERR_WORKSPACE", 6: "TSP_ERR_UNSUPPORTED",
+                7: "TSP_ERR_HIP"}
+OP_MLP, OP_ATTN, OP_LAYER = 0, 1, 2
+
+
+class TspError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {lib.tsp_status_str(status).decode()}")
+
+
+class tsp_shape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("seq", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("ffn", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("degree", ctypes.c_int32),
+                ("rank", ctypes.c_int32), ("layout", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2604_26294_amd.build`")
+    L = ctypes.CDLL(_LIB_PATH)
+    P, VP, SZ, I = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+    SH = ctypes.POINTER(tsp_shape)
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    sig = {
+        "tsp_mlp_rank_fwd": [SH, P, PP, PP, PP, P, I, VP, SZ, VP],
+        "tsp_kv_rank_fwd": [SH, P, PP, P, P, VP],
+        "tsp_attn_rank_fwd": [SH, P, PP, P, P, P, I, VP, SZ, VP],
+        "tsp_layer_rank_fwd": [SH, P, PP, PP, PP, PP, P, P, P, VP, SZ, VP],
+        "tsp_workspace_bytes": [SH, I, ctypes.POINTER(ctypes.c_size_t)],
+        "tsp_status_str": [I],
+        "tsp_abi_version": [],
+    }
+    for name, args in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    L.tsp_status_str.restype = ctypes.c_char_p
+    return L
+
+
+lib = _load()
+
+
+def make_shape(batch, seq, hidden, ffn, n_heads, n_kv_heads, head_dim, degree, rank,
+               layout=0, softmax_scale=0.0) -> tsp_shape:
+    return tsp_shape(batch, seq, hidden, ffn, n_heads, n_kv_heads, head_dim, degree, rank,
+                     layout, softmax_scale)
+
+
+def shape_of(wl, rank=None, softmax_scale=0.0) -> tsp_shape:
+    """tsp_shape of a :class:`~paper_2604_26294_amd.workloads.Workload`."""
+    return make_shape(wl.batch, wl.seq, wl.hidden, wl.ffn, wl.n_heads, wl.n_kv_heads,
+                      wl.head_dim, wl.degree, wl.rank if rank is None else rank, 0,
+                      softmax_scale)
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _ptrs(ts: Sequence):
+    arr = (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])
+    return ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)), arr
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def _check(st: int, where: str):
+    if st != TSP_OK:
+        raise TspError(st, where)
+
+
+def workspace_bytes(shape: tsp_shape, op: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib.tsp_workspace_bytes(ctypes.byref(shape), op, ctypes.byref(out)),
+           "tsp_workspace_bytes")
+    return out.value
+
+
+def _nbytes(ws) -> int:
+    return ws.numel() * ws.element_size() if ws is not None else 0
+
+
+def tsp_mlp_rank_fwd(shape, x_loc, w_gate, w_up, w_down, y_loc, accumulate, ws, stream=None):
+    g, _g = _ptrs(w_gate)
+    u, _u = _ptrs(w_up)
+    d, _d = _ptrs(w_down)
+    _check(lib.tsp_mlp_rank_fwd(ctypes.byref(shape), _ptr(x_loc), g, u, d, _ptr(y_loc),
+                                int(accumulate), _ptr(ws), _nbytes(ws), _stream(stream)),
+           "tsp_mlp_rank_fwd")
+
+
+def tsp_kv_rank_fwd(shape, x_loc, w_attn, k_buf, v_buf, stream=None):
+    a, _a = _ptrs(w_attn)
+    _check(lib.tsp_kv_rank_fwd(ctypes.byref(shape), _ptr(x_loc), a, _ptr(k_buf), _ptr(v_buf),
+                               _stream(stream)), "tsp_kv_rank_fwd")
+
+
+def tsp_attn_rank_fwd(shape, x_loc, w_attn, k_buf, v_buf, y_loc, accumulate, ws, stream=None):
+    a, _a = _ptrs(w_attn)
+    _check(lib.tsp_attn_rank_fwd(ctypes.byref(shape), _ptr(x_loc), a, _ptr(k_buf), _ptr(v_buf),
+                                 _ptr(y_loc), int(accumulate), _ptr(ws), _nbytes(ws),
+                                 _stream(stream)), "tsp_attn_rank_fwd")
+
+
+def tsp_layer_rank_fwd(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf, y_loc, ws,
+                       stream=None):
+    a, _a = _ptrs(w_attn)
+    g, _g = _ptrs(w_gate)
+    u, _u = _ptrs(w_up)
+    d, _d = _ptrs(w_down)
+    _check(lib.tsp_layer_rank_fwd(ctypes.byref(shape), _ptr(x_loc), a, g, u, d, _ptr(k_buf),
+                                  _ptr(v_buf), _ptr(y_loc), _ptr(ws), _nbytes(ws),
+                                  _stream(stream)), "tsp_layer_rank_fwd")

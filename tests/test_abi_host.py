@@ -1,0 +1,130 @@
+"""Host-only checks of the C ABI: the library loads, exports every function that
+include/tsp.h declares, and rejects bad arguments before touching the GPU.
+
+These tests never make a call that passes validation with a non-empty problem, so
+no kernel is launched and no GPU is needed.  Fake device pointers are plain
+aligned integers that the library never dereferences on an error path.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2604_26294_amd import tsp as T
+from paper_2604_26294_amd.workloads import ALL, TINY
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "tsp.h")
+FAKE = 0x7F0000000000  # 16-byte aligned stand-in for a device address
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tsp_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions()
+    assert {"tsp_mlp_rank_fwd", "tsp_attn_rank_fwd", "tsp_layer_rank_fwd", "tsp_kv_rank_fwd",
+            "tsp_workspace_bytes", "tsp_status_str", "tsp_abi_version"} <= set(names)
+    raw = ctypes.CDLL(T._LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+def test_version_and_status_strings():
+    assert T.lib.tsp_abi_version() == 1
+    for code, name in T.STATUS_NAMES.items():
+        assert T.lib.tsp_status_str(code).decode().startswith(name)
+    assert T.lib.tsp_status_str(99).decode() == "TSP_ERR_UNKNOWN"
+
+
+@pytest.mark.parametrize("wl", ALL, ids=lambda w: w.name)
+def test_workspace_covers_intermediates(wl):
+    sh = T.shape_of(wl)
+    m = wl.batch * wl.s_loc
+    mlp = T.workspace_bytes(sh, T.OP_MLP)
+    attn = T.workspace_bytes(sh, T.OP_ATTN)
+    layer = T.workspace_bytes(sh, T.OP_LAYER)
+    assert mlp >= m * (wl.ffn // wl.degree) * 2                        # gated product
+    assert attn >= 2 * m * (wl.n_heads // wl.degree) * wl.head_dim * 2  # Q and A
+    assert layer >= m * wl.hidden * 2 + max(mlp, attn)                 # + bf16(u)
+    for v in (mlp, attn, layer):
+        assert v % 256 == 0
+
+
+def _shape(**kw):
+    base = dict(batch=1, seq=256, hidden=256, ffn=688, n_heads=4, n_kv_heads=4, head_dim=64,
+                degree=2, rank=1, layout=0, softmax_scale=0.0)
+    base.update(kw)
+    return T.tsp_shape(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(rank=2), 3), (dict(rank=-1), 3),
+    (dict(seq=255), 2), (dict(hidden=250), 2), (dict(n_kv_heads=3), 2),
+    (dict(n_heads=2, hidden=128, n_kv_heads=2, degree=4, rank=0, ffn=688 * 2), 2),
+    (dict(ffn=687), 2), (dict(degree=0, rank=0), 2), (dict(batch=-1), 2),
+    (dict(layout=1), 6), (dict(head_dim=32, n_heads=8), 6), (dict(ffn=680), 6),
+])
+def test_shape_validation(kw, code):
+    out = ctypes.c_size_t(0)
+    assert T.lib.tsp_workspace_bytes(ctypes.byref(_shape(**kw)), 0, ctypes.byref(out)) == code
+
+
+def _arr(n, val=FAKE):
+    a = (ctypes.c_void_p * n)(*([val] * n))
+    return ctypes.cast(a, ctypes.POINTER(ctypes.c_void_p)), a
+
+
+def test_entry_points_reject_bad_arguments():
+    sh = _shape()
+    ws_need = T.workspace_bytes(sh, T.OP_LAYER)
+    good, _k1 = _arr(2)
+    nul, _k2 = _arr(2, 0)
+    mis, _k3 = _arr(2, FAKE + 2)
+    L = T.lib
+    # NULL shape / tensors / shard arrays / shard entries
+    assert L.tsp_mlp_rank_fwd(None, FAKE, good, good, good, FAKE, 0, FAKE, ws_need, None) == 1
+    assert L.tsp_mlp_rank_fwd(ctypes.byref(sh), None, good, good, good, FAKE, 0, FAKE, ws_need,
+                              None) == 1
+    assert L.tsp_mlp_rank_fwd(ctypes.byref(sh), FAKE, None, good, good, FAKE, 0, FAKE, ws_need,
+                              None) == 1
+    assert L.tsp_mlp_rank_fwd(ctypes.byref(sh), FAKE, good, nul, good, FAKE, 0, FAKE, ws_need,
+                              None) == 1
+    # misaligned pointers
+    assert L.tsp_mlp_rank_fwd(ctypes.byref(sh), FAKE + 8, good, good, good, FAKE, 0, FAKE,
+                              ws_need, None) == 4
+    assert L.tsp_attn_rank_fwd(ctypes.byref(sh), FAKE, mis, FAKE, FAKE, FAKE, 0, FAKE, ws_need,
+                               None) == 4
+    assert L.tsp_kv_rank_fwd(ctypes.byref(sh), FAKE, good, FAKE + 4, FAKE, None) == 4
+    # workspace too small
+    assert L.tsp_mlp_rank_fwd(ctypes.byref(sh), FAKE, good, good, good, FAKE, 0, FAKE,
+                              T.workspace_bytes(sh, T.OP_MLP) - 1, None) == 5
+    assert L.tsp_attn_rank_fwd(ctypes.byref(sh), FAKE, good, FAKE, FAKE, FAKE, 0, FAKE,
+                               T.workspace_bytes(sh, T.OP_ATTN) - 1, None) == 5
+    assert L.tsp_layer_rank_fwd(ctypes.byref(sh), FAKE, good, good, good, good, FAKE, FAKE, FAKE,
+                                FAKE, ws_need - 1, None) == 5
+    # bad rank on every entry point
+    bad = _shape(rank=5)
+    assert L.tsp_layer_rank_fwd(ctypes.byref(bad), FAKE, good, good, good, good, FAKE, FAKE,
+                                FAKE, FAKE, ws_need, None) == 3
+    assert L.tsp_kv_rank_fwd(ctypes.byref(bad), FAKE, good, FAKE, FAKE, None) == 3
+
+
+def test_empty_batch_is_a_no_op():
+    """batch = 0 passes validation and returns before any launch (no GPU involved)."""
+    sh = _shape(batch=0)
+    good, _k = _arr(2)
+    assert T.lib.tsp_mlp_rank_fwd(ctypes.byref(sh), FAKE, good, good, good, FAKE, 0, FAKE, 0,
+                                  None) == 0
+    assert T.lib.tsp_layer_rank_fwd(ctypes.byref(sh), FAKE, good, good, good, good, FAKE, FAKE,
+                                    FAKE, FAKE, 0, None) == 0
+    assert T.workspace_bytes(sh, T.OP_LAYER) == 0
+
+
+def test_python_binding_raises_named_errors():
+    with pytest.raises(T.TspError, match="TSP_ERR_RANK"):
+        T.workspace_bytes(_shape(rank=9), T.OP_MLP)
+    assert T.workspace_bytes(T.shape_of(TINY), T.OP_MLP) > 0

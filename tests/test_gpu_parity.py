@@ -1,0 +1,155 @@
+"""GPU parity of libtsp against the fp64 oracle at sizes the oracle finishes in
+seconds, plus the special cases the oracle pins (all through the C ABI)."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from oracle import tsp_oracle as O  # noqa: E402
+from paper_2604_26294_amd import inputs as I  # noqa: E402
+from paper_2604_26294_amd import tsp as T  # noqa: E402
+from paper_2604_26294_amd.harness import RankProblem  # noqa: E402
+from paper_2604_26294_amd.workloads import TINY  # noqa: E402
+from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, SINGLE, assert_close,  # noqa: E402
+                              f64, gen, oracle_blocks)
+
+CASES = [(TINY, 0), (TINY, 1), (MID_GQA64, 0), (MID_GQA64, 2), (MID_GQA64, 3),
+         (MID_MHA128, 1), (MID_GQA8, 1), (SINGLE, 0)]
+_IDS = [f"{w.name}-r{p}" for w, p in CASES]
+_cache = {}
+
+
+def _inputs(wl):
+    if wl.name not in _cache:
+        _cache[wl.name] = gen(wl)
+    return _cache[wl.name]
+
+
+def _run(wl, p, block, x_bits=None, w_bits=None):
+    x_bits, w_bits = (x_bits, w_bits) if x_bits is not None else _inputs(wl)
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    prob.prefill_kv()
+    if block == "mlp":
+        y = prob.mlp()
+    elif block == "attn":
+        y = prob.attn_fwd()
+    else:
+        y = prob.layer()
+    torch.cuda.synchronize()
+    return y.double().cpu().numpy(), prob
+
+
+@pytest.mark.parametrize("wl,p", CASES, ids=_IDS)
+@pytest.mark.parametrize("block", ["mlp", "attn", "layer"])
+def test_block_parity(wl, p, block):
+    print(f"[parity] {wl.name} rank {p} {block}", flush=True)
+    got, _ = _run(wl, p, block)
+    ref = oracle_blocks(wl, *_inputs(wl), p, blocks=(block,))[block]
+    assert_close(got, ref, f"{wl.name} r{p} {block}")
+
+
+@pytest.mark.parametrize("wl", [TINY, MID_GQA64], ids=lambda w: w.name)
+def test_rank_concat_equals_unsharded_layer(wl):
+    x_bits, w_bits = _inputs(wl)
+    outs = [_run(wl, p, "layer")[0] for p in range(wl.degree)]
+    x = f64(x_bits)
+    w = {k: f64(v) for k, v in w_bits.items()}
+    ref = O.layer_full(x, w, wl.n_heads, wl.n_kv_heads)
+    assert_close(np.concatenate(outs, axis=1), ref["y"], "concat layer")
+    attn = [_run(wl, p, "attn")[0] for p in range(wl.degree)]
+    assert_close(np.concatenate(attn, axis=1), ref["attn"], "concat attn")
+
+
+def test_v_ones_gives_output_projection_row_sums():
+    """x[..., 0] = 1 and W_V = e_0 make every V row exactly 1, so every attention
+    context is 1 and the block returns the row sums of W_O for every token."""
+    wl = MID_GQA64
+    x_bits, w_bits = _inputs(wl)
+    x_bits = x_bits.copy()
+    x_bits[..., 0] = I.round_to_bf16_bits(np.array([1.0], np.float32))[0]
+    w_bits = dict(w_bits)
+    wv = np.zeros_like(w_bits["wv"])
+    wv[:, 0] = I.round_to_bf16_bits(np.array([1.0], np.float32))[0]
+    w_bits["wv"] = wv
+    for p in (0, 3):
+        got, _ = _run(wl, p, "attn", x_bits, w_bits)
+        rowsum = f64(w_bits["wo"]).sum(axis=1)
+        expect = np.broadcast_to(rowsum, got.shape)
+        assert np.max(np.abs(got - expect)) <= 1e-2 * np.max(np.abs(rowsum)), p
+
+
+def test_zero_queries_give_prefix_mean():
+    wl = MID_MHA128
+    x_bits, w_bits = _inputs(wl)
+    w_bits = dict(w_bits)
+    w_bits["wq"] = np.zeros_like(w_bits["wq"])
+    got, _ = _run(wl, 1, "attn", x_bits, w_bits)
+    x = f64(x_bits)
+    v = x @ f64(w_bits["wv"]).T
+    mean = np.cumsum(v, axis=1) / np.arange(1, x.shape[1] + 1)[None, :, None]
+    expect = (mean @ f64(w_bits["wo"]).T)[:, wl.s_loc:]          # MHA: head i reads kv head i
+    assert_close(got, expect, "prefix mean")
+
+
+def test_future_kv_rows_are_never_read():
+    """Rows of the K/V buffer at or beyond (p+1) S/D are poisoned with NaN: the
+    output must stay finite and bitwise equal to a run with a clean buffer."""
+    wl, p = MID_GQA64, 1
+    x_bits, w_bits = _inputs(wl)
+    clean = RankProblem(wl, x_bits, w_bits, p, kv_fill=0.0)
+    clean.prefill_kv()
+    y_clean = clean.layer().clone()
+    dirty = RankProblem(wl, x_bits, w_bits, p, kv_fill=float("nan"))
+    dirty.prefill_kv()
+    y_dirty = dirty.layer().clone()
+    torch.cuda.synchronize()
+    assert torch.isfinite(y_dirty).all()
+    assert torch.equal(y_clean, y_dirty)
+
+
+def test_deterministic_and_linear():
+    wl, p = MID_MHA128, 1
+    x_bits, w_bits = _inputs(wl)
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    prob.prefill_kv()
+    a = prob.layer().clone()
+    b = prob.layer().clone()
+    assert torch.equal(a, b)
+    y1 = prob.mlp().clone()
+    prob.w2 = [2 * t for t in prob.w2]                      # exact in bf16
+    y2 = prob.mlp().clone()
+    assert torch.equal(y2, 2 * y1)
+    a1 = prob.attn_fwd().clone()
+    qd = wl.n_heads // wl.degree * wl.head_dim
+    kd = wl.n_kv_heads // wl.degree * wl.head_dim
+    for s in prob.attn:
+        s[qd + 2 * kd:] *= 2                               # the W_O^(r)^T block
+    a2 = prob.attn_fwd().clone()
+    torch.cuda.synchronize()
+    assert torch.equal(a2, 2 * a1)
+
+
+def test_accumulate_flag_adds_to_existing_output():
+    wl, p = TINY, 1
+    x_bits, w_bits = _inputs(wl)
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    prob.prefill_kv()
+    y_mlp = prob.mlp().clone()
+    prob.y.fill_(1.5)
+    y_acc = prob.mlp(accumulate=True).clone()
+    torch.cuda.synchronize()
+    assert torch.allclose(y_acc, y_mlp + 1.5, rtol=0, atol=1e-6)
+
+
+def test_empty_batch_leaves_output_untouched():
+    from dataclasses import replace
+    wl = replace(TINY, batch=0)
+    prob = RankProblem(TINY, *_inputs(TINY), 1)
+    sh = T.shape_of(wl, 1)
+    prob.y.fill_(3.0)
+    T.tsp_layer_rank_fwd(sh, prob.x_loc, prob.attn, prob.w1, prob.w3, prob.w2, prob.k_buf,
+                         prob.v_buf, prob.y, prob.ws)
+    torch.cuda.synchronize()
+    assert bool((prob.y == 3.0).all())
