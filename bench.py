@@ -1,0 +1,185 @@
+#!/usr/bin/env python3
+"""Throughput of one rank's TSP layer forward (attention + gated MLP) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--rank P]
+                    [--no-cpu-baseline]
+
+A step is one ``tsp_layer_rank_fwd`` call: all D attention shard steps (Q/K/V
+projection, causal flash attention, output projection) and all D ring MLP steps
+(gate+up with SwiGLU, down projection) for the rank's S/D tokens.  Inputs, weight
+shards and the K/V rows of the earlier ranks (the modelled all-gather) are resident
+in HBM before timing starts.  Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "TFLOP/s per TSP rank layer fwd (MLP+attn), % of bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CUs x 2.4 GHz x 4096 FLOP/clk/CU
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_flops(wl):
+    """Algorithmic FLOPs of one launch of each kernel class (TSP_KERNEL_* order)."""
+    from paper_2604_26294_amd.flops import step_attn_core_flops
+    D = wl.degree
+    m = wl.batch * wl.s_loc
+    h = wl.hidden
+    fs = wl.ffn // D
+    qd = wl.n_heads // D * wl.head_dim
+    kd = wl.n_kv_heads // D * wl.head_dim
+    return {"gate_up": 2.0 * m * 2 * fs * h, "down": 2.0 * m * h * fs,
+            "qkv": 2.0 * m * (qd + 2 * kd) * h, "attn": step_attn_core_flops(wl),
+            "oproj": 2.0 * m * qd * h}
+
+
+def cpu_baseline(wl, x_bits, w_bits, rows: int):
+    """Time the fp64 oracle on a bounded sample of the same rank's work."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import tsp_oracle as O
+    from paper_2604_26294_amd import inputs as I
+
+    p, D = wl.rank, wl.degree
+    hs, ks, d = wl.n_heads // D, wl.n_kv_heads // D, wl.head_dim
+    x = I.bf16_bits_to_f64(x_bits[:, :(p + 1) * wl.s_loc])
+    w = {k: I.bf16_bits_to_f64(v) for k, v in w_bits.items()}
+    chunks = [I.local_chunk(x, q, D) for q in range(p + 1)]
+    attn_sh = [I.attn_shard_packed(w, r, D, wl.n_heads, wl.n_kv_heads, d) for r in range(D)]
+    mlp_sh = [I.mlp_shard(w, j, D) for j in range(D)]
+    log("cpu baseline: gathering K/V of the prefix (untimed)")
+    kv = [O.gather_kv(chunks, attn_sh[r], hs, ks, d) for r in range(D)]
+    sel = np.linspace(0, wl.s_loc - 1, rows).round().astype(int)
+    x_loc = chunks[p]
+    log(f"cpu baseline: timing the oracle on {rows} local rows")
+    t0 = time.perf_counter()
+    attn = O.attn_rank(x_loc, attn_sh, kv, p, wl.n_heads, wl.n_kv_heads, d, rows=sel)
+    mlp = O.mlp_rank(x_loc[:, sel], [m[0] for m in mlp_sh], [m[1] for m in mlp_sh],
+                     [m[2] for m in mlp_sh], p)
+    dt = time.perf_counter() - t0
+    assert np.isfinite(attn).all() and np.isfinite(mlp).all()
+    b, h = wl.batch, wl.hidden
+    qd = wl.n_heads * d
+    keys = float(np.sum(p * wl.s_loc + sel + 1))
+    flops = (b * rows * (6.0 * h * wl.ffn + 4.0 * h * qd)
+             + 4.0 * b * wl.n_heads * d * keys)
+    threads = max((i.get("num_threads", 1) for i in threadpool_info()
+                   if i.get("user_api") == "blas"), default=1)
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle", "seconds": round(dt, 3),
+            "sample": (f"rank {p}: {rows} of {wl.s_loc} local rows per batch entry, all heads "
+                       f"and all {D} shards (Q/O projections, causal attention over the "
+                       f"prefix, gated MLP) in fp64 NumPy; K/V of the prefix gathered "
+                       f"beforehand, untimed")}
+
+
+def main(argv=None):
+    from paper_2604_26294_amd.workloads import BY_NAME, L7B_64K
+
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=L7B_64K.name, choices=sorted(BY_NAME))
+    ap.add_argument("--rank", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=128)
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one rank of a TSP group on ONE GPU; this build has no "
+              "multi-GPU path (--gpus must be 1)", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2604_26294_amd import inputs as I
+    from paper_2604_26294_amd import tsp as T
+    from paper_2604_26294_amd.flops import rank_flops
+    from paper_2604_26294_amd.harness import RankProblem
+
+    wl = BY_NAME[args.workload]
+    if args.rank is not None:
+        wl = wl.at_rank(args.rank)
+    torch.cuda.set_device(0)
+    log(f"workload {wl.name} rank {wl.rank}: generating seeded inputs")
+    x_bits = I.make_x_full(wl)
+    w_bits = I.make_weights(wl)
+    prob = RankProblem(wl, x_bits, w_bits)
+    log("pre-filling the K/V rows of earlier ranks (the modelled all-gather, untimed)")
+    prob.prefill_kv()
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        prob.layer()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    T.tsp_profile_enable(True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        prob.layer()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    T.tsp_profile_enable(False)
+    ms = t0.elapsed_time(t1) / args.steps
+    log(f"{args.steps} steps: {ms:.3f} ms/step")
+
+    rf = rank_flops(wl)
+    tflops = rf.total / (ms * 1e-3) / 1e12
+    kf = kernel_flops(wl)
+    kernels = {}
+    for k, name in enumerate(T.KERNELS):
+        tot, n = T.tsp_profile_read(k)
+        if n == 0:
+            continue
+        avg = tot / n
+        kernels[name] = {"avg_ms": round(avg, 5), "launches_per_step": n // args.steps,
+                         "tflops": round(kf[name] / (avg * 1e-3) / 1e12, 2),
+                         "time_share": round(tot / args.steps / ms, 4)}
+    dom = max(kernels, key=lambda n: kernels[n]["time_share"])
+    dom_avg = kernels[dom]["avg_ms"]
+    achieved = kf[dom] / (dom_avg * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "flops_per_launch": kf[dom], "avg_launch_ms": dom_avg}
+
+    out = {
+        "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "seq": wl.seq, "hidden": wl.hidden,
+                   "ffn": wl.ffn, "n_heads": wl.n_heads, "n_kv_heads": wl.n_kv_heads,
+                   "head_dim": wl.head_dim, "degree": wl.degree, "rank": wl.rank,
+                   "layout": "contiguous"},
+        "pct_of_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "flops_per_step": rf.total,
+        "roofline": roofline,
+        "kernels": kernels,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, x_bits, w_bits, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -28,8 +28,9 @@
  *     elements are device pointers, one per shard, indexed by shard number.
  *   - Every device pointer must be 16-byte aligned.
  *   - The caller owns every buffer.  The library never allocates or frees device
- *     memory and keeps no state between calls; scratch space is the caller's
- *     workspace, sized by tsp_workspace_bytes.
+ *     memory and keeps no state between calls (apart from the opt-in kernel timing
+ *     records of tsp_profile_enable); scratch space is the caller's workspace, sized
+ *     by tsp_workspace_bytes.
  *   - Calls only enqueue work on `stream` (NULL = the default stream) and never
  *     synchronise.  Calls on different streams must use different workspaces and
  *     must not write the same outputs.
@@ -139,6 +140,22 @@ enum { TSP_OP_MLP = 0, TSP_OP_ATTN = 1, TSP_OP_LAYER = 2 };
 
 /* Workspace bytes the entry point `op` needs for `shape` (validated as above). */
 tsp_status tsp_workspace_bytes(const tsp_shape* shape, int op, size_t* bytes);
+
+/* Per-kernel timing for measurement (not for production use; process-wide state,
+ * not thread-safe).  While enabled, every launch of the listed kernel classes is
+ * bracketed by a pair of HIP events recorded on the launch stream.  Enabling
+ * clears the previous records.  tsp_profile_read waits for the recorded events of
+ * one class and returns the summed kernel time and the number of launches. */
+enum {
+  TSP_KERNEL_GATE_UP = 0, /* gate + up projections with fused SwiGLU (Algorithm 2) */
+  TSP_KERNEL_DOWN = 1,    /* down projection + fp32 shard accumulate (Algorithm 2) */
+  TSP_KERNEL_QKV = 2,     /* Q/K/V projections with K/V scatter (Algorithm 1) */
+  TSP_KERNEL_ATTN = 3,    /* causal flash attention of one shard step (Algorithm 1) */
+  TSP_KERNEL_OPROJ = 4,   /* output projection + fp32 shard accumulate (Algorithm 1) */
+  TSP_KERNEL_COUNT = 5
+};
+tsp_status tsp_profile_enable(int enable);
+tsp_status tsp_profile_read(int kernel, double* total_ms, int64_t* launches);
 
 /* Static, human-readable name of a status code. */
 const char* tsp_status_str(tsp_status status);

@@ -4,6 +4,9 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+#include <vector>
+
 #include "internal.h"
 #include "tsp.h"
 
@@ -98,6 +101,47 @@ tsp_status check_shards(const uint16_t* const* arr, int D) {
     if ((expr) != hipSuccess) return TSP_ERR_HIP; \
   } while (0)
 
+
+// ----------------------------------------------------------------- kernel timing
+struct KernelTimer {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> start[TSP_KERNEL_COUNT], stop[TSP_KERNEL_COUNT];
+  size_t used[TSP_KERNEL_COUNT] = {};
+};
+KernelTimer g_timer;
+
+// Records the start event of launch `kind` on `st`; returns the slot or -1.
+long timer_begin(int kind, hipStream_t st) {
+  if (!g_timer.on) return -1;
+  std::lock_guard<std::mutex> lock(g_timer.mu);
+  const size_t i = g_timer.used[kind];
+  if (i == g_timer.start[kind].size()) {
+    hipEvent_t a, b;
+    if (hipEventCreate(&a) != hipSuccess) return -1;
+    if (hipEventCreate(&b) != hipSuccess) {
+      (void)hipEventDestroy(a);
+      return -1;
+    }
+    g_timer.start[kind].push_back(a);
+    g_timer.stop[kind].push_back(b);
+  }
+  if (hipEventRecord(g_timer.start[kind][i], st) != hipSuccess) return -1;
+  g_timer.used[kind] = i + 1;
+  return (long)i;
+}
+
+void timer_end(int kind, long slot, hipStream_t st) {
+  if (slot >= 0) (void)hipEventRecord(g_timer.stop[kind][slot], st);
+}
+
+#define TSP_LAUNCH(kind, st, expr)                    \
+  do {                                                \
+    const long slot_ = timer_begin((kind), (st));     \
+    if ((expr) != hipSuccess) return TSP_ERR_HIP;     \
+    timer_end((kind), slot_, (st));                   \
+  } while (0)
+
 // ----------------------------------------------------------------- launch sequences
 
 // Algorithm 2 on an already validated problem.  Ring step t uses shard (p - t) mod D.
@@ -117,7 +161,7 @@ tsp_status run_mlp(const Dims& d, const uint16_t* x, const uint16_t* const* wg,
     up.K = d.h;
     up.H = hs_ws;
     up.ldh = d.fs;
-    TSP_HIP(tsp::launch_gemm_swiglu(up, st));
+    TSP_LAUNCH(TSP_KERNEL_GATE_UP, st, tsp::launch_gemm_swiglu(up, st));
 
     GemmParams dn = {};
     dn.A = hs_ws;
@@ -130,7 +174,7 @@ tsp_status run_mlp(const Dims& d, const uint16_t* x, const uint16_t* const* wg,
     dn.Y = y;
     dn.ldy = d.h;
     dn.accumulate = (t > 0 || accumulate) ? 1 : 0;
-    TSP_HIP(tsp::launch_gemm_nn_acc(dn, st));
+    TSP_LAUNCH(TSP_KERNEL_DOWN, st, tsp::launch_gemm_nn_acc(dn, st));
   }
   return TSP_OK;
 }
@@ -170,7 +214,7 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
   const float log2e = 1.4426950408889634f;
   for (int r = 0; r < d.D; ++r) {
     GemmParams g = qkv_params(d, x, wa[r], r, q_ws, kb, vb, true);
-    TSP_HIP(tsp::launch_gemm_qkv(g, st));
+    TSP_LAUNCH(TSP_KERNEL_QKV, st, tsp::launch_gemm_qkv(g, st));
 
     AttnParams ap = {};
     ap.Q = q_ws;
@@ -188,7 +232,7 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     ap.q_pos0 = (long long)d.p * d.s_loc;
     ap.kv_len = (long long)(d.p + 1) * d.s_loc;
     ap.scale_log2 = d.scale * log2e;
-    TSP_HIP(tsp::launch_flash_attn(ap, st));
+    TSP_LAUNCH(TSP_KERNEL_ATTN, st, tsp::launch_flash_attn(ap, st));
 
     GemmParams o = {};
     o.A = a_ws;
@@ -209,7 +253,7 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
       o.U = u_out;
       o.ldu = d.h;
     }
-    TSP_HIP(tsp::launch_gemm_nn_acc(o, st));
+    TSP_LAUNCH(TSP_KERNEL_OPROJ, st, tsp::launch_gemm_nn_acc(o, st));
   }
   return TSP_OK;
 }
@@ -260,7 +304,7 @@ tsp_status tsp_kv_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
   if (d.M == 0) return TSP_OK;
   for (int r = 0; r < d.D; ++r) {
     GemmParams g = qkv_params(d, x_loc, w_attn[r], r, nullptr, k_buf, v_buf, false);
-    TSP_HIP(tsp::launch_gemm_qkv(g, stream));
+    TSP_LAUNCH(TSP_KERNEL_QKV, stream, tsp::launch_gemm_qkv(g, stream));
   }
   return TSP_OK;
 }
@@ -313,6 +357,31 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
   // y = u + MLP(bf16 u): the MLP accumulates onto Y, which holds u.
   return run_mlp(d, u_ws, w_gate, w_up, w_down, y_loc, 1, reinterpret_cast<uint16_t*>(rest),
                  stream);
+}
+
+tsp_status tsp_profile_enable(int enable) {
+  std::lock_guard<std::mutex> lock(g_timer.mu);
+  g_timer.on = enable != 0;
+  if (g_timer.on)
+    for (int k = 0; k < TSP_KERNEL_COUNT; ++k) g_timer.used[k] = 0;
+  return TSP_OK;
+}
+
+tsp_status tsp_profile_read(int kernel, double* total_ms, int64_t* launches) {
+  if (!total_ms || !launches) return TSP_ERR_NULL;
+  if (kernel < 0 || kernel >= TSP_KERNEL_COUNT) return TSP_ERR_SHAPE;
+  std::lock_guard<std::mutex> lock(g_timer.mu);
+  double sum = 0.0;
+  for (size_t i = 0; i < g_timer.used[kernel]; ++i) {
+    float ms = 0.f;
+    if (hipEventSynchronize(g_timer.stop[kernel][i]) != hipSuccess ||
+        hipEventElapsedTime(&ms, g_timer.start[kernel][i], g_timer.stop[kernel][i]) != hipSuccess)
+      return TSP_ERR_HIP;
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = (int64_t)g_timer.used[kernel];
+  return TSP_OK;
 }
 
 const char* tsp_status_str(tsp_status status) {

@@ -19,6 +19,7 @@ STATUS_NAMES = {0: "TSP_OK", 1: "TSP_ERR_NULL", 2: "TSP_ERR_SHAPE", 3: "TSP_ERR_
                 4: "TSP_ERR_ALIGN", 5: "TSP_ERR_WORKSPACE", 6: "TSP_ERR_UNSUPPORTED",
                 7: "TSP_ERR_HIP"}
 OP_MLP, OP_ATTN, OP_LAYER = 0, 1, 2
+KERNELS = ("gate_up", "down", "qkv", "attn", "oproj")  # TSP_KERNEL_* order
 
 
 class TspError(RuntimeError):
@@ -51,6 +52,8 @@ def _load() -> ctypes.CDLL:
         "tsp_workspace_bytes": [SH, I, ctypes.POINTER(ctypes.c_size_t)],
         "tsp_status_str": [I],
         "tsp_abi_version": [],
+        "tsp_profile_enable": [I],
+        "tsp_profile_read": [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -143,3 +146,14 @@ def tsp_layer_rank_fwd(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf,
     _check(lib.tsp_layer_rank_fwd(ctypes.byref(shape), _ptr(x_loc), a, g, u, d, _ptr(k_buf),
                                   _ptr(v_buf), _ptr(y_loc), _ptr(ws), _nbytes(ws),
                                   _stream(stream)), "tsp_layer_rank_fwd")
+
+
+def tsp_profile_enable(enable: bool = True):
+    _check(lib.tsp_profile_enable(int(enable)), "tsp_profile_enable")
+
+
+def tsp_profile_read(kernel: int):
+    """(total milliseconds, launches) recorded for kernel class ``kernel``."""
+    ms, n = ctypes.c_double(0), ctypes.c_int64(0)
+    _check(lib.tsp_profile_read(kernel, ctypes.byref(ms), ctypes.byref(n)), "tsp_profile_read")
+    return ms.value, n.value

@@ -1,0 +1,79 @@
+"""Full-size parity on sampled rows, in the launch configuration the benchmark times.
+
+For each of the study's layer shapes the GPU runs the rank's attention block, MLP
+block and whole layer through the C ABI; the oracle recomputes a handful of output
+rows of the unsharded layer exactly (every row of the fold equals the same row of
+the unsharded layer, Section 3.1), from the full weights, in fp64.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from oracle import tsp_oracle as O  # noqa: E402
+from paper_2604_26294_amd import inputs as I  # noqa: E402
+from paper_2604_26294_amd.harness import RankProblem  # noqa: E402
+from paper_2604_26294_amd.workloads import L7B_8K, L7B_64K, L13B_B4, L70B_GQA  # noqa: E402
+from tests.gpu_common import assert_close  # noqa: E402
+
+CASES = [(L7B_8K, 7), (L7B_64K, 7), (L70B_GQA, 7), (L13B_B4, 0), (L13B_B4, 1), (L13B_B4, 2),
+         (L13B_B4, 3)]
+_cache = {}
+
+
+def _data(wl):
+    if _cache.get("name") != wl.name:
+        _cache.clear()
+        x = I.make_x_full(wl)
+        w = I.make_weights(wl)
+        _cache.update(name=wl.name, x=x, w=w, wf={k: I.bf16_bits_to_f64(v) for k, v in w.items()})
+    return _cache["x"], _cache["w"], _cache["wf"]
+
+
+def _rows(s_loc):
+    return sorted({0, 1, 127, 128, s_loc // 2 + 7, s_loc - 1})
+
+
+@pytest.mark.parametrize("wl,p", CASES, ids=[f"{w.name}-r{p}" for w, p in CASES])
+def test_sampled_rows_match_unsharded_layer(wl, p):
+    print(f"[fullsize] {wl.name} rank {p}", flush=True)
+    x_bits, w_bits, wf = _data(wl)
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    prob.prefill_kv()
+    y_layer = prob.layer().clone()
+    y_attn = prob.attn_fwd().clone()
+    y_mlp = prob.mlp().clone()
+    torch.cuda.synchronize()
+    rows = _rows(wl.s_loc)
+    batches = sorted({0, wl.batch - 1})
+    s0 = p * wl.s_loc
+    for b in batches:
+        x_b = I.bf16_bits_to_f64(x_bits[b, :s0 + wl.s_loc])
+        attn = O.attention_rows(x_b, wf["wq"], wf["wk"], wf["wv"], wf["wo"], wl.n_heads,
+                                wl.n_kv_heads, [s0 + r for r in rows])
+        xr = x_b[[s0 + r for r in rows]]
+        mlp_x = O.mlp_full(xr, wf["w1"], wf["w3"], wf["w2"])
+        u = xr + attn
+        y = u + O.mlp_full(u, wf["w1"], wf["w3"], wf["w2"])
+        got = {k: v[b, rows].double().cpu().numpy()
+               for k, v in (("attn", y_attn), ("mlp", y_mlp), ("layer", y_layer))}
+        assert_close(got["attn"], attn, f"{wl.name} r{p} b{b} attn")
+        assert_close(got["mlp"], mlp_x, f"{wl.name} r{p} b{b} mlp")
+        assert_close(got["layer"], y, f"{wl.name} r{p} b{b} layer")
+    del prob
+    torch.cuda.empty_cache()
+
+
+def test_long_context_layer_output_is_finite_everywhere():
+    """Every output element of the last rank of the long-context shape is finite."""
+    wl = L7B_64K
+    x_bits, w_bits, _ = _data(wl)
+    prob = RankProblem(wl, x_bits, w_bits, 7)
+    prob.prefill_kv()
+    y = prob.layer()
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(y).all())
+    assert float(y.abs().max()) < 1e3
+    np.testing.assert_equal(tuple(y.shape), (1, 8192, 4096))
