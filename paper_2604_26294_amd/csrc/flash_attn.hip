@@ -7,19 +7,25 @@
 //
 // Work split.  A workgroup owns 128 queries of one head (GQA: head i reads kv head
 // i / g) and has 8 wavefronts: wavefront w handles queries 32 (w % 4) .. +31 against
-// key group w / 4, i.e. each step stages 128 keys in LDS and the two groups of four
+// key group w / 4, i.e. every step stages 128 keys in LDS and the two groups of four
 // wavefronts consume its two 64-key halves.  Each group keeps its own running max /
 // sum / output; the groups are merged once at the end.  Key tiles beyond the last
 // query's position are never loaded; only tiles that cross the diagonal are masked.
 //
-// Layout trick.  Scores are computed transposed, S^T = K Q^T, with K as the MFMA A
-// operand and Q (held in registers) as B.  The 32 x 32 accumulator then gives each
-// lane 16 keys of ONE query (its partner lane l ^ 32 holds the other 16), so the
-// row max needs one cross-lane exchange and the row sum none until the end.  The
-// probabilities P^T feed the second product O^T = V^T P^T directly as the B operand
-// (contraction over keys), which needs V^T in LDS: V tiles are transposed in
-// registers on their way into LDS, with the keys of every 16-key group stored in the
-// order the accumulator layout delivers them.
+// Scores are computed transposed, S^T = K Q^T, with K as the MFMA A operand and Q
+// (held in registers) as B.  The 32 x 32 accumulator then gives each lane 16 keys of
+// ONE query (its partner lane l ^ 32 holds the other 16), so the row max needs one
+// cross-lane exchange and the row sum none until the end.  The probabilities P^T
+// feed O^T = V^T P^T directly as the B operand (contraction over keys).
+//
+// Data movement.  K and V tiles go from HBM straight into LDS (global_load_lds, no
+// register staging) in their natural [key][d] layout, 16-byte chunks XOR-swizzled by
+// the row.  The V^T operand is read with the gfx950 LDS transpose read
+// (ds_read_b64_tr_b16): in each 16-lane group, source lane s points at row
+// kbase + s/4, columns base + 4 (s % 4), and lane t receives column base + t of rows
+// kbase .. kbase+3 -- four consecutive keys of one head-dim column.  K and V use
+// separate two-slot rings offset by one tile: while tile j's softmax runs, the MFMAs
+// for tile j+1's scores are already issued and tiles j+2 (K) / j+1 (V) are in flight.
 #include <math.h>
 
 #include "common.h"
@@ -32,34 +38,40 @@ constexpr int kThreads = 512;
 constexpr int kQTile = 128;
 constexpr int kKTile = 64;           // keys per group per step
 constexpr int kStepKeys = 2 * kKTile;
+constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (exp2 units)
 
-__device__ __forceinline__ int swz(int row, int chunk) {
-  return chunk ^ ((row ^ (row >> 3)) & 7);
-}
-
-__device__ __forceinline__ uint32_t pick_col(uint32_t row_lo, uint32_t row_hi, int odd) {
-  return odd ? ((row_lo >> 16) | (row_hi & 0xffff0000u)) : ((row_lo & 0xffffu) | (row_hi << 16));
-}
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_char;
 
 template <int D>
 struct FaCfg {
-  static constexpr int KCH = D / 8;                      // 16-byte chunks per K row
-  static constexpr int K_CHUNKS = kStepKeys * KCH;       // K region of one stage
-  static constexpr int VT_CHUNKS = 2 * D * 8;            // 2 groups x D rows x 64 keys
-  static constexpr int STAGE = K_CHUNKS + VT_CHUNKS;
-  static constexpr int K_LOADS = K_CHUNKS / kThreads;
-  static constexpr int V_BLOCKS = (kStepKeys / 4) * (D / 8);  // 4 keys x 8 columns each
-  static constexpr int EB = D / 32;                      // 32-row blocks of O^T
-  static constexpr int KS = D / 16;                      // contraction steps of S^T
-  static_assert(V_BLOCKS <= kThreads, "V blocks");
+  static constexpr int KCH = D / 8;                           // 16-byte chunks per key row
+  static constexpr int ROW_BYTES = D * 2;
+  static constexpr int TILE_BYTES = kStepKeys * ROW_BYTES;    // one K or V tile
+  static constexpr int DMA_PER_LANE = kStepKeys * KCH / kThreads;
+  static constexpr int ROWS_PER_DMA = kWave / KCH;            // rows one wave instruction fills
+  static constexpr int EB = D / 32;                           // 32-row blocks of O^T
+  static constexpr int KS = D / 16;                           // contraction steps of S^T
+  static_assert(DMA_PER_LANE * 8 * ROWS_PER_DMA == kStepKeys, "DMA cover");
 };
+
+template <int KCH>
+__device__ __forceinline__ int phys_chunk(int row, int chunk) {
+  return chunk ^ (row & (KCH - 1));
+}
+
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
   using C = FaCfg<D>;
-  __shared__ u32x4 L[2 * C::STAGE];
+  constexpr int KCH = C::KCH;
+  // [K slot 0][K slot 1][V slot 0][V slot 1]
+  __shared__ __attribute__((aligned(16))) char L[4 * C::TILE_BYTES];
+  lds_char* Ls = (lds_char*)L;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2, wq = wave & 3;
   const int l32 = lane & 31, hh = lane >> 5;
 
@@ -74,13 +86,13 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 
   const int qloc = q0 + 32 * wq + l32;
   const bool qvalid = qloc < P.s_loc;
-  const long long qpos = P.q_pos0 + qloc;
+  const int qpos = P.q_pos0 + qloc;
   const int wq_first = q0 + 32 * wq;
   const bool wave_active = wq_first < P.s_loc;
-  const long long wpos_min = P.q_pos0 + wq_first;
-  const long long wpos_max = P.q_pos0 + min(wq_first + 31, P.s_loc - 1);
-  const long long n_keys = P.q_pos0 + min(q0 + kQTile, P.s_loc);  // <= kv_len
-  const int n_steps = (int)((n_keys + kStepKeys - 1) / kStepKeys);
+  const int wpos_min = P.q_pos0 + wq_first;
+  const int wpos_max = P.q_pos0 + min(wq_first + 31, P.s_loc - 1);
+  const int n_keys = P.q_pos0 + min(q0 + kQTile, P.s_loc);  // <= kv_len
+  const int n_steps = (n_keys + kStepKeys - 1) / kStepKeys;
   const float c = P.scale_log2;
 
   // Q fragments: the B operand of S^T; lane holds Q[qloc][16 s + 8 hh .. +7].
@@ -92,6 +104,51 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
       qf[s] = qvalid ? ld16(qrow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
   }
 
+  const size_t kv_stride = (size_t)P.n_kv * D;
+  const uint16_t* kbase = P.Kb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
+  const uint16_t* vbase = P.Vb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
+
+  // One 128-key tile from HBM into an LDS slot.  Rows past the last needed key are
+  // clamped to it: they are always masked (keys > every query position of this
+  // workgroup) and stay finite, so the P V product never sees garbage.
+  auto dma_tile = [&](const uint16_t* base, int tile, int slot_off) {
+    const int rsub = lane / KCH, pc = lane % KCH;
+#pragma unroll
+    for (int i = 0; i < C::DMA_PER_LANE; ++i) {
+      const int blk = i * 8 + wave;
+      const int row = blk * C::ROWS_PER_DMA + rsub;
+      const int key = min(tile * kStepKeys + row, n_keys - 1);
+      const uint16_t* src = base + (size_t)key * kv_stride + 8 * phys_chunk<KCH>(row, pc);
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(
+                                                  Ls + slot_off + blk * (kWave * 16)),
+                                       16, 0, 0);
+    }
+  };
+  auto k_off = [&](int tile) { return (tile & 1) * C::TILE_BYTES; };
+  auto v_off = [&](int tile) { return (2 + (tile & 1)) * C::TILE_BYTES; };
+
+  // S^T tile of this wave's key group: 2 blocks of 32 keys x 32 queries.
+  auto scores = [&](int tile, f32x16 (&s)[2]) {
+    const lds_char* K = Ls + k_off(tile);
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[bb][e] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb) {
+        const int row = kKTile * grp + 32 * bb + l32;
+        const u32x4 kf = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(
+            K + row * C::ROW_BYTES + 16 * phys_chunk<KCH>(row, 2 * ks + hh));
+        s[bb] = mfma32(kf, qf[ks], s[bb]);
+      }
+    }
+  };
+  auto tile_active = [&](int tile) {
+    return wave_active && tile * kStepKeys + kKTile * grp <= wpos_max;
+  };
+
   f32x16 o[C::EB];
 #pragma unroll
   for (int eb = 0; eb < C::EB; ++eb)
@@ -99,144 +156,111 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     for (int e = 0; e < 16; ++e) o[eb][e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  const size_t kv_stride = (size_t)P.n_kv * D;
-  const uint16_t* kbase = P.Kb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
-  const uint16_t* vbase = P.Vb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
+  // Transpose-read geometry of this lane (see the header comment).
+  const int tr_t = lane & 15, tr_g = lane >> 4;
+  const int tr_row = ((tr_g >> 1) << 2) + (tr_t >> 2);     // 4 hh + t / 4
+  const int tr_col = 16 * (tr_g & 1) + 4 * (tr_t & 3);     // within a 32-column block
 
-  u32x4 rk[C::K_LOADS];
-  u32x4 rv[4];
-  const int v_db = tid % (D / 8), v_kq = tid / (D / 8);
-
-  auto load = [&](int step) {
-    const long long key0 = (long long)step * kStepKeys;
-#pragma unroll
-    for (int i = 0; i < C::K_LOADS; ++i) {
-      const long long gk = key0 + tid / C::KCH + (kThreads / C::KCH) * i;
-      rk[i] = gk < n_keys ? ld16(kbase + gk * kv_stride + 8 * (tid % C::KCH)) : u32x4{0u, 0u, 0u, 0u};
-    }
-    if (tid < C::V_BLOCKS) {
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const long long gk = key0 + 4 * v_kq + rr;
-        rv[rr] = gk < n_keys ? ld16(vbase + gk * kv_stride + 8 * v_db) : u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-  };
-
-  auto store = [&](int stage) {
-    u32x4* S = L + stage * C::STAGE;
-#pragma unroll
-    for (int i = 0; i < C::K_LOADS; ++i) {
-      const int key = tid / C::KCH + (kThreads / C::KCH) * i;
-      S[key * C::KCH + swz(key, tid % C::KCH)] = rk[i];
-    }
-    if (tid < C::V_BLOCKS) {
-      // Keys 4 v_kq .. +3 of the step -> group g2, 16-key group G, quad q inside it.
-      // Within each 16-key group the quads are stored in the order 0, 2, 1, 3 so that
-      // one 16-byte chunk holds the 8 keys a lane half feeds to one MFMA.
-      const int g2 = v_kq >> 4;
-      const int kk = 4 * (v_kq & 15);
-      const int G = kk >> 4, q = (kk & 15) >> 2;
-      const int qp = ((q & 1) << 1) | (q >> 1);
-      const int chunk = 2 * G + (qp >> 1), half = qp & 1;
-      u32x2* VT = reinterpret_cast<u32x2*>(S + C::K_CHUNKS + g2 * D * 8);
-#pragma unroll
-      for (int cc = 0; cc < 8; ++cc) {
-        const int row = 8 * v_db + cc;  // head-dim index
-        u32x2 val;
-        val[0] = pick_col(rv[0][cc >> 1], rv[1][cc >> 1], cc & 1);
-        val[1] = pick_col(rv[2][cc >> 1], rv[3][cc >> 1], cc & 1);
-        VT[(row * 8 + swz(row, chunk)) * 2 + half] = val;
-      }
-    }
-  };
-
-  load(0);
-  store(0);
+  dma_tile(kbase, 0, k_off(0));
+  dma_tile(vbase, 0, v_off(0));
+  if (n_steps > 1) dma_tile(kbase, 1, k_off(1));
+  wait_dma();
   __syncthreads();
+  f32x16 s_cur[2];
+  if (tile_active(0)) scores(0, s_cur);
 
-  for (int step = 0; step < n_steps; ++step) {
-    const int cur = step & 1;
-    if (step + 1 < n_steps) load(step + 1);
+  for (int j = 0; j < n_steps; ++j) {
+    wait_dma();
+    __syncthreads();  // K tile j+1 and V tile j resident; every wave is past step j-1
+    if (j + 2 < n_steps) dma_tile(kbase, j + 2, k_off(j + 2));
+    if (j + 1 < n_steps) dma_tile(vbase, j + 1, v_off(j + 1));
 
-    const long long kt0 = (long long)step * kStepKeys + kKTile * grp;
-    if (wave_active && kt0 <= wpos_max) {
-      const u32x4* S = L + cur * C::STAGE;
-      f32x16 sacc[2];
-#pragma unroll
-      for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[bb][e] = 0.f;
-#pragma unroll
-      for (int s = 0; s < C::KS; ++s) {
-#pragma unroll
-        for (int bb = 0; bb < 2; ++bb) {
-          const int row = kKTile * grp + 32 * bb + l32;
-          sacc[bb] = mfma32(S[row * C::KCH + swz(row, 2 * s + hh)], qf[s], sacc[bb]);
-        }
-      }
+    f32x16 s_next[2];
+    const bool next_active = j + 1 < n_steps && tile_active(j + 1);
+    if (next_active) scores(j + 1, s_next);
+
+    if (tile_active(j)) {
+      const int kt0 = j * kStepKeys + kKTile * grp;
       if (kt0 + kKTile - 1 > wpos_min) {
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const long long key = kt0 + 32 * bb + 8 * (e >> 2) + 4 * hh + (e & 3);
-            if (key > qpos) sacc[bb][e] = -INFINITY;
+            const int key = kt0 + 32 * bb + 8 * (e >> 2) + 4 * hh + (e & 3);
+            if (key > qpos) s_cur[bb][e] = -INFINITY;
           }
       }
-      float mx = sacc[0][0];
+      float mx = s_cur[0][0];
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[bb][e]);
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s_cur[bb][e]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * c);
-      const float mc = m_use * c;
+      // Lazy rescaling: the running max moves only when a score exceeds it by more
+      // than 8 in exp2 units (always on the first visible tile).  Between moves every
+      // probability is bounded by 2^8, and numerator and denominator share the stale
+      // max, so the normalised result is unchanged while the output rescale is
+      // skipped on most tiles.
+      if (__any((mx - m_run) * c > kRescaleLog2)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * c);
+        l_run *= alpha;
+#pragma unroll
+        for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[eb][e] *= alpha;
+        m_run = m_new;
+      }
+      const float mc = (m_run == -INFINITY ? 0.f : m_run) * c;
       float lsum = 0.f;
-#pragma unroll
-      for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[bb][e], c, -mc));
-          sacc[bb][e] = pv;
-          lsum += pv;
-        }
-      l_run = l_run * alpha + lsum;
-      m_run = m_new;
-#pragma unroll
-      for (int eb = 0; eb < C::EB; ++eb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[eb][e] *= alpha;
-
       u32x4 pf[2][2];
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            pf[bb][s2][q] = pack_bf16x2(sacc[bb][8 * s2 + 2 * q], sacc[bb][8 * s2 + 2 * q + 1]);
+          for (int q = 0; q < 4; ++q) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(s_cur[bb][8 * s2 + 2 * q], c, -mc));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(s_cur[bb][8 * s2 + 2 * q + 1], c, -mc));
+            lsum += p0 + p1;
+            pf[bb][s2][q] = pack_bf16x2(p0, p1);
+          }
+      l_run += lsum;
 
-      const u32x4* VT = S + C::K_CHUNKS + grp * D * 8;
+      // O^T += V^T P^T.  k-step (bb, s2) covers keys kt0 + 32 bb + 16 s2 + [0, 16); lane
+      // half hh feeds keys 4 hh + 0..3 (elements 0-3) and 8 + 4 hh + 0..3 (4-7).
+      const lds_char* V = Ls + v_off(j);
 #pragma unroll
-      for (int eb = 0; eb < C::EB; ++eb) {
-        const int row = 32 * eb + l32;
+      for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-        for (int bb = 0; bb < 2; ++bb)
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const int r0 = kKTile * grp + 32 * bb + 16 * s2 + tr_row;
 #pragma unroll
-          for (int s2 = 0; s2 < 2; ++s2)
-            o[eb] = mfma32(VT[row * 8 + swz(row, 4 * bb + 2 * s2 + hh)], pf[bb][s2], o[eb]);
-      }
+          for (int eb = 0; eb < C::EB; ++eb) {
+            const int col = 32 * eb + tr_col;
+            const int ch = col >> 3, half = (col >> 2) & 1;
+            const int ra = r0, rb = r0 + 8;
+            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) i16x4*)(
+                    V + ra * C::ROW_BYTES + 16 * phys_chunk<KCH>(ra, ch) + 8 * half));
+            const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) i16x4*)(
+                    V + rb * C::ROW_BYTES + 16 * phys_chunk<KCH>(rb, ch) + 8 * half));
+            const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
+            o[eb] = mfma32(u32x4{lo2[0], lo2[1], hi2[0], hi2[1]}, pf[bb][s2], o[eb]);
+          }
+        }
     }
-
-    if (step + 1 < n_steps) store(cur ^ 1);
-    __syncthreads();
+    if (next_active) {
+      s_cur[0] = s_next[0];
+      s_cur[1] = s_next[1];
+    }
   }
 
   // Merge the two key groups: group 1 parks its state in LDS, group 0 combines.
   l_run += __shfl_xor(l_run, 32);
+  __syncthreads();
   float* F = reinterpret_cast<float*>(L);
   const int slot = wq * 64 + lane;
   if (grp == 1) {
@@ -266,10 +290,8 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
           const int e = 4 * g + r;
           v[r] = (o[eb][e] * a0 + F[(2 + 16 * eb + e) * 256 + slot] * a1) * inv;
         }
-        u32x2 pk;
-        pk[0] = pack_bf16x2(v[0], v[1]);
-        pk[1] = pack_bf16x2(v[2], v[3]);
-        *reinterpret_cast<u32x2*>(orow + 32 * eb + 8 * g + 4 * hh) = pk;
+        *reinterpret_cast<u32x2*>(orow + 32 * eb + 8 * g + 4 * hh) =
+            u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
       }
   }
 }

@@ -68,62 +68,6 @@ __device__ __forceinline__ uint32_t pick_col(uint32_t row_lo, uint32_t row_hi, i
   return odd ? ((row_lo >> 16) | (row_hi & 0xffff0000u)) : ((row_lo & 0xffffu) | (row_hi << 16));
 }
 
-// Epilogues for one 32 x 32 accumulator tile: element e of lane (l32, hh) is
-// C[mrow + 8 (e / 4) + (e % 4)][nblk + l32], where mrow already includes 4 hh.
-__device__ __forceinline__ void epi_swiglu(const GemmParams& P, const f32x16& g, const f32x16& u,
-                                           int mrow, int nblk, int l32) {
-  const int n = nblk + l32;
-  if (n >= P.N) return;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const int m = mrow + 8 * (e >> 2) + (e & 3);
-    if (m < P.M) {
-      const float v = g[e];
-      P.H[(size_t)m * P.ldh + n] = to_bf16_bits(v / (1.f + __expf(-v)) * u[e]);
-    }
-  }
-}
-
-__device__ __forceinline__ void epi_acc(const GemmParams& P, const f32x16& c, int mrow, int nblk,
-                                        int l32) {
-  const int n = nblk + l32;
-  if (n >= P.N) return;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const int m = mrow + 8 * (e >> 2) + (e & 3);
-    if (m < P.M) {
-      const size_t yi = (size_t)m * P.ldy + n;
-      float out = c[e];
-      if (P.R) out += bf16_bits_to_f32(P.R[(size_t)m * P.ldr + n]);
-      else if (P.accumulate) out += P.Y[yi];
-      P.Y[yi] = out;
-      if (P.U) P.U[(size_t)m * P.ldu + n] = to_bf16_bits(out);
-    }
-  }
-}
-
-__device__ __forceinline__ void epi_qkv(const GemmParams& P, const f32x16& c, int mrow, int nblk,
-                                        int l32) {
-  const int n = nblk + l32;
-  if (n >= P.N) return;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const int m = mrow + 8 * (e >> 2) + (e & 3);
-    if (m < P.M) {
-      const uint16_t bits = to_bf16_bits(c[e]);
-      if (nblk < P.nq) {
-        P.Q[(size_t)m * P.ldq + n] = bits;
-      } else {
-        const int b = m / P.rows_per_batch, t = m - b * P.rows_per_batch;
-        const size_t row = (size_t)b * P.kv_batch_stride +
-                           (size_t)(P.kv_pos0 + t) * P.kv_row_stride + P.kv_col0;
-        if (nblk < P.nq + P.nkv) P.Kb[row + (n - P.nq)] = bits;
-        else P.Vb[row + (n - P.nq - P.nkv)] = bits;
-      }
-    }
-  }
-}
-
 template <int BM, int BN, bool NN, int EPI>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
   using C = Cfg<BM, BN, NN, EPI>;
@@ -236,17 +180,87 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
     __syncthreads();
   }
 
-  // ---------------------------------------------------------------- epilogues
-  const int mw = m0 + wm * C::WM + 4 * hh;
+  // ---------------------------------------------------------------- epilogue
+  // Each wavefront stages one 32-row block of its C tile in LDS as fp32 (the last
+  // main-loop barrier has released the operand stages), then writes it out in
+  // 4-column chunks: consecutive lanes cover consecutive columns, every global access
+  // is 16 bytes (fp32) or 8 bytes (bf16), and all loads of a block are in flight
+  // before the first store.
+  constexpr int EST = C::WN + 4;          // staging row stride in floats
+  constexpr int CPR = C::WN / 4;          // 4-column chunks per row
+  constexpr int PER_LANE = 32 * CPR / kWave;
+  float* E = reinterpret_cast<float*>(L) + wave * 32 * EST;
+  const int ncol0 = n0 + wn * C::WN;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int nblk = n0 + wn * C::WN + 32 * j;
-      if constexpr (EPI == EPI_SWIGLU) epi_swiglu(P, acc[i][j], acc[i][j + TN], mw + 32 * i, nblk, l32);
-      else if constexpr (EPI == EPI_ACC) epi_acc(P, acc[i][j], mw + 32 * i, nblk, l32);
-      else epi_qkv(P, acc[i][j], mw + 32 * i, nblk, l32);
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        float v = acc[i][j][e];
+        if constexpr (EPI == EPI_SWIGLU) v = v / (1.f + __expf(-v)) * acc[i][j + TN][e];
+        E[(8 * (e >> 2) + 4 * hh + (e & 3)) * EST + 32 * j + l32] = v;
+      }
+    __syncthreads();
+    const int mrow0 = m0 + wm * C::WM + 32 * i;
+    f32x4 v[PER_LANE];
+    int mm[PER_LANE], nn[PER_LANE];
+    bool ok[PER_LANE];
+#pragma unroll
+    for (int q = 0; q < PER_LANE; ++q) {
+      const int idx = q * kWave + lane, row = idx / CPR, c4 = idx % CPR;
+      v[q] = *reinterpret_cast<const f32x4*>(E + row * EST + 4 * c4);
+      mm[q] = mrow0 + row;
+      nn[q] = ncol0 + 4 * c4;
+      ok[q] = mm[q] < P.M && nn[q] < P.N;
     }
+    if constexpr (EPI == EPI_ACC) {
+      f32x4 base[PER_LANE];
+#pragma unroll
+      for (int q = 0; q < PER_LANE; ++q) {
+        base[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (ok[q]) {
+          if (P.R) {
+            const u32x2 r = *reinterpret_cast<const u32x2*>(P.R + (size_t)mm[q] * P.ldr + nn[q]);
+            base[q] = f32x4{bf16_bits_to_f32(r[0] & 0xffffu), bf16_bits_to_f32(r[0] >> 16),
+                            bf16_bits_to_f32(r[1] & 0xffffu), bf16_bits_to_f32(r[1] >> 16)};
+          } else if (P.accumulate) {
+            base[q] = *reinterpret_cast<const f32x4*>(P.Y + (size_t)mm[q] * P.ldy + nn[q]);
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < PER_LANE; ++q) {
+        if (!ok[q]) continue;
+        const f32x4 out = v[q] + base[q];
+        *reinterpret_cast<f32x4*>(P.Y + (size_t)mm[q] * P.ldy + nn[q]) = out;
+        if (P.U)
+          *reinterpret_cast<u32x2*>(P.U + (size_t)mm[q] * P.ldu + nn[q]) =
+              u32x2{pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3])};
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < PER_LANE; ++q) {
+        if (!ok[q]) continue;
+        const u32x2 bits{pack_bf16x2(v[q][0], v[q][1]), pack_bf16x2(v[q][2], v[q][3])};
+        uint16_t* dst;
+        if constexpr (EPI == EPI_SWIGLU) {
+          dst = P.H + (size_t)mm[q] * P.ldh + nn[q];
+        } else {
+          const int n = nn[q], m = mm[q];
+          if (n < P.nq) {
+            dst = P.Q + (size_t)m * P.ldq + n;
+          } else {
+            const int b = m / P.rows_per_batch, t = m - b * P.rows_per_batch;
+            const size_t row = (size_t)b * P.kv_batch_stride +
+                               (size_t)(P.kv_pos0 + t) * P.kv_row_stride + P.kv_col0;
+            dst = n < P.nq + P.nkv ? P.Kb + row + (n - P.nq) : P.Vb + row + (n - P.nq - P.nkv);
+          }
+        }
+        *reinterpret_cast<u32x2*>(dst) = bits;
+      }
+    }
+    __syncthreads();
   }
 }
 

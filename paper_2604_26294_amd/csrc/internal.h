@@ -69,8 +69,8 @@ struct AttnParams {
   long long seq;    // S (K/V buffer rows per batch)
   int n_kv;         // kv heads in the buffer
   int kv_head0;     // first kv head of this shard
-  long long q_pos0; // global position of local query 0
-  long long kv_len; // number of readable keys: (p + 1) * S_loc
+  int q_pos0;       // global position of local query 0
+  int kv_len;       // number of readable keys: (p + 1) * S_loc
   float scale_log2; // softmax scale * log2(e)
 };
 

@@ -229,8 +229,8 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     ap.seq = d.S;
     ap.n_kv = d.nkv;
     ap.kv_head0 = r * d.ks;
-    ap.q_pos0 = (long long)d.p * d.s_loc;
-    ap.kv_len = (long long)(d.p + 1) * d.s_loc;
+    ap.q_pos0 = d.p * d.s_loc;
+    ap.kv_len = (d.p + 1) * d.s_loc;
     ap.scale_log2 = d.scale * log2e;
     TSP_LAUNCH(TSP_KERNEL_ATTN, st, tsp::launch_flash_attn(ap, st));
 
