@@ -24,6 +24,7 @@ HIPCC_FLAGS = [
     # keep the compiler from emitting packed fp32 VALU ops
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
+    "-Wl,--no-undefined",
 ]
 
 

@@ -6,11 +6,11 @@
 // online, one key tile at a time, so the (S_loc x S) score matrix never exists.
 //
 // Work split.  A workgroup owns 128 queries of one head (GQA: head i reads kv head
-// i / g) and has 8 wavefronts: wavefront w handles queries 32 (w % 4) .. +31 against
-// key group w / 4, i.e. every step stages 128 keys in LDS and the two groups of four
-// wavefronts consume its two 64-key halves.  Each group keeps its own running max /
-// sum / output; the groups are merged once at the end.  Key tiles beyond the last
-// query's position are never loaded; only tiles that cross the diagonal are masked.
+// i / g) and has 8 wavefronts, two per SIMD: wavefront w handles queries
+// 32 (w % 4) .. +31 against key group w / 4, i.e. every 128-key tile staged in LDS is
+// consumed as two 64-key halves.  Each group keeps its own running max / sum /
+// output; the groups are merged once at the end.  Key tiles beyond the last query's
+// position are never loaded, and only tiles that cross the diagonal are masked.
 //
 // Scores are computed transposed, S^T = K Q^T, with K as the MFMA A operand and Q
 // (held in registers) as B.  The 32 x 32 accumulator then gives each lane 16 keys of
@@ -18,14 +18,19 @@
 // cross-lane exchange and the row sum none until the end.  The probabilities P^T
 // feed O^T = V^T P^T directly as the B operand (contraction over keys).
 //
+// Schedule.  Per step every wavefront computes the scores of its half of tile j,
+// the softmax and the P V product, while tiles j+1 of K and V stream into the other
+// slot of their two-slot rings.  (Variants that delay P V by a step so the two
+// wavefronts of a SIMD alternate matrix and vector phases measured slower.)
+//
 // Data movement.  K and V tiles go from HBM straight into LDS (global_load_lds, no
 // register staging) in their natural [key][d] layout, 16-byte chunks XOR-swizzled by
-// the row.  The V^T operand is read with the gfx950 LDS transpose read
-// (ds_read_b64_tr_b16): in each 16-lane group, source lane s points at row
+// the low bits of the row.  The V^T operand is read with the gfx950 LDS transpose
+// read (ds_read_b64_tr_b16): in each 16-lane group, source lane s points at row
 // kbase + s/4, columns base + 4 (s % 4), and lane t receives column base + t of rows
-// kbase .. kbase+3 -- four consecutive keys of one head-dim column.  K and V use
-// separate two-slot rings offset by one tile: while tile j's softmax runs, the MFMAs
-// for tile j+1's scores are already issued and tiles j+2 (K) / j+1 (V) are in flight.
+// kbase .. kbase+3 -- four consecutive keys of one head-dim column.  Because tile rows
+// are aligned to the row size and the swizzle only touches the in-row offset, every
+// LDS read address is (per-lane base XOR a constant) + an immediate offset.
 #include <math.h>
 
 #include "common.h"
@@ -35,9 +40,10 @@ namespace tsp {
 namespace {
 
 constexpr int kThreads = 512;
-constexpr int kQTile = 128;
-constexpr int kKTile = 64;           // keys per group per step
-constexpr int kStepKeys = 2 * kKTile;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kQTile = 128;          // queries per workgroup
+constexpr int kStepKeys = 128;       // keys staged per step
+constexpr int kGroupKeys = 64;       // keys per group per step
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (exp2 units)
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -48,26 +54,35 @@ struct FaCfg {
   static constexpr int KCH = D / 8;                           // 16-byte chunks per key row
   static constexpr int ROW_BYTES = D * 2;
   static constexpr int TILE_BYTES = kStepKeys * ROW_BYTES;    // one K or V tile
-  static constexpr int DMA_PER_LANE = kStepKeys * KCH / kThreads;
   static constexpr int ROWS_PER_DMA = kWave / KCH;            // rows one wave instruction fills
+  static constexpr int DMA_PER_LANE = kStepKeys / (kWaves * ROWS_PER_DMA);
   static constexpr int EB = D / 32;                           // 32-row blocks of O^T
   static constexpr int KS = D / 16;                           // contraction steps of S^T
-  static_assert(DMA_PER_LANE * 8 * ROWS_PER_DMA == kStepKeys, "DMA cover");
+  static_assert(DMA_PER_LANE * kWaves * ROWS_PER_DMA == kStepKeys, "DMA cover");
 };
 
-template <int KCH>
-__device__ __forceinline__ int phys_chunk(int row, int chunk) {
-  return chunk ^ (row & (KCH - 1));
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane.
+__device__ __forceinline__ void dma16(const void* src, lds_char* lds) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
-__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ u32x4 lds_read16(const lds_char* p) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p);
+}
+
+__device__ __forceinline__ u32x2 lds_read_tr(const lds_char* p) {
+  return __builtin_bit_cast(
+      u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p));
+}
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
   using C = FaCfg<D>;
-  constexpr int KCH = C::KCH;
-  // [K slot 0][K slot 1][V slot 0][V slot 1]
-  __shared__ __attribute__((aligned(16))) char L[4 * C::TILE_BYTES];
+  constexpr int KCH = C::KCH, RB = C::ROW_BYTES;
+  // [K slot 0][K slot 1][V slot 0][V slot 1][Q tile]
+  __shared__ __attribute__((aligned(1024))) char L[4 * C::TILE_BYTES];
   lds_char* Ls = (lds_char*)L;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -95,7 +110,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   const int n_steps = (n_keys + kStepKeys - 1) / kStepKeys;
   const float c = P.scale_log2;
 
-  // Q fragments: the B operand of S^T; lane holds Q[qloc][16 s + 8 hh .. +7].
+  // Q fragments: the B operand of S^T; lane holds Q[qloc][16 ks + 8 hh .. +7].
   u32x4 qf[C::KS];
   {
     const uint16_t* qrow = P.Q + (((size_t)b * P.s_loc + (qvalid ? qloc : 0)) * P.heads + head) * D;
@@ -103,50 +118,67 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     for (int s = 0; s < C::KS; ++s)
       qf[s] = qvalid ? ld16(qrow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
   }
-
-  const size_t kv_stride = (size_t)P.n_kv * D;
+  const size_t kv_stride = (size_t)P.n_kv * D;  // elements between consecutive keys
   const uint16_t* kbase = P.Kb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
   const uint16_t* vbase = P.Vb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
 
-  // One 128-key tile from HBM into an LDS slot.  Rows past the last needed key are
-  // clamped to it: they are always masked (keys > every query position of this
-  // workgroup) and stay finite, so the P V product never sees garbage.
+  // DMA geometry: instruction i of wave w fills rows (i kWaves + w) ROWS_PER_DMA + lane / KCH,
+  // physical chunk lane % KCH, with the logical chunk that the swizzle puts there (the
+  // row's low bits, and so the chunk, are the same for every i).  The source of a full
+  // tile is (wave-uniform tile base) + (per-lane byte offset).
+  constexpr int kRowStep = kWaves * C::ROWS_PER_DMA;  // rows between instructions
+  const int dma_row0 = wave * C::ROWS_PER_DMA + lane / KCH;
+  const int dma_col = 8 * ((lane % KCH) ^ (dma_row0 & (KCH - 1)));
+  const int dma_off0 = 2 * (dma_row0 * (int)kv_stride + dma_col);
+  const int dma_step = 2 * kRowStep * (int)kv_stride;
+  // One 128-key tile from HBM into an LDS slot.  In the last tile, rows past the last
+  // needed key are clamped to it: they are always masked (keys > every query position
+  // of this workgroup) and stay finite, so the P V product never sees garbage.
   auto dma_tile = [&](const uint16_t* base, int tile, int slot_off) {
-    const int rsub = lane / KCH, pc = lane % KCH;
+    const int key0 = tile * kStepKeys;
+    const char* tbase = reinterpret_cast<const char*>(base + (size_t)key0 * kv_stride);
+    lds_char* dst = Ls + slot_off + wave * (kWave * 16);
+    if (key0 + kStepKeys <= n_keys) {
 #pragma unroll
-    for (int i = 0; i < C::DMA_PER_LANE; ++i) {
-      const int blk = i * 8 + wave;
-      const int row = blk * C::ROWS_PER_DMA + rsub;
-      const int key = min(tile * kStepKeys + row, n_keys - 1);
-      const uint16_t* src = base + (size_t)key * kv_stride + 8 * phys_chunk<KCH>(row, pc);
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(
-                                                  Ls + slot_off + blk * (kWave * 16)),
-                                       16, 0, 0);
-    }
-  };
-  auto k_off = [&](int tile) { return (tile & 1) * C::TILE_BYTES; };
-  auto v_off = [&](int tile) { return (2 + (tile & 1)) * C::TILE_BYTES; };
-
-  // S^T tile of this wave's key group: 2 blocks of 32 keys x 32 queries.
-  auto scores = [&](int tile, f32x16 (&s)[2]) {
-    const lds_char* K = Ls + k_off(tile);
+      for (int i = 0; i < C::DMA_PER_LANE; ++i)
+        dma16(tbase + dma_off0 + i * dma_step, dst + i * kWaves * (kWave * 16));
+    } else {
 #pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) s[bb][e] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-#pragma unroll
-      for (int bb = 0; bb < 2; ++bb) {
-        const int row = kKTile * grp + 32 * bb + l32;
-        const u32x4 kf = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(
-            K + row * C::ROW_BYTES + 16 * phys_chunk<KCH>(row, 2 * ks + hh));
-        s[bb] = mfma32(kf, qf[ks], s[bb]);
+      for (int i = 0; i < C::DMA_PER_LANE; ++i) {
+        const int row = min(dma_row0 + i * kRowStep, n_keys - 1 - key0);
+        dma16(tbase + 2 * (row * (int)kv_stride + dma_col), dst + i * kWaves * (kWave * 16));
       }
     }
   };
+  auto k_off = [](int tile) { return (tile & 1) * C::TILE_BYTES; };
+  auto v_off = [](int tile) { return (2 + (tile & 1)) * C::TILE_BYTES; };
+
+  // K operand: row 64 grp + 32 bb + l32, logical chunk 2 ks + hh  ->  byte
+  //   (64 grp + 32 bb) RB + (ka ^ 32 ks),  ka = l32 RB + 16 (hh ^ (l32 mod KCH)).
+  const int ka = l32 * RB + 16 * (hh ^ (l32 & (KCH - 1)));
+  // Q operand (B of S^T): row 32 wq + l32 of the query tile, same chunk pattern as K.
+  // V^T operand (transpose reads): rows 64 grp + 32 bb + 16 s2 + tr_row (+8 for elements
+  // 4-7), columns 32 eb + tr_col  ->  byte (64 grp + 32 bb + 16 s2) RB + (va or vb)[eb].
+  const int tr_t = lane & 15, tr_g = lane >> 4;
+  const int tr_row = ((tr_g >> 1) << 2) + (tr_t >> 2);     // 4 hh + t / 4
+  const int tr_col = 16 * (tr_g & 1) + 4 * (tr_t & 3);     // within a 32-column block
+  int va[C::EB], vb[C::EB];
+  {
+    const int cl = tr_col >> 3, half8 = 8 * ((tr_col >> 2) & 1);
+    const int xa = tr_row & (KCH - 1), xb = (tr_row + 8) & (KCH - 1);
+    const int base_a = tr_row * RB + 16 * (cl ^ xa) + half8;
+    const int base_b = (tr_row + 8) * RB + 16 * (cl ^ xb) + half8;
+#pragma unroll
+    for (int eb = 0; eb < C::EB; ++eb) {
+      va[eb] = base_a ^ (64 * eb);
+      vb[eb] = base_b ^ (64 * eb);
+    }
+  }
+  const int grp_rows = kGroupKeys * grp * RB;  // this group's half of a tile
+
   auto tile_active = [&](int tile) {
-    return wave_active && tile * kStepKeys + kKTile * grp <= wpos_max;
+    return tile >= 0 && tile < n_steps && wave_active &&
+           tile * kStepKeys + kGroupKeys * grp <= wpos_max;
   };
 
   f32x16 o[C::EB];
@@ -155,106 +187,107 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[eb][e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  f32x16 sacc[2];   // scores of this group's 64 keys of one tile
+  u32x4 pf[2][2];   // bf16 probabilities of one tile (B operands of P V)
 
-  // Transpose-read geometry of this lane (see the header comment).
-  const int tr_t = lane & 15, tr_g = lane >> 4;
-  const int tr_row = ((tr_g >> 1) << 2) + (tr_t >> 2);     // 4 hh + t / 4
-  const int tr_col = 16 * (tr_g & 1) + 4 * (tr_t & 3);     // within a 32-column block
+  // S^T of tile j: 2 blocks of 32 keys x 32 queries.
+  auto scores = [&](int j) {
+    const lds_char* K = Ls + k_off(j) + grp_rows;
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sacc[bb][e] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      const lds_char* Kk = K + (ka ^ (32 * ks));
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+        sacc[bb] = mfma32(lds_read16(Kk + 32 * bb * RB), qf[ks], sacc[bb]);
+    }
+  };
+  // Mask (if tile j crosses the diagonal), online-softmax update, probabilities.
+  auto softmax = [&](int j) {
+    const int kt0 = j * kStepKeys + kGroupKeys * grp;
+    if (kt0 + kGroupKeys - 1 > wpos_min) {
+      const int rel = qpos - kt0 - 4 * hh;  // key offset in the group tile must be <= this
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kofs = 32 * bb + 8 * (e >> 2) + (e & 3);
+          sacc[bb][e] = kofs > rel ? -INFINITY : sacc[bb][e];
+        }
+    }
+    float mx = sacc[0][0];
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[bb][e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    // Lazy rescaling, decided per query (both lanes of a query see the same max): the
+    // running max moves only when a score exceeds it by more than 8 in exp2 units
+    // (always on the first visible tile).  Between moves every probability is bounded
+    // by 2^8 and numerator and denominator share the stale max, so the normalised
+    // result is unchanged while the output rescale is skipped.
+    const bool grow = (mx - m_run) * c > kRescaleLog2;
+    if (__any(grow)) {
+      const float m_new = grow ? fmaxf(m_run, mx) : m_run;
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_use) * c) : 1.f;
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[eb][e] *= alpha;
+    }
+    const float mc = (m_run == -INFINITY ? 0.f : m_run) * c;
+    float lsum = 0.f;
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[bb][8 * s2 + 2 * q], c, -mc));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[bb][8 * s2 + 2 * q + 1], c, -mc));
+          lsum += p0 + p1;
+          pf[bb][s2][q] = pack_bf16x2(p0, p1);
+        }
+    l_run += lsum;
+  };
+  // O^T += V^T P^T for tile j.  k-step (bb, s2) covers keys 32 bb + 16 s2 + [0, 16) of
+  // the group tile; lane half hh feeds keys 4 hh + 0..3 (elements 0-3) and 8 + 4 hh +
+  // 0..3 (4-7), matching the accumulator layout of the scores.
+  auto pv = [&](int j) {
+    const lds_char* V = Ls + v_off(j) + grp_rows;
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const lds_char* Vr = V + (32 * bb + 16 * s2) * RB;
+#pragma unroll
+        for (int eb = 0; eb < C::EB; ++eb) {
+          const u32x2 lo = lds_read_tr(Vr + va[eb]);
+          const u32x2 hi = lds_read_tr(Vr + vb[eb]);
+          o[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pf[bb][s2], o[eb]);
+        }
+      }
+  };
 
   dma_tile(kbase, 0, k_off(0));
   dma_tile(vbase, 0, v_off(0));
-  if (n_steps > 1) dma_tile(kbase, 1, k_off(1));
-  wait_dma();
-  __syncthreads();
-  f32x16 s_cur[2];
-  if (tile_active(0)) scores(0, s_cur);
-
   for (int j = 0; j < n_steps; ++j) {
     wait_dma();
-    __syncthreads();  // K tile j+1 and V tile j resident; every wave is past step j-1
-    if (j + 2 < n_steps) dma_tile(kbase, j + 2, k_off(j + 2));
-    if (j + 1 < n_steps) dma_tile(vbase, j + 1, v_off(j + 1));
-
-    f32x16 s_next[2];
-    const bool next_active = j + 1 < n_steps && tile_active(j + 1);
-    if (next_active) scores(j + 1, s_next);
-
-    if (tile_active(j)) {
-      const int kt0 = j * kStepKeys + kKTile * grp;
-      if (kt0 + kKTile - 1 > wpos_min) {
-#pragma unroll
-        for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = kt0 + 32 * bb + 8 * (e >> 2) + 4 * hh + (e & 3);
-            if (key > qpos) s_cur[bb][e] = -INFINITY;
-          }
-      }
-      float mx = s_cur[0][0];
-#pragma unroll
-      for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s_cur[bb][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      // Lazy rescaling: the running max moves only when a score exceeds it by more
-      // than 8 in exp2 units (always on the first visible tile).  Between moves every
-      // probability is bounded by 2^8, and numerator and denominator share the stale
-      // max, so the normalised result is unchanged while the output rescale is
-      // skipped on most tiles.
-      if (__any((mx - m_run) * c > kRescaleLog2)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * c);
-        l_run *= alpha;
-#pragma unroll
-        for (int eb = 0; eb < C::EB; ++eb)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[eb][e] *= alpha;
-        m_run = m_new;
-      }
-      const float mc = (m_run == -INFINITY ? 0.f : m_run) * c;
-      float lsum = 0.f;
-      u32x4 pf[2][2];
-#pragma unroll
-      for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float p0 = __builtin_amdgcn_exp2f(fmaf(s_cur[bb][8 * s2 + 2 * q], c, -mc));
-            const float p1 = __builtin_amdgcn_exp2f(fmaf(s_cur[bb][8 * s2 + 2 * q + 1], c, -mc));
-            lsum += p0 + p1;
-            pf[bb][s2][q] = pack_bf16x2(p0, p1);
-          }
-      l_run += lsum;
-
-      // O^T += V^T P^T.  k-step (bb, s2) covers keys kt0 + 32 bb + 16 s2 + [0, 16); lane
-      // half hh feeds keys 4 hh + 0..3 (elements 0-3) and 8 + 4 hh + 0..3 (4-7).
-      const lds_char* V = Ls + v_off(j);
-#pragma unroll
-      for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const int r0 = kKTile * grp + 32 * bb + 16 * s2 + tr_row;
-#pragma unroll
-          for (int eb = 0; eb < C::EB; ++eb) {
-            const int col = 32 * eb + tr_col;
-            const int ch = col >> 3, half = (col >> 2) & 1;
-            const int ra = r0, rb = r0 + 8;
-            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) i16x4*)(
-                    V + ra * C::ROW_BYTES + 16 * phys_chunk<KCH>(ra, ch) + 8 * half));
-            const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) i16x4*)(
-                    V + rb * C::ROW_BYTES + 16 * phys_chunk<KCH>(rb, ch) + 8 * half));
-            const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
-            o[eb] = mfma32(u32x4{lo2[0], lo2[1], hi2[0], hi2[1]}, pf[bb][s2], o[eb]);
-          }
-        }
+    __syncthreads();  // K and V tile j resident; every wave is past step j-1
+    if (j + 1 < n_steps) {
+      dma_tile(kbase, j + 1, k_off(j + 1));
+      dma_tile(vbase, j + 1, v_off(j + 1));
     }
-    if (next_active) {
-      s_cur[0] = s_next[0];
-      s_cur[1] = s_next[1];
+    if (tile_active(j)) {
+      scores(j);
+      softmax(j);
+      pv(j);
     }
   }
 
