@@ -4,14 +4,26 @@
 //   down / O-proj   Y (+)= Hs W2   or   Y (+)= Flatten(A) W_O^T    Algorithm 2 / 1, "+="
 //   Q/K/V proj      Q = X W_Q^T -> workspace, K, V -> full-sequence buffers  Algorithm 1
 //
-// One workgroup = 256 threads = 4 wavefronts in a 2 x 2 grid; each wavefront owns a
-// (BM/2) x (BN/2) block of C as 32 x 32 MFMA tiles.  K advances in steps of 64: the
-// next A/B panels are fetched into registers while the MFMAs consume the current
-// panels from LDS (two LDS stages, one barrier per step).  Every panel is stored in
-// LDS as rows of eight 16-byte chunks (64 bf16 of the contraction dimension) so each
-// MFMA operand is one 16-byte LDS read.  Operands stored [K, N] (W2, W_O^T) are
-// transposed on the way into LDS with an in-register 8 x 8 (or 4 x 8) block swap, so
-// both operand layouts share one inner loop and no extra pass over HBM is made.
+// One workgroup = WGM x WGN wavefronts (8 by default: two per SIMD); each wavefront owns
+// a (BM/WGM) x (BN/WGN) block of C as 32 x 32 MFMA tiles.  K advances in steps of 64.
+// Operand panels go from HBM straight into LDS (global_load_lds, no register staging),
+// double-buffered: while the MFMAs consume step k the DMA fills step k+1.
+//
+// LDS layouts.  A [M, K] and "NT" B [N, K] panels are rows of 64 bf16 (128 bytes, eight
+// 16-byte chunks, chunk XOR-swizzled by row mod 8); an MFMA operand is one 16-byte read.
+// "NN" B panels ([K, N] operands: W2 and W_O^(r)^T) keep their natural [64][BN] layout
+// (chunks swizzled the same way) and are read with the gfx950 LDS transpose read
+// ds_read_b64_tr_b16: in each 16-lane group, source lane s points at row kbase + s/4,
+// columns base + 4 (s % 4), and lane t receives column base + t of rows kbase..kbase+3,
+// i.e. four consecutive contraction indices of one output column -- no transpose pass
+// over HBM and no register shuffles.  Every LDS address is a per-lane base XOR a
+// wave-uniform constant plus an immediate offset.
+//
+// Tails.  Rows or columns past M / N are clamped to the last valid one on load (finite
+// values, results never stored).  K must be a multiple of 64: the gated product Hs is
+// stored with its width padded to a multiple of 64 with zero columns (written by the
+// SwiGLU epilogue), and the matching W2 rows past F/D are clamped, so padded terms
+// contribute exact zeros.
 #include "common.h"
 #include "internal.h"
 
@@ -19,64 +31,86 @@ namespace tsp {
 namespace {
 
 constexpr int BK = 64;
-constexpr int kThreads = 256;
 enum { EPI_SWIGLU = 0, EPI_ACC = 1, EPI_QKV = 2 };
 
-__device__ __forceinline__ int swz8(int row, int chunk) {
-  return chunk ^ ((row ^ (row >> 3)) & 7);
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_char;
+
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane.
+__device__ __forceinline__ void dma16(const void* src, lds_char* lds) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
-template <int BM, int BN, bool NN, int EPI>
+__device__ __forceinline__ u32x4 lds_read16(const lds_char* p) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p);
+}
+
+__device__ __forceinline__ u32x2 lds_read_tr(const lds_char* p) {
+  return __builtin_bit_cast(
+      u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p));
+}
+
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI>
 struct Cfg {
-  static constexpr int NB = EPI == EPI_SWIGLU ? 2 * BN : BN;  // B rows held in LDS
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int WAVES = WGM * WGN, THREADS = kWave * WAVES;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int TM = WM / 32, TN = WN / 32;
   static constexpr int TNB = EPI == EPI_SWIGLU ? 2 * TN : TN;
-  static constexpr int A_LOADS = BM / 32;
-  static constexpr int B_LOADS = NN ? BN / 32 : NB / 32;      // NN: KH rows of one block
-  static constexpr int STAGE = (BM + NB) * 8;                 // 16-byte chunks per stage
+  static constexpr int NB = EPI == EPI_SWIGLU ? 2 * BN : BN;  // B rows of an NT panel
+  static constexpr int A_BYTES = BM * BK * 2;
+  static constexpr int B_BYTES = NB * BK * 2;                  // NT [NB][64] or NN [64][BN]
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int NN_RB = BN * 2;                         // NN panel row bytes
   static_assert(!(NN && EPI == EPI_SWIGLU), "SwiGLU operands are [N, K]");
-  static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
+  static_assert((BM / 8) % WAVES == 0 && (NB / 8) % WAVES == 0, "NT DMA cover");
+  static_assert(!NN || (BK * NN_RB / 1024) % WAVES == 0, "NN DMA cover");
 };
 
-// Row-major [rows, K] panel rows row0 .. row0+ROWS-1, columns k0 .. k0+63.
-template <int NLOAD>
-__device__ __forceinline__ void load_panel(u32x4 (&r)[NLOAD], const uint16_t* __restrict__ base,
-                                           int ld, int row0, int nrows, int k0, int K,
-                                           int tid) {
-  const int k = k0 + 8 * (tid & 7);
+// NT panel rows [row0, row0 + ROWS) x k [k0, k0 + 64) of a row-major [nrows, ld] matrix
+// into LDS (128-byte rows).  Instruction i of wave w fills rows 8 (i W + w) .. +7.
+template <int ROWS, int WAVES>
+__device__ __forceinline__ void dma_nt(lds_char* dst, const uint16_t* base, int ld, int row0,
+                                       int nrows, int k0, int wave, int lane) {
+  const int rsub = lane >> 3, pc = lane & 7;
 #pragma unroll
-  for (int i = 0; i < NLOAD; ++i) {
-    const int row = row0 + (tid >> 3) + 32 * i;
-    r[i] = (row < nrows && k < K) ? ld16(base + (size_t)row * ld + k) : u32x4{0u, 0u, 0u, 0u};
+  for (int i = 0; i < ROWS / 8 / WAVES; ++i) {
+    const int blk = i * WAVES + wave;
+    const int r = 8 * blk + rsub;
+    const int grow = min(row0 + r, nrows - 1);
+    dma16(base + (size_t)grow * ld + k0 + 8 * (pc ^ (r & 7)), dst + blk * 1024);
   }
 }
 
-template <int NLOAD>
-__device__ __forceinline__ void store_panel(u32x4* L, int lds_row0, const u32x4 (&r)[NLOAD],
-                                            int tid) {
-  const int c = tid & 7;
+// NN panel: k rows [k0, k0 + 64) x n [n0, n0 + BN) of a row-major [K, N] matrix into LDS
+// (natural layout, BN * 2-byte rows).  Rows past krows and columns past ncols are clamped.
+template <int BN, int WAVES>
+__device__ __forceinline__ void dma_nn(lds_char* dst, const uint16_t* base, int ld, int k0,
+                                       int krows, int n0, int ncols, int wave, int lane) {
+  constexpr int CH = BN / 8, RPI = kWave / CH;  // chunks per row, rows per instruction
+  const int rsub = lane / CH, pc = lane % CH;
 #pragma unroll
-  for (int i = 0; i < NLOAD; ++i) {
-    const int row = (tid >> 3) + 32 * i;
-    L[(lds_row0 + row) * 8 + swz8(row, c)] = r[i];
+  for (int i = 0; i < BK / RPI / WAVES; ++i) {
+    const int blk = i * WAVES + wave;
+    const int r = RPI * blk + rsub;
+    const int gk = min(k0 + r, krows - 1);
+    const int gn = min(n0 + 8 * (pc ^ (r & 7)), ncols - 8);
+    dma16(base + (size_t)gk * ld + gn, dst + blk * 1024);
   }
 }
 
-// Two rows of bf16 pairs -> one dword holding column `odd` of each row.
-__device__ __forceinline__ uint32_t pick_col(uint32_t row_lo, uint32_t row_hi, int odd) {
-  return odd ? ((row_lo >> 16) | (row_hi & 0xffff0000u)) : ((row_lo & 0xffffu) | (row_hi << 16));
-}
-
-template <int BM, int BN, bool NN, int EPI>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
-  using C = Cfg<BM, BN, NN, EPI>;
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI>
+__global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParams P) {
+  using C = Cfg<BM, BN, WGM, WGN, NN, EPI>;
   constexpr int TM = C::TM, TN = C::TN, TNB = C::TNB;
-  __shared__ u32x4 L[2 * C::STAGE];
+  __shared__ __attribute__((aligned(1024))) char L[2 * C::STAGE];
+  lds_char* Ls = (lds_char*)L;
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
   const int l32 = lane & 31, hh = lane >> 5;
 
   const int tiles_n = (P.N + BN - 1) / BN;
@@ -93,102 +127,76 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  u32x4 ra[C::A_LOADS];
-  u32x4 rb[C::B_LOADS];
-
-  // NN operand: thread owns a KH x 8 block (KH contraction rows, 8 output columns).
-  constexpr int KH = BN / 32;
-  const int nn_nb = tid % (BN / 8), nn_kb = tid / (BN / 8);
-
-  auto load = [&](int k0) {
-    load_panel<C::A_LOADS>(ra, P.A, P.lda, m0, P.M, k0, P.K, tid);
+  auto dma_stage = [&](int stage, int k0) {
+    lds_char* S = Ls + stage * C::STAGE;
+    dma_nt<BM, C::WAVES>(S, P.A, P.lda, m0, P.M, k0, wave, lane);
     if constexpr (NN) {
-      const int n = n0 + 8 * nn_nb;
-#pragma unroll
-      for (int rr = 0; rr < KH; ++rr) {
-        const int k = k0 + KH * nn_kb + rr;
-        rb[rr] = (k < P.K && n < P.N) ? ld16(P.B + (size_t)k * P.ldb + n) : u32x4{0u, 0u, 0u, 0u};
-      }
+      dma_nn<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, k0, P.Kb_rows, n0, P.N, wave, lane);
     } else if constexpr (EPI == EPI_SWIGLU) {
-      u32x4 g[BN / 32], u[BN / 32];
-      load_panel<BN / 32>(g, P.B, P.ldb, n0, P.N, k0, P.K, tid);
-      load_panel<BN / 32>(u, P.B2, P.ldb, n0, P.N, k0, P.K, tid);
-#pragma unroll
-      for (int i = 0; i < BN / 32; ++i) {
-        rb[i] = g[i];
-        rb[BN / 32 + i] = u[i];
-      }
+      dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
+      dma_nt<BN, C::WAVES>(S + C::A_BYTES + BN * BK * 2, P.B2, P.ldb, n0, P.N, k0, wave, lane);
     } else {
-      load_panel<C::B_LOADS>(rb, P.B, P.ldb, n0, P.N, k0, P.K, tid);
+      dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
     }
   };
 
-  auto store = [&](int stage) {
-    u32x4* S = L + stage * C::STAGE;
-    store_panel<C::A_LOADS>(S, 0, ra, tid);
-    if constexpr (NN) {
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const int row = 8 * nn_nb + c;  // output column n within the tile
-        if constexpr (KH == 8) {
-          u32x4 o;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) o[q] = pick_col(rb[2 * q][c >> 1], rb[2 * q + 1][c >> 1], c & 1);
-          S[(BM + row) * 8 + swz8(row, nn_kb)] = o;
-        } else {
-          static_assert(KH == 4, "KH");
-          u32x2 o;
-#pragma unroll
-          for (int q = 0; q < 2; ++q) o[q] = pick_col(rb[2 * q][c >> 1], rb[2 * q + 1][c >> 1], c & 1);
-          reinterpret_cast<u32x2*>(S)[((BM + row) * 8 + swz8(row, nn_kb >> 1)) * 2 + (nn_kb & 1)] = o;
-        }
-      }
-    } else {
-      store_panel<C::B_LOADS>(S, BM, rb, tid);
-    }
-  };
+  // Operand addressing (see the header): A / NT-B row R, chunk 2 s + hh ->
+  //   R_base * 128 + (opa ^ 32 s),  opa = l32 * 128 + 16 (hh ^ (l32 mod 8)).
+  const int opa = l32 * 128 + 16 * (hh ^ (l32 & 7));
+  // NN-B transpose reads for output column block j: rows 16 s + 8 hh + t/4 (+4), columns
+  // wn WN + 32 j + 16 (g mod 2) + 4 (t mod 4)  ->  16 s NN_RB + (nb ^ 2 (wn WN + 32 j)).
+  int nb_lo = 0, nb_hi = 0;
+  if constexpr (NN) {
+    const int t = lane & 15, g = lane >> 4;
+    const int cl = 2 * (g & 1) + ((t & 3) >> 1), half8 = 8 * (t & 1);
+    const int r_lo = 8 * (g >> 1) + (t >> 2), r_hi = r_lo + 4;
+    nb_lo = r_lo * C::NN_RB + 16 * (cl ^ (r_lo & 7)) + half8;
+    nb_hi = r_hi * C::NN_RB + 16 * (cl ^ (r_hi & 7)) + half8;
+  }
 
-  const int nk = (P.K + BK - 1) / BK;
-  load(0);
-  store(0);
-  __syncthreads();
-
+  const int nk = P.K / BK;
+  dma_stage(0, 0);
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load((kt + 1) * BK);
-    const u32x4* S = L + cur * C::STAGE;
+    wait_dma();
+    __syncthreads();  // stage kt resident; every wave is past step kt-1
+    if (kt + 1 < nk) dma_stage((kt + 1) & 1, (kt + 1) * BK);
+    const lds_char* SA = Ls + (kt & 1) * C::STAGE;
+    const lds_char* SB = SA + C::A_BYTES;
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
-      const int ch = 2 * s + hh;
       u32x4 a[TM], b[TNB];
+      const int xo = opa ^ (32 * s);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int row = wm * C::WM + 32 * i + l32;
-        a[i] = S[row * 8 + swz8(row, ch)];
-      }
+      for (int i = 0; i < TM; ++i) a[i] = lds_read16(SA + (wm * C::WM + 32 * i) * 128 + xo);
 #pragma unroll
       for (int j = 0; j < TNB; ++j) {
-        const int row = (j < TN ? wn * C::WN + 32 * j : BN + wn * C::WN + 32 * (j - TN)) + l32;
-        b[j] = S[(BM + row) * 8 + swz8(row, ch)];
+        if constexpr (NN) {
+          const int cx = 2 * (wn * C::WN + 32 * j);
+          const u32x2 lo = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_lo ^ cx));
+          const u32x2 hi = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_hi ^ cx));
+          b[j] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        } else {
+          const int brow = j < TN ? wn * C::WN + 32 * j : BN + wn * C::WN + 32 * (j - TN);
+          b[j] = lds_read16(SB + brow * 128 + xo);
+        }
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TNB; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
     }
-    if (kt + 1 < nk) store(cur ^ 1);
-    __syncthreads();
   }
+  __syncthreads();  // operand stages are free for the epilogue
 
   // ---------------------------------------------------------------- epilogue
-  // Each wavefront stages one 32-row block of its C tile in LDS as fp32 (the last
-  // main-loop barrier has released the operand stages), then writes it out in
-  // 4-column chunks: consecutive lanes cover consecutive columns, every global access
-  // is 16 bytes (fp32) or 8 bytes (bf16), and all loads of a block are in flight
+  // Each wavefront stages one 32-row block of its C tile in LDS as fp32, then writes it
+  // out in 4-column chunks: consecutive lanes cover consecutive columns, every global
+  // access is 16 bytes (fp32) or 8 bytes (bf16), and all loads of a block are in flight
   // before the first store.
-  constexpr int EST = C::WN + 4;          // staging row stride in floats
-  constexpr int CPR = C::WN / 4;          // 4-column chunks per row
+  constexpr int EST = C::WN + 4;  // staging row stride in floats
+  constexpr int CPR = C::WN / 4;  // 4-column chunks per row
   constexpr int PER_LANE = 32 * CPR / kWave;
+  static_assert(C::WAVES * 32 * EST * 4 <= 2 * C::STAGE, "epilogue staging fits");
   float* E = reinterpret_cast<float*>(L) + wave * 32 * EST;
   const int ncol0 = n0 + wn * C::WN;
 #pragma unroll
@@ -241,13 +249,18 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
     } else {
 #pragma unroll
       for (int q = 0; q < PER_LANE; ++q) {
-        if (!ok[q]) continue;
-        const u32x2 bits{pack_bf16x2(v[q][0], v[q][1]), pack_bf16x2(v[q][2], v[q][3])};
-        uint16_t* dst;
         if constexpr (EPI == EPI_SWIGLU) {
-          dst = P.H + (size_t)mm[q] * P.ldh + nn[q];
+          // Columns [N, ldh) are the zero padding of the gated product.
+          if (mm[q] >= P.M || nn[q] >= P.ldh) continue;
+          const u32x2 bits = nn[q] < P.N ? u32x2{pack_bf16x2(v[q][0], v[q][1]),
+                                                 pack_bf16x2(v[q][2], v[q][3])}
+                                         : u32x2{0u, 0u};
+          *reinterpret_cast<u32x2*>(P.H + (size_t)mm[q] * P.ldh + nn[q]) = bits;
         } else {
+          if (!ok[q]) continue;
+          const u32x2 bits{pack_bf16x2(v[q][0], v[q][1]), pack_bf16x2(v[q][2], v[q][3])};
           const int n = nn[q], m = mm[q];
+          uint16_t* dst;
           if (n < P.nq) {
             dst = P.Q + (size_t)m * P.ldq + n;
           } else {
@@ -256,34 +269,37 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
                                (size_t)(P.kv_pos0 + t) * P.kv_row_stride + P.kv_col0;
             dst = n < P.nq + P.nkv ? P.Kb + row + (n - P.nq) : P.Vb + row + (n - P.nq - P.nkv);
           }
+          *reinterpret_cast<u32x2*>(dst) = bits;
         }
-        *reinterpret_cast<u32x2*>(dst) = bits;
       }
     }
     __syncthreads();
   }
 }
 
-template <int BM, int BN, bool NN, int EPI>
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI>
 hipError_t launch(const GemmParams& p, hipStream_t s) {
+  using C = Cfg<BM, BN, WGM, WGN, NN, EPI>;
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  if (p.K <= 0 || p.K % BK != 0) return hipErrorInvalidValue;
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, NN, EPI>), dim3(tiles), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, WGM, WGN, NN, EPI>), dim3(tiles), dim3(C::THREADS), 0,
+                     s, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s) {
-  return launch<256, 128, false, EPI_SWIGLU>(p, s);
+  return launch<256, 128, 2, 4, false, EPI_SWIGLU>(p, s);
 }
 
 hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s) {
-  return launch<256, 128, true, EPI_ACC>(p, s);
+  return launch<256, 256, 2, 4, true, EPI_ACC>(p, s);
 }
 
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s) {
-  return launch<256, 128, false, EPI_QKV>(p, s);
+  return launch<256, 256, 2, 4, false, EPI_QKV>(p, s);
 }
 
 }  // namespace tsp

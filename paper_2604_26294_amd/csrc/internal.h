@@ -15,9 +15,11 @@ struct GemmParams {
   const uint16_t* B;
   int ldb;
   const uint16_t* B2;  // SwiGLU only: the up-projection operand, same layout as B
-  int M, N, K;
+  int M, N, K;         // K: contraction length, a multiple of 64
+  int Kb_rows;         // [K, N] operands: rows actually present (rows >= Kb_rows are clamped)
 
-  // SwiGLU epilogue: H[m, n] = bf16( SiLU(C_gate) * C_up )
+  // SwiGLU epilogue: H[m, n] = bf16( SiLU(C_gate) * C_up ) for n < N, and 0 for
+  // N <= n < ldh (the zero padding that lets the down projection contract over ldh).
   uint16_t* H;
   int ldh;
 

@@ -24,6 +24,7 @@ struct Dims {
   int ks;      // kv heads per shard
   int g;       // GQA ratio
   int fs;      // MLP rows per shard
+  int fs_pad;  // fs rounded up to a multiple of 64 (width of the gated product in the workspace)
   long long M; // B * S_loc tokens of this rank
   float scale;
 };
@@ -57,6 +58,7 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
   o->ks = s->n_kv_heads / s->degree;
   o->g = s->n_heads / s->n_kv_heads;
   o->fs = s->ffn / s->degree;
+  o->fs_pad = (o->fs + 63) / 64 * 64;
   o->M = (long long)o->B * o->s_loc;
   if (o->M > INT32_MAX / 2) return TSP_ERR_UNSUPPORTED;
   o->scale = s->softmax_scale > 0.f ? s->softmax_scale : 1.0f / sqrtf((float)s->head_dim);
@@ -64,10 +66,10 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
 }
 
 // Workspace regions (each 256-byte aligned):
-//   MLP:   Hs [M, F/D] bf16
+//   MLP:   Hs [M, F/D rounded up to 64] bf16 (zero-padded columns)
 //   ATTN:  Q [M, H_s d] bf16, A [M, H_s d] bf16
 //   LAYER: u [M, h] bf16, then max(MLP, ATTN)
-size_t ws_mlp(const Dims& d) { return align_up((size_t)d.M * d.fs * 2); }
+size_t ws_mlp(const Dims& d) { return align_up((size_t)d.M * d.fs_pad * 2); }
 size_t ws_attn(const Dims& d) { return 2 * align_up((size_t)d.M * d.hs * d.d * 2); }
 size_t ws_layer(const Dims& d) {
   const size_t a = ws_mlp(d), b = ws_attn(d);
@@ -160,17 +162,18 @@ tsp_status run_mlp(const Dims& d, const uint16_t* x, const uint16_t* const* wg,
     up.N = d.fs;
     up.K = d.h;
     up.H = hs_ws;
-    up.ldh = d.fs;
+    up.ldh = d.fs_pad;
     TSP_LAUNCH(TSP_KERNEL_GATE_UP, st, tsp::launch_gemm_swiglu(up, st));
 
     GemmParams dn = {};
     dn.A = hs_ws;
-    dn.lda = d.fs;
+    dn.lda = d.fs_pad;
     dn.B = wd[j];
     dn.ldb = d.h;
     dn.M = (int)d.M;
     dn.N = d.h;
-    dn.K = d.fs;
+    dn.K = d.fs_pad;  // padded columns of Hs are zero; W2 rows past fs are clamped
+    dn.Kb_rows = d.fs;
     dn.Y = y;
     dn.ldy = d.h;
     dn.accumulate = (t > 0 || accumulate) ? 1 : 0;
@@ -242,6 +245,7 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     o.M = (int)d.M;
     o.N = d.h;
     o.K = qd;
+    o.Kb_rows = qd;
     o.Y = y;
     o.ldy = d.h;
     o.accumulate = (r > 0 || accumulate) ? 1 : 0;
