@@ -29,14 +29,15 @@
  *   - Every device pointer must be 16-byte aligned.
  *   - The caller owns every buffer.  The library never allocates or frees device
  *     memory and keeps no state between calls (apart from the opt-in kernel timing
- *     records of tsp_profile_enable); scratch space is the caller's workspace, sized
- *     by tsp_workspace_bytes.
+ *     records of tsp_profile_enable and the per-thread code of the last HIP failure);
+ *     scratch space is the caller's workspace, sized by tsp_workspace_bytes.
  *   - Calls only enqueue work on `stream` (NULL = the default stream) and never
  *     synchronise.  Calls on different streams must use different workspaces and
  *     must not write the same outputs.
  *   - All validation happens on the host, before anything is enqueued; a call that
  *     returns an error has enqueued nothing.  TSP_ERR_HIP reports a failed launch
- *     (work enqueued before the failure may still run).
+ *     (work enqueued before the failure may still run); tsp_last_hip_error names
+ *     the HIP error.
  *   - Results are deterministic: no atomics, fixed reduction orders.
  *   - Supported: head_dim in {64, 128}; hidden, ffn/degree and head_dim multiples
  *     of 8; layout 0 (contiguous chunks).  Anything else valid returns
@@ -159,6 +160,14 @@ tsp_status tsp_profile_read(int kernel, double* total_ms, int64_t* launches);
 
 /* Static, human-readable name of a status code. */
 const char* tsp_status_str(tsp_status status);
+
+/* The hipError_t behind the most recent TSP_ERR_HIP returned on the calling thread
+ * (0 = hipSuccess if no call on this thread has failed that way).  Kept per thread
+ * until the next such failure; no other call resets it. */
+int tsp_last_hip_error(void);
+
+/* Static name of a HIP error code (as hipGetErrorName), e.g. for tsp_last_hip_error. */
+const char* tsp_hip_error_string(int hip_error);
 
 /* TSP_ABI_VERSION of the built library. */
 int tsp_abi_version(void);

@@ -25,7 +25,7 @@
 //
 // Data movement.  K and V tiles go from HBM straight into LDS (global_load_lds, no
 // register staging) in their natural [key][d] layout, 16-byte chunks XOR-swizzled by
-// the low bits of the row.  The V^T operand is read with the gfx950 LDS transpose
+// a function of the row chosen per tile kind so that its reads are bank-conflict free.  The V^T operand is read with the gfx950 LDS transpose
 // read (ds_read_b64_tr_b16): in each 16-lane group, source lane s points at row
 // kbase + s/4, columns base + 4 (s % 4), and lane t receives column base + t of rows
 // kbase .. kbase+3 -- four consecutive keys of one head-dim column.  Because tile rows
@@ -58,7 +58,15 @@ struct FaCfg {
   static constexpr int DMA_PER_LANE = kStepKeys / (kWaves * ROWS_PER_DMA);
   static constexpr int EB = D / 32;                           // 32-row blocks of O^T
   static constexpr int KS = D / 16;                           // contraction steps of S^T
+  static constexpr int RPW = 256 / ROW_BYTES;                 // rows per 256-byte bank window
   static_assert(DMA_PER_LANE * kWaves * ROWS_PER_DMA == kStepKeys, "DMA cover");
+  // Chunk swizzles (physical 16-byte chunk = logical chunk XOR f(row)).  LDS has 64
+  // banks of 4 bytes, so a row's bank window position is (row mod RPW) and its chunk.
+  // K tiles are read 16 rows x one chunk per 16 lanes (ds_read_b128): f_K gives those
+  // rows distinct windows.  V tiles are read by 8-byte transpose reads, 4 rows x 4
+  // chunks per half-wave: f_V moves each of the 4 rows to its own 64-byte block.
+  __device__ static int fk(int row) { return (row / RPW) & (KCH - 1); }
+  __device__ static int fv(int row) { return 4 * ((row / RPW) & (KCH / 4 - 1)); }
 };
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -128,13 +136,15 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   // tile is (wave-uniform tile base) + (per-lane byte offset).
   constexpr int kRowStep = kWaves * C::ROWS_PER_DMA;  // rows between instructions
   const int dma_row0 = wave * C::ROWS_PER_DMA + lane / KCH;
-  const int dma_col = 8 * ((lane % KCH) ^ (dma_row0 & (KCH - 1)));
-  const int dma_off0 = 2 * (dma_row0 * (int)kv_stride + dma_col);
+  const int dma_col_k = 8 * ((lane % KCH) ^ C::fk(dma_row0));
+  const int dma_col_v = 8 * ((lane % KCH) ^ C::fv(dma_row0));
+  const int dma_off_k = 2 * (dma_row0 * (int)kv_stride + dma_col_k);
+  const int dma_off_v = 2 * (dma_row0 * (int)kv_stride + dma_col_v);
   const int dma_step = 2 * kRowStep * (int)kv_stride;
   // One 128-key tile from HBM into an LDS slot.  In the last tile, rows past the last
   // needed key are clamped to it: they are always masked (keys > every query position
   // of this workgroup) and stay finite, so the P V product never sees garbage.
-  auto dma_tile = [&](const uint16_t* base, int tile, int slot_off) {
+  auto dma_tile = [&](const uint16_t* base, int dma_off0, int dma_col, int tile, int slot_off) {
     const int key0 = tile * kStepKeys;
     const char* tbase = reinterpret_cast<const char*>(base + (size_t)key0 * kv_stride);
     lds_char* dst = Ls + slot_off + wave * (kWave * 16);
@@ -154,8 +164,8 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   auto v_off = [](int tile) { return (2 + (tile & 1)) * C::TILE_BYTES; };
 
   // K operand: row 64 grp + 32 bb + l32, logical chunk 2 ks + hh  ->  byte
-  //   (64 grp + 32 bb) RB + (ka ^ 32 ks),  ka = l32 RB + 16 (hh ^ (l32 mod KCH)).
-  const int ka = l32 * RB + 16 * (hh ^ (l32 & (KCH - 1)));
+  //   (64 grp + 32 bb) RB + (ka ^ 32 ks),  ka = l32 RB + 16 (hh ^ f_K(l32)).
+  const int ka = l32 * RB + 16 * (hh ^ C::fk(l32));
   // Q operand (B of S^T): row 32 wq + l32 of the query tile, same chunk pattern as K.
   // V^T operand (transpose reads): rows 64 grp + 32 bb + 16 s2 + tr_row (+8 for elements
   // 4-7), columns 32 eb + tr_col  ->  byte (64 grp + 32 bb + 16 s2) RB + (va or vb)[eb].
@@ -165,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   int va[C::EB], vb[C::EB];
   {
     const int cl = tr_col >> 3, half8 = 8 * ((tr_col >> 2) & 1);
-    const int xa = tr_row & (KCH - 1), xb = (tr_row + 8) & (KCH - 1);
+    const int xa = C::fv(tr_row), xb = C::fv(tr_row + 8);
     const int base_a = tr_row * RB + 16 * (cl ^ xa) + half8;
     const int base_b = (tr_row + 8) * RB + 16 * (cl ^ xb) + half8;
 #pragma unroll
@@ -275,14 +285,14 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
       }
   };
 
-  dma_tile(kbase, 0, k_off(0));
-  dma_tile(vbase, 0, v_off(0));
+  dma_tile(kbase, dma_off_k, dma_col_k, 0, k_off(0));
+  dma_tile(vbase, dma_off_v, dma_col_v, 0, v_off(0));
   for (int j = 0; j < n_steps; ++j) {
     wait_dma();
     __syncthreads();  // K and V tile j resident; every wave is past step j-1
     if (j + 1 < n_steps) {
-      dma_tile(kbase, j + 1, k_off(j + 1));
-      dma_tile(vbase, j + 1, v_off(j + 1));
+      dma_tile(kbase, dma_off_k, dma_col_k, j + 1, k_off(j + 1));
+      dma_tile(vbase, dma_off_v, dma_col_v, j + 1, v_off(j + 1));
     }
     if (tile_active(j)) {
       scores(j);
@@ -335,13 +345,16 @@ hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
   if (p.batch <= 0 || p.s_loc <= 0 || p.heads <= 0) return hipSuccess;
   const int n_qt = (p.s_loc + kQTile - 1) / kQTile;
   const dim3 grid(n_qt * p.heads * p.batch);
+  const void* fn;
   if (p.head_dim == 128)
-    hipLaunchKernelGGL(flash_fwd_kernel<128>, grid, dim3(kThreads), 0, s, p);
+    fn = reinterpret_cast<const void*>(&flash_fwd_kernel<128>);
   else if (p.head_dim == 64)
-    hipLaunchKernelGGL(flash_fwd_kernel<64>, grid, dim3(kThreads), 0, s, p);
+    fn = reinterpret_cast<const void*>(&flash_fwd_kernel<64>);
   else
     return hipErrorInvalidValue;
-  return hipGetLastError();
+  // hipLaunchKernel returns the status of this launch only (not an earlier error).
+  void* args[] = {const_cast<AttnParams*>(&p)};
+  return hipLaunchKernel(fn, grid, dim3(kThreads), args, 0, s);
 }
 
 }  // namespace tsp

@@ -9,10 +9,14 @@
 // Operand panels go from HBM straight into LDS (global_load_lds, no register staging),
 // double-buffered: while the MFMAs consume step k the DMA fills step k+1.
 //
-// LDS layouts.  A [M, K] and "NT" B [N, K] panels are rows of 64 bf16 (128 bytes, eight
-// 16-byte chunks, chunk XOR-swizzled by row mod 8); an MFMA operand is one 16-byte read.
-// "NN" B panels ([K, N] operands: W2 and W_O^(r)^T) keep their natural [64][BN] layout
-// (chunks swizzled the same way) and are read with the gfx950 LDS transpose read
+// LDS layouts.  LDS has 64 banks of 4 bytes, so a byte address maps to bank window
+// position (address mod 256).  A [M, K] and "NT" B [N, K] panels are rows of 64 bf16
+// (128 bytes, eight 16-byte chunks); an MFMA operand is one 16-byte read, 16 lanes of
+// which read 16 consecutive rows at one logical chunk, so the physical chunk is the
+// logical one XOR ((row / 2) mod 8) and those 16 reads hit 16 distinct windows.
+// "NN" B panels ([K, N] operands: W2 and W_O^(r)^T) keep their natural [64][BN] layout,
+// chunk XOR 4 (row mod 4) so that the 4 rows x 64 bytes of a half-wave transpose read
+// cover all 64 banks, and are read with the gfx950 LDS transpose read
 // ds_read_b64_tr_b16: in each 16-lane group, source lane s points at row kbase + s/4,
 // columns base + 4 (s % 4), and lane t receives column base + t of rows kbase..kbase+3,
 // i.e. four consecutive contraction indices of one output column -- no transpose pass
@@ -69,6 +73,10 @@ struct Cfg {
   static_assert(!NN || (BK * NN_RB / 1024) % WAVES == 0, "NN DMA cover");
 };
 
+// Chunk swizzles of the NT and NN panels (physical chunk = logical chunk XOR swz(row)).
+__device__ __forceinline__ int nt_swz(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int nn_swz(int row) { return 4 * (row & 3); }
+
 // NT panel rows [row0, row0 + ROWS) x k [k0, k0 + 64) of a row-major [nrows, ld] matrix
 // into LDS (128-byte rows).  Instruction i of wave w fills rows 8 (i W + w) .. +7.
 template <int ROWS, int WAVES>
@@ -80,7 +88,7 @@ __device__ __forceinline__ void dma_nt(lds_char* dst, const uint16_t* base, int 
     const int blk = i * WAVES + wave;
     const int r = 8 * blk + rsub;
     const int grow = min(row0 + r, nrows - 1);
-    dma16(base + (size_t)grow * ld + k0 + 8 * (pc ^ (r & 7)), dst + blk * 1024);
+    dma16(base + (size_t)grow * ld + k0 + 8 * (pc ^ nt_swz(r)), dst + blk * 1024);
   }
 }
 
@@ -96,7 +104,7 @@ __device__ __forceinline__ void dma_nn(lds_char* dst, const uint16_t* base, int 
     const int blk = i * WAVES + wave;
     const int r = RPI * blk + rsub;
     const int gk = min(k0 + r, krows - 1);
-    const int gn = min(n0 + 8 * (pc ^ (r & 7)), ncols - 8);
+    const int gn = min(n0 + 8 * (pc ^ nn_swz(r)), ncols - 8);
     dma16(base + (size_t)gk * ld + gn, dst + blk * 1024);
   }
 }
@@ -141,8 +149,8 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
   };
 
   // Operand addressing (see the header): A / NT-B row R, chunk 2 s + hh ->
-  //   R_base * 128 + (opa ^ 32 s),  opa = l32 * 128 + 16 (hh ^ (l32 mod 8)).
-  const int opa = l32 * 128 + 16 * (hh ^ (l32 & 7));
+  //   R_base * 128 + (opa ^ 32 s),  opa = l32 * 128 + 16 (hh ^ nt_swz(l32)).
+  const int opa = l32 * 128 + 16 * (hh ^ nt_swz(l32));
   // NN-B transpose reads for output column block j: rows 16 s + 8 hh + t/4 (+4), columns
   // wn WN + 32 j + 16 (g mod 2) + 4 (t mod 4)  ->  16 s NN_RB + (nb ^ 2 (wn WN + 32 j)).
   int nb_lo = 0, nb_hi = 0;
@@ -150,8 +158,8 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
     const int t = lane & 15, g = lane >> 4;
     const int cl = 2 * (g & 1) + ((t & 3) >> 1), half8 = 8 * (t & 1);
     const int r_lo = 8 * (g >> 1) + (t >> 2), r_hi = r_lo + 4;
-    nb_lo = r_lo * C::NN_RB + 16 * (cl ^ (r_lo & 7)) + half8;
-    nb_hi = r_hi * C::NN_RB + 16 * (cl ^ (r_hi & 7)) + half8;
+    nb_lo = r_lo * C::NN_RB + 16 * (cl ^ nn_swz(r_lo)) + half8;
+    nb_hi = r_hi * C::NN_RB + 16 * (cl ^ nn_swz(r_hi)) + half8;
   }
 
   const int nk = P.K / BK;
@@ -283,9 +291,10 @@ hipError_t launch(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   if (p.K <= 0 || p.K % BK != 0) return hipErrorInvalidValue;
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, WGM, WGN, NN, EPI>), dim3(tiles), dim3(C::THREADS), 0,
-                     s, p);
-  return hipGetLastError();
+  // hipLaunchKernel returns the status of this launch only (not an earlier error).
+  void* args[] = {const_cast<GemmParams*>(&p)};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&gemm_kernel<BM, BN, WGM, WGN, NN, EPI>),
+                         dim3(tiles), dim3(C::THREADS), args, 0, s);
 }
 
 }  // namespace

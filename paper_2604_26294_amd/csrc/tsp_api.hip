@@ -98,9 +98,18 @@ tsp_status check_shards(const uint16_t* const* arr, int D) {
     if (st_ != TSP_OK) return st_;             \
   } while (0)
 
-#define TSP_HIP(expr)                          \
-  do {                                         \
-    if ((expr) != hipSuccess) return TSP_ERR_HIP; \
+// HIP error code of the last TSP_ERR_HIP returned on this thread.
+thread_local int g_last_hip_error = 0;
+
+tsp_status hip_failed(hipError_t e) {
+  g_last_hip_error = (int)e;
+  return TSP_ERR_HIP;
+}
+
+#define TSP_HIP(expr)                                \
+  do {                                               \
+    const hipError_t e_ = (expr);                    \
+    if (e_ != hipSuccess) return hip_failed(e_);     \
   } while (0)
 
 
@@ -140,7 +149,8 @@ void timer_end(int kind, long slot, hipStream_t st) {
 #define TSP_LAUNCH(kind, st, expr)                    \
   do {                                                \
     const long slot_ = timer_begin((kind), (st));     \
-    if ((expr) != hipSuccess) return TSP_ERR_HIP;     \
+    const hipError_t e_ = (expr);                     \
+    if (e_ != hipSuccess) return hip_failed(e_);      \
     timer_end((kind), slot_, (st));                   \
   } while (0)
 
@@ -403,5 +413,11 @@ const char* tsp_status_str(tsp_status status) {
 }
 
 int tsp_abi_version(void) { return TSP_ABI_VERSION; }
+
+int tsp_last_hip_error(void) { return g_last_hip_error; }
+
+const char* tsp_hip_error_string(int hip_error) {
+  return hipGetErrorName((hipError_t)hip_error);
+}
 
 }  // extern "C"

@@ -15,6 +15,7 @@ from typing import Sequence
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtsp.so")
 
 TSP_OK = 0
+TSP_ERR_HIP = 7
 STATUS_NAMES = {0: "TSP_OK", 1: "TSP_ERR_NULL", 2: "TSP_ERR_SHAPE", 3: "TSP_ERR_RANK",
                 4: "TSP_ERR_ALIGN", 5: "TSP_ERR_WORKSPACE", 6: "TSP_ERR_UNSUPPORTED",
                 7: "TSP_ERR_HIP"}
@@ -25,7 +26,12 @@ KERNELS = ("gate_up", "down", "qkv", "attn", "oproj")  # TSP_KERNEL_* order
 class TspError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
-        super().__init__(f"{where}: {lib.tsp_status_str(status).decode()}")
+        self.hip_error = lib.tsp_last_hip_error() if status == TSP_ERR_HIP else 0
+        msg = f"{where}: {lib.tsp_status_str(status).decode()}"
+        if status == TSP_ERR_HIP:
+            name = lib.tsp_hip_error_string(self.hip_error).decode()
+            msg += f" ({name}, hipError_t {self.hip_error})"
+        super().__init__(msg)
 
 
 class tsp_shape(ctypes.Structure):
@@ -40,6 +46,11 @@ class tsp_shape(ctypes.Structure):
 def _load() -> ctypes.CDLL:
     if not os.path.exists(_LIB_PATH):
         raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2604_26294_amd.build`")
+    # torch ships its own HIP runtime (libamdhip64.so, SONAME libamdhip64.so.7).  Loading
+    # torch first lets libtsp's libamdhip64.so.7 dependency resolve to that same copy;
+    # loaded the other way round, torch maps a second runtime next to the system one and
+    # the process ends up with two HIP/HSA runtimes, the second of which sees no device.
+    import torch  # noqa: F401
     L = ctypes.CDLL(_LIB_PATH)
     P, VP, SZ, I = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
     SH = ctypes.POINTER(tsp_shape)
@@ -52,6 +63,8 @@ def _load() -> ctypes.CDLL:
         "tsp_workspace_bytes": [SH, I, ctypes.POINTER(ctypes.c_size_t)],
         "tsp_status_str": [I],
         "tsp_abi_version": [],
+        "tsp_last_hip_error": [],
+        "tsp_hip_error_string": [I],
         "tsp_profile_enable": [I],
         "tsp_profile_read": [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
     }
@@ -60,6 +73,7 @@ def _load() -> ctypes.CDLL:
         fn.argtypes = args
         fn.restype = ctypes.c_int
     L.tsp_status_str.restype = ctypes.c_char_p
+    L.tsp_hip_error_string.restype = ctypes.c_char_p
     return L
 
 

@@ -128,3 +128,17 @@ def test_python_binding_raises_named_errors():
     with pytest.raises(T.TspError, match="TSP_ERR_RANK"):
         T.workspace_bytes(_shape(rank=9), T.OP_MLP)
     assert T.workspace_bytes(T.shape_of(TINY), T.OP_MLP) > 0
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Importing the binding before torch must not map a second HIP runtime."""
+    import subprocess
+    import sys
+    code = ("import paper_2604_26294_amd.tsp, torch\n"
+            "maps = open('/proc/self/maps').read().splitlines()\n"
+            "libs = {l.split()[-1] for l in maps if 'libamdhip64' in l}\n"
+            "print(len(libs), sorted(libs))\n")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300,
+                         cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.split()[0] == "1", out.stdout
