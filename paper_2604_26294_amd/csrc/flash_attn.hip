@@ -33,6 +33,8 @@
 // LDS read address is (per-lane base XOR a constant) + an immediate offset.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -71,9 +73,18 @@ struct FaCfg {
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane.
-__device__ __forceinline__ void dma16(const void* src, lds_char* lds) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane: the
+// buffer form, with the address = resource base (scalar) + soff (scalar) + voff (lane).
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff, uint32_t soff,
+                                      lds_char* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds, 16,
+                                           (int)voff, (int)soff, 0, 0);
+}
+
+// Raw buffer resource over [base, base + 4 GiB) (stride 0, no format conversion).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0xffffffff,
+                                           0x00020000);
 }
 
 __device__ __forceinline__ u32x4 lds_read16(const lds_char* p) {
@@ -85,12 +96,15 @@ __device__ __forceinline__ u32x2 lds_read_tr(const lds_char* p) {
       u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p));
 }
 
+template <int N>
+using IC = std::integral_constant<int, N>;
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
   using C = FaCfg<D>;
-  constexpr int KCH = C::KCH, RB = C::ROW_BYTES;
-  // [K slot 0][K slot 1][V slot 0][V slot 1][Q tile]
-  __shared__ __attribute__((aligned(1024))) char L[4 * C::TILE_BYTES];
+  constexpr int KCH = C::KCH, RB = C::ROW_BYTES, TB = C::TILE_BYTES;
+  // [K slot 0][K slot 1][V slot 0][V slot 1]
+  __shared__ __attribute__((aligned(1024))) char L[4 * TB];
   lds_char* Ls = (lds_char*)L;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -116,59 +130,75 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   const int wpos_max = P.q_pos0 + min(wq_first + 31, P.s_loc - 1);
   const int n_keys = P.q_pos0 + min(q0 + kQTile, P.s_loc);  // <= kv_len
   const int n_steps = (n_keys + kStepKeys - 1) / kStepKeys;
-  const float c = P.scale_log2;
 
-  // Q fragments: the B operand of S^T; lane holds Q[qloc][16 ks + 8 hh .. +7].
+  // Q fragments (the B operand of S^T): lane holds Q[qloc][16 ks + 8 hh .. +7], scaled
+  // by c = softmax scale * log2(e) and rounded to bf16 once, so that the score MFMAs
+  // produce base-2 logits directly.
   u32x4 qf[C::KS];
   {
+    const float c = P.scale_log2;
     const uint16_t* qrow = P.Q + (((size_t)b * P.s_loc + (qvalid ? qloc : 0)) * P.heads + head) * D;
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s)
-      qf[s] = qvalid ? ld16(qrow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
+    for (int s = 0; s < C::KS; ++s) {
+      const u32x4 raw = qvalid ? ld16(qrow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        qf[s][e] = pack_bf16x2(bf16_bits_to_f32(raw[e] & 0xffffu) * c,
+                               bf16_bits_to_f32(raw[e] >> 16) * c);
+    }
   }
   const size_t kv_stride = (size_t)P.n_kv * D;  // elements between consecutive keys
   const uint16_t* kbase = P.Kb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
   const uint16_t* vbase = P.Vb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
 
   // DMA geometry: instruction i of wave w fills rows (i kWaves + w) ROWS_PER_DMA + lane / KCH,
-  // physical chunk lane % KCH, with the logical chunk that the swizzle puts there (the
-  // row's low bits, and so the chunk, are the same for every i).  The source of a full
-  // tile is (wave-uniform tile base) + (per-lane byte offset).
+  // physical chunk lane % KCH, with the logical chunk that the tile's swizzle puts there
+  // (the swizzle depends on the row only through bits that are the same for every i).
+  // A full tile's source is (scalar tile base) + (scalar i * row step) + (per-lane 32-bit
+  // offset), so its loads need no vector arithmetic.
   constexpr int kRowStep = kWaves * C::ROWS_PER_DMA;  // rows between instructions
   const int dma_row0 = wave * C::ROWS_PER_DMA + lane / KCH;
   const int dma_col_k = 8 * ((lane % KCH) ^ C::fk(dma_row0));
   const int dma_col_v = 8 * ((lane % KCH) ^ C::fv(dma_row0));
-  const int dma_off_k = 2 * (dma_row0 * (int)kv_stride + dma_col_k);
-  const int dma_off_v = 2 * (dma_row0 * (int)kv_stride + dma_col_v);
-  const int dma_step = 2 * kRowStep * (int)kv_stride;
+  const uint32_t row_bytes = 2u * (uint32_t)kv_stride;
+  const uint32_t dma_off_k = (uint32_t)dma_row0 * row_bytes + 2u * dma_col_k;
+  const uint32_t dma_off_v = (uint32_t)dma_row0 * row_bytes + 2u * dma_col_v;
+  const uint32_t dma_step = (uint32_t)kRowStep * row_bytes;
   // One 128-key tile from HBM into an LDS slot.  In the last tile, rows past the last
   // needed key are clamped to it: they are always masked (keys > every query position
   // of this workgroup) and stay finite, so the P V product never sees garbage.
-  auto dma_tile = [&](const uint16_t* base, int dma_off0, int dma_col, int tile, int slot_off) {
+  auto dma_tile = [&](const uint16_t* base, uint32_t lane_off, int col, int tile,
+                      int slot_off) __attribute__((always_inline)) {
     const int key0 = tile * kStepKeys;
-    const char* tbase = reinterpret_cast<const char*>(base + (size_t)key0 * kv_stride);
+    const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(base + (size_t)key0 * kv_stride);
     lds_char* dst = Ls + slot_off + wave * (kWave * 16);
     if (key0 + kStepKeys <= n_keys) {
 #pragma unroll
       for (int i = 0; i < C::DMA_PER_LANE; ++i)
-        dma16(tbase + dma_off0 + i * dma_step, dst + i * kWaves * (kWave * 16));
+        dma16(rsrc, lane_off, i * dma_step, dst + i * kWaves * (kWave * 16));
     } else {
+      const int last = n_keys - 1 - key0;
 #pragma unroll
       for (int i = 0; i < C::DMA_PER_LANE; ++i) {
-        const int row = min(dma_row0 + i * kRowStep, n_keys - 1 - key0);
-        dma16(tbase + 2 * (row * (int)kv_stride + dma_col), dst + i * kWaves * (kWave * 16));
+        const uint32_t row = (uint32_t)min(dma_row0 + i * kRowStep, last);
+        dma16(rsrc, row * row_bytes + 2u * col, 0u, dst + i * kWaves * (kWave * 16));
       }
     }
   };
-  auto k_off = [](int tile) { return (tile & 1) * C::TILE_BYTES; };
-  auto v_off = [](int tile) { return (2 + (tile & 1)) * C::TILE_BYTES; };
 
-  // K operand: row 64 grp + 32 bb + l32, logical chunk 2 ks + hh  ->  byte
-  //   (64 grp + 32 bb) RB + (ka ^ 32 ks),  ka = l32 RB + 16 (hh ^ f_K(l32)).
-  const int ka = l32 * RB + 16 * (hh ^ C::fk(l32));
-  // Q operand (B of S^T): row 32 wq + l32 of the query tile, same chunk pattern as K.
-  // V^T operand (transpose reads): rows 64 grp + 32 bb + 16 s2 + tr_row (+8 for elements
-  // 4-7), columns 32 eb + tr_col  ->  byte (64 grp + 32 bb + 16 s2) RB + (va or vb)[eb].
+  // LDS read addresses.  Slot offsets and block strides are compile-time immediates;
+  // the per-lane parts below are computed once.
+  //  K operand: row 64 grp + 32 bb + l32, logical chunk 2 ks + hh  ->  byte
+  //    (64 grp + 32 bb) RB + (ka ^ 32 ks),  ka = l32 RB + 16 (hh ^ f_K(l32)).
+  //  V^T operand (transpose reads): rows 64 grp + 32 bb + 16 s2 + tr_row (+8 for elements
+  //    4-7), columns 32 eb + tr_col  ->  byte (64 grp + 32 bb + 16 s2) RB + (va or vb)[eb].
+  const int grp_rows = kGroupKeys * grp * RB;  // this group's half of a tile
+  int kad[C::KS];
+  {
+    const int ka = l32 * RB + 16 * (hh ^ C::fk(l32));
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) kad[ks] = grp_rows + (ka ^ (32 * ks));
+  }
   const int tr_t = lane & 15, tr_g = lane >> 4;
   const int tr_row = ((tr_g >> 1) << 2) + (tr_t >> 2);     // 4 hh + t / 4
   const int tr_col = 16 * (tr_g & 1) + 4 * (tr_t & 3);     // within a 32-column block
@@ -180,43 +210,47 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     const int base_b = (tr_row + 8) * RB + 16 * (cl ^ xb) + half8;
 #pragma unroll
     for (int eb = 0; eb < C::EB; ++eb) {
-      va[eb] = base_a ^ (64 * eb);
-      vb[eb] = base_b ^ (64 * eb);
+      va[eb] = 2 * TB + grp_rows + (base_a ^ (64 * eb));
+      vb[eb] = 2 * TB + grp_rows + (base_b ^ (64 * eb));
     }
   }
-  const int grp_rows = kGroupKeys * grp * RB;  // this group's half of a tile
 
-  auto tile_active = [&](int tile) {
-    return tile >= 0 && tile < n_steps && wave_active &&
-           tile * kStepKeys + kGroupKeys * grp <= wpos_max;
+  auto tile_active = [&](int tile) __attribute__((always_inline)) {
+    return wave_active && tile * kStepKeys + kGroupKeys * grp <= wpos_max;
   };
 
+  // Online-softmax state of this lane's query (shared with its partner lane l ^ 32).
+  // Scores are produced relative to the reference mref (the score MFMAs start from the
+  // accumulator value -mref), so o = sum 2^(s - mref) v and l = sum 2^(s - mref).
+  // mref follows the running maximum lazily: it moves only when a score exceeds it by
+  // more than kRescaleLog2, or to the first visible score of the query; in between,
+  // every probability is bounded by 2^kRescaleLog2 and numerator and denominator share
+  // the stale reference, so the normalised result is unchanged.
   f32x16 o[C::EB];
 #pragma unroll
   for (int eb = 0; eb < C::EB; ++eb)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[eb][e] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  float mref = 0.f, l_run = 0.f;
+  bool seen = false;
+  f32x16 negm;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) negm[e] = 0.f;
   f32x16 sacc[2];   // scores of this group's 64 keys of one tile
   u32x4 pf[2][2];   // bf16 probabilities of one tile (B operands of P V)
 
-  // S^T of tile j: 2 blocks of 32 keys x 32 queries.
-  auto scores = [&](int j) {
-    const lds_char* K = Ls + k_off(j) + grp_rows;
+  // S^T - mref of the tile in slot SLOT: 2 blocks of 32 keys x 32 queries.
+  auto scores = [&](auto slot) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value;
 #pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[bb][e] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-      const lds_char* Kk = K + (ka ^ (32 * ks));
+    for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
-        sacc[bb] = mfma32(lds_read16(Kk + 32 * bb * RB), qf[ks], sacc[bb]);
-    }
+        sacc[bb] = mfma32(lds_read16(Ls + kad[ks] + (S * TB + 32 * bb * RB)), qf[ks],
+                          ks == 0 ? negm : sacc[bb]);
   };
-  // Mask (if tile j crosses the diagonal), online-softmax update, probabilities.
-  auto softmax = [&](int j) {
+  // Mask (if tile j crosses the diagonal), lazy reference update, probabilities.
+  auto softmax = [&](int j) __attribute__((always_inline)) {
     const int kt0 = j * kStepKeys + kGroupKeys * grp;
     if (kt0 + kGroupKeys - 1 > wpos_min) {
       const int rel = qpos - kt0 - 4 * hh;  // key offset in the group tile must be <= this
@@ -233,81 +267,93 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[bb][e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // Lazy rescaling, decided per query (both lanes of a query see the same max): the
-    // running max moves only when a score exceeds it by more than 8 in exp2 units
-    // (always on the first visible tile).  Between moves every probability is bounded
-    // by 2^8 and numerator and denominator share the stale max, so the normalised
-    // result is unchanged while the output rescale is skipped.
-    const bool grow = (mx - m_run) * c > kRescaleLog2;
-    if (__any(grow)) {
-      const float m_new = grow ? fmaxf(m_run, mx) : m_run;
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_use) * c) : 1.f;
-      m_run = m_new;
+    mx = fmaxf(mx, __shfl_xor(mx, 32));  // both lanes of a query decide alike
+    const bool visible = mx != -INFINITY;
+    const bool move = mx > kRescaleLog2 || (!seen && visible);
+    if (__any(move)) {
+      const float shift = move ? mx : 0.f;  // new reference mref + shift
+      const float alpha = move && seen ? __builtin_amdgcn_exp2f(-shift) : (move ? 0.f : 1.f);
+      mref += shift;
+      seen = seen || visible;
       l_run *= alpha;
 #pragma unroll
       for (int eb = 0; eb < C::EB; ++eb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) o[eb][e] *= alpha;
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sacc[bb][e] -= shift;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) negm[e] = -mref;
     }
-    const float mc = (m_run == -INFINITY ? 0.f : m_run) * c;
-    float lsum = 0.f;
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
 #pragma unroll
     for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[bb][8 * s2 + 2 * q], c, -mc));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[bb][8 * s2 + 2 * q + 1], c, -mc));
-          lsum += p0 + p1;
-          pf[bb][s2][q] = pack_bf16x2(p0, p1);
+          const uint32_t pk = pack_bf16x2(__builtin_amdgcn_exp2f(sacc[bb][8 * s2 + 2 * q]),
+                                          __builtin_amdgcn_exp2f(sacc[bb][8 * s2 + 2 * q + 1]));
+          pf[bb][s2][q] = pk;
+          // The denominator sums the same bf16 probabilities the numerator uses.
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk), ones, l_run,
+                                                  false);
         }
-    l_run += lsum;
   };
-  // O^T += V^T P^T for tile j.  k-step (bb, s2) covers keys 32 bb + 16 s2 + [0, 16) of
-  // the group tile; lane half hh feeds keys 4 hh + 0..3 (elements 0-3) and 8 + 4 hh +
-  // 0..3 (4-7), matching the accumulator layout of the scores.
-  auto pv = [&](int j) {
-    const lds_char* V = Ls + v_off(j) + grp_rows;
+  // O^T += V^T P^T for the tile in slot SLOT.  k-step (bb, s2) covers keys 32 bb + 16 s2 +
+  // [0, 16) of the group tile; lane half hh feeds keys 4 hh + 0..3 (elements 0-3) and
+  // 8 + 4 hh + 0..3 (4-7), matching the accumulator layout of the scores.
+  auto pv = [&](auto slot) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value;
 #pragma unroll
     for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        const lds_char* Vr = V + (32 * bb + 16 * s2) * RB;
 #pragma unroll
         for (int eb = 0; eb < C::EB; ++eb) {
-          const u32x2 lo = lds_read_tr(Vr + va[eb]);
-          const u32x2 hi = lds_read_tr(Vr + vb[eb]);
+          const int imm = S * TB + (32 * bb + 16 * s2) * RB;
+          const u32x2 lo = lds_read_tr(Ls + va[eb] + imm);
+          const u32x2 hi = lds_read_tr(Ls + vb[eb] + imm);
           o[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pf[bb][s2], o[eb]);
         }
       }
   };
-
-  dma_tile(kbase, dma_off_k, dma_col_k, 0, k_off(0));
-  dma_tile(vbase, dma_off_v, dma_col_v, 0, v_off(0));
-  for (int j = 0; j < n_steps; ++j) {
+  // One step: tile j (resident in slot SLOT once every wave's DMA has landed) is
+  // consumed while tile j + 1 streams into the other slot.
+  auto step = [&](auto slot, int j) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value;
     wait_dma();
     __syncthreads();  // K and V tile j resident; every wave is past step j-1
     if (j + 1 < n_steps) {
-      dma_tile(kbase, dma_off_k, dma_col_k, j + 1, k_off(j + 1));
-      dma_tile(vbase, dma_off_v, dma_col_v, j + 1, v_off(j + 1));
+      dma_tile(kbase, dma_off_k, dma_col_k, j + 1, (1 - S) * TB);
+      dma_tile(vbase, dma_off_v, dma_col_v, j + 1, (3 - S) * TB);
     }
     if (tile_active(j)) {
-      scores(j);
+      scores(slot);
       softmax(j);
-      pv(j);
+      pv(slot);
     }
+  };
+
+  dma_tile(kbase, dma_off_k, dma_col_k, 0, 0);
+  dma_tile(vbase, dma_off_v, dma_col_v, 0, 2 * TB);
+  for (int j = 0; j < n_steps; j += 2) {
+    step(IC<0>{}, j);
+    if (j + 1 < n_steps) step(IC<1>{}, j + 1);
   }
 
-  // Merge the two key groups: group 1 parks its state in LDS, group 0 combines.
+  // Merge the two key groups: group 1 parks its state in LDS, group 0 combines.  A group
+  // that saw no visible key has l = 0 and takes no part.
   l_run += __shfl_xor(l_run, 32);
+  const float m_own = l_run > 0.f ? mref : -INFINITY;
   __syncthreads();
   float* F = reinterpret_cast<float*>(L);
   const int slot = wq * 64 + lane;
   if (grp == 1) {
-    F[slot] = m_run;
+    F[slot] = m_own;
     F[256 + slot] = l_run;
 #pragma unroll
     for (int eb = 0; eb < C::EB; ++eb)
@@ -317,10 +363,9 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   __syncthreads();
   if (grp == 0 && qvalid) {
     const float m1 = F[slot], l1 = F[256 + slot];
-    const float m = fmaxf(m_run, m1);
-    const float mu = m == -INFINITY ? 0.f : m;
-    const float a0 = __builtin_amdgcn_exp2f((m_run - mu) * c);
-    const float a1 = __builtin_amdgcn_exp2f((m1 - mu) * c);
+    const float m = fmaxf(m_own, m1);  // finite: key 0 is visible to every query
+    const float a0 = __builtin_amdgcn_exp2f(m_own - m);
+    const float a1 = __builtin_amdgcn_exp2f(m1 - m);
     const float inv = 1.f / (l_run * a0 + l1 * a1);
     uint16_t* orow = P.O + (((size_t)b * P.s_loc + qloc) * P.heads + head) * D;
 #pragma unroll
