@@ -248,6 +248,15 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
       for (int bb = 0; bb < 2; ++bb)
         sacc[bb] = mfma32(lds_read16(Ls + kad[ks] + (S * TB + 32 * bb * RB)), qf[ks],
                           ks == 0 ? negm : sacc[bb]);
+    // Issue order: the K fragments run two contraction steps ahead of their MFMAs, so
+    // the LDS latency hides behind the matrix work.
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads
+#pragma unroll
+    for (int i = 0; i < C::KS - 2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMAs
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   };
   // Mask (if tile j crosses the diagonal), lazy reference update, probabilities.
   auto softmax = [&](int j) __attribute__((always_inline)) {
@@ -318,6 +327,21 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
           const u32x2 lo = lds_read_tr(Ls + va[eb] + imm);
           const u32x2 hi = lds_read_tr(Ls + vb[eb] + imm);
           o[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pf[bb][s2], o[eb]);
+        }
+      }
+    // Issue order (this block also holds the exponentials of the tile): the V^T reads
+    // of k-step k+1 and the 16 vector ops that produce its probabilities interleave
+    // with the MFMAs of k-step k, so vector and matrix pipes work at the same time.
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 1);  // LDS reads, k-step 0
+    __builtin_amdgcn_sched_group_barrier(0x002, 16, 1);         // probabilities, k-step 0
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int eb = 0; eb < C::EB; ++eb) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+        if (k < 3) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+          __builtin_amdgcn_sched_group_barrier(0x002, 16 / C::EB, 1);
         }
       }
   };
