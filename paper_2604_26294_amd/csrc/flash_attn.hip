@@ -5,12 +5,17 @@
 // gathered K/V (held resident in a [B, S, n_kv, d] buffer).  The softmax is computed
 // online, one key tile at a time, so the (S_loc x S) score matrix never exists.
 //
-// Work split.  A workgroup owns 128 queries of one head (GQA: head i reads kv head
-// i / g) and has 8 wavefronts, two per SIMD: wavefront w handles queries
-// 32 (w % 4) .. +31 against key group w / 4, i.e. every 128-key tile staged in LDS is
-// consumed as two 64-key halves.  Each group keeps its own running max / sum /
-// output; the groups are merged once at the end.  Key tiles beyond the last query's
-// position are never loaded, and only tiles that cross the diagonal are masked.
+// Work split.  A workgroup owns 256 queries of one head (GQA: head i reads kv head
+// i / g) and one contiguous range of keys; it has 8 wavefronts, two per SIMD, and
+// wavefront w handles queries 32 w .. 32 w + 31 against every key of the range.  The
+// K and V tiles staged in LDS are what each CU pulls through its load path, so the
+// number of queries sharing a tile sets the load traffic per MFMA; 256 halves it
+// against 128-query tiles.  When (query tiles x heads x batch) alone would leave CUs
+// idle, each query tile's keys are split into n_split ranges handled by different
+// workgroups, which write unnormalised partial results (O, reference, sum) that a
+// second kernel combines; with n_split = 1 the workgroup writes bf16 O itself.  Key
+// tiles beyond the last query's position are never loaded, and only tiles that cross
+// a wavefront's diagonal are masked.
 //
 // Scores are computed transposed, S^T = K Q^T, with K as the MFMA A operand and Q
 // (held in registers) as B.  The 32 x 32 accumulator then gives each lane 16 keys of
@@ -18,15 +23,17 @@
 // cross-lane exchange and the row sum none until the end.  The probabilities P^T
 // feed O^T = V^T P^T directly as the B operand (contraction over keys).
 //
-// Schedule.  Per step every wavefront computes the scores of its half of tile j,
-// the softmax and the P V product, while tiles j+1 of K and V stream into the other
-// slot of their two-slot rings.  (Variants that delay P V by a step so the two
-// wavefronts of a SIMD alternate matrix and vector phases measured slower.)
+// Schedule.  Per step every wavefront takes the 128-key tile j in two 64-key halves
+// (scores, softmax, P V each), while tile j+1 of K and V streams into the other slot
+// of the two-slot rings.  (Variants that delay P V by a step so the two wavefronts of
+// a SIMD alternate matrix and vector phases measured slower, as did deeper rings and
+// loads spread across the step.)
 //
-// Data movement.  K and V tiles go from HBM straight into LDS (global_load_lds, no
-// register staging) in their natural [key][d] layout, 16-byte chunks XOR-swizzled by
-// a function of the row chosen per tile kind so that its reads are bank-conflict free.  The V^T operand is read with the gfx950 LDS transpose
-// read (ds_read_b64_tr_b16): in each 16-lane group, source lane s points at row
+// Data movement.  K and V tiles go from HBM straight into LDS (buffer loads with an
+// LDS destination, no register staging) in their natural [key][d] layout, 16-byte
+// chunks XOR-swizzled by a function of the row chosen per tile kind so that its reads
+// are bank-conflict free.  The V^T operand is read with the gfx950 LDS transpose read
+// (ds_read_b64_tr_b16): in each 16-lane group, source lane s points at row
 // kbase + s/4, columns base + 4 (s % 4), and lane t receives column base + t of rows
 // kbase .. kbase+3 -- four consecutive keys of one head-dim column.  Because tile rows
 // are aligned to the row size and the swizzle only touches the in-row offset, every
@@ -43,9 +50,9 @@ namespace {
 
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kQTile = 128;          // queries per workgroup
+constexpr int kQTile = 32 * kWaves;  // queries per workgroup
 constexpr int kStepKeys = 128;       // keys staged per step
-constexpr int kGroupKeys = 64;       // keys per group per step
+constexpr int kHalfKeys = 64;        // keys per sub-step
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (exp2 units)
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -109,27 +116,34 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wave >> 2, wq = wave & 3;
   const int l32 = lane & 31, hh = lane >> 5;
 
+  // Work item -> (batch, head, key range, query tile), query tile fastest, so the
+  // workgroups that share an XCD (contiguous work indices) stream the same keys of the
+  // same head through that XCD's L2.
   const int n_qt = (P.s_loc + kQTile - 1) / kQTile;
-  const int w = xcd_work_index(blockIdx.x, n_qt * P.heads * P.batch);
-  const int b = w / (P.heads * n_qt);
-  const int rem = w - b * (P.heads * n_qt);
-  const int head = rem / n_qt;
-  const int qt = n_qt - 1 - (rem - head * n_qt);  // longest query tiles first
+  const int w = xcd_work_index(blockIdx.x, n_qt * P.n_split * P.heads * P.batch);
+  const int qt = n_qt - 1 - w % n_qt;  // longest query tiles first
+  int rest = w / n_qt;
+  const int split = rest % P.n_split;
+  rest /= P.n_split;
+  const int head = rest % P.heads;
+  const int b = rest / P.heads;
   const int q0 = qt * kQTile;
   const int kvh = P.kv_head0 + head / P.group;
 
-  const int qloc = q0 + 32 * wq + l32;
+  const int qloc = q0 + 32 * wave + l32;
   const bool qvalid = qloc < P.s_loc;
   const int qpos = P.q_pos0 + qloc;
-  const int wq_first = q0 + 32 * wq;
+  const int wq_first = q0 + 32 * wave;
   const bool wave_active = wq_first < P.s_loc;
   const int wpos_min = P.q_pos0 + wq_first;
   const int wpos_max = P.q_pos0 + min(wq_first + 31, P.s_loc - 1);
-  const int n_keys = P.q_pos0 + min(q0 + kQTile, P.s_loc);  // <= kv_len
-  const int n_steps = (n_keys + kStepKeys - 1) / kStepKeys;
+  const int n_keys = P.q_pos0 + min(q0 + kQTile, P.s_loc);  // keys this tile can see
+  const int k_begin = split * P.split_len;                   // a multiple of kStepKeys
+  const int k_end = min(k_begin + P.split_len, n_keys);
+  const int j0 = k_begin / kStepKeys;
+  const int n_steps = k_end > k_begin ? (k_end - k_begin + kStepKeys - 1) / kStepKeys : 0;
 
   // Q fragments (the B operand of S^T): lane holds Q[qloc][16 ks + 8 hh .. +7], scaled
   // by c = softmax scale * log2(e) and rounded to bf16 once, so that the score MFMAs
@@ -164,20 +178,21 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   const uint32_t dma_off_k = (uint32_t)dma_row0 * row_bytes + 2u * dma_col_k;
   const uint32_t dma_off_v = (uint32_t)dma_row0 * row_bytes + 2u * dma_col_v;
   const uint32_t dma_step = (uint32_t)kRowStep * row_bytes;
-  // One 128-key tile from HBM into an LDS slot.  In the last tile, rows past the last
-  // needed key are clamped to it: they are always masked (keys > every query position
-  // of this workgroup) and stay finite, so the P V product never sees garbage.
+  // One 128-key tile from HBM into an LDS slot.  In the last tile of the key range,
+  // rows at or past k_end are clamped to its last key: the range either ends at a
+  // multiple of the tile size or at n_keys, and keys >= n_keys are past every query
+  // of this workgroup, so those rows are always masked and merely need to be finite.
   auto dma_tile = [&](const uint16_t* base, uint32_t lane_off, int col, int tile,
                       int slot_off) __attribute__((always_inline)) {
     const int key0 = tile * kStepKeys;
     const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(base + (size_t)key0 * kv_stride);
     lds_char* dst = Ls + slot_off + wave * (kWave * 16);
-    if (key0 + kStepKeys <= n_keys) {
+    if (key0 + kStepKeys <= k_end) {
 #pragma unroll
       for (int i = 0; i < C::DMA_PER_LANE; ++i)
         dma16(rsrc, lane_off, i * dma_step, dst + i * kWaves * (kWave * 16));
     } else {
-      const int last = n_keys - 1 - key0;
+      const int last = k_end - 1 - key0;
 #pragma unroll
       for (int i = 0; i < C::DMA_PER_LANE; ++i) {
         const uint32_t row = (uint32_t)min(dma_row0 + i * kRowStep, last);
@@ -188,16 +203,15 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 
   // LDS read addresses.  Slot offsets and block strides are compile-time immediates;
   // the per-lane parts below are computed once.
-  //  K operand: row 64 grp + 32 bb + l32, logical chunk 2 ks + hh  ->  byte
-  //    (64 grp + 32 bb) RB + (ka ^ 32 ks),  ka = l32 RB + 16 (hh ^ f_K(l32)).
-  //  V^T operand (transpose reads): rows 64 grp + 32 bb + 16 s2 + tr_row (+8 for elements
-  //    4-7), columns 32 eb + tr_col  ->  byte (64 grp + 32 bb + 16 s2) RB + (va or vb)[eb].
-  const int grp_rows = kGroupKeys * grp * RB;  // this group's half of a tile
+  //  K operand: row 64 h + 32 bb + l32, logical chunk 2 ks + hh  ->  byte
+  //    (64 h + 32 bb) RB + (ka ^ 32 ks),  ka = l32 RB + 16 (hh ^ f_K(l32)).
+  //  V^T operand (transpose reads): rows 64 h + 32 bb + 16 s2 + tr_row (+8 for elements
+  //    4-7), columns 32 eb + tr_col  ->  byte (64 h + 32 bb + 16 s2) RB + (va or vb)[eb].
   int kad[C::KS];
   {
     const int ka = l32 * RB + 16 * (hh ^ C::fk(l32));
 #pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) kad[ks] = grp_rows + (ka ^ (32 * ks));
+    for (int ks = 0; ks < C::KS; ++ks) kad[ks] = ka ^ (32 * ks);
   }
   const int tr_t = lane & 15, tr_g = lane >> 4;
   const int tr_row = ((tr_g >> 1) << 2) + (tr_t >> 2);     // 4 hh + t / 4
@@ -210,13 +224,14 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     const int base_b = (tr_row + 8) * RB + 16 * (cl ^ xb) + half8;
 #pragma unroll
     for (int eb = 0; eb < C::EB; ++eb) {
-      va[eb] = 2 * TB + grp_rows + (base_a ^ (64 * eb));
-      vb[eb] = 2 * TB + grp_rows + (base_b ^ (64 * eb));
+      va[eb] = 2 * TB + (base_a ^ (64 * eb));
+      vb[eb] = 2 * TB + (base_b ^ (64 * eb));
     }
   }
 
-  auto tile_active = [&](int tile) __attribute__((always_inline)) {
-    return wave_active && tile * kStepKeys + kGroupKeys * grp <= wpos_max;
+  // Half h of tile j has keys this wavefront's queries can see.
+  auto half_active = [&](int j, int h) __attribute__((always_inline)) {
+    return wave_active && j * kStepKeys + kHalfKeys * h <= wpos_max;
   };
 
   // Online-softmax state of this lane's query (shared with its partner lane l ^ 32).
@@ -236,18 +251,18 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   f32x16 negm;
 #pragma unroll
   for (int e = 0; e < 16; ++e) negm[e] = 0.f;
-  f32x16 sacc[2];   // scores of this group's 64 keys of one tile
-  u32x4 pf[2][2];   // bf16 probabilities of one tile (B operands of P V)
+  f32x16 sacc[2];   // scores of 64 keys of one tile
+  u32x4 pf[2][2];   // bf16 probabilities of those keys (B operands of P V)
 
-  // S^T - mref of the tile in slot SLOT: 2 blocks of 32 keys x 32 queries.
-  auto scores = [&](auto slot) __attribute__((always_inline)) {
-    constexpr int S = decltype(slot)::value;
+  // S^T - mref of half H of the tile in slot SLOT: 2 blocks of 32 keys x 32 queries.
+  auto scores = [&](auto slot, auto half) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value, H = decltype(half)::value;
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
-        sacc[bb] = mfma32(lds_read16(Ls + kad[ks] + (S * TB + 32 * bb * RB)), qf[ks],
-                          ks == 0 ? negm : sacc[bb]);
+        sacc[bb] = mfma32(lds_read16(Ls + kad[ks] + (S * TB + (kHalfKeys * H + 32 * bb) * RB)),
+                          qf[ks], ks == 0 ? negm : sacc[bb]);
     // Issue order: the K fragments run two contraction steps ahead of their MFMAs, so
     // the LDS latency hides behind the matrix work.
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads
@@ -258,11 +273,11 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   };
-  // Mask (if tile j crosses the diagonal), lazy reference update, probabilities.
-  auto softmax = [&](int j) __attribute__((always_inline)) {
-    const int kt0 = j * kStepKeys + kGroupKeys * grp;
-    if (kt0 + kGroupKeys - 1 > wpos_min) {
-      const int rel = qpos - kt0 - 4 * hh;  // key offset in the group tile must be <= this
+  // Mask (if the keys from kt0 on cross the diagonal), lazy reference update,
+  // probabilities.
+  auto softmax = [&](int kt0) __attribute__((always_inline)) {
+    if (kt0 + kHalfKeys - 1 > wpos_min) {
+      const int rel = qpos - kt0 - 4 * hh;  // key offset in the half tile must be <= this
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
@@ -312,26 +327,27 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
                                                   false);
         }
   };
-  // O^T += V^T P^T for the tile in slot SLOT.  k-step (bb, s2) covers keys 32 bb + 16 s2 +
-  // [0, 16) of the group tile; lane half hh feeds keys 4 hh + 0..3 (elements 0-3) and
-  // 8 + 4 hh + 0..3 (4-7), matching the accumulator layout of the scores.
-  auto pv = [&](auto slot) __attribute__((always_inline)) {
-    constexpr int S = decltype(slot)::value;
+  // O^T += V^T P^T for half H of the tile in slot SLOT.  k-step (bb, s2) covers keys
+  // 32 bb + 16 s2 + [0, 16) of the half tile; lane half hh feeds keys 4 hh + 0..3
+  // (elements 0-3) and 8 + 4 hh + 0..3 (4-7), matching the accumulator layout of the
+  // scores.
+  auto pv = [&](auto slot, auto half) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value, H = decltype(half)::value;
 #pragma unroll
     for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
 #pragma unroll
         for (int eb = 0; eb < C::EB; ++eb) {
-          const int imm = S * TB + (32 * bb + 16 * s2) * RB;
+          const int imm = S * TB + (kHalfKeys * H + 32 * bb + 16 * s2) * RB;
           const u32x2 lo = lds_read_tr(Ls + va[eb] + imm);
           const u32x2 hi = lds_read_tr(Ls + vb[eb] + imm);
           o[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pf[bb][s2], o[eb]);
         }
       }
-    // Issue order (this block also holds the exponentials of the tile): the V^T reads
-    // of k-step k+1 and the 16 vector ops that produce its probabilities interleave
-    // with the MFMAs of k-step k, so vector and matrix pipes work at the same time.
+    // Issue order (this block also holds the exponentials): the V^T reads of k-step
+    // k+1 and the 16 vector ops that produce its probabilities interleave with the
+    // MFMAs of k-step k, so vector and matrix pipes work at the same time.
     __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 1);  // LDS reads, k-step 0
     __builtin_amdgcn_sched_group_barrier(0x002, 16, 1);         // probabilities, k-step 0
 #pragma unroll
@@ -345,85 +361,138 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
         }
       }
   };
+  auto half_step = [&](auto slot, auto half, int j) __attribute__((always_inline)) {
+    constexpr int H = decltype(half)::value;
+    if (half_active(j, H)) {
+      scores(slot, half);
+      softmax(j * kStepKeys + kHalfKeys * H);
+      pv(slot, half);
+    }
+  };
   // One step: tile j (resident in slot SLOT once every wave's DMA has landed) is
   // consumed while tile j + 1 streams into the other slot.
   auto step = [&](auto slot, int j) __attribute__((always_inline)) {
     constexpr int S = decltype(slot)::value;
     wait_dma();
     __syncthreads();  // K and V tile j resident; every wave is past step j-1
-    if (j + 1 < n_steps) {
+    if (j + 1 < j0 + n_steps) {
       dma_tile(kbase, dma_off_k, dma_col_k, j + 1, (1 - S) * TB);
       dma_tile(vbase, dma_off_v, dma_col_v, j + 1, (3 - S) * TB);
     }
-    if (tile_active(j)) {
-      scores(slot);
-      softmax(j);
-      pv(slot);
-    }
+    half_step(slot, IC<0>{}, j);
+    half_step(slot, IC<1>{}, j);
   };
 
-  dma_tile(kbase, dma_off_k, dma_col_k, 0, 0);
-  dma_tile(vbase, dma_off_v, dma_col_v, 0, 2 * TB);
-  for (int j = 0; j < n_steps; j += 2) {
-    step(IC<0>{}, j);
-    if (j + 1 < n_steps) step(IC<1>{}, j + 1);
+  if (n_steps > 0) {
+    dma_tile(kbase, dma_off_k, dma_col_k, j0, 0);
+    dma_tile(vbase, dma_off_v, dma_col_v, j0, 2 * TB);
+  }
+  for (int t = 0; t < n_steps; t += 2) {
+    step(IC<0>{}, j0 + t);
+    if (t + 1 < n_steps) step(IC<1>{}, j0 + t + 1);
   }
 
-  // Merge the two key groups: group 1 parks its state in LDS, group 0 combines.  A group
-  // that saw no visible key has l = 0 and takes no part.
   l_run += __shfl_xor(l_run, 32);
-  const float m_own = l_run > 0.f ? mref : -INFINITY;
-  __syncthreads();
-  float* F = reinterpret_cast<float*>(L);
-  const int slot = wq * 64 + lane;
-  if (grp == 1) {
-    F[slot] = m_own;
-    F[256 + slot] = l_run;
+  if (!qvalid) return;
+  const size_t row = ((size_t)b * P.s_loc + qloc) * P.heads + head;
+  if (P.n_split == 1) {
+    // Whole key range: normalise and write bf16 O (key 0 is visible to every query,
+    // so l > 0).
+    const float inv = 1.f / l_run;
+    uint16_t* orow = P.O + row * D;
 #pragma unroll
     for (int eb = 0; eb < C::EB; ++eb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) F[(2 + 16 * eb + e) * 256 + slot] = o[eb][e];
-  }
-  __syncthreads();
-  if (grp == 0 && qvalid) {
-    const float m1 = F[slot], l1 = F[256 + slot];
-    const float m = fmaxf(m_own, m1);  // finite: key 0 is visible to every query
-    const float a0 = __builtin_amdgcn_exp2f(m_own - m);
-    const float a1 = __builtin_amdgcn_exp2f(m1 - m);
-    const float inv = 1.f / (l_run * a0 + l1 * a1);
-    uint16_t* orow = P.O + (((size_t)b * P.s_loc + qloc) * P.heads + head) * D;
-#pragma unroll
-    for (int eb = 0; eb < C::EB; ++eb)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float v[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int e = 4 * g + r;
-          v[r] = (o[eb][e] * a0 + F[(2 + 16 * eb + e) * 256 + slot] * a1) * inv;
-        }
+      for (int g = 0; g < 4; ++g)
         *reinterpret_cast<u32x2*>(orow + 32 * eb + 8 * g + 4 * hh) =
-            u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-      }
+            u32x2{pack_bf16x2(o[eb][4 * g] * inv, o[eb][4 * g + 1] * inv),
+                  pack_bf16x2(o[eb][4 * g + 2] * inv, o[eb][4 * g + 3] * inv)};
+  } else {
+    // Partial result of this key range: unnormalised O, reference (base-2 logit units;
+    // -inf if no key of the range is visible) and sum.
+    const size_t prow = (size_t)split * P.part_rows + row;
+    float* po = P.part_o + prow * D;
+#pragma unroll
+    for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4*>(po + 32 * eb + 8 * g + 4 * hh) =
+            f32x4{o[eb][4 * g], o[eb][4 * g + 1], o[eb][4 * g + 2], o[eb][4 * g + 3]};
+    if (hh == 0)
+      *reinterpret_cast<float2*>(P.part_ml + 2 * prow) =
+          float2{l_run > 0.f ? mref : -INFINITY, l_run};
   }
+}
+
+// Merges the n_split partial results of each (batch, query, head) row: with
+// M = max_c m_c, O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as bf16.
+// One thread per 4 consecutive head-dim columns of a row.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams P) {
+  constexpr int TPR = D / 4;  // threads per row
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long row = idx / TPR;
+  const int c4 = (int)(idx % TPR);
+  if (row >= P.part_rows) return;
+  float m = -INFINITY;
+  for (int c = 0; c < P.n_split; ++c) m = fmaxf(m, P.part_ml[2 * (c * P.part_rows + row)]);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float l = 0.f;
+  for (int c = 0; c < P.n_split; ++c) {
+    const long long prow = c * P.part_rows + row;
+    const float mc = P.part_ml[2 * prow];
+    if (mc == -INFINITY) continue;  // no visible key in this range
+    const float wgt = __builtin_amdgcn_exp2f(mc - m);
+    l += wgt * P.part_ml[2 * prow + 1];
+    acc += wgt * *reinterpret_cast<const f32x4*>(P.part_o + prow * D + 4 * c4);
+  }
+  const float inv = 1.f / l;
+  *reinterpret_cast<u32x2*>(P.O + row * D + 4 * c4) =
+      u32x2{pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
 }
 
 }  // namespace
 
+int attn_split_count(long long batch, int s_loc, int heads, int q_pos0, int* split_len) {
+  const int n_qt = (s_loc + kQTile - 1) / kQTile;
+  const long long base = batch * heads * (long long)n_qt;
+  const int max_keys = q_pos0 + s_loc;  // keys seen by the last query tile
+  // Enough workgroups for every CU, never fewer than 4 key tiles per range, at most 8
+  // ranges.
+  int n = base > 0 ? (int)((kAttnTargetWorkgroups + base - 1) / base) : 1;
+  n = max(1, min(n, min(8, max_keys / (4 * kStepKeys))));
+  int len = (max(max_keys, 1) + n - 1) / n;
+  len = (len + kStepKeys - 1) / kStepKeys * kStepKeys;
+  n = (max(max_keys, 1) + len - 1) / len;
+  if (split_len) *split_len = len;
+  return n;
+}
+
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
   if (p.batch <= 0 || p.s_loc <= 0 || p.heads <= 0) return hipSuccess;
-  const int n_qt = (p.s_loc + kQTile - 1) / kQTile;
-  const dim3 grid(n_qt * p.heads * p.batch);
-  const void* fn;
-  if (p.head_dim == 128)
-    fn = reinterpret_cast<const void*>(&flash_fwd_kernel<128>);
-  else if (p.head_dim == 64)
-    fn = reinterpret_cast<const void*>(&flash_fwd_kernel<64>);
-  else
+  if (p.n_split < 1 || p.split_len <= 0 || p.split_len % kStepKeys != 0 ||
+      (long long)p.n_split * p.split_len < (long long)p.q_pos0 + p.s_loc ||
+      (p.n_split > 1 && (!p.part_o || !p.part_ml)))
     return hipErrorInvalidValue;
+  const int n_qt = (p.s_loc + kQTile - 1) / kQTile;
+  const dim3 grid(n_qt * p.n_split * p.heads * p.batch);
+  const void* fn;
+  const void* combine;
+  if (p.head_dim == 128) {
+    fn = reinterpret_cast<const void*>(&flash_fwd_kernel<128>);
+    combine = reinterpret_cast<const void*>(&attn_combine_kernel<128>);
+  } else if (p.head_dim == 64) {
+    fn = reinterpret_cast<const void*>(&flash_fwd_kernel<64>);
+    combine = reinterpret_cast<const void*>(&attn_combine_kernel<64>);
+  } else {
+    return hipErrorInvalidValue;
+  }
   // hipLaunchKernel returns the status of this launch only (not an earlier error).
   void* args[] = {const_cast<AttnParams*>(&p)};
-  return hipLaunchKernel(fn, grid, dim3(kThreads), args, 0, s);
+  const hipError_t e = hipLaunchKernel(fn, grid, dim3(kThreads), args, 0, s);
+  if (e != hipSuccess || p.n_split == 1) return e;
+  const long long threads = p.part_rows * (long long)(p.head_dim / 4);
+  return hipLaunchKernel(combine, dim3((unsigned)((threads + 255) / 256)), dim3(256), args, 0, s);
 }
 
 }  // namespace tsp

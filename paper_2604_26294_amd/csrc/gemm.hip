@@ -7,7 +7,8 @@
 // One workgroup = WGM x WGN wavefronts (8 by default: two per SIMD); each wavefront owns
 // a (BM/WGM) x (BN/WGN) block of C as 32 x 32 MFMA tiles.  K advances in steps of 64.
 // Operand panels go from HBM straight into LDS (global_load_lds, no register staging),
-// double-buffered: while the MFMAs consume step k the DMA fills step k+1.
+// in a ring of STAGES slots: while the MFMAs consume step k the DMA fills the steps
+// up to k + STAGES - 1.
 //
 // LDS layouts.  LDS has 64 banks of 4 bytes, so a byte address maps to bank window
 // position (address mod 256).  A [M, K] and "NT" B [N, K] panels are rows of 64 bf16
@@ -40,7 +41,13 @@ enum { EPI_SWIGLU = 0, EPI_ACC = 1, EPI_QKV = 2 };
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) char lds_char;
 
-__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most N of this wavefront's operand loads are still in flight (loads
+// complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_dma() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 // 16 bytes per lane from global memory straight into LDS at lds + 16 * lane.
 __device__ __forceinline__ void dma16(const void* src, lds_char* lds) {
@@ -56,7 +63,7 @@ __device__ __forceinline__ u32x2 lds_read_tr(const lds_char* p) {
       u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p));
 }
 
-template <int BM, int BN, int WGM, int WGN, bool NN, int EPI>
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
 struct Cfg {
   static constexpr int WAVES = WGM * WGN, THREADS = kWave * WAVES;
   static constexpr int WM = BM / WGM, WN = BN / WGN;
@@ -66,6 +73,11 @@ struct Cfg {
   static constexpr int A_BYTES = BM * BK * 2;
   static constexpr int B_BYTES = NB * BK * 2;                  // NT [NB][64] or NN [64][BN]
   static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int LDS_BYTES = STAGES * STAGE;
+  // Operand load instructions one wavefront issues per stage.
+  static constexpr int LOADS = BM / 8 / WAVES + (NN ? BK * (BN * 2) / 1024 / WAVES : NB / 8 / WAVES);
+  static_assert(STAGES >= 2 && LDS_BYTES <= 160 * 1024, "LDS ring");
+  static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
   static constexpr int NN_RB = BN * 2;                         // NN panel row bytes
   static_assert(!(NN && EPI == EPI_SWIGLU), "SwiGLU operands are [N, K]");
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
@@ -109,11 +121,11 @@ __device__ __forceinline__ void dma_nn(lds_char* dst, const uint16_t* base, int 
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, bool NN, int EPI>
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
 __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParams P) {
-  using C = Cfg<BM, BN, WGM, WGN, NN, EPI>;
+  using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
   constexpr int TM = C::TM, TN = C::TN, TNB = C::TNB;
-  __shared__ __attribute__((aligned(1024))) char L[2 * C::STAGE];
+  __shared__ __attribute__((aligned(1024))) char L[C::LDS_BYTES];
   lds_char* Ls = (lds_char*)L;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -162,13 +174,28 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
     nb_hi = r_hi * C::NN_RB + 16 * (cl ^ nn_swz(r_hi)) + half8;
   }
 
+  // STAGES-deep ring: stage k lives in slot k mod STAGES.  Step kt waits for stage kt
+  // (the loads of up to STAGES - 2 later stages stay in flight), then refills the slot
+  // that step kt - 1 read with stage kt + STAGES - 1.
   const int nk = P.K / BK;
-  dma_stage(0, 0);
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < nk) dma_stage(st, st * BK);
   for (int kt = 0; kt < nk; ++kt) {
-    wait_dma();
+    const int ahead = min(STAGES - 2, nk - 1 - kt);  // later stages already issued
+    if constexpr (STAGES >= 4) {
+      if (ahead >= 2) wait_dma<C::LOADS * 2>();
+      else if (ahead == 1) wait_dma<C::LOADS>();
+      else wait_dma<0>();
+    } else if constexpr (STAGES == 3) {
+      if (ahead >= 1) wait_dma<C::LOADS>();
+      else wait_dma<0>();
+    } else {
+      wait_dma<0>();
+    }
     __syncthreads();  // stage kt resident; every wave is past step kt-1
-    if (kt + 1 < nk) dma_stage((kt + 1) & 1, (kt + 1) * BK);
-    const lds_char* SA = Ls + (kt & 1) * C::STAGE;
+    if (kt + STAGES - 1 < nk) dma_stage((kt + STAGES - 1) % STAGES, (kt + STAGES - 1) * BK);
+    const lds_char* SA = Ls + (kt % STAGES) * C::STAGE;
     const lds_char* SB = SA + C::A_BYTES;
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
@@ -193,6 +220,21 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
 #pragma unroll
         for (int j = 0; j < TNB; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
     }
+    // Issue order: the operand reads of k-substep s+1 are spread between the MFMAs of
+    // substep s, so LDS latency hides behind matrix work.
+    {
+      constexpr int R = TM + (NN ? 2 : 1) * TNB;  // LDS reads per substep
+      constexpr int M = TM * TNB;                 // MFMAs per substep
+      static_assert(R <= M, "one read per MFMA at most");
+      __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+#pragma unroll
+      for (int s = 0; s < BK / 16; ++s)
+#pragma unroll
+        for (int i = 0; i < M; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if (s + 1 < BK / 16 && i < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+    }
   }
   __syncthreads();  // operand stages are free for the epilogue
 
@@ -204,7 +246,7 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
   constexpr int EST = C::WN + 4;  // staging row stride in floats
   constexpr int CPR = C::WN / 4;  // 4-column chunks per row
   constexpr int PER_LANE = 32 * CPR / kWave;
-  static_assert(C::WAVES * 32 * EST * 4 <= 2 * C::STAGE, "epilogue staging fits");
+  static_assert(C::WAVES * 32 * EST * 4 <= C::LDS_BYTES, "epilogue staging fits");
   float* E = reinterpret_cast<float*>(L) + wave * 32 * EST;
   const int ncol0 = n0 + wn * C::WN;
 #pragma unroll
@@ -285,15 +327,15 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, bool NN, int EPI>
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
 hipError_t launch(const GemmParams& p, hipStream_t s) {
-  using C = Cfg<BM, BN, WGM, WGN, NN, EPI>;
+  using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   if (p.K <= 0 || p.K % BK != 0) return hipErrorInvalidValue;
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   // hipLaunchKernel returns the status of this launch only (not an earlier error).
   void* args[] = {const_cast<GemmParams*>(&p)};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&gemm_kernel<BM, BN, WGM, WGN, NN, EPI>),
+  return hipLaunchKernel(reinterpret_cast<const void*>(&gemm_kernel<BM, BN, WGM, WGN, NN, EPI, STAGES>),
                          dim3(tiles), dim3(C::THREADS), args, 0, s);
 }
 
@@ -305,15 +347,15 @@ hipError_t launch(const GemmParams& p, hipStream_t s) {
 // 1536) in 256 x 192 tiles makes exactly 256; down / O-proj (N = h = 4096) in
 // 256 x 256 tiles makes 512.
 hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s) {
-  return launch<128, 128, 2, 4, false, EPI_SWIGLU>(p, s);
+  return launch<128, 128, 2, 4, false, EPI_SWIGLU, 2>(p, s);
 }
 
 hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s) {
-  return launch<256, 256, 2, 4, true, EPI_ACC>(p, s);
+  return launch<256, 256, 2, 4, true, EPI_ACC, 2>(p, s);
 }
 
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s) {
-  return launch<256, 192, 4, 2, false, EPI_QKV>(p, s);
+  return launch<256, 192, 4, 2, false, EPI_QKV, 2>(p, s);
 }
 
 }  // namespace tsp

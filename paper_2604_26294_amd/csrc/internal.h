@@ -74,7 +74,25 @@ struct AttnParams {
   int q_pos0;       // global position of local query 0
   int kv_len;       // number of readable keys: (p + 1) * S_loc
   float scale_log2; // softmax scale * log2(e)
+  // Key-range split (attn_split_count): each query tile's keys [0, n) are processed in
+  // ranges [c split_len, (c + 1) split_len), c < n_split.  With n_split > 1 the ranges
+  // write partial results -- part_o [n_split][part_rows][d] fp32 (unnormalised O) and
+  // part_ml [n_split][part_rows][2] fp32 (reference, sum) with part_rows = B S_loc H_s
+  // -- which a second kernel merges into O.
+  int n_split;
+  int split_len;
+  long long part_rows;
+  float* part_o;
+  float* part_ml;
 };
+
+// Workgroups the attention kernel aims to launch: one per CU of an MI355X.
+constexpr int kAttnTargetWorkgroups = 256;
+
+// Number of key ranges (and their length, a multiple of the key tile, in *split_len)
+// for one rank's attention: enough (query tile, head, batch, range) work items to fill
+// the GPU.  Depends on the shape only, so workspace sizes are known up front.
+int attn_split_count(long long batch, int s_loc, int heads, int q_pos0, int* split_len);
 
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s);
 

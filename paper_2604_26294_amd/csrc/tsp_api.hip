@@ -70,7 +70,25 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
 //   ATTN:  Q [M, H_s d] bf16, A [M, H_s d] bf16
 //   LAYER: u [M, h] bf16, then max(MLP, ATTN)
 size_t ws_mlp(const Dims& d) { return align_up((size_t)d.M * d.fs_pad * 2); }
-size_t ws_attn(const Dims& d) { return 2 * align_up((size_t)d.M * d.hs * d.d * 2); }
+// Attention workspace: Q of the current shard and the attention output A (bf16
+// [M, H_s d] each), then the key-range partials when the shard's attention is split.
+struct AttnWs {
+  size_t q, a, po, pml, total;  // byte offsets and total size
+  int n_split, split_len;
+};
+AttnWs attn_ws(const Dims& d) {
+  AttnWs w;
+  w.n_split = tsp::attn_split_count(d.B, d.s_loc, d.hs, d.p * d.s_loc, &w.split_len);
+  const size_t rows = (size_t)d.M * d.hs;
+  const size_t part = w.n_split > 1 ? (size_t)w.n_split * rows : 0;
+  w.q = 0;
+  w.a = align_up(rows * d.d * 2);
+  w.po = w.a + align_up(rows * d.d * 2);
+  w.pml = w.po + align_up(part * d.d * 4);
+  w.total = w.pml + align_up(part * 2 * 4);
+  return w;
+}
+size_t ws_attn(const Dims& d) { return attn_ws(d).total; }
 size_t ws_layer(const Dims& d) {
   const size_t a = ws_mlp(d), b = ws_attn(d);
   return align_up((size_t)d.M * d.h * 2) + (a > b ? a : b);
@@ -221,10 +239,12 @@ GemmParams qkv_params(const Dims& d, const uint16_t* x, const uint16_t* shard, i
 // first shard instead of zero / the old Y; `u_out` receives bf16(Y) after the last.
 tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
                     uint16_t* kb, uint16_t* vb, float* y, int accumulate,
-                    const uint16_t* residual, uint16_t* u_out, uint16_t* q_ws,
-                    uint16_t* a_ws, hipStream_t st) {
+                    const uint16_t* residual, uint16_t* u_out, char* ws, hipStream_t st) {
   const int qd = d.hs * d.d, kd = d.ks * d.d;
   const float log2e = 1.4426950408889634f;
+  const AttnWs aw = attn_ws(d);
+  uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + aw.q);
+  uint16_t* a_ws = reinterpret_cast<uint16_t*>(ws + aw.a);
   for (int r = 0; r < d.D; ++r) {
     GemmParams g = qkv_params(d, x, wa[r], r, q_ws, kb, vb, true);
     TSP_LAUNCH(TSP_KERNEL_QKV, st, tsp::launch_gemm_qkv(g, st));
@@ -245,6 +265,11 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     ap.q_pos0 = d.p * d.s_loc;
     ap.kv_len = (d.p + 1) * d.s_loc;
     ap.scale_log2 = d.scale * log2e;
+    ap.n_split = aw.n_split;
+    ap.split_len = aw.split_len;
+    ap.part_rows = (long long)d.M * d.hs;
+    ap.part_o = reinterpret_cast<float*>(ws + aw.po);
+    ap.part_ml = reinterpret_cast<float*>(ws + aw.pml);
     TSP_LAUNCH(TSP_KERNEL_ATTN, st, tsp::launch_flash_attn(ap, st));
 
     GemmParams o = {};
@@ -337,10 +362,8 @@ tsp_status tsp_attn_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
   TSP_TRY(check_ptr(ws));
   if (ws_bytes < ws_attn(d)) return TSP_ERR_WORKSPACE;
   if (d.M == 0) return TSP_OK;
-  uint16_t* q_ws = static_cast<uint16_t*>(ws);
-  uint16_t* a_ws = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + ws_attn(d) / 2);
-  return run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, accumulate, nullptr, nullptr, q_ws,
-                  a_ws, stream);
+  return run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, accumulate, nullptr, nullptr,
+                  static_cast<char*>(ws), stream);
 }
 
 tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
@@ -364,10 +387,8 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
   char* base = static_cast<char*>(ws);
   uint16_t* u_ws = reinterpret_cast<uint16_t*>(base);
   char* rest = base + align_up((size_t)d.M * d.h * 2);
-  uint16_t* q_ws = reinterpret_cast<uint16_t*>(rest);
-  uint16_t* a_ws = reinterpret_cast<uint16_t*>(rest + ws_attn(d) / 2);
   // u = x + Attn(x): Y starts from x at the first shard; the last shard also writes bf16(u).
-  TSP_TRY(run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, 0, x_loc, u_ws, q_ws, a_ws, stream));
+  TSP_TRY(run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, 0, x_loc, u_ws, rest, stream));
   // y = u + MLP(bf16 u): the MLP accumulates onto Y, which holds u.
   return run_mlp(d, u_ws, w_gate, w_up, w_down, y_loc, 1, reinterpret_cast<uint16_t*>(rest),
                  stream);
