@@ -251,8 +251,8 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   f32x16 negm;
 #pragma unroll
   for (int e = 0; e < 16; ++e) negm[e] = 0.f;
-  f32x16 sacc[2];   // scores of 64 keys of one tile
-  u32x4 pf[2][2];   // bf16 probabilities of those keys (B operands of P V)
+  f32x16 sc[2][2];  // scores of the two 64-key halves of a tile, 2 blocks of 32 keys each
+  u32x4 pf[2][2][2];  // bf16 probabilities of the halves (B operands of P V)
 
   // S^T - mref of half H of the tile in slot SLOT: 2 blocks of 32 keys x 32 queries.
   auto scores = [&](auto slot, auto half) __attribute__((always_inline)) {
@@ -261,10 +261,12 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
-        sacc[bb] = mfma32(lds_read16(Ls + kad[ks] + (S * TB + (kHalfKeys * H + 32 * bb) * RB)),
-                          qf[ks], ks == 0 ? negm : sacc[bb]);
-    // Issue order: the K fragments run two contraction steps ahead of their MFMAs, so
-    // the LDS latency hides behind the matrix work.
+        sc[H][bb] = mfma32(lds_read16(Ls + kad[ks] + (S * TB + (kHalfKeys * H + 32 * bb) * RB)),
+                           qf[ks], ks == 0 ? negm : sc[H][bb]);
+  };
+  // Issue order for a block holding only score MFMAs: K fragments two contraction steps
+  // ahead of their MFMAs, so the LDS latency hides behind the matrix work.
+  auto order_scores = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads
 #pragma unroll
     for (int i = 0; i < C::KS - 2; ++i) {
@@ -273,9 +275,9 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   };
-  // Mask (if the keys from kt0 on cross the diagonal), lazy reference update,
-  // probabilities.
-  auto softmax = [&](int kt0) __attribute__((always_inline)) {
+  // Causal mask of half H (keys from kt0) where it crosses this wavefront's diagonal.
+  auto mask = [&](auto half, int kt0) __attribute__((always_inline)) {
+    constexpr int H = decltype(half)::value;
     if (kt0 + kHalfKeys - 1 > wpos_min) {
       const int rel = qpos - kt0 - 4 * hh;  // key offset in the half tile must be <= this
 #pragma unroll
@@ -283,15 +285,23 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kofs = 32 * bb + 8 * (e >> 2) + (e & 3);
-          sacc[bb][e] = kofs > rel ? -INFINITY : sacc[bb][e];
+          sc[H][bb][e] = kofs > rel ? -INFINITY : sc[H][bb][e];
         }
     }
-    float mx = sacc[0][0];
+  };
+  auto rowmax = [&](auto half) __attribute__((always_inline)) {
+    constexpr int H = decltype(half)::value;
+    float mx = sc[H][0][0];
 #pragma unroll
     for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[bb][e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));  // both lanes of a query decide alike
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[H][bb][e]);
+    return fmaxf(mx, __shfl_xor(mx, 32));  // both lanes of a query decide alike
+  };
+  // Lazy reference update for half H with row max mx (relative to mref).  Must follow
+  // every P V product already issued: it rescales o.
+  auto rescale = [&](auto half, float mx) __attribute__((always_inline)) {
+    constexpr int H = decltype(half)::value;
     const bool visible = mx != -INFINITY;
     const bool move = mx > kRescaleLog2 || (!seen && visible);
     if (__any(move)) {
@@ -307,10 +317,14 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[bb][e] -= shift;
+        for (int e = 0; e < 16; ++e) sc[H][bb][e] -= shift;
 #pragma unroll
       for (int e = 0; e < 16; ++e) negm[e] = -mref;
     }
+  };
+  // Probabilities of half H (bf16) and their row sum.
+  auto probs = [&](auto half) __attribute__((always_inline)) {
+    constexpr int H = decltype(half)::value;
     typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
     const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
 #pragma unroll
@@ -319,9 +333,9 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
       for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const uint32_t pk = pack_bf16x2(__builtin_amdgcn_exp2f(sacc[bb][8 * s2 + 2 * q]),
-                                          __builtin_amdgcn_exp2f(sacc[bb][8 * s2 + 2 * q + 1]));
-          pf[bb][s2][q] = pk;
+          const uint32_t pk = pack_bf16x2(__builtin_amdgcn_exp2f(sc[H][bb][8 * s2 + 2 * q]),
+                                          __builtin_amdgcn_exp2f(sc[H][bb][8 * s2 + 2 * q + 1]));
+          pf[H][bb][s2][q] = pk;
           // The denominator sums the same bf16 probabilities the numerator uses.
           l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk), ones, l_run,
                                                   false);
@@ -342,12 +356,14 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
           const int imm = S * TB + (kHalfKeys * H + 32 * bb + 16 * s2) * RB;
           const u32x2 lo = lds_read_tr(Ls + va[eb] + imm);
           const u32x2 hi = lds_read_tr(Ls + vb[eb] + imm);
-          o[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pf[bb][s2], o[eb]);
+          o[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pf[H][bb][s2], o[eb]);
         }
       }
-    // Issue order (this block also holds the exponentials): the V^T reads of k-step
-    // k+1 and the 16 vector ops that produce its probabilities interleave with the
-    // MFMAs of k-step k, so vector and matrix pipes work at the same time.
+  };
+  // Issue order for a block holding the probabilities of a half and its P V product:
+  // the V^T reads of k-step k+1 and the 16 vector ops that produce its probabilities
+  // interleave with the MFMAs of k-step k.
+  auto order_probs_pv = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 1);  // LDS reads, k-step 0
     __builtin_amdgcn_sched_group_barrier(0x002, 16, 1);         // probabilities, k-step 0
 #pragma unroll
@@ -361,13 +377,52 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
         }
       }
   };
-  auto half_step = [&](auto slot, auto half, int j) __attribute__((always_inline)) {
-    constexpr int H = decltype(half)::value;
-    if (half_active(j, H)) {
-      scores(slot, half);
-      softmax(j * kStepKeys + kHalfKeys * H);
-      pv(slot, half);
+  // Both halves of tile j (slot SLOT), in an order that gives each vector phase an
+  // independent matrix phase to overlap with:
+  //   scores(0) | max(0) | rescale(0) | scores(1) + probs(0) | mask(1) |
+  //   P V(0) + max(1) | rescale(1) | probs(1) + P V(1)
+  auto both_halves = [&](auto slot, int j) __attribute__((always_inline)) {
+    constexpr IC<0> h0{};
+    constexpr IC<1> h1{};
+    const int kt0 = j * kStepKeys, kt1 = kt0 + kHalfKeys;
+    scores(slot, h0);
+    order_scores();
+    mask(h0, kt0);
+    rescale(h0, rowmax(h0));
+    scores(slot, h1);
+    probs(h0);
+    // 16 score MFMAs and their 16 K reads with the 64 vector ops of probs(0).
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 2);
+#pragma unroll
+    for (int i = 0; i < C::KS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 2);
+      if (i + 2 < C::KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 2);
+      __builtin_amdgcn_sched_group_barrier(0x002, 64 / C::KS, 2);
     }
+    // Keep probs(0) in this block: without a use here the compiler sinks it past the
+    // mask branch, next to P V(0), where it has no independent MFMAs to overlap with.
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) asm volatile("" ::"v"(pf[0][bb][s2]));
+    asm volatile("" ::"v"(l_run));
+    mask(h1, kt1);
+    pv(slot, h0);
+    const float mx1 = rowmax(h1);
+    // P V(0): its V^T reads run a k-step ahead; the row max of half 1 fills in.
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 3);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int eb = 0; eb < C::EB; ++eb) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 3);
+        if (k < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 3);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 3);
+      }
+    rescale(h1, mx1);
+    probs(h1);
+    pv(slot, h1);
+    order_probs_pv();
   };
   // One step: tile j (resident in slot SLOT once every wave's DMA has landed) is
   // consumed while tile j + 1 streams into the other slot.
@@ -379,8 +434,9 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
       dma_tile(kbase, dma_off_k, dma_col_k, j + 1, (1 - S) * TB);
       dma_tile(vbase, dma_off_v, dma_col_v, j + 1, (3 - S) * TB);
     }
-    half_step(slot, IC<0>{}, j);
-    half_step(slot, IC<1>{}, j);
+    // A half past every query of the wavefront (only in its last tile) is fully masked
+    // and leaves the softmax state unchanged, so one code path serves every tile.
+    if (half_active(j, 0)) both_halves(slot, j);
   };
 
   if (n_steps > 0) {
