@@ -2,13 +2,18 @@
 """Throughput of one rank's TSP layer forward (attention + gated MLP) on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--rank P]
-                    [--no-cpu-baseline]
+                    [--no-cpu-baseline] [--rank-sweep]
 
 A step is one ``tsp_layer_rank_fwd`` call: all D attention shard steps (Q/K/V
 projection, causal flash attention, output projection) and all D ring MLP steps
 (gate+up with SwiGLU, down projection) for the rank's S/D tokens.  Inputs, weight
 shards and the K/V rows of the earlier ranks (the modelled all-gather) are resident
 in HBM before timing starts.  Prints one JSON line on stdout; progress goes to stderr.
+
+Besides the layer call the line reports the attention-only and MLP-only entry points
+timed separately ("blocks"), the algorithmic HBM bytes of a step and the bandwidth they
+imply ("hbm"), the paper's non-causal F_layer / D for reference, and with --rank-sweep
+the layer time of every rank of the group and the max/min imbalance.
 """
 from __future__ import annotations
 
@@ -109,6 +114,44 @@ def cpu_baseline(wl, x_bits, w_bits, rows: int):
                        f"beforehand, untimed")}
 
 
+def time_calls(fn, steps, warmup):
+    """Average ms of fn() over `steps` calls on the current stream, after `warmup`."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        fn()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def rank_sweep(wl, x_bits, w_bits, steps, warmup):
+    """Layer time of every rank of the group (each with its own K/V prefix pre-filled)."""
+    import torch
+
+    from paper_2604_26294_amd.flops import paper_layer_flops, rank_algorithmic_bytes, rank_flops
+    from paper_2604_26294_amd.harness import RankProblem
+    rows = []
+    for p in range(wl.degree):
+        w = wl.at_rank(p)
+        prob = RankProblem(w, x_bits, w_bits, p)
+        prob.prefill_kv()
+        torch.cuda.synchronize()
+        ms = time_calls(prob.layer, steps, warmup)
+        rows.append({"rank": p, "ms": round(ms, 4),
+                     "tflops": round(rank_flops(w).total / (ms * 1e-3) / 1e12, 2)})
+        log(f"rank {p}: {ms:.3f} ms/step")
+        del prob
+        torch.cuda.empty_cache()
+    times = [r["ms"] for r in rows]
+    return {"ranks": rows, "imbalance_max_over_min": round(max(times) / min(times), 4)}
+
+
 def main(argv=None):
     from paper_2604_26294_amd.workloads import BY_NAME, L7B_64K
 
@@ -120,6 +163,8 @@ def main(argv=None):
     ap.add_argument("--rank", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=128)
+    ap.add_argument("--rank-sweep", action="store_true",
+                    help="also time the layer of every rank of the group")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="run one plain device copy of MB MiB first (a known-size reference "
                          "for hardware byte counters)")
@@ -134,7 +179,7 @@ def main(argv=None):
 
     from paper_2604_26294_amd import inputs as I
     from paper_2604_26294_amd import tsp as T
-    from paper_2604_26294_amd.flops import rank_flops
+    from paper_2604_26294_amd.flops import paper_layer_flops, rank_algorithmic_bytes, rank_flops
     from paper_2604_26294_amd.harness import RankProblem
 
     wl = BY_NAME[args.workload]
@@ -197,6 +242,20 @@ def main(argv=None):
                 "traffic": measured_traffic(wl, dom),
                 "flops_per_launch": kf[dom], "avg_launch_ms": dom_avg}
 
+    # The attention and MLP entry points on their own (same rank, same buffers).
+    ms_attn = time_calls(prob.attn_fwd, args.steps, 2)
+    ms_mlp = time_calls(prob.mlp, args.steps, 2)
+    blocks = {
+        "attn": {"ms": round(ms_attn, 4), "flops": rf.attn,
+                 "tflops": round(rf.attn / (ms_attn * 1e-3) / 1e12, 2)},
+        "mlp": {"ms": round(ms_mlp, 4), "flops": rf.mlp,
+                "tflops": round(rf.mlp / (ms_mlp * 1e-3) / 1e12, 2)},
+    }
+    nbytes = rank_algorithmic_bytes(wl)
+    hbm = {"algorithmic_bytes": nbytes, "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+           "frac_of_peak": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+           "note": "all D weight shards + K/V prefix once + x (bf16) + Y (fp32), per step"}
+
     out = {
         "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
@@ -208,10 +267,15 @@ def main(argv=None):
                    "layout": "contiguous"},
         "pct_of_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "flops_per_step": rf.total,
+        "paper_flops_per_rank_noncausal": paper_layer_flops(wl) / wl.degree,
         "roofline": roofline,
         "kernels": kernels,
+        "blocks": blocks,
+        "hbm": hbm,
         "cpu_baseline": None,
     }
+    if args.rank_sweep:
+        out["rank_sweep"] = rank_sweep(wl, x_bits, w_bits, max(3, args.steps // 4), 2)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, x_bits, w_bits, args.cpu_rows)
     print(json.dumps(out), flush=True)

@@ -73,3 +73,13 @@ def rank_weight_bytes(wl: Workload) -> int:
     qd = wl.n_heads * wl.head_dim
     kvd = wl.n_kv_heads * wl.head_dim
     return 2 * (2 * qd * h + 2 * kvd * h + 3 * wl.ffn * h)
+
+
+def rank_algorithmic_bytes(wl: Workload, p: int | None = None) -> int:
+    """HBM bytes one rank's layer forward must move at least once: every weight shard
+    (bf16), the K/V prefix of keys [0, (p + 1) S_loc) for all kv heads (bf16, read once),
+    the local input x (bf16, read) and the fp32 output Y (written)."""
+    p = wl.rank if p is None else p
+    kv = 2 * wl.batch * (p + 1) * wl.s_loc * wl.n_kv_heads * wl.head_dim * 2
+    xy = wl.batch * wl.s_loc * wl.hidden * (2 + 4)
+    return rank_weight_bytes(wl) + kv + xy

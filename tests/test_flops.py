@@ -52,3 +52,17 @@ def test_causal_pairs_brute_force():
             brute = sum(1 for i in range(s_loc) for j in range((p + 1) * s_loc)
                         if j <= p * s_loc + i)
             assert F.causal_pairs(s_loc, p) == brute
+
+
+def test_algorithmic_bytes_closed_form():
+    """Weights of all D shards once, (2 h n_h d + 2 h n_kv d + 3 h F) x 2 B; the K/V prefix
+    once, 2 B (p+1) S_loc n_kv d x 2 B; x (bf16) and Y (fp32)."""
+    from paper_2604_26294_amd.workloads import L7B_8K
+    for wl, kv_mb in ((L7B_8K, 134.2), (L7B_64K, 1073.7)):
+        total = F.rank_algorithmic_bytes(wl)
+        weights = 2 * (2 * 4096 * 4096 + 2 * 4096 * 4096 + 3 * 4096 * 11008)
+        assert F.rank_weight_bytes(wl) == weights
+        assert weights / 1e6 == pytest.approx(404.8, abs=0.05)
+        kv = 2 * wl.batch * (wl.rank + 1) * wl.s_loc * wl.n_kv_heads * wl.head_dim * 2
+        assert kv / 1e6 == pytest.approx(kv_mb, abs=0.05)
+        assert total == weights + kv + wl.s_loc * 4096 * 6
