@@ -10,7 +10,8 @@ tests absorb that in their tolerance.
 
 Conventions (paper, Sections 3-4):
   x        [B, S, h]  layer input;  rank p holds the contiguous chunk
-           x[:, p*S_loc:(p+1)*S_loc], S_loc = S/D.
+           x[:, p*S_loc:(p+1)*S_loc], S_loc = S/D (or, in the zigzag layout,
+           the rows at zigzag_positions(S, D, p)).
   W_Q      [n_h d, h], W_K / W_V [n_kv d, h]; Q = X W_Q^T etc.
   W_O      [h, n_h d]; the attention block returns Flatten(A) W_O^T.
   W1 (gate), W3 (up), W2 (down)  [F, h]; MLP(u) = (SiLU(u W1^T) * (u W3^T)) W2.
@@ -220,6 +221,95 @@ def layer_rank(x_chunks, attn_shards, w1_shards, w3_shards, w2_shards, p, n_head
     kv = [gather_kv(x_chunks, attn_shards[r], hsh, ksh, head_dim) for r in range(degree)]
     x_loc = x_chunks[p]
     attn = attn_rank(x_loc, attn_shards, kv, p, n_heads, n_kv_heads, head_dim, scale)
+    u = x_loc + attn
+    mlp = mlp_rank(u, w1_shards, w3_shards, w2_shards, p)
+    return {"attn": attn, "u": u, "mlp": mlp, "y": u + mlp}
+
+
+# ---------------------------------------------------------------------------
+# O2, zigzag layout: Algorithm 1 as printed (load-balanced causal partition).
+# ---------------------------------------------------------------------------
+
+def zigzag_positions(seq, degree, p):
+    """Global positions of rank p's local rows in the zigzag layout.
+
+    The sequence is cut into 2D chunks of S_c = S / (2D) tokens; rank p holds chunk p
+    followed by chunk 2D - 1 - p (Section 2 on causal load balancing; Algorithm 1's
+    S_c = S_loc / 2), so its local rows are [chunk p; chunk 2D-1-p]."""
+    s_c = seq // (2 * degree)
+    return np.concatenate([p * s_c + np.arange(s_c),
+                           (2 * degree - 1 - p) * s_c + np.arange(s_c)])
+
+
+def gather_kv_zigzag(x_shards, packed, heads_per_shard, kv_heads_per_shard, head_dim):
+    """Shard r's K and V over ranks holding zigzag shards: the all-gather
+    concatenates the ranks' rows in rank order, then ZigZagReorder puts every row
+    back at its global position, giving sequence order [B, S, K_s, d]."""
+    degree = len(x_shards)
+    parts = [kv_project(xs, packed, heads_per_shard, kv_heads_per_shard, head_dim)
+             for xs in x_shards]
+    k_cat = np.concatenate([k for k, _ in parts], axis=1)
+    v_cat = np.concatenate([v for _, v in parts], axis=1)
+    seq = k_cat.shape[1]
+    # row n of the gathered tensor came from global position order[n]
+    order = np.concatenate([zigzag_positions(seq, degree, q) for q in range(degree)])
+    k_hat = np.empty_like(k_cat)
+    v_hat = np.empty_like(v_cat)
+    k_hat[:, order] = k_cat
+    v_hat[:, order] = v_cat
+    return k_hat, v_hat
+
+
+def attn_rank_zigzag(x_loc, shards, kv_gathered, p, n_heads, n_kv_heads, head_dim,
+                     scale=None):
+    """TSP attention on rank p with zigzag shards (Algorithm 1 as printed).
+
+    For r = 0 .. D-1: unpack shard r and project the local Q; with S_c = S_loc / 2,
+    s1 = (p+1) S_c and s2 = (2D - p) S_c, split Q along the sequence into its two
+    halves, attend causally from the first half to the first s1 gathered keys and
+    from the second half to the first s2 (each query block bottom-right aligned to
+    its key block), concatenate the two outputs along the sequence into A, and
+    accumulate Flatten(A) W_O^(r)^T into Y, which starts at zero.
+    """
+    degree = len(shards)
+    hs_heads = n_heads // degree
+    ks_heads = n_kv_heads // degree
+    g = n_heads // n_kv_heads
+    d = head_dim
+    sc = default_scale(d, scale)
+    b_, s_loc, h = x_loc.shape
+    s_c = s_loc // 2
+    s1 = (p + 1) * s_c
+    s2 = (2 * degree - p) * s_c
+    y = np.zeros((b_, s_loc, h), dtype=np.float64)
+    for r in range(degree):
+        wq, _, _, wo_t = unpack_attn_shard(shards[r], hs_heads, ks_heads, d)
+        q = (x_loc @ wq.T).reshape(b_, s_loc, hs_heads, d)
+        k_hat, v_hat = kv_gathered[r]
+        a = np.empty((b_, s_loc, hs_heads, d), dtype=np.float64)
+        for b in range(b_):
+            for i in range(hs_heads):
+                kh = i // g
+                q1, q2 = q[b, :s_c, i], q[b, s_c:, i]
+                o1 = causal_attention_core(q1, k_hat[b, :s1, kh], v_hat[b, :s1, kh],
+                                           s1 - s_c, sc)
+                o2 = causal_attention_core(q2, k_hat[b, :s2, kh], v_hat[b, :s2, kh],
+                                           s2 - s_c, sc)
+                a[b, :, i] = np.concatenate([o1, o2], axis=0)
+        y += a.reshape(b_, s_loc, hs_heads * d) @ wo_t
+    return y
+
+
+def layer_rank_zigzag(x_shards, attn_shards, w1_shards, w3_shards, w2_shards, p, n_heads,
+                      n_kv_heads, head_dim, scale=None):
+    """One rank's layer forward with zigzag shards: u = x_loc + TSP-Attn(x),
+    y = u + TSP-MLP(u) (the MLP is row-local, so its ring is unchanged)."""
+    degree = len(attn_shards)
+    hsh, ksh = n_heads // degree, n_kv_heads // degree
+    kv = [gather_kv_zigzag(x_shards, attn_shards[r], hsh, ksh, head_dim)
+          for r in range(degree)]
+    x_loc = x_shards[p]
+    attn = attn_rank_zigzag(x_loc, attn_shards, kv, p, n_heads, n_kv_heads, head_dim, scale)
     u = x_loc + attn
     mlp = mlp_rank(u, w1_shards, w3_shards, w2_shards, p)
     return {"attn": attn, "u": u, "mlp": mlp, "y": u + mlp}

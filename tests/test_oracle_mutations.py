@@ -65,7 +65,31 @@ def _mlp_rank_skips_last_step(x_loc, w1s, w3s, w2s, p):
     return y
 
 
+_orig_zz_pos = O.zigzag_positions
+_orig_zz_gather = O.gather_kv_zigzag
+
+
+def _zigzag_halves_swapped(seq, degree, p):             # [chunk 2D-1-p; chunk p]
+    pos = _orig_zz_pos(seq, degree, p)
+    half = pos.shape[0] // 2
+    return np.concatenate([pos[half:], pos[:half]])
+
+
+def _zigzag_reorder_dropped(x_shards, packed, hs, ks, d):  # gathered rows left in rank order
+    parts = [O.kv_project(xs, packed, hs, ks, d) for xs in x_shards]
+    return (np.concatenate([k for k, _ in parts], axis=1),
+            np.concatenate([v for _, v in parts], axis=1))
+
+
+def _zigzag_plain_prefix(x_loc, shards, kv, p, n_heads, n_kv, d, scale=None):
+    # treats the zigzag shard like a contiguous chunk (one causal call, offset p S_loc)
+    return _orig_attn_rank(x_loc, shards, kv, p, n_heads, n_kv, d, scale)
+
+
 MUTATIONS = {
+    "zigzag_halves_swapped": ("zigzag_positions", _zigzag_halves_swapped),
+    "zigzag_reorder_dropped": ("gather_kv_zigzag", _zigzag_reorder_dropped),
+    "zigzag_as_contiguous": ("attn_rank_zigzag", _zigzag_plain_prefix),
     "mask_excludes_diagonal": ("causal_probs", _probs_strict_mask),
     "mask_dropped": ("causal_probs", _probs_no_mask),
     "scale_dropped": ("causal_probs", _probs_no_scale),
@@ -87,6 +111,8 @@ PINS = [
     (P.test_softmax_rows_sum_to_one_and_first_query_sees_key0, ()),
     (P.test_linearity_in_output_projections, ()),
     (P.test_mlp_ring_order_and_row_permutation_invariance, ()),
+    (P.test_zigzag_partition_and_causal_balance, ()),
+    (P.test_zigzag_fold_equals_unsharded, (4, 2, 2)),
 ]
 
 

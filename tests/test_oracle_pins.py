@@ -291,3 +291,44 @@ def test_attn_rank_row_subset_matches_full_rank():
     rows = [0, 5, 15]
     sub = O.attn_rank(chunks[1], attn_sh, kv, 1, 4, 4, 4, rows=rows)
     assert _rel(sub, full[:, rows]) < 1e-13
+
+
+# ---------------------------------------------------------------------------
+# Zigzag layout (Algorithm 1 as printed)
+# ---------------------------------------------------------------------------
+
+def test_zigzag_partition_and_causal_balance():
+    """Rank p holds chunks p and 2D-1-p of 2D equal chunks; every rank then has the
+    same number of unmasked (query, key) pairs, (2D-1) S_c^2 + S_c (S_c + 1)."""
+    for degree in (1, 2, 3, 4, 8):
+        s_c = 5
+        seq = 2 * degree * s_c
+        chunks = np.arange(seq).reshape(2 * degree, s_c)
+        seen = []
+        for p in range(degree):
+            pos = O.zigzag_positions(seq, degree, p)
+            assert np.array_equal(pos, np.concatenate([chunks[p], chunks[2 * degree - 1 - p]]))
+            seen.append(pos)
+            pairs = int(np.sum(pos + 1))          # query at position t sees t + 1 keys
+            assert pairs == (2 * degree - 1) * s_c * s_c + s_c * (s_c + 1)
+        assert np.array_equal(np.sort(np.concatenate(seen)), np.arange(seq))
+
+
+@pytest.mark.parametrize("n_heads,n_kv,degree", [(2, 2, 1), (2, 2, 2), (4, 2, 2), (8, 4, 4),
+                                                 (4, 4, 4)])
+def test_zigzag_fold_equals_unsharded(n_heads, n_kv, degree):
+    """Every zigzag rank's block outputs are the unsharded layer's rows at that rank's
+    positions (the property Algorithm 1's split bounds s1, s2 and ZigZagReorder exist
+    to guarantee)."""
+    wl = _micro(n_heads, n_kv, degree, seq=16, d=4, ffn=24, batch=2)
+    x, w = _inputs(wl)
+    ref = O.layer_full(x, w, n_heads, n_kv)
+    attn_sh, w1s, w3s, w2s = _shards(wl, w)
+    seq = x.shape[1]
+    parts = np.arange(seq).reshape(2 * degree, seq // (2 * degree))
+    pos = [np.concatenate([parts[p], parts[2 * degree - 1 - p]]) for p in range(degree)]
+    shards = [x[:, pos[p]] for p in range(degree)]
+    for p in range(degree):
+        o = O.layer_rank_zigzag(shards, attn_sh, w1s, w3s, w2s, p, n_heads, n_kv, wl.head_dim)
+        for key in ("attn", "mlp", "y"):
+            assert _rel(o[key], ref[key][:, pos[p]]) < 1e-12, (p, key)
