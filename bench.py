@@ -2,7 +2,7 @@
 """Throughput of one rank's TSP layer forward (attention + gated MLP) on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--rank P]
-                    [--no-cpu-baseline] [--rank-sweep]
+                    [--layout contiguous|zigzag] [--no-cpu-baseline] [--rank-sweep]
 
 A step is one ``tsp_layer_rank_fwd`` call: all D attention shard steps (Q/K/V
 projection, causal flash attention, output projection) and all D ring MLP steps
@@ -162,6 +162,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=L7B_64K.name, choices=sorted(BY_NAME))
     ap.add_argument("--rank", type=int, default=None)
+    ap.add_argument("--layout", default="contiguous", choices=["contiguous", "zigzag"],
+                    help="sequence layout of the ranks (zigzag: Algorithm 1 as printed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=128)
     ap.add_argument("--rank-sweep", action="store_true",
@@ -183,7 +185,7 @@ def main(argv=None):
     from paper_2604_26294_amd.flops import paper_layer_flops, rank_algorithmic_bytes, rank_flops
     from paper_2604_26294_amd.harness import RankProblem
 
-    wl = BY_NAME[args.workload]
+    wl = BY_NAME[args.workload].with_layout(1 if args.layout == "zigzag" else 0)
     if args.rank is not None:
         wl = wl.at_rank(args.rank)
     torch.cuda.set_device(0)
@@ -265,7 +267,7 @@ def main(argv=None):
         "config": {"workload": wl.name, "batch": wl.batch, "seq": wl.seq, "hidden": wl.hidden,
                    "ffn": wl.ffn, "n_heads": wl.n_heads, "n_kv_heads": wl.n_kv_heads,
                    "head_dim": wl.head_dim, "degree": wl.degree, "rank": wl.rank,
-                   "layout": "contiguous"},
+                   "layout": wl.layout_name},
         "pct_of_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "flops_per_step": rf.total,
         "paper_flops_per_rank_noncausal": paper_layer_flops(wl) / wl.degree,
@@ -277,7 +279,7 @@ def main(argv=None):
     }
     if args.rank_sweep:
         out["rank_sweep"] = rank_sweep(wl, x_bits, w_bits, max(3, args.steps // 4), 2)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and wl.layout == 0:  # the sampled oracle leg is contiguous-only
         out["cpu_baseline"] = cpu_baseline(wl, x_bits, w_bits, args.cpu_rows)
     print(json.dumps(out), flush=True)
     return 0

@@ -4,8 +4,13 @@
  *
  * Paper: "Folding Tensor and Sequence Parallelism for Memory-Efficient Transformer
  * Training & Inference" (arXiv 2604.26294).  A TSP group of D ranks shards both the
- * sequence and the layer weights over one device axis: rank p holds the contiguous
- * token chunk [p*S/D, (p+1)*S/D) and, over D steps, applies every weight shard to it.
+ * sequence and the layer weights over one device axis: rank p holds S/D tokens and,
+ * over D steps, applies every weight shard to them.  The tokens of rank p are
+ *   layout 0 (contiguous): positions [p*S_loc, (p+1)*S_loc), S_loc = S/D;
+ *   layout 1 (zigzag, Algorithm 1 as printed): with S_c = S_loc/2, chunk p followed by
+ *     chunk 2D-1-p, i.e. local row t < S_c at position p*S_c + t and local row
+ *     t >= S_c at position (2D-1-p)*S_c + (t - S_c).
+ * "The position of local row t" below means this mapping.
  *
  *   - Attention (Algorithm 1): for r = 0..D-1 the rank projects Q, K, V of its chunk
  *     with shard r, attends causally against the full-sequence K/V of shard r (the
@@ -17,9 +22,11 @@
  *
  * On one GPU the exchanges are modelled by resident buffers: every weight shard is
  * already in device memory (the broadcast / ring hand-off has happened), and the
- * K/V buffer holds the full sequence (the all-gather).  Each attention call WRITES
- * its own chunk's K/V rows for every shard and READS the causal prefix
- * [0, (p+1)*S/D); rows of earlier ranks are the caller's (see tsp_kv_rank_fwd).
+ * K/V buffer holds the full sequence in sequence order (the all-gather, reordered).
+ * Each attention call WRITES the K/V rows at its own tokens' positions for every shard
+ * and READS the keys its queries can see: [0, (p+1)*S_loc) for layout 0,
+ * [0, (2D-p)*S_c) for layout 1; the other ranks' rows are the caller's (see
+ * tsp_kv_rank_fwd).
  *
  * Conventions shared by every entry point
  *   - All tensor arguments are DEVICE pointers to dense row-major arrays.  bf16
@@ -40,8 +47,8 @@
  *     the HIP error.
  *   - Results are deterministic: no atomics, fixed reduction orders.
  *   - Supported: head_dim in {64, 128}; hidden, ffn/degree and head_dim multiples
- *     of 8; layout 0 (contiguous chunks).  Anything else valid returns
- *     TSP_ERR_UNSUPPORTED.
+ *     of 8; layout 0 or 1 (layout 1 needs S divisible by 2D, else TSP_ERR_SHAPE).
+ *     Anything else valid returns TSP_ERR_UNSUPPORTED.
  */
 #ifndef TSP_H
 #define TSP_H
@@ -83,7 +90,7 @@ typedef struct tsp_shape {
   int32_t head_dim;     /* d */
   int32_t degree;       /* D: TSP degree (number of shards) */
   int32_t rank;         /* p: this rank */
-  int32_t layout;       /* 0 = contiguous chunks (rank p owns [p*S_loc, (p+1)*S_loc)) */
+  int32_t layout;       /* 0 = contiguous chunks, 1 = zigzag (see the top of this file) */
   float softmax_scale;  /* <= 0 selects 1/sqrt(head_dim) */
 } tsp_shape;
 
@@ -103,26 +110,30 @@ tsp_status tsp_mlp_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                             void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* This rank's contribution to the sequence-wise K/V all-gather of every shard
- * (Algorithm 1, the local K and V projections): for r = 0..D-1 writes
- *   k_buf[b, p*S_loc + t, r*n_kv/D + j, :] = (x_loc[b, t] W_K^(r)^T) head j, bf16
- * and the same for V.  Used to fill the K/V rows of ranks other than the caller.
+ * (Algorithm 1, the local K and V projections, with ZigZagReorder folded into the
+ * addresses): for r = 0..D-1 writes
+ *   k_buf[b, pos(t), r*n_kv/D + j, :] = (x_loc[b, t] W_K^(r)^T) head j, bf16
+ * with pos(t) the position of local row t, and the same for V.  Used to fill the K/V
+ * rows of ranks other than the caller.
  *   x_loc      [B, S_loc, h] bf16
  *   w_attn[r]  packed shard r, [(2*n_h/D + 2*n_kv/D) * d, h] bf16: rows
  *              [W_Q^(r) ; W_K^(r) ; W_V^(r) ; W_O^(r)^T] (the packed broadcast buffer)
- *   k_buf, v_buf [B, S, n_kv, d] bf16   rows [p*S_loc, (p+1)*S_loc) written */
+ *   k_buf, v_buf [B, S, n_kv, d] bf16   rows at this rank's positions written */
 tsp_status tsp_kv_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                            const uint16_t* const* w_attn, uint16_t* k_buf, uint16_t* v_buf,
                            hipStream_t stream);
 
-/* TSP attention of rank p (Algorithm 1, contiguous chunks): for r = 0..D-1,
+/* TSP attention of rank p (Algorithm 1): for r = 0..D-1,
  *   Q = X W_Q^(r)^T; K, V rows of this rank written into k_buf / v_buf;
- *   A = causal softmax(Q K^T * scale) V over keys [0, (p+1)*S_loc), where local query
- *       row t sits at global position p*S_loc + t and sees keys j <= p*S_loc + t;
+ *   A = causal softmax(Q K^T * scale) V, where local query row t at position pos(t)
+ *       sees keys j <= pos(t) (layout 1: the two CausalAttn calls of Algorithm 1, the
+ *       first half of the rows against keys [0, s1 = (p+1)*S_c), the second against
+ *       [0, s2 = (2D-p)*S_c));
  *   Y (+)= Flatten(A) W_O^(r)^T   (fp32, shards accumulated in order r = 0..D-1).
  * Q, K, V, the softmax probabilities and A are rounded to bf16 for the matrix cores.
  *   x_loc, w_attn as for tsp_kv_rank_fwd;  k_buf, v_buf [B, S, n_kv, d] bf16: this
- *   rank's rows are written, rows [0, p*S_loc) must already hold ranks 0..p-1's K/V,
- *   rows at or beyond (p+1)*S_loc are never read.
+ *   rank's rows are written; every other row its queries can see must already hold
+ *   the other ranks' K/V; rows past the last visible key are never read.
  *   y_loc [B, S_loc, h] fp32, overwritten (accumulate == 0) or added to. */
 tsp_status tsp_attn_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                              const uint16_t* const* w_attn, uint16_t* k_buf, uint16_t* v_buf,

@@ -1,8 +1,10 @@
 // Causal flash attention of one TSP rank's query chunk (gfx950, bf16 MFMA).
 //
-// Algorithm 1's CausalAttn for contiguous chunks: local query t of rank p sits at
-// global position q_pos0 + t (q_pos0 = p S_loc) and sees keys j <= q_pos0 + t of the
-// gathered K/V (held resident in a [B, S, n_kv, d] buffer).  The softmax is computed
+// Algorithm 1's CausalAttn calls: the rank's local queries form one segment of
+// consecutive global positions (contiguous chunks: rank p's rows start at p S_loc) or
+// two (the zigzag shard's chunks p and 2D-1-p, the two CausalAttn calls with bounds
+// s1 and s2); a query at position t sees keys j <= t of the gathered K/V (held
+// resident, in sequence order, in a [B, S, n_kv, d] buffer).  The softmax is computed
 // online, one key tile at a time, so the (S_loc x S) score matrix never exists.
 //
 // Work split.  A workgroup owns 256 queries of one head (GQA: head i reads kv head
@@ -120,26 +122,32 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 
   // Work item -> (batch, head, key range, query tile), query tile fastest, so the
   // workgroups that share an XCD (contiguous work indices) stream the same keys of the
-  // same head through that XCD's L2.
-  const int n_qt = (P.s_loc + kQTile - 1) / kQTile;
+  // same head through that XCD's L2.  Query tiles run over the segments' rows, last
+  // segment (latest positions, most keys) first and, within one, last tile first.
+  const int nt0 = (P.seg_rows[0] + kQTile - 1) / kQTile;
+  const int nt1 = P.n_seg > 1 ? (P.seg_rows[1] + kQTile - 1) / kQTile : 0;
+  const int n_qt = nt0 + nt1;
   const int w = xcd_work_index(blockIdx.x, n_qt * P.n_split * P.heads * P.batch);
-  const int qt = n_qt - 1 - w % n_qt;  // longest query tiles first
+  const int order = w % n_qt;
+  const int seg = order < nt1 ? 1 : 0;
+  const int qt = seg == 1 ? nt1 - 1 - order : nt0 - 1 - (order - nt1);
   int rest = w / n_qt;
   const int split = rest % P.n_split;
   rest /= P.n_split;
   const int head = rest % P.heads;
   const int b = rest / P.heads;
-  const int q0 = qt * kQTile;
+  const int q0 = qt * kQTile;                    // first query of the tile, within its segment
+  const int seg_rows = P.seg_rows[seg], row0 = P.seg_row0[seg], pos0 = P.seg_pos0[seg];
   const int kvh = P.kv_head0 + head / P.group;
 
-  const int qloc = q0 + 32 * wave + l32;
-  const bool qvalid = qloc < P.s_loc;
-  const int qpos = P.q_pos0 + qloc;
+  const int qloc = q0 + 32 * wave + l32;         // within the segment
+  const bool qvalid = qloc < seg_rows;
+  const int qpos = pos0 + qloc;
   const int wq_first = q0 + 32 * wave;
-  const bool wave_active = wq_first < P.s_loc;
-  const int wpos_min = P.q_pos0 + wq_first;
-  const int wpos_max = P.q_pos0 + min(wq_first + 31, P.s_loc - 1);
-  const int n_keys = P.q_pos0 + min(q0 + kQTile, P.s_loc);  // keys this tile can see
+  const bool wave_active = wq_first < seg_rows;
+  const int wpos_min = pos0 + wq_first;
+  const int wpos_max = pos0 + min(wq_first + 31, seg_rows - 1);
+  const int n_keys = pos0 + min(q0 + kQTile, seg_rows);  // keys this tile can see
   const int k_begin = split * P.split_len;                   // a multiple of kStepKeys
   const int k_end = min(k_begin + P.split_len, n_keys);
   const int j0 = k_begin / kStepKeys;
@@ -151,7 +159,8 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   u32x4 qf[C::KS];
   {
     const float c = P.scale_log2;
-    const uint16_t* qrow = P.Q + (((size_t)b * P.s_loc + (qvalid ? qloc : 0)) * P.heads + head) * D;
+    const uint16_t* qrow =
+        P.Q + (((size_t)b * P.s_loc + row0 + (qvalid ? qloc : 0)) * P.heads + head) * D;
 #pragma unroll
     for (int s = 0; s < C::KS; ++s) {
       const u32x4 raw = qvalid ? ld16(qrow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
@@ -450,7 +459,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 
   l_run += __shfl_xor(l_run, 32);
   if (!qvalid) return;
-  const size_t row = ((size_t)b * P.s_loc + qloc) * P.heads + head;
+  const size_t row = ((size_t)b * P.s_loc + row0 + qloc) * P.heads + head;
   if (P.n_split == 1) {
     // Whole key range: normalise and write bf16 O (key 0 is visible to every query,
     // so l > 0).
@@ -509,28 +518,100 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams P) {
 
 }  // namespace
 
-int attn_split_count(long long batch, int s_loc, int heads, int q_pos0, int* split_len) {
-  const int n_qt = (s_loc + kQTile - 1) / kQTile;
-  const long long base = batch * heads * (long long)n_qt;
-  const int max_keys = q_pos0 + s_loc;  // keys seen by the last query tile
-  // Enough workgroups for every CU, never fewer than 4 key tiles per range, at most 8
-  // ranges.
-  int n = base > 0 ? (int)((kAttnTargetWorkgroups + base - 1) / base) : 1;
-  n = max(1, min(n, min(8, max_keys / (4 * kStepKeys))));
-  int len = (max(max_keys, 1) + n - 1) / n;
-  len = (len + kStepKeys - 1) / kStepKeys * kStepKeys;
-  n = (max(max_keys, 1) + len - 1) / len;
-  if (split_len) *split_len = len;
-  return n;
+namespace {
+
+// Makespan, in keys visited by one workgroup plus fixed costs, of dispatching the work
+// items of a split into n key ranges of `len` keys: the kernel's work order, each XCD
+// taking its contiguous share of work indices and giving each next item to its first
+// free CU.  tile_keys lists the keys of the query tiles in the kernel's tile order.
+long long split_makespan(const int* tile_keys, int n_qt, long long bh, int n, int len) {
+  constexpr int kCusPerXcd = kAttnTargetWorkgroups / kXcds;
+  constexpr long long kPieceCost = kStepKeys;      // setup and partial write: ~one step
+  constexpr long long kEmptyCost = kStepKeys / 8;  // a workgroup with no keys to visit
+  const long long total = bh * n_qt * n;
+  const long long q = total / kXcds, rem = total % kXcds;
+  long long worst = 0;
+  for (int x = 0; x < kXcds; ++x) {
+    long long finish[kCusPerXcd] = {};
+    const long long w0 = x * q + (x < rem ? x : rem), w1 = w0 + q + (x < rem ? 1 : 0);
+    for (long long w = w0; w < w1; ++w) {
+      const int t = (int)(w % n_qt);
+      const int split = (int)((w / n_qt) % n);
+      const long long keys = min(max((long long)tile_keys[t] - (long long)split * len, 0LL),
+                                 (long long)len);
+      const long long cost = keys > 0 ? keys + kPieceCost : kEmptyCost;
+      int c = 0;
+      for (int i = 1; i < kCusPerXcd; ++i)
+        if (finish[i] < finish[c]) c = i;
+      finish[c] += cost;
+    }
+    for (int i = 0; i < kCusPerXcd; ++i) worst = max(worst, finish[i]);
+  }
+  return worst;
+}
+
+}  // namespace
+
+int attn_split_count(const AttnParams& p, int* split_len) {
+  // Keys of each query tile, in the kernel's order (last segment first, last tile first).
+  constexpr int kMaxTiles = 1024;
+  int tile_keys[kMaxTiles];
+  int n_qt = 0, max_keys = 1;
+  for (int k = p.n_seg - 1; k >= 0; --k) {
+    const int nt = (p.seg_rows[k] + kQTile - 1) / kQTile;
+    for (int t = nt - 1; t >= 0; --t) {
+      const int keys = p.seg_pos0[k] + min((t + 1) * kQTile, p.seg_rows[k]);
+      if (n_qt < kMaxTiles) tile_keys[n_qt] = keys;
+      ++n_qt;
+      max_keys = max(max_keys, keys);
+    }
+  }
+  auto len_of = [&](int n) {
+    const int len = (max_keys + n - 1) / n;
+    return (len + kStepKeys - 1) / kStepKeys * kStepKeys;
+  };
+  const long long bh = (long long)p.batch * p.heads;
+  int best_n = 1;
+  if (bh > 0 && n_qt <= kMaxTiles) {
+    // Candidate range counts 1..8, at least 4 key tiles per range.  Estimated time =
+    // simulated makespan x the time a workgroup spends per key (~30 ns at d = 128, from
+    // the measured step rate) + the partials' HBM traffic (written, read back and
+    // merged, at ~4 TB/s); the smallest wins, ties going to fewer ranges.
+    const double t_key = 30e-9 * p.head_dim / 128.0, bw = 4e12;
+    const double rows = (double)bh * p.s_loc;
+    double best = -1.0;
+    for (int n = 1; n <= 8; ++n) {
+      const int len = len_of(n);
+      if (n > 1 && len < 4 * kStepKeys) break;
+      if ((max_keys + len - 1) / len != n) continue;  // same ranges as a smaller n
+      const double traffic =
+          n > 1 ? (2.0 * n * rows * (p.head_dim + 2) * 4 + rows * p.head_dim * 2) / bw : 0.0;
+      const double t = split_makespan(tile_keys, n_qt, bh, n, len) * t_key + traffic;
+      if (best < 0 || t < best) {
+        best = t;
+        best_n = n;
+      }
+    }
+  }
+  if (split_len) *split_len = len_of(best_n);
+  return best_n;
 }
 
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
   if (p.batch <= 0 || p.s_loc <= 0 || p.heads <= 0) return hipSuccess;
-  if (p.n_split < 1 || p.split_len <= 0 || p.split_len % kStepKeys != 0 ||
-      (long long)p.n_split * p.split_len < (long long)p.q_pos0 + p.s_loc ||
+  if (p.n_seg < 1 || p.n_seg > 2) return hipErrorInvalidValue;
+  int n_qt = 0, rows = 0;
+  for (int k = 0; k < p.n_seg; ++k) {
+    const long long end = (long long)p.seg_pos0[k] + p.seg_rows[k];
+    if (p.seg_rows[k] < 1 || p.seg_row0[k] != rows || p.seg_pos0[k] < 0 || end > p.kv_len ||
+        (long long)p.n_split * p.split_len < end)
+      return hipErrorInvalidValue;
+    rows += p.seg_rows[k];
+    n_qt += (p.seg_rows[k] + kQTile - 1) / kQTile;
+  }
+  if (rows != p.s_loc || p.n_split < 1 || p.split_len <= 0 || p.split_len % kStepKeys != 0 ||
       (p.n_split > 1 && (!p.part_o || !p.part_ml)))
     return hipErrorInvalidValue;
-  const int n_qt = (p.s_loc + kQTile - 1) / kQTile;
   const dim3 grid(n_qt * p.n_split * p.heads * p.batch);
   const void* fn;
   const void* combine;

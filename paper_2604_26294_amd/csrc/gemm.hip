@@ -2,7 +2,8 @@
 //
 //   gate+up+SwiGLU  Hs = bf16( SiLU(X W1^T) * (X W3^T) )          Algorithm 2, gate/up
 //   down / O-proj   Y (+)= Hs W2   or   Y (+)= Flatten(A) W_O^T    Algorithm 2 / 1, "+="
-//   Q/K/V proj      Q = X W_Q^T -> workspace, K, V -> full-sequence buffers  Algorithm 1
+//   Q/K/V proj      Q = X W_Q^T -> workspace, K, V -> full-sequence buffers at the
+//                   rows' sequence positions (zigzag reorder folded in)  Algorithm 1
 //
 // One workgroup = WGM x WGN wavefronts (8 by default: two per SIMD); each wavefront owns
 // a (BM/WGM) x (BN/WGN) block of C as 32 x 32 MFMA tiles.  K advances in steps of 64.
@@ -315,8 +316,9 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
             dst = P.Q + (size_t)m * P.ldq + n;
           } else {
             const int b = m / P.rows_per_batch, t = m - b * P.rows_per_batch;
+            const long long pos = t < P.kv_seg ? P.kv_pos0 + t : P.kv_pos1 + (t - P.kv_seg);
             const size_t row = (size_t)b * P.kv_batch_stride +
-                               (size_t)(P.kv_pos0 + t) * P.kv_row_stride + P.kv_col0;
+                               (size_t)pos * P.kv_row_stride + P.kv_col0;
             dst = n < P.nq + P.nkv ? P.Kb + row + (n - P.nq) : P.Vb + row + (n - P.nq - P.nkv);
           }
           *reinterpret_cast<u32x2*>(dst) = bits;

@@ -35,7 +35,8 @@ struct GemmParams {
 
   // Q/K/V epilogue: columns [0, nq) -> Q[m, n]; [nq, nq+nkv) -> K buffer;
   // [nq+nkv, nq+2nkv) -> V buffer.  Row m = b*rows_per_batch + t lands at sequence
-  // position kv_pos0 + t of batch b; column c of the K (or V) block lands at
+  // position kv_pos0 + t of batch b if t < kv_seg, else at kv_pos1 + (t - kv_seg)
+  // (the zigzag layout's second chunk); column c of the K (or V) block lands at
   // element kv_col0 + c of that position's row.
   uint16_t* Q;
   int ldq;
@@ -46,6 +47,8 @@ struct GemmParams {
   long long kv_batch_stride;
   int kv_row_stride;
   long long kv_pos0;
+  int kv_seg;
+  long long kv_pos1;
   int kv_col0;
 };
 
@@ -53,11 +56,13 @@ hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s);
 hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s);
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s);
 
-// Causal flash attention of one rank's query chunk for the heads of one shard.
+// Causal flash attention of one rank's queries for the heads of one shard.
 //   Q [B, S_loc, H_s, d] bf16;  K/V buffers [B, S, n_kv, d] bf16 (heads
 //   kv_head0 .. kv_head0 + H_s/g - 1 are this shard's);  O [B, S_loc, H_s, d] bf16.
-//   Local query t sits at global position q_pos0 + t and sees keys j <= q_pos0 + t;
-//   keys at or beyond kv_len are never read.
+//   The local rows form n_seg segments of consecutive global positions: rows
+//   [seg_row0[k], seg_row0[k] + seg_rows[k]) sit at positions seg_pos0[k] + (row -
+//   seg_row0[k]) (one segment for contiguous chunks, two for a zigzag shard).  A query
+//   at position t sees keys j <= t; keys at or beyond kv_len are never read.
 struct AttnParams {
   const uint16_t* Q;
   const uint16_t* Kb;
@@ -71,8 +76,11 @@ struct AttnParams {
   long long seq;    // S (K/V buffer rows per batch)
   int n_kv;         // kv heads in the buffer
   int kv_head0;     // first kv head of this shard
-  int q_pos0;       // global position of local query 0
-  int kv_len;       // number of readable keys: (p + 1) * S_loc
+  int n_seg;        // 1 or 2
+  int seg_row0[2];
+  int seg_rows[2];
+  int seg_pos0[2];
+  int kv_len;       // number of readable keys: the last segment position + 1
   float scale_log2; // softmax scale * log2(e)
   // Key-range split (attn_split_count): each query tile's keys [0, n) are processed in
   // ranges [c split_len, (c + 1) split_len), c < n_split.  With n_split > 1 the ranges
@@ -90,9 +98,10 @@ struct AttnParams {
 constexpr int kAttnTargetWorkgroups = 256;
 
 // Number of key ranges (and their length, a multiple of the key tile, in *split_len)
-// for one rank's attention: enough (query tile, head, batch, range) work items to fill
-// the GPU.  Depends on the shape only, so workspace sizes are known up front.
-int attn_split_count(long long batch, int s_loc, int heads, int q_pos0, int* split_len);
+// for one rank's attention (uses batch, heads and the segments of p): enough (query
+// tile, head, batch, range) work items to fill the GPU.  Depends on the shape only, so
+// workspace sizes are known up front.
+int attn_split_count(const AttnParams& p, int* split_len);
 
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s);
 

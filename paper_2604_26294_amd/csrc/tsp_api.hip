@@ -27,6 +27,8 @@ struct Dims {
   int fs_pad;  // fs rounded up to a multiple of 64 (width of the gated product in the workspace)
   long long M; // B * S_loc tokens of this rank
   float scale;
+  bool zz;     // zigzag layout: local rows = [chunk p; chunk 2D-1-p] of S/(2D) tokens each
+  int s_c;     // S_loc / 2 (zigzag chunk length)
 };
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -41,7 +43,8 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
       s->n_heads % s->n_kv_heads != 0 || s->n_heads % s->degree != 0 ||
       s->n_kv_heads % s->degree != 0 || s->ffn % s->degree != 0)
     return TSP_ERR_SHAPE;
-  if (s->layout != 0) return TSP_ERR_UNSUPPORTED;
+  if (s->layout != 0 && s->layout != 1) return TSP_ERR_UNSUPPORTED;
+  if (s->layout == 1 && s->seq % (2 * s->degree) != 0) return TSP_ERR_SHAPE;
   if (s->head_dim != 64 && s->head_dim != 128) return TSP_ERR_UNSUPPORTED;
   if (s->hidden % 8 != 0 || (s->ffn / s->degree) % 8 != 0) return TSP_ERR_UNSUPPORTED;
   o->B = s->batch;
@@ -62,6 +65,8 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
   o->M = (long long)o->B * o->s_loc;
   if (o->M > INT32_MAX / 2) return TSP_ERR_UNSUPPORTED;
   o->scale = s->softmax_scale > 0.f ? s->softmax_scale : 1.0f / sqrtf((float)s->head_dim);
+  o->zz = s->layout == 1;
+  o->s_c = o->s_loc / 2;
   return TSP_OK;
 }
 
@@ -72,13 +77,41 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
 size_t ws_mlp(const Dims& d) { return align_up((size_t)d.M * d.fs_pad * 2); }
 // Attention workspace: Q of the current shard and the attention output A (bf16
 // [M, H_s d] each), then the key-range partials when the shard's attention is split.
+// The rank's query rows as segments of consecutive global positions (Algorithm 1):
+// contiguous chunks are one segment starting at p S_loc; a zigzag shard is chunk p
+// (first s1 = (p+1) S_c keys) followed by chunk 2D-1-p (first s2 = (2D-p) S_c keys).
+void attn_segments(const Dims& d, AttnParams* ap) {
+  ap->batch = d.B;
+  ap->s_loc = d.s_loc;
+  ap->heads = d.hs;
+  ap->head_dim = d.d;
+  if (!d.zz) {
+    ap->n_seg = 1;
+    ap->seg_row0[0] = 0;
+    ap->seg_rows[0] = d.s_loc;
+    ap->seg_pos0[0] = d.p * d.s_loc;
+    ap->kv_len = (d.p + 1) * d.s_loc;
+  } else {
+    ap->n_seg = 2;
+    ap->seg_row0[0] = 0;
+    ap->seg_rows[0] = d.s_c;
+    ap->seg_pos0[0] = d.p * d.s_c;
+    ap->seg_row0[1] = d.s_c;
+    ap->seg_rows[1] = d.s_c;
+    ap->seg_pos0[1] = (2 * d.D - 1 - d.p) * d.s_c;
+    ap->kv_len = (2 * d.D - d.p) * d.s_c;
+  }
+}
+
 struct AttnWs {
   size_t q, a, po, pml, total;  // byte offsets and total size
   int n_split, split_len;
 };
 AttnWs attn_ws(const Dims& d) {
   AttnWs w;
-  w.n_split = tsp::attn_split_count(d.B, d.s_loc, d.hs, d.p * d.s_loc, &w.split_len);
+  AttnParams ap = {};
+  attn_segments(d, &ap);
+  w.n_split = tsp::attn_split_count(ap, &w.split_len);
   const size_t rows = (size_t)d.M * d.hs;
   const size_t part = w.n_split > 1 ? (size_t)w.n_split * rows : 0;
   w.q = 0;
@@ -230,7 +263,15 @@ GemmParams qkv_params(const Dims& d, const uint16_t* x, const uint16_t* shard, i
   g.rows_per_batch = d.s_loc;
   g.kv_batch_stride = (long long)d.S * d.nkv * d.d;
   g.kv_row_stride = d.nkv * d.d;
-  g.kv_pos0 = (long long)d.p * d.s_loc;
+  if (!d.zz) {
+    g.kv_pos0 = (long long)d.p * d.s_loc;
+    g.kv_seg = d.s_loc;
+    g.kv_pos1 = 0;
+  } else {  // ZigZagReorder folded into the write addresses
+    g.kv_pos0 = (long long)d.p * d.s_c;
+    g.kv_seg = d.s_c;
+    g.kv_pos1 = (long long)(2 * d.D - 1 - d.p) * d.s_c;
+  }
   g.kv_col0 = r * kd;
   return g;
 }
@@ -254,16 +295,12 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     ap.Kb = kb;
     ap.Vb = vb;
     ap.O = a_ws;
-    ap.batch = d.B;
-    ap.s_loc = d.s_loc;
-    ap.heads = d.hs;
+    attn_segments(d, &ap);
     ap.group = d.g;
     ap.head_dim = d.d;
     ap.seq = d.S;
     ap.n_kv = d.nkv;
     ap.kv_head0 = r * d.ks;
-    ap.q_pos0 = d.p * d.s_loc;
-    ap.kv_len = (d.p + 1) * d.s_loc;
     ap.scale_log2 = d.scale * log2e;
     ap.n_split = aw.n_split;
     ap.split_len = aw.split_len;

@@ -20,6 +20,22 @@ def to_device_bf16(bits: np.ndarray, device="cuda") -> torch.Tensor:
     return t.view(torch.bfloat16).to(device)
 
 
+def local_positions(wl: Workload, p: int) -> np.ndarray:
+    """Global sequence positions of rank p's local rows: a contiguous chunk, or for the
+    zigzag layout chunk p then chunk 2D-1-p of S/(2D) tokens (the C ABI's mapping)."""
+    if wl.layout == 0:
+        return np.arange(p * wl.s_loc, (p + 1) * wl.s_loc)
+    s_c = wl.s_loc // 2
+    first = np.arange(p * s_c, (p + 1) * s_c)
+    second = np.arange((2 * wl.degree - 1 - p) * s_c, (2 * wl.degree - p) * s_c)
+    return np.concatenate([first, second])
+
+
+def local_rows(x_full: np.ndarray, wl: Workload, p: int) -> np.ndarray:
+    """Rank p's local input rows [B, S_loc, h] of the full-sequence input."""
+    return np.ascontiguousarray(x_full[:, local_positions(wl, p)])
+
+
 def bf16_tensor_to_f64(t: torch.Tensor) -> np.ndarray:
     bits = t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     return I.bf16_bits_to_f64(bits)
@@ -39,8 +55,12 @@ class RankProblem:
         self.device = device
         D = wl.degree
         self.shape = T.shape_of(wl, self.p)
-        self.x_chunks = [to_device_bf16(I.local_chunk(x_full, q, D), device)
-                         for q in range(self.p + 1)]
+        # ranks whose K/V rows this rank's queries can see: the earlier ones for
+        # contiguous chunks, every one for a zigzag shard
+        self.kv_ranks = list(range(self.p)) if wl.layout == 0 else \
+            [q for q in range(D) if q != self.p]
+        self.x_chunks = {q: to_device_bf16(local_rows(x_full, wl, q), device)
+                         for q in self.kv_ranks + [self.p]}
         self.x_loc = self.x_chunks[self.p]
         self.attn = [to_device_bf16(I.attn_shard_packed(w, r, D, wl.n_heads, wl.n_kv_heads,
                                                         wl.head_dim), device)
@@ -60,8 +80,8 @@ class RankProblem:
         self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
 
     def prefill_kv(self):
-        """The modelled all-gather: ranks 0 .. p-1 write their K/V rows of every shard."""
-        for q in range(self.p):
+        """The modelled all-gather: the other ranks write their K/V rows of every shard."""
+        for q in self.kv_ranks:
             T.tsp_kv_rank_fwd(T.shape_of(self.wl, q), self.x_chunks[q], self.attn, self.k_buf,
                               self.v_buf)
 

@@ -20,6 +20,7 @@ STATUS_NAMES = {0: "TSP_OK", 1: "TSP_ERR_NULL", 2: "TSP_ERR_SHAPE", 3: "TSP_ERR_
                 4: "TSP_ERR_ALIGN", 5: "TSP_ERR_WORKSPACE", 6: "TSP_ERR_UNSUPPORTED",
                 7: "TSP_ERR_HIP"}
 OP_MLP, OP_ATTN, OP_LAYER = 0, 1, 2
+LAYOUT_CONTIGUOUS, LAYOUT_ZIGZAG = 0, 1
 KERNELS = ("gate_up", "down", "qkv", "attn", "oproj")  # TSP_KERNEL_* order
 
 
@@ -89,7 +90,7 @@ def make_shape(batch, seq, hidden, ffn, n_heads, n_kv_heads, head_dim, degree, r
 def shape_of(wl, rank=None, softmax_scale=0.0) -> tsp_shape:
     """tsp_shape of a :class:`~paper_2604_26294_amd.workloads.Workload`."""
     return make_shape(wl.batch, wl.seq, wl.hidden, wl.ffn, wl.n_heads, wl.n_kv_heads,
-                      wl.head_dim, wl.degree, wl.rank if rank is None else rank, 0,
+                      wl.head_dim, wl.degree, wl.rank if rank is None else rank, wl.layout,
                       softmax_scale)
 
 

@@ -24,10 +24,18 @@ class Workload:
     w_std: float = 0.02
     x_std: float = 1.0
     seed: int = 0
+    layout: int = 0     # 0 contiguous chunks, 1 zigzag (two chunks of S/(2D) per rank)
 
     @property
     def s_loc(self) -> int:
         return self.seq // self.degree
+
+    @property
+    def layout_name(self) -> str:
+        return ("contiguous", "zigzag")[self.layout]
+
+    def with_layout(self, layout: int) -> "Workload":
+        return replace(self, layout=layout)
 
     @property
     def gqa(self) -> int:

@@ -54,7 +54,11 @@ def oracle_blocks(wl: Workload, x_bits, w_bits, p, blocks=("mlp", "attn", "layer
     w = {k: f64(v) for k, v in w_bits.items()}
     D = wl.degree
     hs, ks, d = wl.n_heads // D, wl.n_kv_heads // D, wl.head_dim
-    chunks = [I.local_chunk(x, q, D) for q in range(D)]
+    zz = wl.layout == 1
+    if zz:
+        chunks = [x[:, O.zigzag_positions(wl.seq, D, q)] for q in range(D)]
+    else:
+        chunks = [I.local_chunk(x, q, D) for q in range(D)]
     attn_sh = [I.attn_shard_packed(w, r, D, wl.n_heads, wl.n_kv_heads, d) for r in range(D)]
     mlp_sh = [I.mlp_shard(w, j, D) for j in range(D)]
     w1s, w3s, w2s = [m[0] for m in mlp_sh], [m[1] for m in mlp_sh], [m[2] for m in mlp_sh]
@@ -62,9 +66,14 @@ def oracle_blocks(wl: Workload, x_bits, w_bits, p, blocks=("mlp", "attn", "layer
     if "mlp" in blocks:
         out["mlp"] = O.mlp_rank(chunks[p], w1s, w3s, w2s, p)
     if "attn" in blocks:
-        kv = [O.gather_kv(chunks, attn_sh[r], hs, ks, d) for r in range(D)]
-        out["attn"] = O.attn_rank(chunks[p], attn_sh, kv, p, wl.n_heads, wl.n_kv_heads, d)
+        if zz:
+            kv = [O.gather_kv_zigzag(chunks, attn_sh[r], hs, ks, d) for r in range(D)]
+            out["attn"] = O.attn_rank_zigzag(chunks[p], attn_sh, kv, p, wl.n_heads,
+                                             wl.n_kv_heads, d)
+        else:
+            kv = [O.gather_kv(chunks, attn_sh[r], hs, ks, d) for r in range(D)]
+            out["attn"] = O.attn_rank(chunks[p], attn_sh, kv, p, wl.n_heads, wl.n_kv_heads, d)
     if "layer" in blocks:
-        out["layer"] = O.layer_rank(chunks, attn_sh, w1s, w3s, w2s, p, wl.n_heads,
-                                    wl.n_kv_heads, d)["y"]
+        fn = O.layer_rank_zigzag if zz else O.layer_rank
+        out["layer"] = fn(chunks, attn_sh, w1s, w3s, w2s, p, wl.n_heads, wl.n_kv_heads, d)["y"]
     return out

@@ -66,7 +66,8 @@ def _shape(**kw):
     (dict(seq=255), 2), (dict(hidden=250), 2), (dict(n_kv_heads=3), 2),
     (dict(n_heads=2, hidden=128, n_kv_heads=2, degree=4, rank=0, ffn=688 * 2), 2),
     (dict(ffn=687), 2), (dict(degree=0, rank=0), 2), (dict(batch=-1), 2),
-    (dict(layout=1), 6), (dict(head_dim=32, n_heads=8), 6), (dict(ffn=680), 6),
+    (dict(layout=2), 6), (dict(layout=-1), 6), (dict(layout=1, seq=258), 2),
+    (dict(layout=1), 0), (dict(head_dim=32, n_heads=8), 6), (dict(ffn=680), 6),
 ])
 def test_shape_validation(kw, code):
     out = ctypes.c_size_t(0)

@@ -66,3 +66,21 @@ def test_algorithmic_bytes_closed_form():
         kv = 2 * wl.batch * (wl.rank + 1) * wl.s_loc * wl.n_kv_heads * wl.head_dim * 2
         assert kv / 1e6 == pytest.approx(kv_mb, abs=0.05)
         assert total == weights + kv + wl.s_loc * 4096 * 6
+
+
+def test_zigzag_pairs_brute_force_and_balance():
+    """A zigzag shard's pair count, by brute force over its positions, equals the closed
+    form for every rank, and summed over ranks gives the causal half of the square."""
+    from paper_2604_26294_amd.workloads import TINY
+    for degree, s_c in ((1, 3), (2, 4), (4, 2)):
+        seq = 2 * degree * s_c
+        total = 0
+        for p in range(degree):
+            pos = [p * s_c + i for i in range(s_c)] + \
+                  [(2 * degree - 1 - p) * s_c + i for i in range(s_c)]
+            brute = sum(1 for t in pos for j in range(seq) if j <= t)
+            assert F.causal_pairs_zigzag(2 * s_c, degree) == brute
+            total += brute
+        assert total == seq * (seq + 1) // 2
+    zz = TINY.with_layout(1)
+    assert F.rank_flops(zz, 0).total == F.rank_flops(zz, 1).total

@@ -18,8 +18,9 @@ from paper_2604_26294_amd.harness import RankProblem  # noqa: E402
 from paper_2604_26294_amd.workloads import L7B_8K, L7B_64K, L13B_B4, L70B_GQA  # noqa: E402
 from tests.gpu_common import assert_close  # noqa: E402
 
-CASES = [(L7B_8K, 7), (L7B_64K, 7), (L70B_GQA, 7), (L13B_B4, 0), (L13B_B4, 1), (L13B_B4, 2),
-         (L13B_B4, 3)]
+CASES = [(L7B_8K, 7), (L7B_64K, 7), (L7B_64K.with_layout(1), 0), (L70B_GQA, 7),
+         (L13B_B4, 0), (L13B_B4, 1), (L13B_B4, 2), (L13B_B4, 3),
+         (L13B_B4.with_layout(1), 0), (L13B_B4.with_layout(1), 3)]
 _cache = {}
 
 
@@ -33,10 +34,11 @@ def _data(wl):
 
 
 def _rows(s_loc):
-    return sorted({0, 1, 127, 128, s_loc // 2 + 7, s_loc - 1})
+    # both ends of the local rows and of each half (the zigzag layout's two chunks)
+    return sorted({0, 1, 127, 128, s_loc // 2 - 1, s_loc // 2, s_loc // 2 + 7, s_loc - 1})
 
 
-@pytest.mark.parametrize("wl,p", CASES, ids=[f"{w.name}-r{p}" for w, p in CASES])
+@pytest.mark.parametrize("wl,p", CASES, ids=[f"{w.name}-{w.layout_name}-r{p}" for w, p in CASES])
 def test_sampled_rows_match_unsharded_layer(wl, p):
     print(f"[fullsize] {wl.name} rank {p}", flush=True)
     x_bits, w_bits, wf = _data(wl)
@@ -48,12 +50,15 @@ def test_sampled_rows_match_unsharded_layer(wl, p):
     torch.cuda.synchronize()
     rows = _rows(wl.s_loc)
     batches = sorted({0, wl.batch - 1})
-    s0 = p * wl.s_loc
+    if wl.layout == 1:
+        pos = O.zigzag_positions(wl.seq, wl.degree, p)[rows]
+    else:
+        pos = [p * wl.s_loc + r for r in rows]
     for b in batches:
-        x_b = I.bf16_bits_to_f64(x_bits[b, :s0 + wl.s_loc])
+        x_b = I.bf16_bits_to_f64(x_bits[b, :max(pos) + 1])
         attn = O.attention_rows(x_b, wf["wq"], wf["wk"], wf["wv"], wf["wo"], wl.n_heads,
-                                wl.n_kv_heads, [s0 + r for r in rows])
-        xr = x_b[[s0 + r for r in rows]]
+                                wl.n_kv_heads, pos)
+        xr = x_b[pos]
         mlp_x = O.mlp_full(xr, wf["w1"], wf["w3"], wf["w2"])
         u = xr + attn
         y = u + O.mlp_full(u, wf["w1"], wf["w3"], wf["w2"])

@@ -16,13 +16,18 @@ from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, SINGLE, assert_cl
                               f64, gen, oracle_blocks)
 
 CASES = [(TINY, 0), (TINY, 1), (MID_GQA64, 0), (MID_GQA64, 2), (MID_GQA64, 3),
-         (MID_MHA128, 1), (MID_GQA8, 1), (SINGLE, 0)]
-_IDS = [f"{w.name}-r{p}" for w, p in CASES]
+         (MID_MHA128, 1), (MID_GQA8, 1), (SINGLE, 0),
+         # zigzag shards (Algorithm 1 as printed): two query segments, K/V rows written
+         # at reordered positions, every other rank's rows visible
+         (TINY.with_layout(1), 0), (TINY.with_layout(1), 1), (MID_GQA64.with_layout(1), 0),
+         (MID_GQA64.with_layout(1), 3), (MID_MHA128.with_layout(1), 0),
+         (MID_GQA8.with_layout(1), 1), (SINGLE.with_layout(1), 0)]
+_IDS = [f"{w.name}-{w.layout_name}-r{p}" for w, p in CASES]
 _cache = {}
 
 
 def _inputs(wl):
-    if wl.name not in _cache:
+    if wl.name not in _cache:       # the inputs do not depend on the layout
         _cache[wl.name] = gen(wl)
     return _cache[wl.name]
 
@@ -50,13 +55,19 @@ def test_block_parity(wl, p, block):
     assert_close(got, ref, f"{wl.name} r{p} {block}")
 
 
-@pytest.mark.parametrize("wl", [TINY, MID_GQA64], ids=lambda w: w.name)
+@pytest.mark.parametrize("wl", [TINY, MID_GQA64, TINY.with_layout(1), MID_GQA64.with_layout(1)],
+                         ids=lambda w: f"{w.name}-{w.layout_name}")
 def test_rank_concat_equals_unsharded_layer(wl):
+    """All ranks together give the unsharded layer, each row at its rank's positions."""
     x_bits, w_bits = _inputs(wl)
     outs = [_run(wl, p, "layer")[0] for p in range(wl.degree)]
     x = f64(x_bits)
     w = {k: f64(v) for k, v in w_bits.items()}
     ref = O.layer_full(x, w, wl.n_heads, wl.n_kv_heads)
+    if wl.layout == 1:
+        pos = np.concatenate([O.zigzag_positions(wl.seq, wl.degree, p)
+                              for p in range(wl.degree)])
+        ref = {k: v[:, pos] for k, v in ref.items()}
     assert_close(np.concatenate(outs, axis=1), ref["y"], "concat layer")
     attn = [_run(wl, p, "attn")[0] for p in range(wl.degree)]
     assert_close(np.concatenate(attn, axis=1), ref["attn"], "concat attn")
