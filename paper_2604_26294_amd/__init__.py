@@ -10,4 +10,4 @@ Importing this package loads nothing native.  The compute entry points live in
 hand-written HIP kernels for gfx950); that module raises if the library is missing.
 """
 
-__all__ = ["inputs", "workloads", "flops"]
+__all__ = ["inputs", "workloads", "flops", "costmodel"]
