@@ -83,17 +83,33 @@ struct FaCfg {
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // 16 bytes per lane from global memory straight into LDS at lds + 16 * lane: the
-// buffer form, with the address = resource base (scalar) + soff (scalar) + voff (lane).
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff, uint32_t soff,
+// buffer form, with the address = resource base (scalar) + soff (scalar) + voff (lane);
+// M0 holds the wave's LDS destination.
+//
+// Issued from inline assembly on purpose.  The compiler cannot tell which LDS bytes an
+// LDS-destination load writes, so after one it puts a full vmcnt(0) wait in front of
+// the next LDS read it cannot prove disjoint (here: the first V^T transpose read of the
+// step), which would stall every step on the load of the NEXT tile.  Hidden in asm,
+// the load is ordered only by this kernel's own waits: every slot is read after the
+// vmcnt(0) + barrier at the top of the step that consumes it, and a slot is refilled
+// only after the barrier that follows its last read.  The compiler's own waits stay
+// correct because loads complete in issue order.  No other code in this kernel uses
+// M0 (a reserved register the compiler does not track through asm).
+typedef u32x4 rsrc_t;
+__device__ __forceinline__ void dma16(const rsrc_t& rsrc, uint32_t voff, uint32_t soff,
                                       lds_char* lds) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds, 16,
-                                           (int)voff, (int)soff, 0, 0);
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :: "v"(voff), "s"(rsrc), "s"(soff), "s"(m0) : "memory", "m0");
 }
 
-// Raw buffer resource over [base, base + 4 GiB) (stride 0, no format conversion).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0xffffffff,
-                                           0x00020000);
+// Raw buffer resource over [base, base + 4 GiB) (stride 0, no format conversion): base
+// address (48 bits), number of records, and the data-format word of a raw resource.
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  return rsrc_t{(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a),
+                (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32) & 0xffffu),
+                0xffffffffu, 0x00020000u};
 }
 
 __device__ __forceinline__ u32x4 lds_read16(const lds_char* p) {
@@ -194,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   auto dma_tile = [&](const uint16_t* base, uint32_t lane_off, int col, int tile,
                       int slot_off) __attribute__((always_inline)) {
     const int key0 = tile * kStepKeys;
-    const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(base + (size_t)key0 * kv_stride);
+    const rsrc_t rsrc = make_rsrc(base + (size_t)key0 * kv_stride);
     lds_char* dst = Ls + slot_off + wave * (kWave * 16);
     if (key0 + kStepKeys <= k_end) {
 #pragma unroll

@@ -50,9 +50,18 @@ __device__ __forceinline__ void wait_dma() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane.
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane (M0 holds
+// the wave's LDS destination).  Issued from inline assembly: the compiler cannot tell
+// which LDS bytes such a load writes and would otherwise wait for ALL of them (vmcnt(0))
+// before the first transpose read of the NN panels, i.e. for the next stage's loads at
+// the start of every K step.  The loads are ordered by the ring's own counted waits and
+// barriers instead; loads complete in issue order, so the compiler's own waits remain
+// correct.  No other code in this kernel uses M0 (a reserved register the compiler
+// does not track through asm).
 __device__ __forceinline__ void dma16(const void* src, lds_char* lds) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(m0) : "memory", "m0");
 }
 
 __device__ __forceinline__ u32x4 lds_read16(const lds_char* p) {
