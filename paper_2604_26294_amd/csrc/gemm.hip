@@ -354,11 +354,12 @@ hipError_t launch(const GemmParams& p, hipStream_t s) {
 
 // Tile shapes are chosen for the shard products of the 7B-class layer on 256 CUs
 // (one workgroup per CU): gate+up (M = S_loc, N = F/D = 1376) in 128 x 128 tiles makes
-// 704 tiles, 2.75 full rounds instead of 1.4 with 256 x 128; Q/K/V (N = 3 d H_s =
-// 1536) in 256 x 192 tiles makes exactly 256; down / O-proj (N = h = 4096) in
-// 256 x 256 tiles makes 512.
+// 704 tiles, 2.75 full rounds instead of 1.4 with 256 x 128 (measured 5 % slower
+// despite the lower L2 traffic), with a 3-slot ring (144 KB) because its 48 KB per
+// K step of operands otherwise arrive late; Q/K/V (N = 3 d H_s = 1536) in 256 x 192
+// tiles makes exactly 256; down / O-proj (N = h = 4096) in 256 x 256 tiles makes 512.
 hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s) {
-  return launch<128, 128, 2, 4, false, EPI_SWIGLU, 2>(p, s);
+  return launch<128, 128, 2, 4, false, EPI_SWIGLU, 3>(p, s);
 }
 
 hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s) {
