@@ -124,6 +124,25 @@ __device__ __forceinline__ u32x2 lds_read_tr(const lds_char* p) {
 template <int N>
 using IC = std::integral_constant<int, N>;
 
+// x combined with the value of lane l ^ 32.  v_permlane32_swap exchanges the upper 32
+// lanes of its first operand with the lower 32 lanes of its second, so with both
+// holding x they become [x_lo, x_lo] and [x_hi, x_hi]; a VALU op, where a shuffle
+// through LDS (ds_bpermute) would wait on every LDS read still in flight.  Written as
+// asm: this compiler folds the builtin's second result away.
+__device__ __forceinline__ void swap_halves(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ float max_with_partner(float x) {
+  float a = x, b = x;
+  swap_halves(a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float sum_with_partner(float x) {
+  float a = x, b = x;
+  swap_halves(a, b);
+  return a + b;
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
   using C = FaCfg<D>;
@@ -321,7 +340,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[H][bb][e]);
-    return fmaxf(mx, __shfl_xor(mx, 32));  // both lanes of a query decide alike
+    return max_with_partner(mx);  // both lanes of a query decide alike
   };
   // Lazy reference update for half H with row max mx (relative to mref).  Must follow
   // every P V product already issued: it rescales o.
@@ -473,7 +492,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     if (t + 1 < n_steps) step(IC<1>{}, j0 + t + 1);
   }
 
-  l_run += __shfl_xor(l_run, 32);
+  l_run = sum_with_partner(l_run);
   if (!qvalid) return;
   const size_t row = ((size_t)b * P.s_loc + row0 + qloc) * P.heads + head;
   if (P.n_split == 1) {
