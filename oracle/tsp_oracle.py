@@ -132,6 +132,50 @@ def mlp_rank(x_loc, w1_shards, w3_shards, w2_shards, p):
     return y
 
 
+# ---------------------------------------------------------------------------
+# Backward of the ring MLP (per rank).  The paper costs TSP's backward (Section 4: it
+# mirrors the forward weight movement, and each weight shard's partial gradients are
+# summed to the shard's owner) but prints no algorithm; these are the gradients of
+# Algorithm 2's forward, by the chain rule.
+# ---------------------------------------------------------------------------
+
+def silu_grad(z: np.ndarray) -> np.ndarray:
+    """d SiLU(z) / dz = sigmoid(z) (1 + z (1 - sigmoid(z)))."""
+    with np.errstate(over="ignore"):
+        sg = 1.0 / (1.0 + np.exp(-z))
+    return sg * (1.0 + z * (1.0 - sg))
+
+
+def swiglu_bwd(g, u, dhs):
+    """Gradients of Hs = SiLU(G) * U with respect to G and U, given dL/dHs."""
+    return dhs * u * silu_grad(g), dhs * silu(g)
+
+
+def mlp_rank_bwd(x_loc, w1_shards, w3_shards, w2_shards, dy, p):
+    """Backward of mlp_rank on rank p for the upstream gradient dy = dL/dY
+    [B, S_loc, h].  Visits the shards in the forward's ring order and returns dX
+    [B, S_loc, h] and this rank's contribution to each shard's weight gradients:
+    lists dW1, dW3, dW2 indexed by shard, [F/D, h] each.  Summing shard j's
+    contributions over the D ranks gives the gradient of shard j (sum-to-owner)."""
+    degree = len(w1_shards)
+    h = x_loc.shape[-1]
+    x2 = x_loc.reshape(-1, h)
+    dy2 = dy.reshape(-1, h)
+    dx = np.zeros_like(x2, dtype=np.float64)
+    dw1, dw3, dw2 = [None] * degree, [None] * degree, [None] * degree
+    for t in range(degree):
+        j = (p - t) % degree
+        g = x2 @ w1_shards[j].T
+        u = x2 @ w3_shards[j].T
+        dhs = dy2 @ w2_shards[j].T
+        dg, du = swiglu_bwd(g, u, dhs)
+        dx += dg @ w1_shards[j] + du @ w3_shards[j]
+        dw1[j] = dg.T @ x2
+        dw3[j] = du.T @ x2
+        dw2[j] = (silu(g) * u).T @ dy2
+    return dx.reshape(x_loc.shape), dw1, dw3, dw2
+
+
 def unpack_attn_shard(packed, heads_per_shard, kv_heads_per_shard, head_dim):
     """Split a packed shard [W_Q^(r); W_K^(r); W_V^(r); W_O^(r)^T] (Algorithm 1's
     packed broadcast buffer) into its four row blocks."""

@@ -7,6 +7,7 @@ import numpy as np
 import pytest
 
 import oracle.tsp_oracle as O
+from tests import test_oracle_bwd_pins as PB
 from tests import test_oracle_pins as P
 
 _orig_probs = O.causal_probs
@@ -86,7 +87,45 @@ def _zigzag_plain_prefix(x_loc, shards, kv, p, n_heads, n_kv, d, scale=None):
     return _orig_attn_rank(x_loc, shards, kv, p, n_heads, n_kv, d, scale)
 
 
+_orig_silu_grad = O.silu_grad
+_orig_swiglu_bwd = O.swiglu_bwd
+_orig_mlp_rank_bwd = O.mlp_rank_bwd
+
+
+def _silu_grad_sigmoid_only(z):                         # drops the (1 + z (1 - s)) factor
+    return 1.0 / (1.0 + np.exp(-z))
+
+
+def _swiglu_bwd_swapped(g, u, dhs):                     # gate / up gradients exchanged
+    dg, du = _orig_swiglu_bwd(g, u, dhs)
+    return du, dg
+
+
+def _mlp_rank_bwd_no_up_path(x_loc, w1s, w3s, w2s, dy, p):  # dX misses the dU W3 term
+    degree, h = len(w1s), x_loc.shape[-1]
+    x2, dy2 = x_loc.reshape(-1, h), dy.reshape(-1, h)
+    dx = np.zeros_like(x2)
+    dw1, dw3, dw2 = [None] * degree, [None] * degree, [None] * degree
+    for t in range(degree):
+        j = (p - t) % degree
+        g, u, dhs = x2 @ w1s[j].T, x2 @ w3s[j].T, dy2 @ w2s[j].T
+        dg, du = O.swiglu_bwd(g, u, dhs)
+        dx += dg @ w1s[j]
+        dw1[j], dw3[j], dw2[j] = dg.T @ x2, du.T @ x2, (O.silu(g) * u).T @ dy2
+    return dx.reshape(x_loc.shape), dw1, dw3, dw2
+
+
+def _mlp_rank_bwd_skips_last_step(x_loc, w1s, w3s, w2s, dy, p):
+    degree = len(w1s)
+    dx, dw1, dw3, dw2 = _orig_mlp_rank_bwd(x_loc, w1s[:-1] + [0 * w1s[-1]], w3s, w2s, dy, p)
+    return dx, dw1, dw3, dw2
+
+
 MUTATIONS = {
+    "silu_grad_is_sigmoid": ("silu_grad", _silu_grad_sigmoid_only),
+    "swiglu_bwd_swapped": ("swiglu_bwd", _swiglu_bwd_swapped),
+    "bwd_dx_misses_up_path": ("mlp_rank_bwd", _mlp_rank_bwd_no_up_path),
+    "bwd_last_shard_dropped": ("mlp_rank_bwd", _mlp_rank_bwd_skips_last_step),
     "zigzag_halves_swapped": ("zigzag_positions", _zigzag_halves_swapped),
     "zigzag_reorder_dropped": ("gather_kv_zigzag", _zigzag_reorder_dropped),
     "zigzag_as_contiguous": ("attn_rank_zigzag", _zigzag_plain_prefix),
@@ -113,6 +152,9 @@ PINS = [
     (P.test_mlp_ring_order_and_row_permutation_invariance, ()),
     (P.test_zigzag_partition_and_causal_balance, ()),
     (P.test_zigzag_fold_equals_unsharded, (4, 2, 2)),
+    (PB.test_rank_backward_matches_finite_differences, ()),
+    (PB.test_weight_gradients_sum_to_owner_and_dx_is_local, ()),
+    (PB.test_backward_special_cases, ()),
 ]
 
 
