@@ -109,6 +109,31 @@ tsp_status tsp_mlp_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                             const uint16_t* const* w_down, float* y_loc, int accumulate,
                             void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Backward of tsp_mlp_rank_fwd on rank p.  The paper costs TSP's backward (Section 4:
+ * it mirrors the forward weight movement, and each weight shard's partial gradients
+ * are summed to the rank that owns the shard) without printing an algorithm; these
+ * are the chain-rule gradients of Algorithm 2, shards visited in the same ring order.
+ * For each j, with G = X W_gate[j]^T, U = X W_up[j]^T recomputed, s = SiLU(G),
+ * s' = sigmoid(G) (1 + G (1 - sigmoid(G))), Hs = s * U:
+ *   dHs = dY W_down[j]^T;   dG = dHs * U * s';   dU = dHs * s
+ *   dX (+)= dG W_gate[j] + dU W_up[j]                     (fp32, ring order)
+ *   dw_gate[j] (+)= dG^T X;  dw_up[j] (+)= dU^T X;  dw_down[j] (+)= Hs^T dY
+ * The dw outputs are this rank's contributions; summing them over the D ranks (the
+ * sum-to-owner reduction, a collective outside this single-GPU library) gives the
+ * gradients of the shards.  dG, dU and Hs are rounded to bf16 for the matrix cores.
+ *   x_loc, w_gate, w_up, w_down  as for tsp_mlp_rank_fwd
+ *   dy_loc     [B, S_loc, h] bf16       gradient of the MLP output for these tokens
+ *   dx_loc     [B, S_loc, h] fp32       accumulate == 0: overwritten; != 0: added to
+ *   dw_gate[j], dw_up[j], dw_down[j]  [ffn/D, h] fp32 (host arrays of D device
+ *              pointers)                 overwritten or added to, as dx_loc
+ *   ws         workspace of at least tsp_workspace_bytes(shape, TSP_OP_MLP_BWD) bytes */
+tsp_status tsp_mlp_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
+                            const uint16_t* dy_loc, const uint16_t* const* w_gate,
+                            const uint16_t* const* w_up, const uint16_t* const* w_down,
+                            float* dx_loc, int accumulate, float* const* dw_gate,
+                            float* const* dw_up, float* const* dw_down, void* ws,
+                            size_t ws_bytes, hipStream_t stream);
+
 /* This rank's contribution to the sequence-wise K/V all-gather of every shard
  * (Algorithm 1, the local K and V projections, with ZigZagReorder folded into the
  * addresses): for r = 0..D-1 writes
@@ -148,7 +173,7 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                               uint16_t* k_buf, uint16_t* v_buf, float* y_loc, void* ws,
                               size_t ws_bytes, hipStream_t stream);
 
-enum { TSP_OP_MLP = 0, TSP_OP_ATTN = 1, TSP_OP_LAYER = 2 };
+enum { TSP_OP_MLP = 0, TSP_OP_ATTN = 1, TSP_OP_LAYER = 2, TSP_OP_MLP_BWD = 3 };
 
 /* Workspace bytes the entry point `op` needs for `shape` (validated as above). */
 tsp_status tsp_workspace_bytes(const tsp_shape* shape, int op, size_t* bytes);
@@ -164,7 +189,10 @@ enum {
   TSP_KERNEL_QKV = 2,     /* Q/K/V projections with K/V scatter (Algorithm 1) */
   TSP_KERNEL_ATTN = 3,    /* causal flash attention of one shard step (Algorithm 1) */
   TSP_KERNEL_OPROJ = 4,   /* output projection + fp32 shard accumulate (Algorithm 1) */
-  TSP_KERNEL_COUNT = 5
+  TSP_KERNEL_BWD_GATE = 5, /* MLP backward: G, U, dHs products with the SwiGLU backward */
+  TSP_KERNEL_BWD_DX = 6,   /* MLP backward: dX accumulate */
+  TSP_KERNEL_BWD_DW = 7,   /* MLP backward: weight-gradient products */
+  TSP_KERNEL_COUNT = 8
 };
 tsp_status tsp_profile_enable(int enable);
 tsp_status tsp_profile_read(int kernel, double* total_ms, int64_t* launches);

@@ -2,6 +2,8 @@
 //
 //   gate+up+SwiGLU  Hs = bf16( SiLU(X W1^T) * (X W3^T) )          Algorithm 2, gate/up
 //   down / O-proj   Y (+)= Hs W2   or   Y (+)= Flatten(A) W_O^T    Algorithm 2 / 1, "+="
+//   SwiGLU backward G = X W1^T, U = X W3^T, dHs = dY W2^T in one pass; dG, dU and the
+//                   transposes of dG, dU, Hs for the weight-gradient products
 //   Q/K/V proj      Q = X W_Q^T -> workspace, K, V -> full-sequence buffers at the
 //                   rows' sequence positions (zigzag reorder folded in)  Algorithm 1
 //
@@ -37,7 +39,7 @@ namespace tsp {
 namespace {
 
 constexpr int BK = 64;
-enum { EPI_SWIGLU = 0, EPI_ACC = 1, EPI_QKV = 2 };
+enum { EPI_SWIGLU = 0, EPI_ACC = 1, EPI_QKV = 2, EPI_SWIGLU_BWD = 3 };
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) char lds_char;
@@ -78,18 +80,21 @@ struct Cfg {
   static constexpr int WAVES = WGM * WGN, THREADS = kWave * WAVES;
   static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int TM = WM / 32, TN = WN / 32;
-  static constexpr int TNB = EPI == EPI_SWIGLU ? 2 * TN : TN;
-  static constexpr int NB = EPI == EPI_SWIGLU ? 2 * BN : BN;  // B rows of an NT panel
-  static constexpr int A_BYTES = BM * BK * 2;
+  static constexpr bool BWD = EPI == EPI_SWIGLU_BWD;
+  static constexpr int NAP = BWD ? 2 : 1;                                  // A panels
+  static constexpr int NBP = EPI == EPI_SWIGLU ? 2 : (BWD ? 3 : 1);        // B panels
+  static constexpr int TNB = NBP * TN;
+  static constexpr int NB = NBP * BN;                         // B rows of an NT panel
+  static constexpr int A_BYTES = NAP * BM * BK * 2;
   static constexpr int B_BYTES = NB * BK * 2;                  // NT [NB][64] or NN [64][BN]
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int LDS_BYTES = STAGES * STAGE;
   // Operand load instructions one wavefront issues per stage.
-  static constexpr int LOADS = BM / 8 / WAVES + (NN ? BK * (BN * 2) / 1024 / WAVES : NB / 8 / WAVES);
+  static constexpr int LOADS = NAP * BM / 8 / WAVES + (NN ? BK * (BN * 2) / 1024 / WAVES : NB / 8 / WAVES);
   static_assert(STAGES >= 2 && LDS_BYTES <= 160 * 1024, "LDS ring");
   static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
   static constexpr int NN_RB = BN * 2;                         // NN panel row bytes
-  static_assert(!(NN && EPI == EPI_SWIGLU), "SwiGLU operands are [N, K]");
+  static_assert(!(NN && (EPI == EPI_SWIGLU || BWD)), "SwiGLU operands are [N, K]");
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
   static_assert((BM / 8) % WAVES == 0 && (NB / 8) % WAVES == 0, "NT DMA cover");
   static_assert(!NN || (BK * NN_RB / 1024) % WAVES == 0, "NN DMA cover");
@@ -160,11 +165,15 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
   auto dma_stage = [&](int stage, int k0) {
     lds_char* S = Ls + stage * C::STAGE;
     dma_nt<BM, C::WAVES>(S, P.A, P.lda, m0, P.M, k0, wave, lane);
+    if constexpr (C::BWD) dma_nt<BM, C::WAVES>(S + BM * BK * 2, P.A2, P.lda, m0, P.M, k0, wave, lane);
     if constexpr (NN) {
       dma_nn<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, k0, P.Kb_rows, n0, P.N, wave, lane);
-    } else if constexpr (EPI == EPI_SWIGLU) {
+    } else if constexpr (EPI == EPI_SWIGLU || C::BWD) {
       dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
       dma_nt<BN, C::WAVES>(S + C::A_BYTES + BN * BK * 2, P.B2, P.ldb, n0, P.N, k0, wave, lane);
+      if constexpr (C::BWD)
+        dma_nt<BN, C::WAVES>(S + C::A_BYTES + 2 * BN * BK * 2, P.B3, P.ldb, n0, P.N, k0, wave,
+                             lane);
     } else {
       dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
     }
@@ -209,10 +218,15 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
     const lds_char* SB = SA + C::A_BYTES;
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
-      u32x4 a[TM], b[TNB];
+      u32x4 a[TM], a2[TM], b[TNB];
       const int xo = opa ^ (32 * s);
 #pragma unroll
       for (int i = 0; i < TM; ++i) a[i] = lds_read16(SA + (wm * C::WM + 32 * i) * 128 + xo);
+      if constexpr (C::BWD) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          a2[i] = lds_read16(SA + BM * BK * 2 + (wm * C::WM + 32 * i) * 128 + xo);
+      }
 #pragma unroll
       for (int j = 0; j < TNB; ++j) {
         if constexpr (NN) {
@@ -221,28 +235,33 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
           const u32x2 hi = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_hi ^ cx));
           b[j] = u32x4{lo[0], lo[1], hi[0], hi[1]};
         } else {
-          const int brow = j < TN ? wn * C::WN + 32 * j : BN + wn * C::WN + 32 * (j - TN);
+          const int brow = (j / TN) * BN + wn * C::WN + 32 * (j % TN);  // panel j / TN
           b[j] = lds_read16(SB + brow * 128 + xo);
         }
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TNB; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < TNB; ++j)
+          acc[i][j] = mfma32(C::BWD && j >= 2 * TN ? a2[i] : a[i], b[j], acc[i][j]);
     }
     // Issue order: the operand reads of k-substep s+1 are spread between the MFMAs of
-    // substep s, so LDS latency hides behind matrix work.
+    // substep s (R / M per MFMA, one more for the first R mod M), so LDS latency hides
+    // behind matrix work.
     {
-      constexpr int R = TM + (NN ? 2 : 1) * TNB;  // LDS reads per substep
-      constexpr int M = TM * TNB;                 // MFMAs per substep
-      static_assert(R <= M, "one read per MFMA at most");
+      constexpr int R = C::NAP * TM + (NN ? 2 : 1) * TNB;  // LDS reads per substep
+      constexpr int M = TM * TNB;                          // MFMAs per substep
+      constexpr int RM = R / M;
       __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
 #pragma unroll
       for (int s = 0; s < BK / 16; ++s)
 #pragma unroll
         for (int i = 0; i < M; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          if (s + 1 < BK / 16 && i < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          if (s + 1 < BK / 16) {
+            if (i < R % M) __builtin_amdgcn_sched_group_barrier(0x100, RM + 1, 0);
+            else if (RM > 0) __builtin_amdgcn_sched_group_barrier(0x100, RM, 0);
+          }
         }
     }
   }
@@ -259,6 +278,65 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
   static_assert(C::WAVES * 32 * EST * 4 <= C::LDS_BYTES, "epilogue staging fits");
   float* E = reinterpret_cast<float*>(L) + wave * 32 * EST;
   const int ncol0 = n0 + wn * C::WN;
+  if constexpr (C::BWD) {
+    // SwiGLU backward.  Per 32-row block: dG, dU and Hs replace G, U and dHs in the
+    // accumulators, then each goes through LDS once: dG and dU to their row-major
+    // outputs (4-column chunks, as the forward's Hs), and all three transposed (each
+    // lane writes 8 consecutive rows of one column as one 16-byte vector).
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float g = acc[i][j][e], u = acc[i][j + TN][e], dh = acc[i][j + 2 * TN][e];
+          const float sg = 1.f / (1.f + __expf(-g));
+          const float sl = g * sg;
+          acc[i][j][e] = dh * u * (sg * (1.f + g * (1.f - sg)));  // dG
+          acc[i][j + TN][e] = dh * sl;                           // dU
+          acc[i][j + 2 * TN][e] = sl * u;                        // Hs
+        }
+      const int mrow0 = m0 + wm * C::WM + 32 * i;
+#pragma unroll
+      for (int q = 0; q < 3; ++q) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            E[(8 * (e >> 2) + 4 * hh + (e & 3)) * EST + 32 * j + l32] = acc[i][q * TN + j][e];
+        __syncthreads();
+        if (q < 2) {
+          uint16_t* H = q == 0 ? P.H : P.H2;
+#pragma unroll
+          for (int r = 0; r < PER_LANE; ++r) {
+            const int idx = r * kWave + lane, row = idx / CPR, c4 = idx % CPR;
+            const int mm = mrow0 + row, nn = ncol0 + 4 * c4;
+            if (mm >= P.M || nn >= P.ldh) continue;  // columns N..ldh: zero padding
+            const f32x4 v = *reinterpret_cast<const f32x4*>(E + row * EST + 4 * c4);
+            *reinterpret_cast<u32x2*>(H + (size_t)mm * P.ldh + nn) =
+                nn < P.N ? u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])}
+                         : u32x2{0u, 0u};
+          }
+        }
+        uint16_t* T = q == 0 ? P.T0 : (q == 1 ? P.T1 : P.T2);
+        for (int k = lane; k < 4 * C::WN; k += kWave) {
+          const int c = k % C::WN, r0 = 8 * (k / C::WN);
+          const int nn = ncol0 + c, mm = mrow0 + r0;
+          if (nn >= P.N || mm >= P.ldt) continue;  // rows M..ldt: zero padding
+          uint32_t w[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float v0 = mm + 2 * e < P.M ? E[(r0 + 2 * e) * EST + c] : 0.f;
+            const float v1 = mm + 2 * e + 1 < P.M ? E[(r0 + 2 * e + 1) * EST + c] : 0.f;
+            w[e] = pack_bf16x2(v0, v1);
+          }
+          *reinterpret_cast<u32x4*>(T + (size_t)nn * P.ldt + mm) = u32x4{w[0], w[1], w[2], w[3]};
+        }
+        __syncthreads();
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -364,6 +442,19 @@ hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s) {
 
 hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s) {
   return launch<256, 256, 2, 4, true, EPI_ACC, 2>(p, s);
+}
+
+// SwiGLU backward (M = S_loc, N = F/D): 128 x 128 tiles with five 16 KB operand panels
+// per K step (X, dY; W1, W3, W2), two slots = 160 KB.
+hipError_t launch_gemm_swiglu_bwd(const GemmParams& p, hipStream_t s) {
+  if (p.ldt % 8 != 0 || p.ldt < p.M) return hipErrorInvalidValue;
+  return launch<128, 128, 2, 4, false, EPI_SWIGLU_BWD, 2>(p, s);
+}
+
+// Weight gradients (M = F/D, N = h, K = tokens): 128 x 128 tiles make 352 at the 7B
+// shape where 256 x 256 would make 96.
+hipError_t launch_gemm_nn_acc_small(const GemmParams& p, hipStream_t s) {
+  return launch<128, 128, 2, 4, true, EPI_ACC, 2>(p, s);
 }
 
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s) {

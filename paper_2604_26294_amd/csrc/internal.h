@@ -14,7 +14,7 @@ struct GemmParams {
   int lda;
   const uint16_t* B;
   int ldb;
-  const uint16_t* B2;  // SwiGLU only: the up-projection operand, same layout as B
+  const uint16_t* B2;  // SwiGLU (both directions): the up-projection operand, layout of B
   int M, N, K;         // K: contraction length, a multiple of 64
   int Kb_rows;         // [K, N] operands: rows actually present (rows >= Kb_rows are clamped)
 
@@ -22,6 +22,19 @@ struct GemmParams {
   // N <= n < ldh (the zero padding that lets the down projection contract over ldh).
   uint16_t* H;
   int ldh;
+
+  // SwiGLU backward (fused products G = A B^T, U = A B2^T and dHs = A2 B3^T, all NT
+  // with the same K): with s = SiLU(G), s' its derivative,
+  //   dG = dHs * U * s'  and  dU = dHs * s  -> H, H2 [M, ldh] bf16 (columns N..ldh zero),
+  //   dG^T, dU^T and Hs^T = (s * U)^T       -> T0, T1, T2 [N, ldt] bf16, row n holding
+  //   column n of the product for every m < M (columns M..ldt zero).
+  const uint16_t* A2;
+  const uint16_t* B3;
+  uint16_t* H2;
+  uint16_t* T0;
+  uint16_t* T1;
+  uint16_t* T2;
+  int ldt;
 
   // Accumulate epilogue: Y[m, n] = base + C, base = bf16 R[m, n] if R, else Y[m, n]
   // if accumulate, else 0; optionally U[m, n] = bf16(Y[m, n]).
@@ -53,7 +66,11 @@ struct GemmParams {
 };
 
 hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s);
+hipError_t launch_gemm_swiglu_bwd(const GemmParams& p, hipStream_t s);
 hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s);
+// The accumulate epilogue on 128 x 128 tiles, for products with few output tiles
+// (the weight gradients: F/D x h outputs).
+hipError_t launch_gemm_nn_acc_small(const GemmParams& p, hipStream_t s);
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s);
 
 // Causal flash attention of one rank's queries for the heads of one shard.

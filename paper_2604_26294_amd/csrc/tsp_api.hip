@@ -122,6 +122,25 @@ AttnWs attn_ws(const Dims& d) {
   return w;
 }
 size_t ws_attn(const Dims& d) { return attn_ws(d).total; }
+// MLP backward workspace: dG, dU [M, F/D rounded up to 64] bf16 (the A operands of the
+// dX products), then dG^T, dU^T, Hs^T [F/D, M rounded up to 64] bf16 (the A operands of
+// the weight-gradient products, zero-padded past M).
+struct MlpBwdWs {
+  size_t dg, du, dgt, dut, hst, total;
+  int m_pad;
+};
+MlpBwdWs mlp_bwd_ws(const Dims& d) {
+  MlpBwdWs w;
+  w.m_pad = (int)((d.M + 63) / 64 * 64);
+  const size_t rm = align_up((size_t)d.M * d.fs_pad * 2), tr = align_up((size_t)d.fs * w.m_pad * 2);
+  w.dg = 0;
+  w.du = rm;
+  w.dgt = 2 * rm;
+  w.dut = 2 * rm + tr;
+  w.hst = 2 * rm + 2 * tr;
+  w.total = 2 * rm + 3 * tr;
+  return w;
+}
 size_t ws_layer(const Dims& d) {
   const size_t a = ws_mlp(d), b = ws_attn(d);
   return align_up((size_t)d.M * d.h * 2) + (a > b ? a : b);
@@ -134,7 +153,8 @@ tsp_status check_ptr(const void* p) {
   return aligned(p) ? TSP_OK : TSP_ERR_ALIGN;
 }
 
-tsp_status check_shards(const uint16_t* const* arr, int D) {
+template <typename T>
+tsp_status check_shards(T* const* arr, int D) {
   if (!arr) return TSP_ERR_NULL;
   for (int i = 0; i < D; ++i) {
     const tsp_status st = check_ptr(arr[i]);
@@ -243,6 +263,78 @@ tsp_status run_mlp(const Dims& d, const uint16_t* x, const uint16_t* const* wg,
   return TSP_OK;
 }
 
+// Backward of run_mlp (same ring order).  Per shard: one fused GEMM for G, U, dHs and
+// the SwiGLU backward, two accumulating products for dX, three for the weight
+// gradients (each [F/D, h], contracting over the M tokens).
+tsp_status run_mlp_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
+                       const uint16_t* const* wg, const uint16_t* const* wu,
+                       const uint16_t* const* wd, float* dx, int accumulate,
+                       float* const* dwg, float* const* dwu, float* const* dwd, char* ws,
+                       hipStream_t st) {
+  const MlpBwdWs w = mlp_bwd_ws(d);
+  uint16_t* dg = reinterpret_cast<uint16_t*>(ws + w.dg);
+  uint16_t* du = reinterpret_cast<uint16_t*>(ws + w.du);
+  uint16_t* dgt = reinterpret_cast<uint16_t*>(ws + w.dgt);
+  uint16_t* dut = reinterpret_cast<uint16_t*>(ws + w.dut);
+  uint16_t* hst = reinterpret_cast<uint16_t*>(ws + w.hst);
+  for (int t = 0; t < d.D; ++t) {
+    const int j = ((d.p - t) % d.D + d.D) % d.D;
+    GemmParams g = {};
+    g.A = x;
+    g.A2 = dy;
+    g.lda = d.h;
+    g.B = wg[j];
+    g.B2 = wu[j];
+    g.B3 = wd[j];
+    g.ldb = d.h;
+    g.M = (int)d.M;
+    g.N = d.fs;
+    g.K = d.h;
+    g.H = dg;
+    g.H2 = du;
+    g.ldh = d.fs_pad;
+    g.T0 = dgt;
+    g.T1 = dut;
+    g.T2 = hst;
+    g.ldt = w.m_pad;
+    TSP_LAUNCH(TSP_KERNEL_BWD_GATE, st, tsp::launch_gemm_swiglu_bwd(g, st));
+
+    // dX (+)= dG W_gate[j] + dU W_up[j]: [M, F/D] x [F/D, h], padded columns are zero.
+    for (int k = 0; k < 2; ++k) {
+      GemmParams p = {};
+      p.A = k == 0 ? dg : du;
+      p.lda = d.fs_pad;
+      p.B = k == 0 ? wg[j] : wu[j];
+      p.ldb = d.h;
+      p.M = (int)d.M;
+      p.N = d.h;
+      p.K = d.fs_pad;
+      p.Kb_rows = d.fs;
+      p.Y = dx;
+      p.ldy = d.h;
+      p.accumulate = (t > 0 || k > 0 || accumulate) ? 1 : 0;
+      TSP_LAUNCH(TSP_KERNEL_BWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+    }
+    // dW (+)= (dG^T | dU^T | Hs^T) (X | X | dY): [F/D, M] x [M, h], padded rows are zero.
+    for (int k = 0; k < 3; ++k) {
+      GemmParams p = {};
+      p.A = k == 0 ? dgt : (k == 1 ? dut : hst);
+      p.lda = w.m_pad;
+      p.B = k < 2 ? x : dy;
+      p.ldb = d.h;
+      p.M = d.fs;
+      p.N = d.h;
+      p.K = w.m_pad;
+      p.Kb_rows = (int)d.M;
+      p.Y = k == 0 ? dwg[j] : (k == 1 ? dwu[j] : dwd[j]);
+      p.ldy = d.h;
+      p.accumulate = accumulate ? 1 : 0;
+      TSP_LAUNCH(TSP_KERNEL_BWD_DW, st, tsp::launch_gemm_nn_acc_small(p, st));
+    }
+  }
+  return TSP_OK;
+}
+
 GemmParams qkv_params(const Dims& d, const uint16_t* x, const uint16_t* shard, int r,
                       uint16_t* q_ws, uint16_t* kb, uint16_t* vb, bool with_q) {
   GemmParams g = {};
@@ -346,6 +438,7 @@ tsp_status tsp_workspace_bytes(const tsp_shape* shape, int op, size_t* bytes) {
     case TSP_OP_MLP: *bytes = ws_mlp(d); return TSP_OK;
     case TSP_OP_ATTN: *bytes = ws_attn(d); return TSP_OK;
     case TSP_OP_LAYER: *bytes = ws_layer(d); return TSP_OK;
+    case TSP_OP_MLP_BWD: *bytes = mlp_bwd_ws(d).total; return TSP_OK;
     default: return TSP_ERR_SHAPE;
   }
 }
@@ -366,6 +459,30 @@ tsp_status tsp_mlp_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
   if (d.M == 0) return TSP_OK;
   return run_mlp(d, x_loc, w_gate, w_up, w_down, y_loc, accumulate,
                  static_cast<uint16_t*>(ws), stream);
+}
+
+tsp_status tsp_mlp_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
+                            const uint16_t* dy_loc, const uint16_t* const* w_gate,
+                            const uint16_t* const* w_up, const uint16_t* const* w_down,
+                            float* dx_loc, int accumulate, float* const* dw_gate,
+                            float* const* dw_up, float* const* dw_down, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_ptr(dy_loc));
+  TSP_TRY(check_ptr(dx_loc));
+  TSP_TRY(check_shards(w_gate, d.D));
+  TSP_TRY(check_shards(w_up, d.D));
+  TSP_TRY(check_shards(w_down, d.D));
+  TSP_TRY(check_shards(dw_gate, d.D));
+  TSP_TRY(check_shards(dw_up, d.D));
+  TSP_TRY(check_shards(dw_down, d.D));
+  TSP_TRY(check_ptr(ws));
+  if (ws_bytes < mlp_bwd_ws(d).total) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  return run_mlp_bwd(d, x_loc, dy_loc, w_gate, w_up, w_down, dx_loc, accumulate, dw_gate,
+                     dw_up, dw_down, static_cast<char*>(ws), stream);
 }
 
 tsp_status tsp_kv_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,

@@ -95,6 +95,22 @@ class RankProblem:
                             accumulate, self.ws)
         return self.y
 
+    def mlp_bwd(self, dy_loc, accumulate=False):
+        """MLP backward of this rank for the bf16 upstream gradient dy_loc [B, S_loc, h];
+        returns (dx, dw_gate, dw_up, dw_down), fp32 device tensors (lists per shard)."""
+        wl = self.wl
+        if not hasattr(self, "dx"):
+            fs = wl.ffn // wl.degree
+            dev = self.device
+            self.dx = torch.zeros((wl.batch, wl.s_loc, wl.hidden), dtype=torch.float32, device=dev)
+            self.dw = [[torch.zeros((fs, wl.hidden), dtype=torch.float32, device=dev)
+                        for _ in range(wl.degree)] for _ in range(3)]
+            nbytes = T.workspace_bytes(self.shape, T.OP_MLP_BWD)
+            self.ws_bwd = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+        T.tsp_mlp_rank_bwd(self.shape, self.x_loc, dy_loc, self.w1, self.w3, self.w2, self.dx,
+                           accumulate, self.dw[0], self.dw[1], self.dw[2], self.ws_bwd)
+        return self.dx, self.dw[0], self.dw[1], self.dw[2]
+
     def layer(self):
         T.tsp_layer_rank_fwd(self.shape, self.x_loc, self.attn, self.w1, self.w3, self.w2,
                              self.k_buf, self.v_buf, self.y, self.ws)

@@ -7,7 +7,8 @@ parity test start from the same bf16 bit patterns.
 
 Recipe: tensor ``k`` of a workload is drawn with
 ``numpy.random.default_rng([seed, k]).standard_normal(..., dtype=float32) * std``,
-then rounded to bf16.  Tensor ids: x=0, W_Q=1, W_K=2, W_V=3, W_O=4, W1=5, W3=6, W2=7.
+then rounded to bf16.  Tensor ids: x=0, W_Q=1, W_K=2, W_V=3, W_O=4, W1=5, W3=6, W2=7,
+and dY=8 (the upstream gradient of the MLP output for the backward).
 Activations use ``x_std`` (1.0), weights ``w_std`` (0.02, or 0.015 for the 70B shape).
 
 Weight orientations are the paper's (Algorithms 1 and 2): W_Q [n_h d, h],
@@ -20,7 +21,7 @@ import numpy as np
 
 from .workloads import Workload
 
-TENSOR_ID = {"x": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4, "w1": 5, "w3": 6, "w2": 7}
+TENSOR_ID = {"x": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4, "w1": 5, "w3": 6, "w2": 7, "dy": 8}
 
 _CHUNK_ELEMS = 1 << 24
 
@@ -67,6 +68,11 @@ def gaussian_bf16(seed: int, tensor_id: int, shape, std: float) -> np.ndarray:
 def make_x_full(wl: Workload) -> np.ndarray:
     """Activations of the whole sequence, [B, S, h] bf16 bits."""
     return gaussian_bf16(wl.seed, TENSOR_ID["x"], (wl.batch, wl.seq, wl.hidden), wl.x_std)
+
+
+def make_dy_full(wl: Workload) -> np.ndarray:
+    """Upstream gradient of the MLP output for the whole sequence, [B, S, h] bf16 bits."""
+    return gaussian_bf16(wl.seed, TENSOR_ID["dy"], (wl.batch, wl.seq, wl.hidden), wl.x_std)
 
 
 def make_weights(wl: Workload) -> dict:

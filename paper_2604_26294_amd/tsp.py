@@ -19,9 +19,10 @@ TSP_ERR_HIP = 7
 STATUS_NAMES = {0: "TSP_OK", 1: "TSP_ERR_NULL", 2: "TSP_ERR_SHAPE", 3: "TSP_ERR_RANK",
                 4: "TSP_ERR_ALIGN", 5: "TSP_ERR_WORKSPACE", 6: "TSP_ERR_UNSUPPORTED",
                 7: "TSP_ERR_HIP"}
-OP_MLP, OP_ATTN, OP_LAYER = 0, 1, 2
+OP_MLP, OP_ATTN, OP_LAYER, OP_MLP_BWD = 0, 1, 2, 3
 LAYOUT_CONTIGUOUS, LAYOUT_ZIGZAG = 0, 1
-KERNELS = ("gate_up", "down", "qkv", "attn", "oproj")  # TSP_KERNEL_* order
+KERNELS = ("gate_up", "down", "qkv", "attn", "oproj",  # TSP_KERNEL_* order
+           "bwd_gate", "bwd_dx", "bwd_dw")
 
 
 class TspError(RuntimeError):
@@ -58,6 +59,7 @@ def _load() -> ctypes.CDLL:
     PP = ctypes.POINTER(ctypes.c_void_p)
     sig = {
         "tsp_mlp_rank_fwd": [SH, P, PP, PP, PP, P, I, VP, SZ, VP],
+        "tsp_mlp_rank_bwd": [SH, P, P, PP, PP, PP, P, I, PP, PP, PP, VP, SZ, VP],
         "tsp_kv_rank_fwd": [SH, P, PP, P, P, VP],
         "tsp_attn_rank_fwd": [SH, P, PP, P, P, P, I, VP, SZ, VP],
         "tsp_layer_rank_fwd": [SH, P, PP, PP, PP, PP, P, P, P, VP, SZ, VP],
@@ -137,6 +139,19 @@ def tsp_mlp_rank_fwd(shape, x_loc, w_gate, w_up, w_down, y_loc, accumulate, ws, 
     _check(lib.tsp_mlp_rank_fwd(ctypes.byref(shape), _ptr(x_loc), g, u, d, _ptr(y_loc),
                                 int(accumulate), _ptr(ws), _nbytes(ws), _stream(stream)),
            "tsp_mlp_rank_fwd")
+
+
+def tsp_mlp_rank_bwd(shape, x_loc, dy_loc, w_gate, w_up, w_down, dx_loc, accumulate, dw_gate,
+                     dw_up, dw_down, ws, stream=None):
+    g, _g = _ptrs(w_gate)
+    u, _u = _ptrs(w_up)
+    d, _d = _ptrs(w_down)
+    dg, _dg = _ptrs(dw_gate)
+    du, _du = _ptrs(dw_up)
+    dd, _dd = _ptrs(dw_down)
+    _check(lib.tsp_mlp_rank_bwd(ctypes.byref(shape), _ptr(x_loc), _ptr(dy_loc), g, u, d,
+                                _ptr(dx_loc), int(accumulate), dg, du, dd, _ptr(ws),
+                                _nbytes(ws), _stream(stream)), "tsp_mlp_rank_bwd")
 
 
 def tsp_kv_rank_fwd(shape, x_loc, w_attn, k_buf, v_buf, stream=None):

@@ -27,7 +27,8 @@ def _declared_functions():
 def test_every_declared_symbol_is_exported():
     names = _declared_functions()
     assert {"tsp_mlp_rank_fwd", "tsp_attn_rank_fwd", "tsp_layer_rank_fwd", "tsp_kv_rank_fwd",
-            "tsp_workspace_bytes", "tsp_status_str", "tsp_abi_version"} <= set(names)
+            "tsp_mlp_rank_bwd", "tsp_workspace_bytes", "tsp_status_str",
+            "tsp_abi_version"} <= set(names)
     raw = ctypes.CDLL(T._LIB_PATH)
     for n in names:
         assert hasattr(raw, n), n
@@ -50,7 +51,11 @@ def test_workspace_covers_intermediates(wl):
     assert mlp >= m * (wl.ffn // wl.degree) * 2                        # gated product
     assert attn >= 2 * m * (wl.n_heads // wl.degree) * wl.head_dim * 2  # Q and A
     assert layer >= m * wl.hidden * 2 + max(mlp, attn)                 # + bf16(u)
-    for v in (mlp, attn, layer):
+    bwd = T.workspace_bytes(sh, T.OP_MLP_BWD)
+    m_pad = (m + 63) // 64 * 64
+    fs = wl.ffn // wl.degree
+    assert bwd >= 2 * m * fs * 2 + 3 * fs * m_pad * 2  # dG, dU and three transposes
+    for v in (mlp, attn, layer, bwd):
         assert v % 256 == 0
 
 
@@ -112,6 +117,30 @@ def test_entry_points_reject_bad_arguments():
     assert L.tsp_layer_rank_fwd(ctypes.byref(bad), FAKE, good, good, good, good, FAKE, FAKE,
                                 FAKE, FAKE, ws_need, None) == 3
     assert L.tsp_kv_rank_fwd(ctypes.byref(bad), FAKE, good, FAKE, FAKE, None) == 3
+
+
+def test_backward_rejects_bad_arguments():
+    sh = _shape()
+    need = T.workspace_bytes(sh, T.OP_MLP_BWD)
+    good, _k1 = _arr(2)
+    nul, _k2 = _arr(2, 0)
+    mis, _k3 = _arr(2, FAKE + 4)
+    L = T.lib
+    # argument list that would pass validation; every call below breaks one argument, so
+    # none of them reaches a launch
+    args = [ctypes.byref(sh), FAKE, FAKE, good, good, good, FAKE, 0, good, good, good, FAKE, need,
+            None]
+    for pos, val, code in [(1, None, 1), (2, None, 1), (6, None, 1), (8, None, 1), (9, nul, 1),
+                           (10, mis, 4), (2, FAKE + 2, 4), (12, need - 1, 5)]:
+        a = list(args)
+        a[pos] = val
+        if pos == 12:
+            a[11] = FAKE
+        assert L.tsp_mlp_rank_bwd(*a) == code, (pos, code)
+    bad = _shape(rank=7)
+    a = list(args)
+    a[0] = ctypes.byref(bad)
+    assert L.tsp_mlp_rank_bwd(*a) == 3
 
 
 def test_empty_batch_is_a_no_op():
