@@ -11,9 +11,11 @@ shards and the K/V rows of the earlier ranks (the modelled all-gather) are resid
 in HBM before timing starts.  Prints one JSON line on stdout; progress goes to stderr.
 
 Besides the layer call the line reports the attention-only and MLP-only entry points
-timed separately ("blocks"), the algorithmic HBM bytes of a step and the bandwidth they
-imply ("hbm"), the paper's non-causal F_layer / D for reference, and with --rank-sweep
-the layer time of every rank of the group and the max/min imbalance.
+timed separately ("blocks"), the per-rank MLP backward (``tsp_mlp_rank_bwd``, with its
+kernel classes) on the same rank ("blocks.mlp_bwd"), the algorithmic HBM bytes of a step
+and the bandwidth they imply ("hbm"), the paper's non-causal F_layer / D for reference,
+and with --rank-sweep the layer time of every rank of the group and the max/min
+imbalance.
 """
 from __future__ import annotations
 
@@ -71,7 +73,10 @@ def kernel_flops(wl):
     kd = wl.n_kv_heads // D * wl.head_dim
     return {"gate_up": 2.0 * m * 2 * fs * h, "down": 2.0 * m * h * fs,
             "qkv": 2.0 * m * (qd + 2 * kd) * h, "attn": step_attn_core_flops(wl),
-            "oproj": 2.0 * m * qd * h}
+            "oproj": 2.0 * m * qd * h,
+            # MLP backward: G, U and dHs in one pass; one dX product; one weight gradient
+            "bwd_gate": 2.0 * m * 3 * fs * h, "bwd_dx": 2.0 * m * fs * h,
+            "bwd_dw": 2.0 * m * fs * h}
 
 
 def cpu_baseline(wl, x_bits, w_bits, rows: int):
@@ -183,7 +188,7 @@ def main(argv=None):
     from paper_2604_26294_amd import inputs as I
     from paper_2604_26294_amd import tsp as T
     from paper_2604_26294_amd.flops import paper_layer_flops, rank_algorithmic_bytes, rank_flops
-    from paper_2604_26294_amd.harness import RankProblem
+    from paper_2604_26294_amd.harness import RankProblem, to_device_bf16
 
     wl = BY_NAME[args.workload].with_layout(1 if args.layout == "zigzag" else 0)
     if args.rank is not None:
@@ -254,6 +259,34 @@ def main(argv=None):
         "mlp": {"ms": round(ms_mlp, 4), "flops": rf.mlp,
                 "tflops": round(rf.mlp / (ms_mlp * 1e-3) / 1e12, 2)},
     }
+    # The per-rank MLP backward on the same rank: dX and this rank's contribution to
+    # every shard's weight gradients, for a synthetic upstream gradient.  Executed
+    # products: G, U (recomputed) and dHs, dX (two), the three weight gradients = 16 M F h
+    # FLOPs; the backward alone (without recomputing G, U) is 12 M F h.
+    dy = to_device_bf16(I.gaussian_bf16(wl.seed, I.TENSOR_ID["dy"],
+                                        (wl.batch, wl.s_loc, wl.hidden), wl.x_std))
+    for _ in range(2):
+        prob.mlp_bwd(dy)
+    torch.cuda.synchronize()
+    T.tsp_profile_enable(True)
+    ms_bwd = time_calls(lambda: prob.mlp_bwd(dy), args.steps, 0)
+    T.tsp_profile_enable(False)
+    m_tok = wl.batch * wl.s_loc
+    bwd_flops = 16.0 * m_tok * wl.ffn * wl.hidden
+    bwd_kernels = {}
+    for k, name in enumerate(T.KERNELS):
+        if not name.startswith("bwd_"):
+            continue
+        tot, n = T.tsp_profile_read(k)
+        if n:
+            bwd_kernels[name] = {"avg_ms": round(tot / n, 5), "launches": n // args.steps,
+                                 "tflops": round(kf[name] / (tot / n * 1e-3) / 1e12, 2)}
+    blocks["mlp_bwd"] = {"ms": round(ms_bwd, 4), "flops": bwd_flops,
+                         "tflops": round(bwd_flops / (ms_bwd * 1e-3) / 1e12, 2),
+                         "flops_note": "16 M F h executed (G, U recomputed); 12 M F h without",
+                         "kernels": bwd_kernels}
+    del dy
+
     nbytes = rank_algorithmic_bytes(wl)
     hbm = {"algorithmic_bytes": nbytes, "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
            "frac_of_peak": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),

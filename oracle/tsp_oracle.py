@@ -176,6 +176,27 @@ def mlp_rank_bwd(x_loc, w1_shards, w3_shards, w2_shards, dy, p):
     return dx.reshape(x_loc.shape), dw1, dw3, dw2
 
 
+def mlp_rank_bwd_rows(x2, w1_shards, w3_shards, w2_shards, dy2, rows, shards, feats):
+    """Selected entries of mlp_rank_bwd for large shapes, each computed exactly from its
+    own definition: dX rows `rows` (sum over every shard) and, for each shard j in
+    `shards`, rows `feats` of dW1_j, dW3_j, dW2_j (sums over every token).  x2 and dy2
+    are the rank's tokens flattened, [M, h].  Returns (dx [len(rows), h], {j: (dW1,
+    dW3, dW2) rows [len(feats), h]})."""
+    dx = np.zeros((len(rows), x2.shape[1]))
+    for j in range(len(w1_shards)):
+        xr, dyr = x2[rows], dy2[rows]
+        dg, du = swiglu_bwd(xr @ w1_shards[j].T, xr @ w3_shards[j].T, dyr @ w2_shards[j].T)
+        dx += dg @ w1_shards[j] + du @ w3_shards[j]
+    dw = {}
+    for j in shards:
+        g = x2 @ w1_shards[j][feats].T          # [M, len(feats)]: columns feats of G
+        u = x2 @ w3_shards[j][feats].T
+        dhs = dy2 @ w2_shards[j][feats].T
+        dg, du = swiglu_bwd(g, u, dhs)
+        dw[j] = (dg.T @ x2, du.T @ x2, (silu(g) * u).T @ dy2)
+    return dx, dw
+
+
 def unpack_attn_shard(packed, heads_per_shard, kv_heads_per_shard, head_dim):
     """Split a packed shard [W_Q^(r); W_K^(r); W_V^(r); W_O^(r)^T] (Algorithm 1's
     packed broadcast buffer) into its four row blocks."""

@@ -71,6 +71,41 @@ def test_sampled_rows_match_unsharded_layer(wl, p):
     torch.cuda.empty_cache()
 
 
+BWD_CASES = [(L7B_64K, 7), (L70B_GQA, 7)]
+
+
+@pytest.mark.parametrize("wl,p", BWD_CASES, ids=[f"{w.name}-r{p}" for w, p in BWD_CASES])
+def test_mlp_backward_sampled_rows(wl, p):
+    """The ring-MLP backward at full size: sampled rows of dX and sampled feature rows of
+    two shards' weight gradients against the oracle's exact per-row sums."""
+    from paper_2604_26294_amd.harness import local_rows, to_device_bf16
+    print(f"[fullsize bwd] {wl.name} rank {p}", flush=True)
+    x_bits, w_bits, wf = _data(wl)
+    dy_bits = I.gaussian_bf16(wl.seed, I.TENSOR_ID["dy"], (wl.batch, wl.s_loc, wl.hidden),
+                              wl.x_std)
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    dx, dwg, dwu, dwd = prob.mlp_bwd(to_device_bf16(dy_bits))
+    torch.cuda.synchronize()
+    D, h = wl.degree, wl.hidden
+    fs = wl.ffn // D
+    m = wl.batch * wl.s_loc
+    rows = sorted({0, 1, m // 2, m - 1})
+    feats = sorted({0, 1, fs // 2, fs - 1})
+    shards = sorted({p, (p + 1) % D})
+    shard = [I.mlp_shard(wf, j, D) for j in range(D)]
+    x2 = I.bf16_bits_to_f64(local_rows(x_bits, wl, p)).reshape(m, h)
+    dy2 = I.bf16_bits_to_f64(dy_bits).reshape(m, h)
+    ref_dx, ref_dw = O.mlp_rank_bwd_rows(x2, [s[0] for s in shard], [s[1] for s in shard],
+                                         [s[2] for s in shard], dy2, rows, shards, feats)
+    assert_close(dx.reshape(m, h)[rows].double().cpu().numpy(), ref_dx, f"{wl.name} dX rows")
+    for j in shards:
+        for name, got, ref in zip(("dW_gate", "dW_up", "dW_down"), (dwg[j], dwu[j], dwd[j]),
+                                  ref_dw[j]):
+            assert_close(got[feats].double().cpu().numpy(), ref, f"{wl.name} {name}[{j}] rows")
+    del prob, dx, dwg, dwu, dwd
+    torch.cuda.empty_cache()
+
+
 def test_long_context_layer_output_is_finite_everywhere():
     """Every output element of the last rank of the long-context shape is finite."""
     wl = L7B_64K

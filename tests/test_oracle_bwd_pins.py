@@ -106,3 +106,18 @@ def test_backward_special_cases():
     assert O.silu_grad(np.array([0.0]))[0] == 0.5
     assert abs(O.silu_grad(np.array([40.0]))[0] - 1.0) < 1e-12
     assert abs(O.silu_grad(np.array([-40.0]))[0]) < 1e-12
+
+
+def test_sampled_rows_equal_the_full_backward():
+    x, w1, w3, w2, dy, degree = _problem(seed=7)
+    s1, s3, s2 = _shards(w1, degree), _shards(w3, degree), _shards(w2, degree)
+    xl, dyl = x[:, 2:4], dy[:, 2:4]
+    dx, dw1, dw3, dw2 = O.mlp_rank_bwd(xl, s1, s3, s2, dyl, 1)
+    h = x.shape[-1]
+    rows, feats, shards = [0, 3], [1, 2], [0, 2]
+    dxr, dwr = O.mlp_rank_bwd_rows(xl.reshape(-1, h), s1, s3, s2, dyl.reshape(-1, h), rows,
+                                   shards, feats)
+    assert np.allclose(dxr, dx.reshape(-1, h)[rows], rtol=1e-12, atol=1e-12)
+    for j in shards:
+        for got, full in zip(dwr[j], (dw1[j], dw3[j], dw2[j])):
+            assert np.allclose(got, full[feats], rtol=1e-12, atol=1e-12)
