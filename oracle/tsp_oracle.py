@@ -381,6 +381,146 @@ def layer_rank_zigzag(x_shards, attn_shards, w1_shards, w3_shards, w2_shards, p,
 
 
 # ---------------------------------------------------------------------------
+# Backward of the attention block (per rank).  As for the MLP, the paper costs the
+# backward (Section 4) without printing it; these are the chain-rule gradients of
+# Algorithm 1's forward.  The all-gather of K and V becomes, in the backward, a
+# reduce-scatter of their gradients, so the work splits in two stages: every rank
+# produces contributions to the gradient of the whole gathered K-hat / V-hat of each
+# shard (attn_rank_bwd); the sum over ranks, restricted to a rank's own rows, is what
+# that rank back-propagates through its K / V projections (attn_kv_bwd).
+# ---------------------------------------------------------------------------
+
+def causal_attention_core_bwd(q, k, v, do, q_offset, scale):
+    """Gradients of o = causal_attention_core(q, k, v, q_offset, scale) for one head,
+    given do = dL/do [Lq, d].  With P the masked softmax of scale q k^T and o = P v:
+      dv = P^T do,   dP = do v^T,   dS_tj = P_tj (dP_tj - sum_m P_tm dP_tm),
+      dq = scale dS k,   dk = scale dS^T q.
+    Returns dq [Lq, d], dk [Lk, d], dv [Lk, d] (keys no query sees get zero)."""
+    lq = q.shape[0]
+    dq = np.zeros_like(q, dtype=np.float64)
+    dk = np.zeros_like(k, dtype=np.float64)
+    dv = np.zeros_like(v, dtype=np.float64)
+    for lo in range(0, lq, _Q_CHUNK):
+        hi = min(lq, lo + _Q_CHUNK)
+        kmax = min(k.shape[0], q_offset + hi)
+        p = causal_probs(q[lo:hi], k[:kmax], q_offset + lo, scale)
+        dp = do[lo:hi] @ v[:kmax].T
+        ds = p * (dp - np.sum(p * dp, axis=1, keepdims=True))
+        dv[:kmax] += p.T @ do[lo:hi]
+        dq[lo:hi] = scale * (ds @ k[:kmax])
+        dk[:kmax] += scale * (ds.T @ q[lo:hi])
+    return dq, dk, dv
+
+
+def rank_positions(seq, degree, p, layout):
+    """Global positions of rank p's local rows: a contiguous chunk, or the zigzag pair."""
+    if layout == "zigzag":
+        return zigzag_positions(seq, degree, p)
+    s_loc = seq // degree
+    return p * s_loc + np.arange(s_loc)
+
+
+def causal_calls(s_loc, degree, p, layout):
+    """Algorithm 1's CausalAttn calls on rank p as (first local row, end row, global
+    position of the first row, number of gathered keys the block attends to)."""
+    if layout == "zigzag":
+        s_c = s_loc // 2
+        s1, s2 = (p + 1) * s_c, (2 * degree - p) * s_c
+        return [(0, s_c, s1 - s_c, s1), (s_c, s_loc, s2 - s_c, s2)]
+    return [(0, s_loc, p * s_loc, (p + 1) * s_loc)]
+
+
+def attn_rank_bwd(x_loc, shards, kv_gathered, p, n_heads, n_kv_heads, head_dim, dy,
+                  scale=None, layout="contiguous"):
+    """First stage of the attention backward on rank p, for dy = dL/dY [B, S_loc, h].
+
+    For each shard r: recompute Q = X W_Q^(r)^T and A as the forward does; the block
+    output is Flatten(A) W_O^(r)^T, so dA = dY W_O^(r) and W_O^(r)^T's gradient gets
+    A^T dY; per query head, the causal attention backward against the gathered K-hat,
+    V-hat of shard r (prefix and alignment of each CausalAttn call as in the forward);
+    then dX gets dQ W_Q^(r) and W_Q^(r) gets dQ^T X.
+
+    Returns a dict:
+      dx        [B, S_loc, h]         the query path's part of dX;
+      dwq[r]    [H_s d, h]            this rank's contribution to dW_Q^(r);
+      dwo_t[r]  [H_s d, h]            its contribution to the gradient of W_O^(r)^T
+                                      (the packed shard's last block);
+      dk[r], dv[r]  [B, S, K_s, d]    its contributions to the gradients of shard r's
+                                      gathered K-hat and V-hat, in sequence order (zero
+                                      for keys none of its queries sees).
+    """
+    degree = len(shards)
+    hs_heads, ks_heads = n_heads // degree, n_kv_heads // degree
+    g = n_heads // n_kv_heads
+    d = head_dim
+    sc = default_scale(d, scale)
+    b_, s_loc, h = x_loc.shape
+    calls = causal_calls(s_loc, degree, p, layout)
+    x2 = x_loc.reshape(-1, h)
+    dy2 = dy.reshape(-1, h)
+    dx = np.zeros_like(x2, dtype=np.float64)
+    out = {"dwq": [None] * degree, "dwo_t": [None] * degree,
+           "dk": [None] * degree, "dv": [None] * degree}
+    for r in range(degree):
+        wq, _, _, wo_t = unpack_attn_shard(shards[r], hs_heads, ks_heads, d)
+        k_hat, v_hat = kv_gathered[r]
+        q = (x_loc @ wq.T).reshape(b_, s_loc, hs_heads, d)
+        da = (dy @ wo_t.T).reshape(b_, s_loc, hs_heads, d)
+        a = np.empty_like(q)
+        dq = np.empty_like(q)
+        dk = np.zeros_like(k_hat, dtype=np.float64)
+        dv = np.zeros_like(v_hat, dtype=np.float64)
+        for b in range(b_):
+            for i in range(hs_heads):
+                kh = i // g
+                for lo, hi, off, n_keys in calls:
+                    kk, vv = k_hat[b, :n_keys, kh], v_hat[b, :n_keys, kh]
+                    a[b, lo:hi, i] = causal_attention_core(q[b, lo:hi, i], kk, vv, off, sc)
+                    gq, gk, gv = causal_attention_core_bwd(q[b, lo:hi, i], kk, vv,
+                                                           da[b, lo:hi, i], off, sc)
+                    dq[b, lo:hi, i] = gq
+                    dk[b, :n_keys, kh] += gk
+                    dv[b, :n_keys, kh] += gv
+        dq2 = dq.reshape(-1, hs_heads * d)
+        dx += dq2 @ wq
+        out["dwq"][r] = dq2.T @ x2
+        out["dwo_t"][r] = a.reshape(-1, hs_heads * d).T @ dy2
+        out["dk"][r], out["dv"][r] = dk, dv
+    out["dx"] = dx.reshape(x_loc.shape)
+    return out
+
+
+def reduce_scatter_rows(contribs, degree, layout):
+    """The backward of the sequence-wise all-gather: sum the ranks' contributions
+    [B, S, ...] and hand rank q the rows at its own positions."""
+    total = np.sum(contribs, axis=0)
+    seq = total.shape[1]
+    return [total[:, rank_positions(seq, degree, q, layout)] for q in range(degree)]
+
+
+def attn_kv_bwd(x_loc, shards, dk_own, dv_own, n_heads, n_kv_heads, head_dim):
+    """Second stage of the attention backward on one rank: K = X W_K^(r)^T and
+    V = X W_V^(r)^T on its own rows, so with dk_own[r], dv_own[r] [B, S_loc, K_s, d] the
+    reduce-scattered gradients of its rows of K-hat, V-hat: dX gets dK W_K^(r) + dV W_V^(r),
+    and the rank contributes dK^T X to dW_K^(r) and dV^T X to dW_V^(r).
+    Returns (dx [B, S_loc, h], dwk list, dwv list)."""
+    degree = len(shards)
+    hs_heads, ks_heads = n_heads // degree, n_kv_heads // degree
+    h = x_loc.shape[-1]
+    x2 = x_loc.reshape(-1, h)
+    dx = np.zeros_like(x2, dtype=np.float64)
+    dwk, dwv = [None] * degree, [None] * degree
+    for r in range(degree):
+        _, wk, wv, _ = unpack_attn_shard(shards[r], hs_heads, ks_heads, head_dim)
+        gk = dk_own[r].reshape(-1, ks_heads * head_dim)
+        gv = dv_own[r].reshape(-1, ks_heads * head_dim)
+        dx += gk @ wk + gv @ wv
+        dwk[r] = gk.T @ x2
+        dwv[r] = gv.T @ x2
+    return dx.reshape(x_loc.shape), dwk, dwv
+
+
+# ---------------------------------------------------------------------------
 # Sampled rows of the unsharded attention block, for full-size checks.
 # ---------------------------------------------------------------------------
 

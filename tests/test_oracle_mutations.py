@@ -7,12 +7,16 @@ import numpy as np
 import pytest
 
 import oracle.tsp_oracle as O
+from tests import test_oracle_attn_bwd_pins as PA
 from tests import test_oracle_bwd_pins as PB
 from tests import test_oracle_pins as P
 
 _orig_probs = O.causal_probs
 _orig_unpack = O.unpack_attn_shard
 _orig_silu = O.silu
+_orig_core_bwd = O.causal_attention_core_bwd
+_orig_kv_bwd = O.attn_kv_bwd
+_orig_calls = O.causal_calls
 
 
 def _probs_strict_mask(q, k, q_offset, scale):          # j < t instead of j <= t
@@ -121,7 +125,56 @@ def _mlp_rank_bwd_skips_last_step(x_loc, w1s, w3s, w2s, dy, p):
     return dx, dw1, dw3, dw2
 
 
+def _core_bwd_no_rowsum(q, k, v, do, q_offset, scale):   # dS = P * dP (softmax term lost)
+    p = O.causal_probs(q, k[:q_offset + q.shape[0]], q_offset, scale)
+    kk, vv = k[:p.shape[1]], v[:p.shape[1]]
+    dp = do @ vv.T
+    ds = p * dp
+    dk, dv = np.zeros_like(k), np.zeros_like(v)
+    dk[:p.shape[1]] = scale * ds.T @ q
+    dv[:p.shape[1]] = p.T @ do
+    return scale * ds @ kk, dk, dv
+
+
+def _core_bwd_dq_unscaled(q, k, v, do, q_offset, scale):  # dQ misses the softmax scale
+    dq, dk, dv = _orig_core_bwd(q, k, v, do, q_offset, scale)
+    return dq / scale, dk, dv
+
+
+def _core_bwd_dk_from_probs(q, k, v, do, q_offset, scale):  # dK built from P, not dS
+    dq, _, dv = _orig_core_bwd(q, k, v, do, q_offset, scale)
+    p = O.causal_probs(q, k[:q_offset + q.shape[0]], q_offset, scale)
+    dk = np.zeros_like(k)
+    dk[:p.shape[1]] = scale * p.T @ q
+    return dq, dk, dv
+
+
+def _kv_bwd_no_v_path(x_loc, shards, dk_own, dv_own, n_heads, n_kv, d):
+    dx, dwk, dwv = _orig_kv_bwd(x_loc, shards, dk_own, [0 * t for t in dv_own], n_heads, n_kv, d)
+    _, dwk2, dwv2 = _orig_kv_bwd(x_loc, shards, dk_own, dv_own, n_heads, n_kv, d)
+    return dx, dwk2, dwv2
+
+
+def _reduce_scatter_no_sum(contribs, degree, layout):       # each rank keeps only its own
+    seq = contribs[0].shape[1]
+    return [contribs[q][:, O.rank_positions(seq, degree, q, layout)] for q in range(degree)]
+
+
+def _calls_zigzag_offsets_swapped(s_loc, degree, p, layout):
+    calls = _orig_calls(s_loc, degree, p, layout)
+    if len(calls) == 2:
+        (a0, a1, o1, n1), (b0, b1, o2, n2) = calls
+        return [(a0, a1, o2, n2), (b0, b1, o1, n1)]
+    return calls
+
+
 MUTATIONS = {
+    "attn_bwd_rowsum_dropped": ("causal_attention_core_bwd", _core_bwd_no_rowsum),
+    "attn_bwd_dq_unscaled": ("causal_attention_core_bwd", _core_bwd_dq_unscaled),
+    "attn_bwd_dk_from_probs": ("causal_attention_core_bwd", _core_bwd_dk_from_probs),
+    "attn_kv_bwd_misses_v_path": ("attn_kv_bwd", _kv_bwd_no_v_path),
+    "kv_grad_not_reduced": ("reduce_scatter_rows", _reduce_scatter_no_sum),
+    "attn_bwd_zigzag_calls_swapped": ("causal_calls", _calls_zigzag_offsets_swapped),
     "silu_grad_is_sigmoid": ("silu_grad", _silu_grad_sigmoid_only),
     "swiglu_bwd_swapped": ("swiglu_bwd", _swiglu_bwd_swapped),
     "bwd_dx_misses_up_path": ("mlp_rank_bwd", _mlp_rank_bwd_no_up_path),
@@ -155,6 +208,10 @@ PINS = [
     (PB.test_rank_backward_matches_finite_differences, ()),
     (PB.test_weight_gradients_sum_to_owner_and_dx_is_local, ()),
     (PB.test_backward_special_cases, ()),
+    (PA.test_two_stage_backward_is_the_unsharded_gradient, ("contiguous", 4, 2)),
+    (PA.test_two_stage_backward_is_the_unsharded_gradient, ("zigzag", 4, 2)),
+    (PA.test_first_stage_is_the_gradient_of_the_rank_forward, ("zigzag",)),
+    (PA.test_backward_special_cases, ()),
 ]
 
 
