@@ -165,6 +165,54 @@ tsp_status tsp_attn_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                              float* y_loc, int accumulate, void* ws, size_t ws_bytes,
                              hipStream_t stream);
 
+/* Backward of tsp_attn_rank_fwd on rank p, first stage.  As for the MLP, the paper
+ * costs the backward (Section 4) without printing it; these are the chain-rule
+ * gradients of Algorithm 1.  The forward's K/V all-gather becomes a reduce-scatter of
+ * the K/V gradients, so the backward has two stages: this one produces the rank's
+ * contributions to the gradients of every shard's gathered K-hat / V-hat; their sum
+ * over ranks, restricted to a rank's own rows (a collective outside this single-GPU
+ * library), is the input of tsp_attn_kv_rank_bwd.  For r = 0..D-1:
+ *   Q, A recomputed as in the forward (A with the log-sum-exp of every query's logits);
+ *   dA = dY W_O^(r);   dw_attn[r] W_O^T block (+)= A^T dY;
+ *   per head, with P the causal softmax weights, dP = dA V^T, dS = P * (dP - rowsum(dA * A)):
+ *     dQ = scale dS K,   dK-hat (+)= scale dS^T Q,   dV-hat (+)= P^T dA;
+ *   dX (+)= dQ W_Q^(r);   dw_attn[r] W_Q block (+)= dQ^T X.
+ * Q, A, dA, dQ, P, dS are rounded to bf16 for the matrix cores.
+ *   x_loc, w_attn        as for tsp_attn_rank_fwd
+ *   dy_loc  [B, S_loc, h] bf16     gradient of the attention block output (Y)
+ *   k_buf, v_buf [B, S, n_kv, d] bf16   the gathered K/V as the forward used them
+ *                                       (read only; rows past the last visible key unread)
+ *   dx_loc  [B, S_loc, h] fp32     the query path of dX: overwritten (accumulate == 0)
+ *                                  or added to
+ *   dw_attn[r] [(2*n_h/D + 2*n_kv/D) * d, h] fp32, the packed shard's layout (host array
+ *              of D device pointers): the W_Q and W_O^T row blocks are overwritten or
+ *              added to, as dx_loc; the W_K, W_V blocks are not touched
+ *   dk_buf, dv_buf [B, S, n_kv, d] fp32   this rank's contributions for all S rows
+ *              (zero where none of its queries sees the key), overwritten or added to
+ *   ws      workspace of at least tsp_workspace_bytes(shape, TSP_OP_ATTN_BWD) bytes */
+tsp_status tsp_attn_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
+                             const uint16_t* dy_loc, const uint16_t* const* w_attn,
+                             const uint16_t* k_buf, const uint16_t* v_buf, float* dx_loc,
+                             int accumulate, float* const* dw_attn, float* dk_buf,
+                             float* dv_buf, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Backward of the rank's K/V projections, second stage of the attention backward:
+ * with dK, dV the reduce-scattered gradients of this rank's rows of every shard's
+ * K-hat / V-hat (K = X W_K^(r)^T, V = X W_V^(r)^T on the rank's own rows), for r = 0..D-1:
+ *   dX (+)= dK_r W_K^(r) + dV_r W_V^(r);
+ *   dw_attn[r] W_K block (+)= dK_r^T X;   W_V block (+)= dV_r^T X.
+ *   x_loc, w_attn      as for tsp_attn_rank_fwd
+ *   dk_loc, dv_loc [B, S_loc, n_kv, d] bf16   rows in local order; columns of shard r's
+ *                      kv heads r*n_kv/D .. are dK_r, dV_r
+ *   dx_loc [B, S_loc, h] fp32   overwritten (accumulate == 0) or added to
+ *   dw_attn[r]         as for tsp_attn_rank_bwd; only the W_K, W_V blocks are written
+ *   ws      workspace of at least tsp_workspace_bytes(shape, TSP_OP_ATTN_KV_BWD) bytes */
+tsp_status tsp_attn_kv_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
+                                const uint16_t* const* w_attn, const uint16_t* dk_loc,
+                                const uint16_t* dv_loc, float* dx_loc, int accumulate,
+                                float* const* dw_attn, void* ws, size_t ws_bytes,
+                                hipStream_t stream);
+
 /* One rank's layer forward: u = x + Attn(x); y = u + MLP(bf16(u)).
  * Arguments as above; y_loc [B, S_loc, h] fp32 is overwritten with y. */
 tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
@@ -173,7 +221,14 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                               uint16_t* k_buf, uint16_t* v_buf, float* y_loc, void* ws,
                               size_t ws_bytes, hipStream_t stream);
 
-enum { TSP_OP_MLP = 0, TSP_OP_ATTN = 1, TSP_OP_LAYER = 2, TSP_OP_MLP_BWD = 3 };
+enum {
+  TSP_OP_MLP = 0,
+  TSP_OP_ATTN = 1,
+  TSP_OP_LAYER = 2,
+  TSP_OP_MLP_BWD = 3,
+  TSP_OP_ATTN_BWD = 4,
+  TSP_OP_ATTN_KV_BWD = 5
+};
 
 /* Workspace bytes the entry point `op` needs for `shape` (validated as above). */
 tsp_status tsp_workspace_bytes(const tsp_shape* shape, int op, size_t* bytes);
@@ -192,7 +247,14 @@ enum {
   TSP_KERNEL_BWD_GATE = 5, /* MLP backward: G, U, dHs products with the SwiGLU backward */
   TSP_KERNEL_BWD_DX = 6,   /* MLP backward: dX accumulate */
   TSP_KERNEL_BWD_DW = 7,   /* MLP backward: weight-gradient products */
-  TSP_KERNEL_COUNT = 8
+  TSP_KERNEL_ABWD_PROJ = 8,  /* attention backward: Q and dA = dY W_O products */
+  TSP_KERNEL_ABWD_FWD = 9,   /* attention backward: forward recomputation with lse */
+  TSP_KERNEL_ABWD_KV = 10,   /* attention backward: dK / dV (key-stationary) */
+  TSP_KERNEL_ABWD_Q = 11,    /* attention backward: dQ (query-stationary) */
+  TSP_KERNEL_ABWD_DX = 12,   /* attention backward: dX accumulate (both stages) */
+  TSP_KERNEL_ABWD_DW = 13,   /* attention backward: weight-gradient products */
+  TSP_KERNEL_ABWD_AUX = 14,  /* attention backward: delta / scaled-Q prep, transposes */
+  TSP_KERNEL_COUNT = 15
 };
 tsp_status tsp_profile_enable(int enable);
 tsp_status tsp_profile_read(int kernel, double* total_ms, int64_t* launches);

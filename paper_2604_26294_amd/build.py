@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libtsp.so")
-SOURCES = ("tsp_api.hip", "gemm.hip", "flash_attn.hip")
+SOURCES = ("tsp_api.hip", "gemm.hip", "flash_attn.hip", "flash_bwd.hip")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -46,6 +46,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "lds_dma.h"
 
 namespace tsp {
 namespace {
@@ -56,9 +57,6 @@ constexpr int kQTile = 32 * kWaves;  // queries per workgroup
 constexpr int kStepKeys = 128;       // keys staged per step
 constexpr int kHalfKeys = 64;        // keys per sub-step
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (exp2 units)
-
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) char lds_char;
 
 template <int D>
 struct FaCfg {
@@ -79,47 +77,6 @@ struct FaCfg {
   __device__ static int fk(int row) { return (row / RPW) & (KCH - 1); }
   __device__ static int fv(int row) { return 4 * ((row / RPW) & (KCH / 4 - 1)); }
 };
-
-__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane: the
-// buffer form, with the address = resource base (scalar) + soff (scalar) + voff (lane);
-// M0 holds the wave's LDS destination.
-//
-// Issued from inline assembly on purpose.  The compiler cannot tell which LDS bytes an
-// LDS-destination load writes, so after one it puts a full vmcnt(0) wait in front of
-// the next LDS read it cannot prove disjoint (here: the first V^T transpose read of the
-// step), which would stall every step on the load of the NEXT tile.  Hidden in asm,
-// the load is ordered only by this kernel's own waits: every slot is read after the
-// vmcnt(0) + barrier at the top of the step that consumes it, and a slot is refilled
-// only after the barrier that follows its last read.  The compiler's own waits stay
-// correct because loads complete in issue order.  No other code in this kernel uses
-// M0 (a reserved register the compiler does not track through asm).
-typedef u32x4 rsrc_t;
-__device__ __forceinline__ void dma16(const rsrc_t& rsrc, uint32_t voff, uint32_t soff,
-                                      lds_char* lds) {
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-  asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
-               :: "v"(voff), "s"(rsrc), "s"(soff), "s"(m0) : "memory", "m0");
-}
-
-// Raw buffer resource over [base, base + 4 GiB) (stride 0, no format conversion): base
-// address (48 bits), number of records, and the data-format word of a raw resource.
-__device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
-  const uint64_t a = (uint64_t)(uintptr_t)base;
-  return rsrc_t{(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a),
-                (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32) & 0xffffu),
-                0xffffffffu, 0x00020000u};
-}
-
-__device__ __forceinline__ u32x4 lds_read16(const lds_char* p) {
-  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p);
-}
-
-__device__ __forceinline__ u32x2 lds_read_tr(const lds_char* p) {
-  return __builtin_bit_cast(
-      u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p));
-}
 
 template <int N>
 using IC = std::integral_constant<int, N>;
@@ -143,7 +100,7 @@ __device__ __forceinline__ float sum_with_partner(float x) {
   return a + b;
 }
 
-template <int D>
+template <int D, bool LSE>
 __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
   using C = FaCfg<D>;
   constexpr int KCH = C::KCH, RB = C::ROW_BYTES, TB = C::TILE_BYTES;
@@ -499,6 +456,11 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
     // Whole key range: normalise and write bf16 O (key 0 is visible to every query,
     // so l > 0).
     const float inv = 1.f / l_run;
+    if constexpr (LSE) {
+      if (hh == 0)
+        P.lse[((size_t)b * P.heads + head) * P.s_loc + row0 + qloc] =
+            mref + __builtin_amdgcn_logf(l_run);
+    }
     uint16_t* orow = P.O + row * D;
 #pragma unroll
     for (int eb = 0; eb < C::EB; ++eb)
@@ -527,7 +489,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 // Merges the n_split partial results of each (batch, query, head) row: with
 // M = max_c m_c, O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as bf16.
 // One thread per 4 consecutive head-dim columns of a row.
-template <int D>
+template <int D, bool LSE>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams P) {
   constexpr int TPR = D / 4;  // threads per row
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -547,6 +509,14 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams P) {
     acc += wgt * *reinterpret_cast<const f32x4*>(P.part_o + prow * D + 4 * c4);
   }
   const float inv = 1.f / l;
+  if constexpr (LSE) {
+    if (c4 == 0) {
+      // row = (b S_loc + t) H_s + head  ->  the [B, H_s, S_loc] log-sum-exp layout
+      const long long bt = row / P.heads, b = bt / P.s_loc;
+      const int head = (int)(row - bt * P.heads), t = (int)(bt - b * P.s_loc);
+      P.lse[((size_t)b * P.heads + head) * P.s_loc + t] = m + __builtin_amdgcn_logf(l);
+    }
+  }
   *reinterpret_cast<u32x2*>(P.O + row * D + 4 * c4) =
       u32x2{pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
 }
@@ -651,11 +621,15 @@ hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
   const void* fn;
   const void* combine;
   if (p.head_dim == 128) {
-    fn = reinterpret_cast<const void*>(&flash_fwd_kernel<128>);
-    combine = reinterpret_cast<const void*>(&attn_combine_kernel<128>);
+    fn = p.lse ? reinterpret_cast<const void*>(&flash_fwd_kernel<128, true>)
+               : reinterpret_cast<const void*>(&flash_fwd_kernel<128, false>);
+    combine = p.lse ? reinterpret_cast<const void*>(&attn_combine_kernel<128, true>)
+                    : reinterpret_cast<const void*>(&attn_combine_kernel<128, false>);
   } else if (p.head_dim == 64) {
-    fn = reinterpret_cast<const void*>(&flash_fwd_kernel<64>);
-    combine = reinterpret_cast<const void*>(&attn_combine_kernel<64>);
+    fn = p.lse ? reinterpret_cast<const void*>(&flash_fwd_kernel<64, true>)
+               : reinterpret_cast<const void*>(&flash_fwd_kernel<64, false>);
+    combine = p.lse ? reinterpret_cast<const void*>(&attn_combine_kernel<64, true>)
+                    : reinterpret_cast<const void*>(&attn_combine_kernel<64, false>);
   } else {
     return hipErrorInvalidValue;
   }

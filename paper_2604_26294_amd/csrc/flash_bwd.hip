@@ -1,0 +1,579 @@
+// Backward of the causal flash attention of one TSP rank (gfx950, bf16 MFMA).
+//
+// For one shard's heads, given the rank's queries Q, the upstream gradient dO = dA of
+// the attention output, the resident gathered K / V (sequence order), the base-2
+// log-sum-exp of every query's logits (from the forward recomputation) and
+// delta = rowsum(dO * O), the chain rule through O = P V, P = softmax(scale Q K^T)
+// gives, with dP = dO V^T and dS = P * (dP - delta):
+//   dV = P^T dO,  dK = scale dS^T Q   (contributions to every key of the prefix)
+//   dQ = scale dS K.
+// Two kernels share the work without atomics: one is key-stationary (a workgroup owns
+// 128 keys of one kv head, keeps their K and V in registers and streams the queries of
+// the g query heads that read them: dK, dV accumulate in registers and are written
+// once), the other query-stationary (a workgroup owns 128 queries of one head and
+// streams the keys: dQ accumulates in registers).  Both recompute the scores; only
+// the query-stationary one needs dP's row sums, which delta already holds.
+//
+// The logits are formed exactly as the forward formed them: Q scaled by
+// scale * log2(e) and rounded to bf16 (Qs), so that P = 2^(Qs K^T - lse) reproduces
+// the forward's probabilities.  Since scale Q = Qs / log2(e) up to that rounding,
+// dK = ln(2) dS^T Qs.
+//
+// MFMA layouts (32 x 32 x 16).  Key-stationary: S = Qs K^T and dP = dO V^T with the
+// queries as rows (A operands read from LDS row by row, K and V fragments as B from
+// registers); the accumulator then holds 16 queries of one key per lane, which is
+// the B-operand layout of dV^T = dO^T P and dK^T = Qs^T dS (contraction over queries
+// in the accumulator's row order), whose A operands dO^T and Qs^T come from the same
+// LDS tiles through transpose reads.  Query-stationary: S^T = K Qs^T and
+// dP^T = V dO^T with keys as rows (Qs and dO fragments in registers), so each lane
+// holds 16 keys of one query, the B-operand layout of dQ^T = K^T dS^T, whose A
+// operand K^T comes from the K tile through transpose reads.
+//
+// LDS tiles are rows of 16-byte chunks; the physical chunk is the logical chunk XOR
+// f(row), with f chosen so that both read forms are bank-conflict free: 16 rows at one
+// logical chunk (row reads) and 4 rows x 4 chunks (transpose reads of a 32-column
+// block).
+#include <math.h>
+
+#include <type_traits>
+
+#include "common.h"
+#include "internal.h"
+#include "lds_dma.h"
+
+namespace tsp {
+namespace {
+
+constexpr int kBwdWaves = 4;
+constexpr int kBwdThreads = kBwdWaves * kWave;
+constexpr int kKvTile = 32 * kBwdWaves;  // keys per key-stationary workgroup
+constexpr int kQStage = 64;              // queries staged per step (key-stationary)
+constexpr int kDqTile = 32 * kBwdWaves;  // queries per query-stationary workgroup
+constexpr int kKStage = 64;              // keys staged per step (query-stationary)
+constexpr float kLn2 = 0.69314718055994531f;
+
+template <int D>
+struct BwCfg {
+  static constexpr int KCH = D / 8;             // 16-byte chunks per row
+  static constexpr int RB = D * 2;              // row bytes
+  static constexpr int RPW = 256 / RB;          // rows per 256-byte bank window
+  static constexpr int KS = D / 16;             // contraction steps over d
+  static constexpr int EB = D / 32;             // 32-row blocks of d
+  static constexpr int T64 = 64 * RB;           // bytes of a 64-row tile
+  static constexpr int RPD = kWave / KCH;       // rows one wave-wide LDS load fills
+  static constexpr int DMA64 = 64 / (kBwdWaves * RPD);  // such loads per wave per tile
+  static_assert(DMA64 * kBwdWaves * RPD == 64, "tile cover");
+  // m = row / RPW indexes the row's bank window.  d = 128 (one row per window):
+  // f = 4 (m mod 4) + (m / 4 mod 4), distinct over 16 consecutive rows, and distinct
+  // in its upper two bits over 4 consecutive rows.  d = 64 (two rows per window, at
+  // chunk offsets 0 and 8): f = 4 (m mod 2) + (m / 2 mod 4), distinct over 8
+  // consecutive windows, and rows r, r + 2 (same half of a window) differ in bit 2.
+  __device__ static int f(int row) {
+    const int m = row / RPW;
+    return D == 128 ? (((m & 3) << 2) | ((m >> 2) & 3)) : (((m & 1) << 2) | ((m >> 1) & 3));
+  }
+  // Byte offset of (row, column) in a tile (column a multiple of 4 for transpose reads).
+  __device__ static int off(int row, int col) {
+    return row * RB + 16 * ((col >> 3) ^ f(row)) + 2 * (col & 7);
+  }
+};
+
+// One 64-row tile into LDS at `dst`.  Row r of the tile comes from base + min(r, last)
+// rows of `row_bytes` each; rows past `last` repeat it (finite values that the caller
+// masks).  Wave w's load i fills rows (4 i + w) RPD .. + RPD - 1.
+template <int D>
+__device__ __forceinline__ void load_tile64(const uint16_t* base, uint32_t row_bytes, int last,
+                                            lds_char* dst, int wave, int lane) {
+  using C = BwCfg<D>;
+  const rsrc_t rsrc = make_rsrc(base);
+#pragma unroll
+  for (int i = 0; i < C::DMA64; ++i) {
+    const int blk = i * kBwdWaves + wave;
+    const int r = blk * C::RPD + lane / C::KCH;
+    const uint32_t rr = (uint32_t)min(r, last);
+    const uint32_t voff = rr * row_bytes + 16u * (uint32_t)((lane % C::KCH) ^ C::f(r));
+    dma16(rsrc, voff, 0u, dst + blk * (kWave * 16));
+  }
+}
+
+// Lane layout of the transpose reads: source lane (t, group g) of a 16-lane group
+// points at row 4 (g / 2) + t / 4 and column 16 (g % 2) + 4 (t % 4) of a 32-column
+// block, so lane l receives column l % 32 of rows 4 (l / 32) + 0..3: the contraction
+// slots 0-3 of the accumulator-ordered B operands; rows + 8 give slots 4-7.
+__device__ __forceinline__ int tr_row(int lane) { return (((lane >> 4) >> 1) << 2) + ((lane & 15) >> 2); }
+__device__ __forceinline__ int tr_col(int lane) { return 16 * ((lane >> 4) & 1) + 4 * (lane & 3); }
+
+// ---------------------------------------------------------------------------------
+// delta = rowsum(dO * O) per (query, head) and Qs = bf16(c Q).  A group of D / 8
+// lanes handles one (row, head): 8 elements per lane, reduced across the group.
+template <int D>
+__global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const AttnBwdParams P) {
+  constexpr int G = D / 8;
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long rh = idx / G;                    // (b S_loc + t) H_s + head
+  const int part = (int)(idx % G);
+  const long long n_rows = (long long)P.batch * P.s_loc * P.heads;
+  const bool valid = rh < n_rows;
+  const size_t e0 = (size_t)(valid ? rh : 0) * D + 8 * part;
+  float acc = 0.f;
+  if (valid) {
+    const u32x4 o = ld16(P.O + e0), g = ld16(P.dO + e0), q = ld16(P.Qin + e0);
+    u32x4 qs;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc += bf16_bits_to_f32(o[e] & 0xffffu) * bf16_bits_to_f32(g[e] & 0xffffu);
+      acc += bf16_bits_to_f32(o[e] >> 16) * bf16_bits_to_f32(g[e] >> 16);
+      qs[e] = pack_bf16x2(bf16_bits_to_f32(q[e] & 0xffffu) * P.scale_log2,
+                          bf16_bits_to_f32(q[e] >> 16) * P.scale_log2);
+    }
+    st16(P.Qs + e0, qs);
+  }
+#pragma unroll
+  for (int m = 1; m < G; m <<= 1) acc += __shfl_xor(acc, m);
+  if (valid && part == 0) {
+    const long long bt = rh / P.heads, b = bt / P.s_loc;
+    const int head = (int)(rh - bt * P.heads), t = (int)(bt - b * P.s_loc);
+    P.delta[((size_t)b * P.heads + head) * P.s_loc + t] = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// Key-stationary kernel: dK, dV of 128 keys of one kv head.
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
+  using C = BwCfg<D>;
+  constexpr int RB = C::RB, T64 = C::T64;
+  // [Qs slot 0][Qs slot 1][dO slot 0][dO slot 1][lse, delta slot 0][lse, delta slot 1]
+  __shared__ __attribute__((aligned(1024))) char L[4 * T64 + 2 * 2 * kQStage * 4];
+  lds_char* Ls = (lds_char*)L;
+  float* Lf = reinterpret_cast<float*>(L + 4 * T64);
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int kv_heads = P.heads / P.group;
+
+  // Work item -> (batch, kv head, key tile), key tile fastest: an XCD's contiguous share
+  // of work indices streams the same queries through its L2.  Early keys see the most
+  // queries and come first.
+  const int n_kt = (int)((P.seq + kKvTile - 1) / kKvTile);
+  const int w = xcd_work_index(blockIdx.x, n_kt * kv_heads * P.batch);
+  const int kt = w % n_kt;
+  const int kvl = (w / n_kt) % kv_heads;
+  const int b = w / n_kt / kv_heads;
+  const int kvh = P.kv_head0 + kvl;
+  const int k0 = kt * kKvTile;
+  const int wk0 = k0 + 32 * wave;  // this wave's first key
+  const int key = wk0 + l32;       // this lane's key (the accumulator column)
+
+  // K and V fragments of this lane's key (B operands of S and dP): d slots 16 s + 8 hh.
+  // Keys past the last query position are never read (zero fragments: their dK, dV come
+  // out exactly zero, whatever those buffer rows hold).
+  int kv_len = 0;
+  for (int sg = 0; sg < P.n_seg; ++sg) kv_len = max(kv_len, P.seg_pos0[sg] + P.seg_rows[sg]);
+  const size_t kv_stride = (size_t)P.n_kv * D;
+  const bool kread = key < kv_len;
+  const size_t krow = ((size_t)b * P.seq + (kread ? key : 0)) * kv_stride + (size_t)kvh * D;
+  u32x4 kf[C::KS], vf[C::KS];
+#pragma unroll
+  for (int s = 0; s < C::KS; ++s) {
+    kf[s] = kread ? ld16(P.Kb + krow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
+    vf[s] = kread ? ld16(P.Vb + krow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
+  }
+
+  // Query tiles of 64 rows that can see key k0 or later: per segment, tiles from tf.
+  int tf[2] = {0, 0}, nv[2] = {0, 0};
+  for (int sg = 0; sg < P.n_seg; ++sg) {
+    const int nt = (P.seg_rows[sg] + kQStage - 1) / kQStage;
+    const int num = k0 - P.seg_pos0[sg] - (kQStage - 1);
+    tf[sg] = num <= 0 ? 0 : (num + kQStage - 1) / kQStage;
+    nv[sg] = max(0, nt - tf[sg]);
+  }
+  const int per_head = nv[0] + nv[1];
+  const int n_steps = per_head * P.group;
+  struct Tile {
+    int head, seg, r0;
+  };
+  auto tile_of = [&](int t) __attribute__((always_inline)) {
+    Tile T;
+    const int u = t % per_head;
+    T.head = kvl * P.group + t / per_head;
+    T.seg = u < nv[0] ? 0 : 1;
+    T.r0 = kQStage * (T.seg == 0 ? tf[0] + u : tf[1] + u - nv[0]);
+    return T;
+  };
+  const uint32_t q_row_bytes = 2u * (uint32_t)(P.heads * D);
+  float pend_l = 0.f, pend_d = 0.f;  // lse / delta of the next tile (wave 0, one row per lane)
+  auto issue = [&](int t, int slot) __attribute__((always_inline)) {
+    const Tile T = tile_of(t);
+    const int rows = P.seg_rows[T.seg];
+    const size_t g0 = (size_t)b * P.s_loc + P.seg_row0[T.seg] + T.r0;
+    const size_t e0 = (g0 * P.heads + T.head) * D;
+    const int last = rows - 1 - T.r0;
+    load_tile64<D>(P.Qs + e0, q_row_bytes, last, Ls + slot * T64, wave, lane);
+    load_tile64<D>(P.dO + e0, q_row_bytes, last, Ls + (2 + slot) * T64, wave, lane);
+    if (wave == 0) {
+      const size_t li =
+          ((size_t)b * P.heads + T.head) * P.s_loc + P.seg_row0[T.seg] + T.r0 + min(lane, last);
+      const float l = P.lse[li], d = P.delta[li];
+      pend_l = lane <= last ? l : INFINITY;  // rows past the segment: P = 0
+      pend_d = lane <= last ? d : 0.f;
+    }
+  };
+
+  f32x16 dkT[C::EB], dvT[C::EB];
+#pragma unroll
+  for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) dkT[eb][e] = dvT[eb][e] = 0.f;
+
+  const int trr = tr_row(lane), trc = tr_col(lane);
+  if (n_steps > 0) issue(0, 0);
+  for (int t = 0; t < n_steps; ++t) {
+    const int slot = t & 1;
+    if (wave == 0) {
+      Lf[slot * 2 * kQStage + lane] = pend_l;
+      Lf[slot * 2 * kQStage + kQStage + lane] = pend_d;
+    }
+    wait_dma();
+    __syncthreads();  // tile t resident in `slot`; every wave is done with tile t - 1
+    if (t + 1 < n_steps) issue(t + 1, slot ^ 1);
+
+    const Tile T = tile_of(t);
+    const int rows = P.seg_rows[T.seg];
+    const int tpos0 = P.seg_pos0[T.seg] + T.r0;  // position of tile row 0
+    const lds_char* Lq = Ls + slot * T64;
+    const lds_char* Lo = Ls + (2 + slot) * T64;
+    const float* lse_t = Lf + slot * 2 * kQStage;
+    const float* del_t = lse_t + kQStage;
+#pragma unroll
+    for (int qb = 0; qb < kQStage / 32; ++qb) {
+      if (T.r0 + 32 * qb >= rows) break;                        // past the segment
+      const int qpos_first = tpos0 + 32 * qb;
+      const int qpos_last = tpos0 + min(32 * qb + 31, rows - 1 - T.r0);
+      if (qpos_last < wk0) continue;                           // every key after every query
+      const bool need_mask = wk0 + 31 > qpos_first;
+
+      f32x16 s, dp;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[e] = dp[e] = 0.f;
+      const int arow = 32 * qb + l32;
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        const int o = C::off(arow, 16 * ks + 8 * hh);
+        s = mfma32(lds_read16(Lq + o), kf[ks], s);
+        dp = mfma32(lds_read16(Lo + o), vf[ks], dp);
+      }
+      // Element 4 g + r: query row 32 qb + 8 g + 4 hh + r of the tile, key `key`.
+      u32x4 pf[2], df[2];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int qr = 32 * qb + 8 * g + 4 * hh;
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_t + qr);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(del_t + qr);
+        float pv[4], dv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float p = __builtin_amdgcn_exp2f(s[4 * g + r] - l4[r]);
+          if (need_mask && key > tpos0 + qr + r) p = 0.f;
+          pv[r] = p;
+          dv[r] = p * (dp[4 * g + r] - d4[r]);
+        }
+        pf[g >> 1][2 * (g & 1)] = pack_bf16x2(pv[0], pv[1]);
+        pf[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(pv[2], pv[3]);
+        df[g >> 1][2 * (g & 1)] = pack_bf16x2(dv[0], dv[1]);
+        df[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
+      }
+      // dV^T += dO^T P, dK^T += Qs^T dS; k-step s2 covers query rows 32 qb + 16 s2 + ..
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int ra = 32 * qb + 16 * s2 + trr;
+#pragma unroll
+        for (int eb = 0; eb < C::EB; ++eb) {
+          const int ca = 32 * eb + trc;
+          const int oa = C::off(ra, ca), ob = C::off(ra + 8, ca);
+          const u32x2 olo = lds_read_tr(Lo + oa), ohi = lds_read_tr(Lo + ob);
+          dvT[eb] = mfma32(u32x4{olo[0], olo[1], ohi[0], ohi[1]}, pf[s2], dvT[eb]);
+          const u32x2 qlo = lds_read_tr(Lq + oa), qhi = lds_read_tr(Lq + ob);
+          dkT[eb] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, df[s2], dkT[eb]);
+        }
+      }
+    }
+  }
+
+  // Accumulator element 4 g + r of block eb: d = 32 eb + 8 g + 4 hh + r, key = `key`.
+  if (key < P.seq) {
+    float* dkrow = P.dK + ((size_t)b * P.seq + key) * kv_stride + (size_t)kvh * D;
+    float* dvrow = P.dV + ((size_t)b * P.seq + key) * kv_stride + (size_t)kvh * D;
+#pragma unroll
+    for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = 32 * eb + 8 * g + 4 * hh;
+        f32x4 k4{dkT[eb][4 * g] * kLn2, dkT[eb][4 * g + 1] * kLn2, dkT[eb][4 * g + 2] * kLn2,
+                 dkT[eb][4 * g + 3] * kLn2};
+        f32x4 v4{dvT[eb][4 * g], dvT[eb][4 * g + 1], dvT[eb][4 * g + 2], dvT[eb][4 * g + 3]};
+        if (P.accumulate) {
+          k4 += *reinterpret_cast<const f32x4*>(dkrow + c);
+          v4 += *reinterpret_cast<const f32x4*>(dvrow + c);
+        }
+        *reinterpret_cast<f32x4*>(dkrow + c) = k4;
+        *reinterpret_cast<f32x4*>(dvrow + c) = v4;
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// Query-stationary kernel: dQ of 128 queries of one head.
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void attn_bwd_dq_kernel(const AttnBwdParams P) {
+  using C = BwCfg<D>;
+  constexpr int T64 = C::T64;
+  // [K slot 0][K slot 1][V slot 0][V slot 1]
+  __shared__ __attribute__((aligned(1024))) char L[4 * T64];
+  lds_char* Ls = (lds_char*)L;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+
+  // Work item -> (batch, head, query tile), query tile fastest; last segment and last
+  // tile (most keys) first.
+  const int nt0 = (P.seg_rows[0] + kDqTile - 1) / kDqTile;
+  const int nt1 = P.n_seg > 1 ? (P.seg_rows[1] + kDqTile - 1) / kDqTile : 0;
+  const int n_qt = nt0 + nt1;
+  const int w = xcd_work_index(blockIdx.x, n_qt * P.heads * P.batch);
+  const int order = w % n_qt;
+  const int seg = order < nt1 ? 1 : 0;
+  const int qt = seg == 1 ? nt1 - 1 - order : nt0 - 1 - (order - nt1);
+  const int head = (w / n_qt) % P.heads;
+  const int b = w / n_qt / P.heads;
+  const int seg_rows = P.seg_rows[seg], row0 = P.seg_row0[seg], pos0 = P.seg_pos0[seg];
+  const int kvh = P.kv_head0 + head / P.group;
+  const int q0 = qt * kDqTile;
+
+  const int qloc = q0 + 32 * wave + l32;  // this lane's query (accumulator column)
+  const bool qvalid = qloc < seg_rows;
+  const int qpos = pos0 + qloc;
+  const bool wave_active = q0 + 32 * wave < seg_rows;
+  const int wpos_min = pos0 + q0 + 32 * wave;
+  const int wpos_max = pos0 + min(q0 + 32 * wave + 31, seg_rows - 1);
+  const int n_keys = pos0 + min(q0 + kDqTile, seg_rows);  // keys this tile can see
+  const int n_steps = (n_keys + kKStage - 1) / kKStage;
+
+  // Qs and dO fragments of this lane's query (B operands of S^T and dP^T); the score
+  // and dP accumulators start from -lse and -delta.
+  const size_t qrow = (((size_t)b * P.s_loc + row0 + (qvalid ? qloc : 0)) * P.heads + head) * D;
+  u32x4 qf[C::KS], of[C::KS];
+#pragma unroll
+  for (int s = 0; s < C::KS; ++s) {
+    qf[s] = ld16(P.Qs + qrow + 16 * s + 8 * hh);
+    of[s] = ld16(P.dO + qrow + 16 * s + 8 * hh);
+  }
+  const size_t li = ((size_t)b * P.heads + head) * P.s_loc + row0 + (qvalid ? qloc : 0);
+  const float neg_lse = qvalid ? -P.lse[li] : -INFINITY;  // invalid query: P = 0
+  const float neg_del = qvalid ? -P.delta[li] : 0.f;
+
+  const size_t kv_stride = (size_t)P.n_kv * D;
+  const uint32_t kv_row_bytes = 2u * (uint32_t)kv_stride;
+  const uint16_t* kbase = P.Kb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
+  const uint16_t* vbase = P.Vb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
+  auto issue = [&](int j, int slot) __attribute__((always_inline)) {
+    const int key0 = j * kKStage;
+    const int last = n_keys - 1 - key0;  // keys past n_keys are past every query here
+    load_tile64<D>(kbase + (size_t)key0 * kv_stride, kv_row_bytes, last, Ls + slot * T64, wave, lane);
+    load_tile64<D>(vbase + (size_t)key0 * kv_stride, kv_row_bytes, last, Ls + (2 + slot) * T64,
+                   wave, lane);
+  };
+
+  f32x16 dqT[C::EB];
+#pragma unroll
+  for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) dqT[eb][e] = 0.f;
+
+  const int trr = tr_row(lane), trc = tr_col(lane);
+  if (n_steps > 0) issue(0, 0);
+  for (int j = 0; j < n_steps; ++j) {
+    const int slot = j & 1;
+    wait_dma();
+    __syncthreads();  // tile j resident; every wave is done with tile j - 1
+    if (j + 1 < n_steps) issue(j + 1, slot ^ 1);
+    if (!wave_active) continue;
+    const lds_char* Lk = Ls + slot * T64;
+    const lds_char* Lv = Ls + (2 + slot) * T64;
+#pragma unroll
+    for (int kb = 0; kb < kKStage / 32; ++kb) {
+      const int kbase0 = j * kKStage + 32 * kb;
+      if (kbase0 > wpos_max) break;                 // every key after every query
+      const bool need_mask = kbase0 + 31 > wpos_min;
+      f32x16 s, dp;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        s[e] = neg_lse;
+        dp[e] = neg_del;
+      }
+      const int arow = 32 * kb + l32;
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        const int o = C::off(arow, 16 * ks + 8 * hh);
+        s = mfma32(lds_read16(Lk + o), qf[ks], s);
+        dp = mfma32(lds_read16(Lv + o), of[ks], dp);
+      }
+      // Element 4 g + r: key kbase0 + 8 g + 4 hh + r, this lane's query.
+      u32x4 df[2];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float dv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float p = __builtin_amdgcn_exp2f(s[4 * g + r]);
+          if (need_mask && kbase0 + 8 * g + 4 * hh + r > qpos) p = 0.f;
+          dv[r] = p * dp[4 * g + r];
+        }
+        df[g >> 1][2 * (g & 1)] = pack_bf16x2(dv[0], dv[1]);
+        df[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
+      }
+      // dQ^T += K^T dS^T; k-step s2 covers keys 32 kb + 16 s2 + ..
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int ra = 32 * kb + 16 * s2 + trr;
+#pragma unroll
+        for (int eb = 0; eb < C::EB; ++eb) {
+          const int ca = 32 * eb + trc;
+          const u32x2 lo = lds_read_tr(Lk + C::off(ra, ca)), hi = lds_read_tr(Lk + C::off(ra + 8, ca));
+          dqT[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, df[s2], dqT[eb]);
+        }
+      }
+    }
+  }
+
+  if (!qvalid) return;
+  // Element 4 g + r of block eb: d = 32 eb + 8 g + 4 hh + r of this lane's query.
+  uint16_t* dqrow = P.dQ + qrow;
+#pragma unroll
+  for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<u32x2*>(dqrow + 32 * eb + 8 * g + 4 * hh) =
+          u32x2{pack_bf16x2(dqT[eb][4 * g] * P.scale, dqT[eb][4 * g + 1] * P.scale),
+                pack_bf16x2(dqT[eb][4 * g + 2] * P.scale, dqT[eb][4 * g + 3] * P.scale)};
+}
+
+// ---------------------------------------------------------------------------------
+// out[n][m] = in[m][n] for m < rows, n < cols; out[n][m] = 0 for rows <= m < ld_out.
+// 64 x 64 tiles through LDS; 16-byte loads and stores.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* in, int ld_in,
+                                                             int rows, int cols, uint16_t* out,
+                                                             int ld_out) {
+  __shared__ uint16_t T[64][64 + 2];
+  const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = tid + 256 * k;          // 512 chunks of 8 elements
+    const int r = i >> 3, c8 = (i & 7) * 8;
+    const int m = m0 + r, n = n0 + c8;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (m < rows) {
+      if (n + 8 <= cols) {
+        v = ld16(in + (size_t)m * ld_in + n);
+      } else {
+        for (int e = 0; e < 8; ++e)
+          if (n + e < cols) {
+            const uint32_t x = in[(size_t)m * ld_in + n + e];
+            v[e >> 1] |= (e & 1) ? (x << 16) : x;
+          }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      T[r][c8 + 2 * e] = (uint16_t)(v[e] & 0xffffu);
+      T[r][c8 + 2 * e + 1] = (uint16_t)(v[e] >> 16);
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = tid + 256 * k;
+    const int nr = i >> 3, m8 = (i & 7) * 8;  // output row n0 + nr, columns m0 + m8 ..
+    const int n = n0 + nr, m = m0 + m8;
+    if (n >= cols || m >= ld_out) continue;
+    u32x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] = (uint32_t)T[m8 + 2 * e][nr] | ((uint32_t)T[m8 + 2 * e + 1][nr] << 16);
+    st16(out + (size_t)n * ld_out + m, v);
+  }
+}
+
+hipError_t check_bwd(const AttnBwdParams& p) {
+  if (p.n_seg < 1 || p.n_seg > 2 || p.group < 1 || p.heads % p.group != 0 || p.seq < 1 ||
+      p.seq > (1LL << 30) || (p.head_dim != 64 && p.head_dim != 128))
+    return hipErrorInvalidValue;
+  int rows = 0;
+  for (int k = 0; k < p.n_seg; ++k) {
+    if (p.seg_rows[k] < 1 || p.seg_row0[k] != rows || p.seg_pos0[k] < 0 ||
+        (long long)p.seg_pos0[k] + p.seg_rows[k] > p.seq)
+      return hipErrorInvalidValue;
+    rows += p.seg_rows[k];
+  }
+  if (rows != p.s_loc || p.kv_head0 < 0 || p.kv_head0 + p.heads / p.group > p.n_kv)
+    return hipErrorInvalidValue;
+  // Byte offsets inside one staged tile must fit the 32-bit buffer offsets.
+  if ((long long)kKStage * p.n_kv * p.head_dim * 2 >= (1LL << 31) ||
+      (long long)kQStage * p.heads * p.head_dim * 2 >= (1LL << 31))
+    return hipErrorInvalidValue;
+  return hipSuccess;
+}
+
+bool bwd_empty(const AttnBwdParams& p) { return p.batch <= 0 || p.s_loc <= 0 || p.heads <= 0; }
+
+}  // namespace
+
+hipError_t launch_attn_bwd_prep(const AttnBwdParams& p, hipStream_t s) {
+  if (bwd_empty(p)) return hipSuccess;
+  const hipError_t e = check_bwd(p);
+  if (e != hipSuccess) return e;
+  void* args[] = {const_cast<AttnBwdParams*>(&p)};
+  const long long threads = (long long)p.batch * p.s_loc * p.heads * (p.head_dim / 8);
+  const void* fn = p.head_dim == 128 ? reinterpret_cast<const void*>(&attn_bwd_prep_kernel<128>)
+                                     : reinterpret_cast<const void*>(&attn_bwd_prep_kernel<64>);
+  return hipLaunchKernel(fn, dim3((unsigned)((threads + 255) / 256)), dim3(256), args, 0, s);
+}
+
+hipError_t launch_attn_bwd_dkdv(const AttnBwdParams& p, hipStream_t s) {
+  if (bwd_empty(p)) return hipSuccess;
+  const hipError_t e = check_bwd(p);
+  if (e != hipSuccess) return e;
+  void* args[] = {const_cast<AttnBwdParams*>(&p)};
+  const int n_kt = (int)((p.seq + kKvTile - 1) / kKvTile);
+  const void* fn = p.head_dim == 128 ? reinterpret_cast<const void*>(&attn_bwd_dkdv_kernel<128>)
+                                     : reinterpret_cast<const void*>(&attn_bwd_dkdv_kernel<64>);
+  return hipLaunchKernel(fn, dim3(n_kt * (p.heads / p.group) * p.batch), dim3(kBwdThreads), args,
+                         0, s);
+}
+
+hipError_t launch_attn_bwd_dq(const AttnBwdParams& p, hipStream_t s) {
+  if (bwd_empty(p)) return hipSuccess;
+  const hipError_t e = check_bwd(p);
+  if (e != hipSuccess) return e;
+  void* args[] = {const_cast<AttnBwdParams*>(&p)};
+  int n_qt = 0;
+  for (int k = 0; k < p.n_seg; ++k) n_qt += (p.seg_rows[k] + kDqTile - 1) / kDqTile;
+  const void* fn = p.head_dim == 128 ? reinterpret_cast<const void*>(&attn_bwd_dq_kernel<128>)
+                                     : reinterpret_cast<const void*>(&attn_bwd_dq_kernel<64>);
+  return hipLaunchKernel(fn, dim3(n_qt * p.heads * p.batch), dim3(kBwdThreads), args, 0, s);
+}
+
+hipError_t launch_transpose_bf16(const uint16_t* in, int ld_in, int rows, int cols,
+                                 uint16_t* out, int ld_out, hipStream_t s) {
+  if (rows < 0 || cols <= 0 || ld_out < rows || ld_out % 8 != 0) return hipErrorInvalidValue;
+  if (ld_out == 0) return hipSuccess;
+  const dim3 grid((ld_out + 63) / 64, (cols + 63) / 64);
+  void* args[] = {const_cast<uint16_t**>(&in), &ld_in, &rows, &cols, &out, &ld_out};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&transpose_bf16_kernel), grid, dim3(256),
+                         args, 0, s);
+}
+
+}  // namespace tsp

@@ -109,6 +109,10 @@ struct AttnParams {
   long long part_rows;
   float* part_o;
   float* part_ml;
+  // Optional: the log-sum-exp of each query's base-2 logits (scores times scale_log2,
+  // with Q rounded to bf16 after scaling, as the kernel computes them), fp32
+  // [B, H_s, S_loc]; written when non-null.
+  float* lse;
 };
 
 // Workgroups the attention kernel aims to launch: one per CU of an MI355X.
@@ -121,5 +125,53 @@ constexpr int kAttnTargetWorkgroups = 256;
 int attn_split_count(const AttnParams& p, int* split_len);
 
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s);
+
+// Backward of launch_flash_attn for one shard's heads (same segments and buffers).
+//   Qin  [B, S_loc, H_s, d] bf16   the recomputed queries;
+//   O    [B, S_loc, H_s, d] bf16   the recomputed attention output;
+//   dO   [B, S_loc, H_s, d] bf16   its upstream gradient;
+//   lse  [B, H_s, S_loc] fp32      base-2 log-sum-exp from the forward (AttnParams::lse).
+// Writes Qs = bf16(scale_log2 Qin) (may alias Qin), delta = rowsum(dO * O) [B, H_s, S_loc],
+// dQ [B, S_loc, H_s, d] bf16, and the contributions to the gradients of the gathered
+// K / V: dK, dV [B, S, n_kv, d] fp32, columns of kv heads kv_head0 .. + H_s/g - 1, every
+// one of the S rows (overwritten, or added to if accumulate).
+struct AttnBwdParams {
+  const uint16_t* Qin;
+  uint16_t* Qs;
+  const uint16_t* O;
+  const uint16_t* dO;
+  const uint16_t* Kb;
+  const uint16_t* Vb;
+  const float* lse;
+  float* delta;
+  uint16_t* dQ;
+  float* dK;
+  float* dV;
+  int accumulate;
+  int batch;
+  int s_loc;
+  int heads;
+  int group;
+  int head_dim;
+  long long seq;
+  int n_kv;
+  int kv_head0;
+  int n_seg;
+  int seg_row0[2];
+  int seg_rows[2];
+  int seg_pos0[2];
+  float scale_log2;  // softmax scale * log2(e)
+  float scale;       // softmax scale
+};
+
+// The three kernels of the backward, in this order: delta and Qs; dK / dV; dQ.
+hipError_t launch_attn_bwd_prep(const AttnBwdParams& p, hipStream_t s);
+hipError_t launch_attn_bwd_dkdv(const AttnBwdParams& p, hipStream_t s);
+hipError_t launch_attn_bwd_dq(const AttnBwdParams& p, hipStream_t s);
+
+// out[n][m] = in[m][n] (bf16) for m < rows, n < cols, and 0 for rows <= m < ld_out
+// (ld_out a multiple of 8; in rows 16-byte aligned).
+hipError_t launch_transpose_bf16(const uint16_t* in, int ld_in, int rows, int cols,
+                                 uint16_t* out, int ld_out, hipStream_t s);
 
 }  // namespace tsp

@@ -13,6 +13,7 @@
 namespace {
 
 using tsp::AttnParams;
+using tsp::AttnBwdParams;
 using tsp::GemmParams;
 
 constexpr size_t kAlign = 256;
@@ -140,6 +141,43 @@ MlpBwdWs mlp_bwd_ws(const Dims& d) {
   w.hst = 2 * rm + 2 * tr;
   w.total = 2 * rm + 3 * tr;
   return w;
+}
+// Attention backward, first stage: Q (recomputed, then scaled in place), A, dA, dQ
+// [M, H_s d] bf16; lse, delta [B, H_s, S_loc] fp32; A^T and dQ^T [H_s d, M rounded up
+// to 64] bf16 (the A operands of the weight-gradient products, zero past M); then the
+// forward recomputation's key-range partials, as for the forward.
+struct AttnBwdWs {
+  size_t q, a, da, dq, lse, delta, at, dqt, po, pml, total;
+  int m_pad, n_split, split_len;
+};
+AttnBwdWs attn_bwd_ws(const Dims& d) {
+  AttnBwdWs w;
+  AttnParams ap = {};
+  attn_segments(d, &ap);
+  w.n_split = tsp::attn_split_count(ap, &w.split_len);
+  w.m_pad = (int)((d.M + 63) / 64 * 64);
+  const size_t rows = (size_t)d.M * d.hs;
+  const size_t qa = align_up(rows * d.d * 2), f = align_up(rows * 4);
+  const size_t tr = align_up((size_t)d.hs * d.d * w.m_pad * 2);
+  const size_t part = w.n_split > 1 ? (size_t)w.n_split * rows : 0;
+  w.q = 0;
+  w.a = qa;
+  w.da = 2 * qa;
+  w.dq = 3 * qa;
+  w.lse = 4 * qa;
+  w.delta = w.lse + f;
+  w.at = w.delta + f;
+  w.dqt = w.at + tr;
+  w.po = w.dqt + tr;
+  w.pml = w.po + align_up(part * d.d * 4);
+  w.total = w.pml + align_up(part * 2 * 4);
+  return w;
+}
+// Attention backward, second stage: the transposed gradient of one shard's K or V rows,
+// [K_s d, M rounded up to 64] bf16.
+size_t ws_attn_kv_bwd(const Dims& d) {
+  const size_t m_pad = (size_t)((d.M + 63) / 64 * 64);
+  return align_up((size_t)d.ks * d.d * m_pad * 2);
 }
 size_t ws_layer(const Dims& d) {
   const size_t a = ws_mlp(d), b = ws_attn(d);
@@ -426,6 +464,183 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
   return TSP_OK;
 }
 
+// C[M, n] = A[M, h] B[n, h]^T, bf16 out (the Q epilogue of the projection kernel with
+// every column in the Q block).
+GemmParams nt_params(const Dims& d, const uint16_t* a, const uint16_t* b, int n, uint16_t* out) {
+  GemmParams g = {};
+  g.A = a;
+  g.lda = d.h;
+  g.B = b;
+  g.ldb = d.h;
+  g.M = (int)d.M;
+  g.N = n;
+  g.K = d.h;
+  g.Q = out;
+  g.ldq = n;
+  g.nq = n;
+  g.rows_per_batch = d.s_loc;
+  return g;
+}
+
+// Backward of run_attn, first stage (see tsp_attn_rank_bwd).
+tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
+                        const uint16_t* const* wa, const uint16_t* kb, const uint16_t* vb,
+                        float* dx, int accumulate, float* const* dw, float* dk, float* dv,
+                        char* ws, hipStream_t st) {
+  const int qd = d.hs * d.d, kd = d.ks * d.d;
+  const float log2e = 1.4426950408889634f;
+  const AttnBwdWs w = attn_bwd_ws(d);
+  uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + w.q);
+  uint16_t* a_ws = reinterpret_cast<uint16_t*>(ws + w.a);
+  uint16_t* da_ws = reinterpret_cast<uint16_t*>(ws + w.da);
+  uint16_t* dq_ws = reinterpret_cast<uint16_t*>(ws + w.dq);
+  uint16_t* at_ws = reinterpret_cast<uint16_t*>(ws + w.at);
+  uint16_t* dqt_ws = reinterpret_cast<uint16_t*>(ws + w.dqt);
+  float* lse = reinterpret_cast<float*>(ws + w.lse);
+  float* delta = reinterpret_cast<float*>(ws + w.delta);
+  for (int r = 0; r < d.D; ++r) {
+    const uint16_t* wq = wa[r];
+    const uint16_t* wo_t = wa[r] + (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T [H_s d, h]
+    GemmParams g = nt_params(d, x, wq, qd, q_ws);
+    TSP_LAUNCH(TSP_KERNEL_ABWD_PROJ, st, tsp::launch_gemm_qkv(g, st));
+
+    AttnParams ap = {};
+    ap.Q = q_ws;
+    ap.Kb = kb;
+    ap.Vb = vb;
+    ap.O = a_ws;
+    attn_segments(d, &ap);
+    ap.group = d.g;
+    ap.head_dim = d.d;
+    ap.seq = d.S;
+    ap.n_kv = d.nkv;
+    ap.kv_head0 = r * d.ks;
+    ap.scale_log2 = d.scale * log2e;
+    ap.n_split = w.n_split;
+    ap.split_len = w.split_len;
+    ap.part_rows = (long long)d.M * d.hs;
+    ap.part_o = reinterpret_cast<float*>(ws + w.po);
+    ap.part_ml = reinterpret_cast<float*>(ws + w.pml);
+    ap.lse = lse;
+    TSP_LAUNCH(TSP_KERNEL_ABWD_FWD, st, tsp::launch_flash_attn(ap, st));
+
+    g = nt_params(d, dy, wo_t, qd, da_ws);  // dA = dY W_O^(r)
+    TSP_LAUNCH(TSP_KERNEL_ABWD_PROJ, st, tsp::launch_gemm_qkv(g, st));
+
+    AttnBwdParams bp = {};
+    bp.Qin = q_ws;
+    bp.Qs = q_ws;
+    bp.O = a_ws;
+    bp.dO = da_ws;
+    bp.Kb = kb;
+    bp.Vb = vb;
+    bp.lse = lse;
+    bp.delta = delta;
+    bp.dQ = dq_ws;
+    bp.dK = dk;
+    bp.dV = dv;
+    bp.accumulate = accumulate ? 1 : 0;
+    bp.batch = d.B;
+    bp.s_loc = d.s_loc;
+    bp.heads = d.hs;
+    bp.group = d.g;
+    bp.head_dim = d.d;
+    bp.seq = d.S;
+    bp.n_kv = d.nkv;
+    bp.kv_head0 = r * d.ks;
+    bp.n_seg = ap.n_seg;
+    for (int k = 0; k < 2; ++k) {
+      bp.seg_row0[k] = ap.seg_row0[k];
+      bp.seg_rows[k] = ap.seg_rows[k];
+      bp.seg_pos0[k] = ap.seg_pos0[k];
+    }
+    bp.scale_log2 = ap.scale_log2;
+    bp.scale = d.scale;
+    TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st, tsp::launch_attn_bwd_prep(bp, st));
+    TSP_LAUNCH(TSP_KERNEL_ABWD_KV, st, tsp::launch_attn_bwd_dkdv(bp, st));
+    TSP_LAUNCH(TSP_KERNEL_ABWD_Q, st, tsp::launch_attn_bwd_dq(bp, st));
+
+    GemmParams p = {};  // dX (+)= dQ W_Q^(r): [M, H_s d] x [H_s d, h]
+    p.A = dq_ws;
+    p.lda = qd;
+    p.B = wq;
+    p.ldb = d.h;
+    p.M = (int)d.M;
+    p.N = d.h;
+    p.K = qd;
+    p.Kb_rows = qd;
+    p.Y = dx;
+    p.ldy = d.h;
+    p.accumulate = (r > 0 || accumulate) ? 1 : 0;
+    TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+
+    TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
+               tsp::launch_transpose_bf16(dq_ws, qd, (int)d.M, qd, dqt_ws, w.m_pad, st));
+    TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
+               tsp::launch_transpose_bf16(a_ws, qd, (int)d.M, qd, at_ws, w.m_pad, st));
+    // W_Q block (+)= dQ^T X;  W_O^T block (+)= A^T dY: [H_s d, M] x [M, h].
+    for (int k = 0; k < 2; ++k) {
+      GemmParams q = {};
+      q.A = k == 0 ? dqt_ws : at_ws;
+      q.lda = w.m_pad;
+      q.B = k == 0 ? x : dy;
+      q.ldb = d.h;
+      q.M = qd;
+      q.N = d.h;
+      q.K = w.m_pad;
+      q.Kb_rows = (int)d.M;
+      q.Y = dw[r] + (k == 0 ? (size_t)0 : (size_t)(qd + 2 * kd) * d.h);
+      q.ldy = d.h;
+      q.accumulate = accumulate ? 1 : 0;
+      TSP_LAUNCH(TSP_KERNEL_ABWD_DW, st, tsp::launch_gemm_nn_acc_small(q, st));
+    }
+  }
+  return TSP_OK;
+}
+
+// Second stage (see tsp_attn_kv_rank_bwd).
+tsp_status run_attn_kv_bwd(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
+                           const uint16_t* dkl, const uint16_t* dvl, float* dx, int accumulate,
+                           float* const* dw, char* ws, hipStream_t st) {
+  const int qd = d.hs * d.d, kd = d.ks * d.d, ld = d.nkv * d.d;
+  const int m_pad = (int)((d.M + 63) / 64 * 64);
+  uint16_t* t_ws = reinterpret_cast<uint16_t*>(ws);
+  for (int r = 0; r < d.D; ++r)
+    for (int k = 0; k < 2; ++k) {
+      const uint16_t* g = (k == 0 ? dkl : dvl) + (size_t)r * kd;  // [M, K_s d], row stride ld
+      const size_t blk = (size_t)(qd + k * kd) * d.h;             // W_K or W_V block
+      GemmParams p = {};  // dX (+)= g W_{K|V}^(r)
+      p.A = g;
+      p.lda = ld;
+      p.B = wa[r] + blk;
+      p.ldb = d.h;
+      p.M = (int)d.M;
+      p.N = d.h;
+      p.K = kd;
+      p.Kb_rows = kd;
+      p.Y = dx;
+      p.ldy = d.h;
+      p.accumulate = (r > 0 || k > 0 || accumulate) ? 1 : 0;
+      TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+      TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
+                 tsp::launch_transpose_bf16(g, ld, (int)d.M, kd, t_ws, m_pad, st));
+      GemmParams q = {};  // block (+)= g^T X
+      q.A = t_ws;
+      q.lda = m_pad;
+      q.B = x;
+      q.ldb = d.h;
+      q.M = kd;
+      q.N = d.h;
+      q.K = m_pad;
+      q.Kb_rows = (int)d.M;
+      q.Y = dw[r] + blk;
+      q.ldy = d.h;
+      q.accumulate = accumulate ? 1 : 0;
+      TSP_LAUNCH(TSP_KERNEL_ABWD_DW, st, tsp::launch_gemm_nn_acc_small(q, st));
+    }
+  return TSP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -439,6 +654,8 @@ tsp_status tsp_workspace_bytes(const tsp_shape* shape, int op, size_t* bytes) {
     case TSP_OP_ATTN: *bytes = ws_attn(d); return TSP_OK;
     case TSP_OP_LAYER: *bytes = ws_layer(d); return TSP_OK;
     case TSP_OP_MLP_BWD: *bytes = mlp_bwd_ws(d).total; return TSP_OK;
+    case TSP_OP_ATTN_BWD: *bytes = attn_bwd_ws(d).total; return TSP_OK;
+    case TSP_OP_ATTN_KV_BWD: *bytes = ws_attn_kv_bwd(d); return TSP_OK;
     default: return TSP_ERR_SHAPE;
   }
 }
@@ -518,6 +735,49 @@ tsp_status tsp_attn_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
   if (d.M == 0) return TSP_OK;
   return run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, accumulate, nullptr, nullptr,
                   static_cast<char*>(ws), stream);
+}
+
+tsp_status tsp_attn_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
+                             const uint16_t* dy_loc, const uint16_t* const* w_attn,
+                             const uint16_t* k_buf, const uint16_t* v_buf, float* dx_loc,
+                             int accumulate, float* const* dw_attn, float* dk_buf,
+                             float* dv_buf, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_ptr(dy_loc));
+  TSP_TRY(check_shards(w_attn, d.D));
+  TSP_TRY(check_ptr(k_buf));
+  TSP_TRY(check_ptr(v_buf));
+  TSP_TRY(check_ptr(dx_loc));
+  TSP_TRY(check_shards(dw_attn, d.D));
+  TSP_TRY(check_ptr(dk_buf));
+  TSP_TRY(check_ptr(dv_buf));
+  TSP_TRY(check_ptr(ws));
+  if (ws_bytes < attn_bwd_ws(d).total) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  return run_attn_bwd(d, x_loc, dy_loc, w_attn, k_buf, v_buf, dx_loc, accumulate, dw_attn,
+                      dk_buf, dv_buf, static_cast<char*>(ws), stream);
+}
+
+tsp_status tsp_attn_kv_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
+                                const uint16_t* const* w_attn, const uint16_t* dk_loc,
+                                const uint16_t* dv_loc, float* dx_loc, int accumulate,
+                                float* const* dw_attn, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_shards(w_attn, d.D));
+  TSP_TRY(check_ptr(dk_loc));
+  TSP_TRY(check_ptr(dv_loc));
+  TSP_TRY(check_ptr(dx_loc));
+  TSP_TRY(check_shards(dw_attn, d.D));
+  TSP_TRY(check_ptr(ws));
+  if (ws_bytes < ws_attn_kv_bwd(d)) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  return run_attn_kv_bwd(d, x_loc, w_attn, dk_loc, dv_loc, dx_loc, accumulate, dw_attn,
+                         static_cast<char*>(ws), stream);
 }
 
 tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,

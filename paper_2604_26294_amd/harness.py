@@ -79,11 +79,44 @@ class RankProblem:
         nbytes = max(T.workspace_bytes(self.shape, op) for op in (T.OP_MLP, T.OP_ATTN, T.OP_LAYER))
         self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
 
-    def prefill_kv(self):
-        """The modelled all-gather: the other ranks write their K/V rows of every shard."""
-        for q in self.kv_ranks:
+    def prefill_kv(self, include_self=False):
+        """The modelled all-gather: the other ranks write their K/V rows of every shard
+        (and this rank its own, for a backward run without the forward before it)."""
+        for q in self.kv_ranks + ([self.p] if include_self else []):
             T.tsp_kv_rank_fwd(T.shape_of(self.wl, q), self.x_chunks[q], self.attn, self.k_buf,
                               self.v_buf)
+
+    def _attn_grads(self):
+        if not hasattr(self, "adx"):
+            wl, dev = self.wl, self.device
+            rows = (2 * wl.n_heads // wl.degree + 2 * wl.n_kv_heads // wl.degree) * wl.head_dim
+            self.adx = torch.zeros((wl.batch, wl.s_loc, wl.hidden), dtype=torch.float32,
+                                   device=dev)
+            self.adw = [torch.zeros((rows, wl.hidden), dtype=torch.float32, device=dev)
+                        for _ in range(wl.degree)]
+            kv_shape = (wl.batch, wl.seq, wl.n_kv_heads, wl.head_dim)
+            self.dk_buf = torch.zeros(kv_shape, dtype=torch.float32, device=dev)
+            self.dv_buf = torch.zeros(kv_shape, dtype=torch.float32, device=dev)
+            nbytes = max(T.workspace_bytes(self.shape, op)
+                         for op in (T.OP_ATTN_BWD, T.OP_ATTN_KV_BWD))
+            self.ws_abwd = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+
+    def attn_bwd(self, dy_loc, accumulate=False):
+        """First stage of the attention backward for the bf16 gradient dy_loc [B, S_loc, h]
+        of the block output (the K/V buffers must hold the gathered K/V).  Returns (dx,
+        dw_attn list, dk_buf, dv_buf), fp32 device tensors."""
+        self._attn_grads()
+        T.tsp_attn_rank_bwd(self.shape, self.x_loc, dy_loc, self.attn, self.k_buf, self.v_buf,
+                            self.adx, accumulate, self.adw, self.dk_buf, self.dv_buf, self.ws_abwd)
+        return self.adx, self.adw, self.dk_buf, self.dv_buf
+
+    def attn_kv_bwd(self, dk_loc, dv_loc, accumulate=True):
+        """Second stage: the K/V projection backward for the bf16 reduce-scattered
+        gradients of this rank's rows [B, S_loc, n_kv, d].  Returns (dx, dw_attn list)."""
+        self._attn_grads()
+        T.tsp_attn_kv_rank_bwd(self.shape, self.x_loc, self.attn, dk_loc, dv_loc, self.adx,
+                               accumulate, self.adw, self.ws_abwd)
+        return self.adx, self.adw
 
     def mlp(self, x=None, accumulate=False):
         T.tsp_mlp_rank_fwd(self.shape, self.x_loc if x is None else x, self.w1, self.w3,

@@ -21,7 +21,8 @@ import numpy as np
 
 from .workloads import Workload
 
-TENSOR_ID = {"x": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4, "w1": 5, "w3": 6, "w2": 7, "dy": 8}
+TENSOR_ID = {"x": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4, "w1": 5, "w3": 6, "w2": 7, "dy": 8,
+             "dk_own": 9, "dv_own": 10}
 
 _CHUNK_ELEMS = 1 << 24
 
@@ -73,6 +74,14 @@ def make_x_full(wl: Workload) -> np.ndarray:
 def make_dy_full(wl: Workload) -> np.ndarray:
     """Upstream gradient of the MLP output for the whole sequence, [B, S, h] bf16 bits."""
     return gaussian_bf16(wl.seed, TENSOR_ID["dy"], (wl.batch, wl.seq, wl.hidden), wl.x_std)
+
+
+def make_dkv_own(wl: Workload, p: int) -> tuple:
+    """Stand-ins for the reduce-scattered K / V gradients of rank p's own rows,
+    [B, S_loc, n_kv, d] bf16 bits each (the input of the K/V projection backward)."""
+    shape = (wl.batch, wl.s_loc, wl.n_kv_heads, wl.head_dim)
+    return (gaussian_bf16(wl.seed + 7919 * (p + 1), TENSOR_ID["dk_own"], shape, wl.x_std),
+            gaussian_bf16(wl.seed + 7919 * (p + 1), TENSOR_ID["dv_own"], shape, wl.x_std))
 
 
 def make_weights(wl: Workload) -> dict:

@@ -19,10 +19,11 @@ TSP_ERR_HIP = 7
 STATUS_NAMES = {0: "TSP_OK", 1: "TSP_ERR_NULL", 2: "TSP_ERR_SHAPE", 3: "TSP_ERR_RANK",
                 4: "TSP_ERR_ALIGN", 5: "TSP_ERR_WORKSPACE", 6: "TSP_ERR_UNSUPPORTED",
                 7: "TSP_ERR_HIP"}
-OP_MLP, OP_ATTN, OP_LAYER, OP_MLP_BWD = 0, 1, 2, 3
+OP_MLP, OP_ATTN, OP_LAYER, OP_MLP_BWD, OP_ATTN_BWD, OP_ATTN_KV_BWD = 0, 1, 2, 3, 4, 5
 LAYOUT_CONTIGUOUS, LAYOUT_ZIGZAG = 0, 1
 KERNELS = ("gate_up", "down", "qkv", "attn", "oproj",  # TSP_KERNEL_* order
-           "bwd_gate", "bwd_dx", "bwd_dw")
+           "bwd_gate", "bwd_dx", "bwd_dw",
+           "abwd_proj", "abwd_fwd", "abwd_kv", "abwd_q", "abwd_dx", "abwd_dw", "abwd_aux")
 
 
 class TspError(RuntimeError):
@@ -61,6 +62,8 @@ def _load() -> ctypes.CDLL:
         "tsp_mlp_rank_fwd": [SH, P, PP, PP, PP, P, I, VP, SZ, VP],
         "tsp_mlp_rank_bwd": [SH, P, P, PP, PP, PP, P, I, PP, PP, PP, VP, SZ, VP],
         "tsp_kv_rank_fwd": [SH, P, PP, P, P, VP],
+        "tsp_attn_rank_bwd": [SH, P, P, PP, P, P, P, I, PP, P, P, VP, SZ, VP],
+        "tsp_attn_kv_rank_bwd": [SH, P, PP, P, P, P, I, PP, VP, SZ, VP],
         "tsp_attn_rank_fwd": [SH, P, PP, P, P, P, I, VP, SZ, VP],
         "tsp_layer_rank_fwd": [SH, P, PP, PP, PP, PP, P, P, P, VP, SZ, VP],
         "tsp_workspace_bytes": [SH, I, ctypes.POINTER(ctypes.c_size_t)],
@@ -165,6 +168,25 @@ def tsp_attn_rank_fwd(shape, x_loc, w_attn, k_buf, v_buf, y_loc, accumulate, ws,
     _check(lib.tsp_attn_rank_fwd(ctypes.byref(shape), _ptr(x_loc), a, _ptr(k_buf), _ptr(v_buf),
                                  _ptr(y_loc), int(accumulate), _ptr(ws), _nbytes(ws),
                                  _stream(stream)), "tsp_attn_rank_fwd")
+
+
+def tsp_attn_rank_bwd(shape, x_loc, dy_loc, w_attn, k_buf, v_buf, dx_loc, accumulate, dw_attn,
+                      dk_buf, dv_buf, ws, stream=None):
+    a, _a = _ptrs(w_attn)
+    dw, _dw = _ptrs(dw_attn)
+    _check(lib.tsp_attn_rank_bwd(ctypes.byref(shape), _ptr(x_loc), _ptr(dy_loc), a, _ptr(k_buf),
+                                 _ptr(v_buf), _ptr(dx_loc), int(accumulate), dw, _ptr(dk_buf),
+                                 _ptr(dv_buf), _ptr(ws), _nbytes(ws), _stream(stream)),
+           "tsp_attn_rank_bwd")
+
+
+def tsp_attn_kv_rank_bwd(shape, x_loc, w_attn, dk_loc, dv_loc, dx_loc, accumulate, dw_attn, ws,
+                         stream=None):
+    a, _a = _ptrs(w_attn)
+    dw, _dw = _ptrs(dw_attn)
+    _check(lib.tsp_attn_kv_rank_bwd(ctypes.byref(shape), _ptr(x_loc), a, _ptr(dk_loc),
+                                    _ptr(dv_loc), _ptr(dx_loc), int(accumulate), dw, _ptr(ws),
+                                    _nbytes(ws), _stream(stream)), "tsp_attn_kv_rank_bwd")
 
 
 def tsp_layer_rank_fwd(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf, y_loc, ws,

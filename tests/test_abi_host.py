@@ -27,8 +27,8 @@ def _declared_functions():
 def test_every_declared_symbol_is_exported():
     names = _declared_functions()
     assert {"tsp_mlp_rank_fwd", "tsp_attn_rank_fwd", "tsp_layer_rank_fwd", "tsp_kv_rank_fwd",
-            "tsp_mlp_rank_bwd", "tsp_workspace_bytes", "tsp_status_str",
-            "tsp_abi_version"} <= set(names)
+            "tsp_mlp_rank_bwd", "tsp_attn_rank_bwd", "tsp_attn_kv_rank_bwd",
+            "tsp_workspace_bytes", "tsp_status_str", "tsp_abi_version"} <= set(names)
     raw = ctypes.CDLL(T._LIB_PATH)
     for n in names:
         assert hasattr(raw, n), n
@@ -55,7 +55,14 @@ def test_workspace_covers_intermediates(wl):
     m_pad = (m + 63) // 64 * 64
     fs = wl.ffn // wl.degree
     assert bwd >= 2 * m * fs * 2 + 3 * fs * m_pad * 2  # dG, dU and three transposes
-    for v in (mlp, attn, layer, bwd):
+    qd = wl.n_heads // wl.degree * wl.head_dim
+    kd = wl.n_kv_heads // wl.degree * wl.head_dim
+    abwd = T.workspace_bytes(sh, T.OP_ATTN_BWD)
+    akv = T.workspace_bytes(sh, T.OP_ATTN_KV_BWD)
+    # Q, A, dA, dQ; lse and delta; A^T and dQ^T
+    assert abwd >= 4 * m * qd * 2 + 2 * m * (wl.n_heads // wl.degree) * 4 + 2 * qd * m_pad * 2
+    assert akv >= kd * m_pad * 2                        # one transposed K or V gradient
+    for v in (mlp, attn, layer, bwd, abwd, akv):
         assert v % 256 == 0
 
 
@@ -143,6 +150,37 @@ def test_backward_rejects_bad_arguments():
     assert L.tsp_mlp_rank_bwd(*a) == 3
 
 
+def test_attention_backward_rejects_bad_arguments():
+    sh = _shape()
+    L = T.lib
+    good, _k1 = _arr(2)
+    nul, _k2 = _arr(2, 0)
+    mis, _k3 = _arr(2, FAKE + 4)
+    need = T.workspace_bytes(sh, T.OP_ATTN_BWD)
+    # argument lists that would pass validation; every call below breaks one argument
+    args = [ctypes.byref(sh), FAKE, FAKE, good, FAKE, FAKE, FAKE, 0, good, FAKE, FAKE, FAKE,
+            need, None]
+    for pos, val, code in [(1, None, 1), (2, None, 1), (3, nul, 1), (4, None, 1),
+                           (5, FAKE + 2, 4), (6, None, 1), (8, mis, 4), (9, None, 1),
+                           (10, FAKE + 4, 4), (11, None, 1), (12, need - 1, 5)]:
+        a = list(args)
+        a[pos] = val
+        assert L.tsp_attn_rank_bwd(*a) == code, (pos, code)
+    a = list(args)
+    a[0] = ctypes.byref(_shape(rank=5))
+    assert L.tsp_attn_rank_bwd(*a) == 3
+    need = T.workspace_bytes(sh, T.OP_ATTN_KV_BWD)
+    args = [ctypes.byref(sh), FAKE, good, FAKE, FAKE, FAKE, 1, good, FAKE, need, None]
+    for pos, val, code in [(1, FAKE + 8, 4), (2, nul, 1), (3, None, 1), (4, FAKE + 2, 4),
+                           (5, None, 1), (7, mis, 4), (8, None, 1), (9, need - 1, 5)]:
+        a = list(args)
+        a[pos] = val
+        assert L.tsp_attn_kv_rank_bwd(*a) == code, (pos, code)
+    a = list(args)
+    a[0] = ctypes.byref(_shape(seq=255))
+    assert L.tsp_attn_kv_rank_bwd(*a) == 2
+
+
 def test_empty_batch_is_a_no_op():
     """batch = 0 passes validation and returns before any launch (no GPU involved)."""
     sh = _shape(batch=0)
@@ -152,6 +190,11 @@ def test_empty_batch_is_a_no_op():
     assert T.lib.tsp_layer_rank_fwd(ctypes.byref(sh), FAKE, good, good, good, good, FAKE, FAKE,
                                     FAKE, FAKE, 0, None) == 0
     assert T.workspace_bytes(sh, T.OP_LAYER) == 0
+    assert T.workspace_bytes(sh, T.OP_ATTN_BWD) == 0
+    assert T.lib.tsp_attn_rank_bwd(ctypes.byref(sh), FAKE, FAKE, good, FAKE, FAKE, FAKE, 0, good,
+                                   FAKE, FAKE, FAKE, 0, None) == 0
+    assert T.lib.tsp_attn_kv_rank_bwd(ctypes.byref(sh), FAKE, good, FAKE, FAKE, FAKE, 0, good,
+                                      FAKE, 0, None) == 0
 
 
 def test_python_binding_raises_named_errors():
