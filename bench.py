@@ -12,7 +12,9 @@ in HBM before timing starts.  Prints one JSON line on stdout; progress goes to s
 
 Besides the layer call the line reports the attention-only and MLP-only entry points
 timed separately ("blocks"), the per-rank MLP backward (``tsp_mlp_rank_bwd``, with its
-kernel classes) on the same rank ("blocks.mlp_bwd"), the algorithmic HBM bytes of a step
+kernel classes) on the same rank ("blocks.mlp_bwd"), the two-stage attention backward
+(``tsp_attn_rank_bwd`` and ``tsp_attn_kv_rank_bwd``, "blocks.attn_bwd"), the algorithmic
+HBM bytes of a step
 and the bandwidth they imply ("hbm"), the paper's non-causal F_layer / D for reference,
 and with --rank-sweep the layer time of every rank of the group and the max/min
 imbalance.
@@ -76,7 +78,15 @@ def kernel_flops(wl):
             "oproj": 2.0 * m * qd * h,
             # MLP backward: G, U and dHs in one pass; one dX product; one weight gradient
             "bwd_gate": 2.0 * m * 3 * fs * h, "bwd_dx": 2.0 * m * fs * h,
-            "bwd_dw": 2.0 * m * fs * h}
+            "bwd_dw": 2.0 * m * fs * h,
+            # attention backward, first stage: the Q / dA products; the forward recomputation;
+            # dK/dV recomputes S and forms dP, dV, dK (4 of the forward's 2 products' cost
+            # each pair = 2x the core); dQ recomputes S, dP and forms dQ (1.5x); the
+            # stage's dX and weight-gradient products (second-stage launches are K_s/H_s
+            # of these)
+            "abwd_proj": 2.0 * m * qd * h, "abwd_fwd": step_attn_core_flops(wl),
+            "abwd_kv": 2.0 * step_attn_core_flops(wl), "abwd_q": 1.5 * step_attn_core_flops(wl),
+            "abwd_dx": 2.0 * m * qd * h, "abwd_dw": 2.0 * m * qd * h}
 
 
 def cpu_baseline(wl, x_bits, w_bits, rows: int):
@@ -285,7 +295,53 @@ def main(argv=None):
                          "tflops": round(bwd_flops / (ms_bwd * 1e-3) / 1e12, 2),
                          "flops_note": "16 M F h executed (G, U recomputed); 12 M F h without",
                          "kernels": bwd_kernels}
-    del dy
+
+    # The per-rank attention backward: first stage (all D shards: recomputation, dA, the
+    # flash backward, dX query path, dW_Q and dW_O^T contributions, this rank's dK/dV
+    # contributions for every key) and second stage (K/V projection backward on the
+    # rank's rows, fed with synthetic reduce-scattered gradients).
+    prob.prefill_kv(include_self=True)
+    dk_bits, dv_bits = I.make_dkv_own(wl, wl.rank)
+    dkl, dvl = to_device_bf16(dk_bits), to_device_bf16(dv_bits)
+    del dk_bits, dv_bits
+    for _ in range(2):
+        prob.attn_bwd(dy)
+        prob.attn_kv_bwd(dkl, dvl)
+    torch.cuda.synchronize()
+    T.tsp_profile_enable(True)
+    ms_ab1 = time_calls(lambda: prob.attn_bwd(dy), args.steps, 0)
+    ab1_kernels = {}
+    for k, name in enumerate(T.KERNELS):
+        if not name.startswith("abwd_"):
+            continue
+        tot, n = T.tsp_profile_read(k)
+        if n:
+            e = {"avg_ms": round(tot / n, 5), "launches": n // args.steps,
+                 "time_share": round(tot / args.steps / ms_ab1, 4)}
+            if name != "abwd_aux":
+                e["tflops"] = round(kf[name] / (tot / n * 1e-3) / 1e12, 2)
+            ab1_kernels[name] = e
+    T.tsp_profile_enable(False)
+    ms_ab2 = time_calls(lambda: prob.attn_kv_bwd(dkl, dvl), args.steps, 0)
+    core = kf["attn"]
+    D = wl.degree
+    qd = wl.n_heads // D * wl.head_dim
+    kd = wl.n_kv_heads // D * wl.head_dim
+    gemm1 = 5 * 2.0 * m_tok * qd * wl.hidden          # Q, dA, dX, dW_Q, dW_O^T per shard
+    exec1 = D * (gemm1 + (1 + 2 + 1.5) * core)
+    alg1 = D * (4 * 2.0 * m_tok * qd * wl.hidden + 2.5 * core)  # without Q, S, A recompute
+    flops2 = D * 4 * 2.0 * m_tok * kd * wl.hidden      # dX (K, V) and dW_K, dW_V per shard
+    blocks["attn_bwd"] = {
+        "ms": round(ms_ab1 + ms_ab2, 4), "stage1_ms": round(ms_ab1, 4),
+        "stage2_ms": round(ms_ab2, 4),
+        "flops_executed": exec1 + flops2, "flops_backward": alg1 + flops2,
+        "tflops_executed": round((exec1 + flops2) / ((ms_ab1 + ms_ab2) * 1e-3) / 1e12, 2),
+        "tflops_backward": round((alg1 + flops2) / ((ms_ab1 + ms_ab2) * 1e-3) / 1e12, 2),
+        "flops_note": "executed: with the Q / attention recomputation and the two flash "
+                      "backward kernels' repeated score and dP products (4.5x the forward "
+                      "core); backward: 2.5x the forward core plus the gradient products",
+        "kernels": ab1_kernels}
+    del dy, dkl, dvl
 
     nbytes = rank_algorithmic_bytes(wl)
     hbm = {"algorithmic_bytes": nbytes, "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),

@@ -557,3 +557,50 @@ def attention_rows(x_b, wq, wk, wv, wo, n_heads, n_kv_heads, positions, scale=No
     for i in range(n_heads):
         a[:, i] = z[:, i] @ wv_h[i // g].T
     return a.reshape(n_r, n_heads * d) @ wo.T
+
+
+def attention_bwd_rows(x_b, wq, wk, wv, wo, n_heads, n_kv_heads, positions, dy_rows,
+                       scale=None):
+    """Query path of the attention block's dX (K and V held fixed) at the given global
+    positions of one sequence: sum over heads i of dq_i W_Q,i, where dq_i is the gradient
+    of head i's query for the upstream rows dy_rows [len(positions), h] at those
+    positions.  Uses only associativity, as attention_rows does: with k_j = W_K x_j and
+    v_j = W_V x_j, every product over keys runs against the layer input rows x_b [S, h],
+    so no K or V of the prefix is formed.  Per head (dA = dY W_O):
+      P = causal softmax of scale q k^T;  dP_tj = dA_t . v_j;  o_t = sum_j P_tj v_j;
+      dS = P * (dP - dA . o);  dq_t = scale sum_j dS_tj k_j.
+    Returns [len(positions), h]."""
+    positions = np.asarray(positions, dtype=np.int64)
+    d = wq.shape[0] // n_heads
+    g = n_heads // n_kv_heads
+    sc = default_scale(d, scale)
+    t_max = int(positions.max()) + 1
+    x_pre = x_b[:t_max]
+    n_r, h = positions.shape[0], x_b.shape[1]
+    q = (x_b[positions] @ wq.T).reshape(n_r, n_heads, d)
+    da = (dy_rows @ wo).reshape(n_r, n_heads, d)
+    wk_h = wk.reshape(n_kv_heads, d, h)
+    wv_h = wv.reshape(n_kv_heads, d, h)
+    u = np.empty((n_r, n_heads, h))
+    w = np.empty((n_r, n_heads, h))
+    for i in range(n_heads):
+        u[:, i] = q[:, i] @ wk_h[i // g]     # score of key j = u . x_j
+        w[:, i] = da[:, i] @ wv_h[i // g]    # dP of key j = w . x_j
+    pos_rows = np.repeat(positions, n_heads)
+    allowed = np.arange(t_max)[None, :] <= pos_rows[:, None]
+    s = np.where(allowed, (u.reshape(-1, h) @ x_pre.T) * sc, -np.inf)
+    s -= s.max(axis=1, keepdims=True)
+    e = np.exp(s)
+    pmat = e / e.sum(axis=1, keepdims=True)
+    dp = np.where(allowed, w.reshape(-1, h) @ x_pre.T, 0.0)
+    z = (pmat @ x_pre).reshape(n_r, n_heads, h)          # o_i = W_V z_i
+    o = np.empty((n_r, n_heads, d))
+    for i in range(n_heads):
+        o[:, i] = z[:, i] @ wv_h[i // g].T
+    delta = np.sum(da * o, axis=2).reshape(-1)
+    ds = pmat * (dp - delta[:, None])
+    y = (ds @ x_pre).reshape(n_r, n_heads, h)            # dq_i = scale W_K y_i
+    dq = np.empty((n_r, n_heads, d))
+    for i in range(n_heads):
+        dq[:, i] = sc * (y[:, i] @ wk_h[i // g].T)
+    return dq.reshape(n_r, n_heads * d) @ wq

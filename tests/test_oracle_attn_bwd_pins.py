@@ -168,3 +168,46 @@ def test_backward_special_cases():
     q = rng.standard_normal((s, d))
     dq, _, _ = O.causal_attention_core_bwd(q, k, v, do, 0, 0.7)
     assert np.allclose(dq[0], 0.0, atol=1e-15)
+
+
+@pytest.mark.parametrize("n_heads,n_kv", [(4, 2), (4, 4)])
+def test_sampled_rows_backward_is_the_query_path(n_heads, n_kv):
+    """attention_bwd_rows (the full-size checker) against finite differences of the
+    unsharded block with the input of the K / V projections held fixed, and against the
+    query path of the first stage on every rank."""
+    pb = _problem("contiguous", seed=9, n_heads=n_heads, n_kv=n_kv, degree=2)
+    x, w, dy = pb["x"], pb["w"], pb["dy"]
+    d, seq = pb["d"], x.shape[1]
+    rows = np.array([0, 3, seq - 1])
+    got = O.attention_bwd_rows(x[1], w["wq"], w["wk"], w["wv"], w["wo"], n_heads, n_kv, rows,
+                               dy[1, rows])
+
+    def block(xq):   # the attention block with queries from xq, keys / values from x
+        b_, s_, _ = x.shape
+        g = n_heads // n_kv
+        q = (xq @ w["wq"].T).reshape(b_, s_, n_heads, d)
+        k = (x @ w["wk"].T).reshape(b_, s_, n_kv, d)
+        v = (x @ w["wv"].T).reshape(b_, s_, n_kv, d)
+        a = np.empty_like(q)
+        for b in range(b_):
+            for i in range(n_heads):
+                a[b, :, i] = O.causal_attention_core(q[b, :, i], k[b, :, i // g], v[b, :, i // g],
+                                                     0, 1 / np.sqrt(d))
+        return a.reshape(b_, s_, -1) @ w["wo"].T
+
+    xq = x.copy()
+    loss = lambda: float(np.sum(dy * block(xq)))  # noqa: E731
+    rng = np.random.default_rng(4)
+    for n, t in enumerate(rows):
+        v = np.zeros_like(xq)
+        v[1, t] = rng.standard_normal(x.shape[2])
+        assert abs(_fd_dir(loss, xq, v) - got[n] @ v[1, t]) < 1e-7
+    D = pb["degree"]
+    shards = [_packed(w, r, D, n_heads, n_kv, d) for r in range(D)]
+    xs = [x[:, O.rank_positions(seq, D, p, "contiguous")] for p in range(D)]
+    kv = [O.gather_kv(xs, shards[r], n_heads // D, n_kv // D, d) for r in range(D)]
+    s_loc = seq // D
+    for n, t in enumerate(rows):
+        p = t // s_loc
+        out = O.attn_rank_bwd(xs[p], shards, kv, p, n_heads, n_kv, d, dy[:, p * s_loc:(p + 1) * s_loc])
+        assert np.allclose(out["dx"][1, t - p * s_loc], got[n], rtol=1e-10, atol=1e-12)
