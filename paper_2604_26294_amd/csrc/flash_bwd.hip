@@ -52,6 +52,9 @@ constexpr int kDqTile = 32 * kBwdWaves;  // queries per query-stationary workgro
 constexpr int kKStage = 64;              // keys staged per step (query-stationary)
 constexpr float kLn2 = 0.69314718055994531f;
 
+template <int N>
+using IC = std::integral_constant<int, N>;
+
 template <int D>
 struct BwCfg {
   static constexpr int KCH = D / 8;             // 16-byte chunks per row
@@ -139,14 +142,26 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const AttnBwdParams 
 
 // ---------------------------------------------------------------------------------
 // Key-stationary kernel: dK, dV of 128 keys of one kv head.
+//
+// The query tiles (64 rows of Qs and dO with their lse and delta) stream through a
+// three-slot LDS ring; each wave takes every tile in two 32-query blocks.  Block n's
+// work has three parts: M1 (the S and dP products, 16 MFMAs on row reads), V (the
+// probabilities and dS, vector ops only) and M2 (the dV^T and dK^T products, 16 MFMAs
+// on transpose reads).  They are software-pipelined over the blocks of all tiles:
+// iteration n issues M1(n + 1) interleaved with V(n), then M2(n), so the vector work of
+// one block runs under the matrix work of the next.  M1(n + 1) may start a new tile
+// while M2(n) still reads the previous one; with three slots and each tile's loads
+// issued one tile ahead (after the barrier that opens the tile before it), a slot is
+// refilled only after every wave has finished the block that last read it.
 template <int D>
 __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   using C = BwCfg<D>;
-  constexpr int RB = C::RB, T64 = C::T64;
-  // [Qs slot 0][Qs slot 1][dO slot 0][dO slot 1][lse, delta slot 0][lse, delta slot 1]
-  __shared__ __attribute__((aligned(1024))) char L[4 * T64 + 2 * 2 * kQStage * 4];
+  constexpr int T64 = C::T64;
+  constexpr int kSlots = 3;
+  // [Qs slots][dO slots][lse, delta slots]
+  __shared__ __attribute__((aligned(1024))) char L[2 * kSlots * T64 + kSlots * 2 * kQStage * 4];
   lds_char* Ls = (lds_char*)L;
-  float* Lf = reinterpret_cast<float*>(L + 4 * T64);
+  float* Lf = reinterpret_cast<float*>(L + 2 * kSlots * T64);
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -154,11 +169,13 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
   const int kv_heads = P.heads / P.group;
 
   // Work item -> (batch, kv head, key tile), key tile fastest: an XCD's contiguous share
-  // of work indices streams the same queries through its L2.  Early keys see the most
-  // queries and come first.
+  // of work indices streams the same queries through its L2.  Key tiles alternate from
+  // both ends of the sequence (early keys see the most queries), so that every XCD's
+  // share holds as much light work as heavy.
   const int n_kt = (int)((P.seq + kKvTile - 1) / kKvTile);
   const int w = xcd_work_index(blockIdx.x, n_kt * kv_heads * P.batch);
-  const int kt = w % n_kt;
+  const int kj = w % n_kt;
+  const int kt = (kj & 1) ? n_kt - 1 - (kj >> 1) : (kj >> 1);
   const int kvl = (w / n_kt) % kv_heads;
   const int b = w / n_kt / kv_heads;
   const int kvh = P.kv_head0 + kvl;
@@ -190,7 +207,7 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
     nv[sg] = max(0, nt - tf[sg]);
   }
   const int per_head = nv[0] + nv[1];
-  const int n_steps = per_head * P.group;
+  const int n_tiles = per_head * P.group;
   struct Tile {
     int head, seg, r0;
   };
@@ -203,101 +220,203 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
     return T;
   };
   const uint32_t q_row_bytes = 2u * (uint32_t)(P.heads * D);
-  float pend_l = 0.f, pend_d = 0.f;  // lse / delta of the next tile (wave 0, one row per lane)
-  auto issue = [&](int t, int slot) __attribute__((always_inline)) {
+  // Qs and dO rows of tile t into its slot (LDS-destination loads).
+  auto issue = [&](int t) __attribute__((always_inline)) {
+    const int slot = t % kSlots;
     const Tile T = tile_of(t);
-    const int rows = P.seg_rows[T.seg];
-    const size_t g0 = (size_t)b * P.s_loc + P.seg_row0[T.seg] + T.r0;
-    const size_t e0 = (g0 * P.heads + T.head) * D;
-    const int last = rows - 1 - T.r0;
+    const size_t e0 = (((size_t)b * P.s_loc + P.seg_row0[T.seg] + T.r0) * P.heads + T.head) * D;
+    const int last = P.seg_rows[T.seg] - 1 - T.r0;
     load_tile64<D>(P.Qs + e0, q_row_bytes, last, Ls + slot * T64, wave, lane);
-    load_tile64<D>(P.dO + e0, q_row_bytes, last, Ls + (2 + slot) * T64, wave, lane);
-    if (wave == 0) {
-      const size_t li =
-          ((size_t)b * P.heads + T.head) * P.s_loc + P.seg_row0[T.seg] + T.r0 + min(lane, last);
-      const float l = P.lse[li], d = P.delta[li];
-      pend_l = lane <= last ? l : INFINITY;  // rows past the segment: P = 0
-      pend_d = lane <= last ? d : 0.f;
-    }
+    load_tile64<D>(P.dO + e0, q_row_bytes, last, Ls + (kSlots + slot) * T64, wave, lane);
   };
-
+  // lse and delta of tile t (t past the last tile: the last one again), fetched two
+  // tiles ahead into a register: wave w takes rows 16 w .. 16 w + 15, lanes 0-15 lse and
+  // 16-31 delta (lanes 32-63 repeat them).  One unconditional load per wave per tile, so
+  // the count of loads in flight behind a tile's LDS-destination loads is the same in
+  // every wave; rows past the segment (clamped on load) get lse = +inf, delta = 0 when
+  // they are written to LDS (P = 0 there).
+  const int pr = 16 * wave + (lane & 15), pwhich = (lane >> 4) & 1;
+  // (the array base is chosen from two scalar values, not by indexing the parameter
+  // block per lane, which would load the pointer from memory)
+  const float* const pbase = pwhich ? P.delta : P.lse;
+  float pend[kSlots];
+  int pend_last[kSlots];
+  auto pend_load = [&](auto slot_x, int t) __attribute__((always_inline)) {
+    constexpr int X = decltype(slot_x)::value;
+    const Tile T = tile_of(min(t, n_tiles - 1));
+    const int last = P.seg_rows[T.seg] - 1 - T.r0;
+    const size_t li = ((size_t)b * P.heads + T.head) * P.s_loc + P.seg_row0[T.seg] + T.r0 +
+                      min(pr, last);
+    pend[X] = pbase[li];
+    pend_last[X] = last;
+  };
+  // Make tile t (slot U = t mod 3) resident: its lse / delta into LDS, every wave's
+  // loads of it landed, and every wave past block 2 t - 2 (so the slot refilled next,
+  // last read by block 2 t - 3, is free); then start tile t + 1's rows and tile t + 2's
+  // lse / delta.
+  auto open_tile = [&](auto slot_u, int t) __attribute__((always_inline)) {
+    constexpr int U = decltype(slot_u)::value;
+    if (lane < 32)
+      Lf[U * 2 * kQStage + pwhich * kQStage + pr] =
+          pr <= pend_last[U] ? pend[U] : (pwhich ? 0.f : INFINITY);
+    asm volatile("s_waitcnt vmcnt(1)" ::: "memory");  // all but tile t + 1's lse / delta
+    __syncthreads();
+    if (t + 1 < n_tiles) issue(t + 1);
+    pend_load(IC<(U + 2) % kSlots>{}, t + 2);
+  };
+  // Per-lane LDS offsets (within a slot and block; the swizzle of a row depends only on
+  // its index mod 16, which the slot, block and k-step offsets preserve):
+  //  M1 row reads of k-step ks: row l32, logical chunk 2 ks + hh -> kad ^ (32 ks);
+  //  M2 transpose reads, column block eb: rows trr and trr + 8 -> tra[eb], trb[eb].
+  const int kad = l32 * C::RB + 16 * (hh ^ C::f(l32));
+  const int trr = tr_row(lane), trc = tr_col(lane);
+  int tra[C::EB], trb[C::EB];
+#pragma unroll
+  for (int eb = 0; eb < C::EB; ++eb) {
+    tra[eb] = C::off(trr, 32 * eb + trc);
+    trb[eb] = C::off(trr + 8, 32 * eb + trc);
+  }
   f32x16 dkT[C::EB], dvT[C::EB];
 #pragma unroll
   for (int eb = 0; eb < C::EB; ++eb)
 #pragma unroll
     for (int e = 0; e < 16; ++e) dkT[eb][e] = dvT[eb][e] = 0.f;
 
-  const int trr = tr_row(lane), trc = tr_col(lane);
-  if (n_steps > 0) issue(0, 0);
-  for (int t = 0; t < n_steps; ++t) {
-    const int slot = t & 1;
-    if (wave == 0) {
-      Lf[slot * 2 * kQStage + lane] = pend_l;
-      Lf[slot * 2 * kQStage + kQStage + lane] = pend_d;
+  // One block: V on (s, dp) -- block HALF of the tile in slot SLOT, at position tpos --
+  // spread over the steps of M1 of the next block into (s_out, dp_out), then M2.
+  // Element 4 g + r is query row 32 HALF + 8 g + 4 hh + r of the tile.  The slots are
+  // compile-time constants, so every LDS address is a per-lane register plus an
+  // immediate.  After the last block, M1 reads stale rows of a free slot (in bounds)
+  // and its result is never used.
+  constexpr int EPC = 16 / C::KS;  // vector elements per M1 step
+  auto block = [&](auto slot, auto half, int tpos, const f32x16& s, const f32x16& dp,
+                   f32x16& s_out, f32x16& dp_out) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value, HF = decltype(half)::value;
+    constexpr int NS = HF == 0 ? S : (S + 1) % kSlots, NH = 1 - HF;  // the next block
+    constexpr int QB = S * T64 + HF * 32 * C::RB;     // this block's rows in the Qs ring
+    constexpr int NQB = NS * T64 + NH * 32 * C::RB;   // the next block's rows
+    constexpr int OR = kSlots * T64;                  // Qs ring -> dO ring
+    const float* lse_t = Lf + S * 2 * kQStage + 32 * HF + 4 * hh;
+    const int rel = key - (tpos + 32 * HF + 4 * hh);  // masked where rel > 8 g + r
+    constexpr int H = C::KS / 2;
+    u32x4 qa[C::KS], oa[C::KS];
+#pragma unroll
+    for (int ks = 0; ks < H; ++ks) {
+      qa[ks] = lds_read16(Ls + NQB + (kad ^ (32 * ks)));
+      oa[ks] = lds_read16(Ls + OR + NQB + (kad ^ (32 * ks)));
     }
-    wait_dma();
-    __syncthreads();  // tile t resident in `slot`; every wave is done with tile t - 1
-    if (t + 1 < n_steps) issue(t + 1, slot ^ 1);
-
-    const Tile T = tile_of(t);
-    const int rows = P.seg_rows[T.seg];
-    const int tpos0 = P.seg_pos0[T.seg] + T.r0;  // position of tile row 0
-    const lds_char* Lq = Ls + slot * T64;
-    const lds_char* Lo = Ls + (2 + slot) * T64;
-    const float* lse_t = Lf + slot * 2 * kQStage;
-    const float* del_t = lse_t + kQStage;
+    f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_t);
+    f32x4 d4 = *reinterpret_cast<const f32x4*>(lse_t + kQStage);
+    float pv[16], dv[16];
+    // M2 operands: transpose reads of dO^T and Qs^T for pair i = (s2, eb) of this block.
+    auto rd = [&](int i, u32x4& ot, u32x4& qt) __attribute__((always_inline)) {
+      const int s2 = i / C::EB, eb = i % C::EB;
+      const lds_char* bq = Ls + QB + 16 * s2 * C::RB;
+      const u32x2 olo = lds_read_tr(bq + OR + tra[eb]), ohi = lds_read_tr(bq + OR + trb[eb]);
+      const u32x2 qlo = lds_read_tr(bq + tra[eb]), qhi = lds_read_tr(bq + trb[eb]);
+      ot = u32x4{olo[0], olo[1], ohi[0], ohi[1]};
+      qt = u32x4{qlo[0], qlo[1], qhi[0], qhi[1]};
+    };
+    constexpr int NI = 2 * C::EB;
+    u32x4 ot[C::EB], qt[C::EB];
 #pragma unroll
-    for (int qb = 0; qb < kQStage / 32; ++qb) {
-      if (T.r0 + 32 * qb >= rows) break;                        // past the segment
-      const int qpos_first = tpos0 + 32 * qb;
-      const int qpos_last = tpos0 + min(32 * qb + 31, rows - 1 - T.r0);
-      if (qpos_last < wk0) continue;                           // every key after every query
-      const bool need_mask = wk0 + 31 > qpos_first;
-
-      f32x16 s, dp;
+    for (int e = 0; e < 16; ++e) s_out[e] = dp_out[e] = 0.f;
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) s[e] = dp[e] = 0.f;
-      const int arow = 32 * qb + l32;
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (ks == C::KS - 1) {
+#pragma unroll
+        for (int i = 0; i < C::EB; ++i) rd(i, ot[i], qt[i]);
+      }
+      if (ks == 0) {  // second half of the M1 operands
+#pragma unroll
+        for (int k2 = H; k2 < C::KS; ++k2) {
+          qa[k2] = lds_read16(Ls + NQB + (kad ^ (32 * k2)));
+          oa[k2] = lds_read16(Ls + OR + NQB + (kad ^ (32 * k2)));
+        }
+      }
+      s_out = mfma32(qa[ks], kf[ks], s_out);
+      dp_out = mfma32(oa[ks], vf[ks], dp_out);
+      // Pin the two MFMAs here: being pure, they would otherwise float to their uses.
+      asm volatile("" : "+a"(s_out), "+a"(dp_out));
+#pragma unroll
+      for (int e = ks * EPC; e < (ks + 1) * EPC; ++e) {
+        const int g = e >> 2, r = e & 3;
+        if (r == 0 && g > 0) {
+          l4 = *reinterpret_cast<const f32x4*>(lse_t + 8 * g);
+          d4 = *reinterpret_cast<const f32x4*>(lse_t + kQStage + 8 * g);
+        }
+        pv[e] = __builtin_amdgcn_exp2f(s[e] - l4[r]);
+        dv[e] = pv[e] * (dp[e] - d4[r]);
+        asm volatile("" : "+v"(pv[e]), "+v"(dv[e]));  // computed here, under M1
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // Causal mask, only in blocks that cross this wave's diagonal: P and dS are zero
+    // where the key comes after the query (rel > 8 g + r).
+    if (wk0 + 31 > tpos + 32 * HF) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const bool off = rel > 8 * (e >> 2) + (e & 3);
+        pv[e] = off ? 0.f : pv[e];
+        dv[e] = off ? 0.f : dv[e];
+      }
+    }
+    u32x4 pf[2], df[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        pf[h][q] = pack_bf16x2(pv[8 * h + 2 * q], pv[8 * h + 2 * q + 1]);
+        df[h][q] = pack_bf16x2(dv[8 * h + 2 * q], dv[8 * h + 2 * q + 1]);
+      }
+    // M2: 2 EB MFMA pairs over (s2, eb); the transpose reads of the first EB pairs were
+    // issued in the last M1 step, each later pair's EB pairs ahead.
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int s2 = i / C::EB, eb = i % C::EB;
+      dvT[eb] = mfma32(ot[i % C::EB], pf[s2], dvT[eb]);
+      dkT[eb] = mfma32(qt[i % C::EB], df[s2], dkT[eb]);
+      if (i + C::EB < NI) rd(i + C::EB, ot[i % C::EB], qt[i % C::EB]);
+    }
+  };
+
+  // Tile t holds blocks 2 t (scores in sA) and 2 t + 1 (scores in sB, made while the
+  // first is finished); the next tile opens between them.  Tiles go round the ring
+  // three at a time, so that each one's slot is a constant.
+  if (n_tiles > 0) {
+    f32x16 sA, dpA, sB, dpB;
+    pend_load(IC<0>{}, 0);
+    issue(0);
+    pend_load(IC<1>{}, 1);
+    open_tile(IC<0>{}, 0);
+    int tpos;
+    {
+      const Tile T = tile_of(0);
+      tpos = P.seg_pos0[T.seg] + T.r0;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sA[e] = dpA[e] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < C::KS; ++ks) {
-        const int o = C::off(arow, 16 * ks + 8 * hh);
-        s = mfma32(lds_read16(Lq + o), kf[ks], s);
-        dp = mfma32(lds_read16(Lo + o), vf[ks], dp);
+        sA = mfma32(lds_read16(Ls + (kad ^ (32 * ks))), kf[ks], sA);
+        dpA = mfma32(lds_read16(Ls + kSlots * T64 + (kad ^ (32 * ks))), vf[ks], dpA);
       }
-      // Element 4 g + r: query row 32 qb + 8 g + 4 hh + r of the tile, key `key`.
-      u32x4 pf[2], df[2];
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int qr = 32 * qb + 8 * g + 4 * hh;
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_t + qr);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(del_t + qr);
-        float pv[4], dv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float p = __builtin_amdgcn_exp2f(s[4 * g + r] - l4[r]);
-          if (need_mask && key > tpos0 + qr + r) p = 0.f;
-          pv[r] = p;
-          dv[r] = p * (dp[4 * g + r] - d4[r]);
-        }
-        pf[g >> 1][2 * (g & 1)] = pack_bf16x2(pv[0], pv[1]);
-        pf[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(pv[2], pv[3]);
-        df[g >> 1][2 * (g & 1)] = pack_bf16x2(dv[0], dv[1]);
-        df[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
+    }
+    auto tile = [&](auto slot, int t) __attribute__((always_inline)) {
+      block(slot, IC<0>{}, tpos, sA, dpA, sB, dpB);
+      int tpos_next = tpos;
+      if (t + 1 < n_tiles) {
+        open_tile(IC<(decltype(slot)::value + 1) % kSlots>{}, t + 1);
+        const Tile T = tile_of(t + 1);
+        tpos_next = P.seg_pos0[T.seg] + T.r0;
       }
-      // dV^T += dO^T P, dK^T += Qs^T dS; k-step s2 covers query rows 32 qb + 16 s2 + ..
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        const int ra = 32 * qb + 16 * s2 + trr;
-#pragma unroll
-        for (int eb = 0; eb < C::EB; ++eb) {
-          const int ca = 32 * eb + trc;
-          const int oa = C::off(ra, ca), ob = C::off(ra + 8, ca);
-          const u32x2 olo = lds_read_tr(Lo + oa), ohi = lds_read_tr(Lo + ob);
-          dvT[eb] = mfma32(u32x4{olo[0], olo[1], ohi[0], ohi[1]}, pf[s2], dvT[eb]);
-          const u32x2 qlo = lds_read_tr(Lq + oa), qhi = lds_read_tr(Lq + ob);
-          dkT[eb] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, df[s2], dkT[eb]);
-        }
-      }
+      block(slot, IC<1>{}, tpos, sB, dpB, sA, dpA);
+      tpos = tpos_next;
+    };
+    for (int t = 0; t < n_tiles; t += kSlots) {
+      tile(IC<0>{}, t);
+      if (t + 1 < n_tiles) tile(IC<1>{}, t + 1);
+      if (t + 2 < n_tiles) tile(IC<2>{}, t + 2);
     }
   }
 
