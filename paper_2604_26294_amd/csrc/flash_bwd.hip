@@ -211,19 +211,35 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
   struct Tile {
     int head, seg, r0;
   };
-  auto tile_of = [&](int t) __attribute__((always_inline)) {
+  // Tiles in order: for each of the g query heads, the visible tiles of segment 0 then
+  // segment 1.  A cursor (u = tile within the head, gi = head) walks them without
+  // divisions; `adv` stops at the last tile.
+  struct Cursor {
+    int u, gi, t;
+  };
+  auto adv = [&](Cursor& c) __attribute__((always_inline)) {
+    if (c.t + 1 < n_tiles) {
+      ++c.t;
+      if (++c.u == per_head) {
+        c.u = 0;
+        ++c.gi;
+      }
+    }
+  };
+  auto tile_at = [&](const Cursor& c) __attribute__((always_inline)) {
     Tile T;
-    const int u = t % per_head;
-    T.head = kvl * P.group + t / per_head;
-    T.seg = u < nv[0] ? 0 : 1;
-    T.r0 = kQStage * (T.seg == 0 ? tf[0] + u : tf[1] + u - nv[0]);
+    T.head = kvl * P.group + c.gi;
+    T.seg = c.u < nv[0] ? 0 : 1;
+    T.r0 = kQStage * (T.seg == 0 ? tf[0] + c.u : tf[1] + c.u - nv[0]);
     return T;
   };
+  Cursor c_dma{0, 0, 0}, c_lse{0, 0, 0}, c_pos{0, 0, 0};
   const uint32_t q_row_bytes = 2u * (uint32_t)(P.heads * D);
   // Qs and dO rows of tile t into its slot (LDS-destination loads).
   auto issue = [&](int t) __attribute__((always_inline)) {
     const int slot = t % kSlots;
-    const Tile T = tile_of(t);
+    const Tile T = tile_at(c_dma);
+    adv(c_dma);
     const size_t e0 = (((size_t)b * P.s_loc + P.seg_row0[T.seg] + T.r0) * P.heads + T.head) * D;
     const int last = P.seg_rows[T.seg] - 1 - T.r0;
     load_tile64<D>(P.Qs + e0, q_row_bytes, last, Ls + slot * T64, wave, lane);
@@ -241,9 +257,10 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
   const float* const pbase = pwhich ? P.delta : P.lse;
   float pend[kSlots];
   int pend_last[kSlots];
-  auto pend_load = [&](auto slot_x, int t) __attribute__((always_inline)) {
+  auto pend_load = [&](auto slot_x) __attribute__((always_inline)) {
     constexpr int X = decltype(slot_x)::value;
-    const Tile T = tile_of(min(t, n_tiles - 1));
+    const Tile T = tile_at(c_lse);
+    adv(c_lse);
     const int last = P.seg_rows[T.seg] - 1 - T.r0;
     const size_t li = ((size_t)b * P.heads + T.head) * P.s_loc + P.seg_row0[T.seg] + T.r0 +
                       min(pr, last);
@@ -262,7 +279,7 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
     asm volatile("s_waitcnt vmcnt(1)" ::: "memory");  // all but tile t + 1's lse / delta
     __syncthreads();
     if (t + 1 < n_tiles) issue(t + 1);
-    pend_load(IC<(U + 2) % kSlots>{}, t + 2);
+    pend_load(IC<(U + 2) % kSlots>{});  // tile t + 2 (the last tile once past it)
   };
   // Per-lane LDS offsets (within a slot and block; the swizzle of a row depends only on
   // its index mod 16, which the slot, block and k-step offsets preserve):
@@ -386,13 +403,14 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
   // three at a time, so that each one's slot is a constant.
   if (n_tiles > 0) {
     f32x16 sA, dpA, sB, dpB;
-    pend_load(IC<0>{}, 0);
+    pend_load(IC<0>{});
     issue(0);
-    pend_load(IC<1>{}, 1);
+    pend_load(IC<1>{});
     open_tile(IC<0>{}, 0);
     int tpos;
     {
-      const Tile T = tile_of(0);
+      const Tile T = tile_at(c_pos);
+      adv(c_pos);
       tpos = P.seg_pos0[T.seg] + T.r0;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sA[e] = dpA[e] = 0.f;
@@ -407,7 +425,8 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
       int tpos_next = tpos;
       if (t + 1 < n_tiles) {
         open_tile(IC<(decltype(slot)::value + 1) % kSlots>{}, t + 1);
-        const Tile T = tile_of(t + 1);
+        const Tile T = tile_at(c_pos);
+        adv(c_pos);
         tpos_next = P.seg_pos0[T.seg] + T.r0;
       }
       block(slot, IC<1>{}, tpos, sB, dpB, sA, dpA);
