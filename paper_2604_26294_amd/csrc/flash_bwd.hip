@@ -462,9 +462,18 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
 }
 
 // ---------------------------------------------------------------------------------
-// Query-stationary kernel: dQ of 128 queries of one head.
+// Query-stationary kernel: dQ of 128 queries of one head over one range of keys.
+//
+// Built for two waves per SIMD (at most 256 registers, 64 KB of LDS, two workgroups
+// per CU): one wave's vector and LDS phases overlap the other's matrix work.  When the
+// (query tile, head, batch) work items alone cannot fill the GPU twice over, each
+// tile's keys are split into n_split ranges whose partial dQ (fp32) a second kernel
+// sums; with n_split = 1 the workgroup writes bf16 dQ itself.  The K / V tiles go round
+// a two-slot ring, unrolled by slot so that LDS addresses are registers plus
+// immediates.
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void attn_bwd_dq_kernel(const AttnBwdParams P) {
+__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_bwd_dq_kernel(const AttnBwdParams P) {
   using C = BwCfg<D>;
   constexpr int T64 = C::T64;
   // [K slot 0][K slot 1][V slot 0][V slot 1]
@@ -475,17 +484,18 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dq_kernel(const AttnBwdP
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
 
-  // Work item -> (batch, head, query tile), query tile fastest; last segment and last
-  // tile (most keys) first.
+  // Work item -> (batch, head, key range, query tile), query tile fastest; last segment
+  // and last tile (most keys) first.
   const int nt0 = (P.seg_rows[0] + kDqTile - 1) / kDqTile;
   const int nt1 = P.n_seg > 1 ? (P.seg_rows[1] + kDqTile - 1) / kDqTile : 0;
   const int n_qt = nt0 + nt1;
-  const int w = xcd_work_index(blockIdx.x, n_qt * P.heads * P.batch);
+  const int w = xcd_work_index(blockIdx.x, n_qt * P.dq_split * P.heads * P.batch);
   const int order = w % n_qt;
   const int seg = order < nt1 ? 1 : 0;
   const int qt = seg == 1 ? nt1 - 1 - order : nt0 - 1 - (order - nt1);
-  const int head = (w / n_qt) % P.heads;
-  const int b = w / n_qt / P.heads;
+  const int split = (w / n_qt) % P.dq_split;
+  const int head = (w / n_qt / P.dq_split) % P.heads;
+  const int b = w / n_qt / P.dq_split / P.heads;
   const int seg_rows = P.seg_rows[seg], row0 = P.seg_row0[seg], pos0 = P.seg_pos0[seg];
   const int kvh = P.kv_head0 + head / P.group;
   const int q0 = qt * kDqTile;
@@ -497,7 +507,10 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dq_kernel(const AttnBwdP
   const int wpos_min = pos0 + q0 + 32 * wave;
   const int wpos_max = pos0 + min(q0 + 32 * wave + 31, seg_rows - 1);
   const int n_keys = pos0 + min(q0 + kDqTile, seg_rows);  // keys this tile can see
-  const int n_steps = (n_keys + kKStage - 1) / kKStage;
+  const int k_begin = split * P.dq_split_len;              // a multiple of kKStage
+  const int k_end = min(k_begin + P.dq_split_len, n_keys);
+  const int j0 = k_begin / kKStage;
+  const int n_steps = k_end > k_begin ? (k_end - k_begin + kKStage - 1) / kKStage : 0;
 
   // Qs and dO fragments of this lane's query (B operands of S^T and dP^T); the score
   // and dP accumulators start from -lse and -delta.
@@ -516,9 +529,11 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dq_kernel(const AttnBwdP
   const uint32_t kv_row_bytes = 2u * (uint32_t)kv_stride;
   const uint16_t* kbase = P.Kb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
   const uint16_t* vbase = P.Vb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;
-  auto issue = [&](int j, int slot) __attribute__((always_inline)) {
-    const int key0 = j * kKStage;
-    const int last = n_keys - 1 - key0;  // keys past n_keys are past every query here
+  // Keys of stage j into slot j % 2; keys at or past k_end repeat the range's last key
+  // (it either ends at a multiple of the stage or at n_keys, past every query here).
+  auto issue = [&](int j) __attribute__((always_inline)) {
+    const int key0 = j * kKStage, slot = (j - j0) & 1;
+    const int last = k_end - 1 - key0;
     load_tile64<D>(kbase + (size_t)key0 * kv_stride, kv_row_bytes, last, Ls + slot * T64, wave, lane);
     load_tile64<D>(vbase + (size_t)key0 * kv_stride, kv_row_bytes, last, Ls + (2 + slot) * T64,
                    wave, lane);
@@ -530,72 +545,111 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dq_kernel(const AttnBwdP
 #pragma unroll
     for (int e = 0; e < 16; ++e) dqT[eb][e] = 0.f;
 
+  // Per-lane LDS offsets: row reads of k-step ks at ka ^ (32 ks); transpose reads of
+  // column block eb at tra[eb] (rows trr) and trb[eb] (rows trr + 8).
+  const int ka = l32 * C::RB + 16 * (hh ^ C::f(l32));
   const int trr = tr_row(lane), trc = tr_col(lane);
-  if (n_steps > 0) issue(0, 0);
-  for (int j = 0; j < n_steps; ++j) {
-    const int slot = j & 1;
+  int tra[C::EB], trb[C::EB];
+#pragma unroll
+  for (int eb = 0; eb < C::EB; ++eb) {
+    tra[eb] = C::off(trr, 32 * eb + trc);
+    trb[eb] = C::off(trr + 8, 32 * eb + trc);
+  }
+
+  // One step: the 64 keys of stage j (slot SLOT) in two blocks of 32.
+  auto step = [&](auto slot, int j) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value;
     wait_dma();
-    __syncthreads();  // tile j resident; every wave is done with tile j - 1
-    if (j + 1 < n_steps) issue(j + 1, slot ^ 1);
-    if (!wave_active) continue;
-    const lds_char* Lk = Ls + slot * T64;
-    const lds_char* Lv = Ls + (2 + slot) * T64;
+    __syncthreads();  // stage j resident; every wave is done with stage j - 1
+    if (j + 1 < j0 + n_steps) issue(j + 1);
+    if (!wave_active) return;
 #pragma unroll
     for (int kb = 0; kb < kKStage / 32; ++kb) {
       const int kbase0 = j * kKStage + 32 * kb;
-      if (kbase0 > wpos_max) break;                 // every key after every query
-      const bool need_mask = kbase0 + 31 > wpos_min;
+      if (kbase0 > wpos_max) break;  // every key after every query
+      constexpr int KO = S * T64;    // this slot's K tile; the V tile follows at 2 T64
       f32x16 s, dp;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         s[e] = neg_lse;
         dp[e] = neg_del;
       }
-      const int arow = 32 * kb + l32;
 #pragma unroll
       for (int ks = 0; ks < C::KS; ++ks) {
-        const int o = C::off(arow, 16 * ks + 8 * hh);
-        s = mfma32(lds_read16(Lk + o), qf[ks], s);
-        dp = mfma32(lds_read16(Lv + o), of[ks], dp);
+        const int o = (ka ^ (32 * ks)) + 32 * kb * C::RB;
+        s = mfma32(lds_read16(Ls + KO + o), qf[ks], s);
+        dp = mfma32(lds_read16(Ls + KO + 2 * T64 + o), of[ks], dp);
       }
       // Element 4 g + r: key kbase0 + 8 g + 4 hh + r, this lane's query.
+      float pv[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) pv[e] = __builtin_amdgcn_exp2f(s[e]);
+      if (kbase0 + 31 > wpos_min) {  // the block crosses this wave's diagonal
+        const int rel = qpos - kbase0 - 4 * hh;  // key offset 8 g + r must be <= rel
+#pragma unroll
+        for (int e = 0; e < 16; ++e) pv[e] = 8 * (e >> 2) + (e & 3) > rel ? 0.f : pv[e];
+      }
       u32x4 df[2];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float dv[4];
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float p = __builtin_amdgcn_exp2f(s[4 * g + r]);
-          if (need_mask && kbase0 + 8 * g + 4 * hh + r > qpos) p = 0.f;
-          dv[r] = p * dp[4 * g + r];
-        }
-        df[g >> 1][2 * (g & 1)] = pack_bf16x2(dv[0], dv[1]);
-        df[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
-      }
+        for (int q = 0; q < 4; ++q)
+          df[h][q] = pack_bf16x2(pv[8 * h + 2 * q] * dp[8 * h + 2 * q],
+                                 pv[8 * h + 2 * q + 1] * dp[8 * h + 2 * q + 1]);
       // dQ^T += K^T dS^T; k-step s2 covers keys 32 kb + 16 s2 + ..
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        const int ra = 32 * kb + 16 * s2 + trr;
+      for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int eb = 0; eb < C::EB; ++eb) {
-          const int ca = 32 * eb + trc;
-          const u32x2 lo = lds_read_tr(Lk + C::off(ra, ca)), hi = lds_read_tr(Lk + C::off(ra + 8, ca));
+          const int ro = (32 * kb + 16 * s2) * C::RB;
+          const u32x2 lo = lds_read_tr(Ls + KO + ro + tra[eb]);
+          const u32x2 hi = lds_read_tr(Ls + KO + ro + trb[eb]);
           dqT[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, df[s2], dqT[eb]);
         }
-      }
     }
+  };
+
+  if (n_steps > 0) issue(j0);
+  for (int j = j0; j < j0 + n_steps; j += 2) {
+    step(IC<0>{}, j);
+    if (j + 1 < j0 + n_steps) step(IC<1>{}, j + 1);
   }
 
   if (!qvalid) return;
   // Element 4 g + r of block eb: d = 32 eb + 8 g + 4 hh + r of this lane's query.
-  uint16_t* dqrow = P.dQ + qrow;
+  if (P.dq_split == 1) {
+    uint16_t* dqrow = P.dQ + qrow;
 #pragma unroll
-  for (int eb = 0; eb < C::EB; ++eb)
+    for (int eb = 0; eb < C::EB; ++eb)
 #pragma unroll
-    for (int g = 0; g < 4; ++g)
-      *reinterpret_cast<u32x2*>(dqrow + 32 * eb + 8 * g + 4 * hh) =
-          u32x2{pack_bf16x2(dqT[eb][4 * g] * P.scale, dqT[eb][4 * g + 1] * P.scale),
-                pack_bf16x2(dqT[eb][4 * g + 2] * P.scale, dqT[eb][4 * g + 3] * P.scale)};
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<u32x2*>(dqrow + 32 * eb + 8 * g + 4 * hh) =
+            u32x2{pack_bf16x2(dqT[eb][4 * g] * P.scale, dqT[eb][4 * g + 1] * P.scale),
+                  pack_bf16x2(dqT[eb][4 * g + 2] * P.scale, dqT[eb][4 * g + 3] * P.scale)};
+  } else {
+    const size_t rows = (size_t)P.batch * P.s_loc * P.heads;
+    float* prow = P.dq_part + ((size_t)split * rows +
+                               ((size_t)b * P.s_loc + row0 + qloc) * P.heads + head) * D;
+#pragma unroll
+    for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4*>(prow + 32 * eb + 8 * g + 4 * hh) =
+            f32x4{dqT[eb][4 * g], dqT[eb][4 * g + 1], dqT[eb][4 * g + 2], dqT[eb][4 * g + 3]};
+  }
+}
+
+// Sums the key-range partials of dQ: dQ = bf16(scale sum_c part_c), 4 columns a thread.
+__global__ __launch_bounds__(256) void attn_bwd_dq_combine_kernel(const AttnBwdParams P) {
+  const long long n4 = (long long)P.batch * P.s_loc * P.heads * P.head_dim / 4;
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < P.dq_split; ++c)
+    acc += *reinterpret_cast<const f32x4*>(P.dq_part + ((size_t)c * n4 + i) * 4);
+  *reinterpret_cast<u32x2*>(P.dQ + 4 * i) =
+      u32x2{pack_bf16x2(acc[0] * P.scale, acc[1] * P.scale),
+            pack_bf16x2(acc[2] * P.scale, acc[3] * P.scale)};
 }
 
 // ---------------------------------------------------------------------------------
@@ -697,11 +751,42 @@ hipError_t launch_attn_bwd_dq(const AttnBwdParams& p, hipStream_t s) {
   const hipError_t e = check_bwd(p);
   if (e != hipSuccess) return e;
   void* args[] = {const_cast<AttnBwdParams*>(&p)};
-  int n_qt = 0;
-  for (int k = 0; k < p.n_seg; ++k) n_qt += (p.seg_rows[k] + kDqTile - 1) / kDqTile;
+  int n_qt = 0, max_keys = 0;
+  for (int k = 0; k < p.n_seg; ++k) {
+    n_qt += (p.seg_rows[k] + kDqTile - 1) / kDqTile;
+    max_keys = max(max_keys, p.seg_pos0[k] + p.seg_rows[k]);
+  }
+  if (p.dq_split < 1 || p.dq_split_len % kKStage != 0 ||
+      (long long)p.dq_split * p.dq_split_len < max_keys || (p.dq_split > 1 && !p.dq_part))
+    return hipErrorInvalidValue;
   const void* fn = p.head_dim == 128 ? reinterpret_cast<const void*>(&attn_bwd_dq_kernel<128>)
                                      : reinterpret_cast<const void*>(&attn_bwd_dq_kernel<64>);
-  return hipLaunchKernel(fn, dim3(n_qt * p.heads * p.batch), dim3(kBwdThreads), args, 0, s);
+  const hipError_t e2 = hipLaunchKernel(fn, dim3(n_qt * p.dq_split * p.heads * p.batch),
+                                        dim3(kBwdThreads), args, 0, s);
+  if (e2 != hipSuccess || p.dq_split == 1) return e2;
+  const long long n4 = (long long)p.batch * p.s_loc * p.heads * p.head_dim / 4;
+  return hipLaunchKernel(reinterpret_cast<const void*>(&attn_bwd_dq_combine_kernel),
+                         dim3((unsigned)((n4 + 255) / 256)), dim3(256), args, 0, s);
+}
+
+int attn_bwd_dq_split(const AttnBwdParams& p, int* split_len) {
+  // Enough (query tile, head, batch, key range) items for two workgroups per CU, each
+  // range at least four key stages long.
+  int n_qt = 0, max_keys = 1;
+  for (int k = 0; k < p.n_seg; ++k) {
+    n_qt += (p.seg_rows[k] + kDqTile - 1) / kDqTile;
+    max_keys = max(max_keys, p.seg_pos0[k] + p.seg_rows[k]);
+  }
+  const long long items = (long long)n_qt * p.heads * p.batch;
+  int n = 1;
+  while (n < 4 && items * n < 2LL * kAttnTargetWorkgroups) ++n;
+  auto len_of = [&](int c) {
+    const int len = (max_keys + c - 1) / c;
+    return (len + kKStage - 1) / kKStage * kKStage;
+  };
+  while (n > 1 && len_of(n) < 4 * kKStage) --n;
+  if (split_len) *split_len = len_of(n);
+  return n;
 }
 
 hipError_t launch_transpose_bf16(const uint16_t* in, int ld_in, int rows, int cols,

@@ -162,7 +162,17 @@ struct AttnBwdParams {
   int seg_pos0[2];
   float scale_log2;  // softmax scale * log2(e)
   float scale;       // softmax scale
+  // dQ key-range split (attn_bwd_dq_split): with dq_split > 1 each query tile's keys
+  // [c dq_split_len, (c + 1) dq_split_len) write fp32 partials dq_part
+  // [dq_split][B S_loc H_s][d], summed into dQ by a second kernel.
+  int dq_split;
+  int dq_split_len;
+  float* dq_part;
 };
+
+// Number of key ranges for the dQ kernel (and their length, a multiple of the key
+// stage, in *split_len); depends on the shape only.
+int attn_bwd_dq_split(const AttnBwdParams& p, int* split_len);
 
 // The three kernels of the backward, in this order: delta and Qs; dK / dV; dQ.
 hipError_t launch_attn_bwd_prep(const AttnBwdParams& p, hipStream_t s);

@@ -145,16 +145,28 @@ MlpBwdWs mlp_bwd_ws(const Dims& d) {
 // Attention backward, first stage: Q (recomputed, then scaled in place), A, dA, dQ
 // [M, H_s d] bf16; lse, delta [B, H_s, S_loc] fp32; A^T and dQ^T [H_s d, M rounded up
 // to 64] bf16 (the A operands of the weight-gradient products, zero past M); then the
-// forward recomputation's key-range partials, as for the forward.
+// forward recomputation's key-range partials, as for the forward, and the dQ kernel's
+// key-range partials.
 struct AttnBwdWs {
-  size_t q, a, da, dq, lse, delta, at, dqt, po, pml, total;
-  int m_pad, n_split, split_len;
+  size_t q, a, da, dq, lse, delta, at, dqt, po, pml, dqp, total;
+  int m_pad, n_split, split_len, dq_split, dq_split_len;
 };
 AttnBwdWs attn_bwd_ws(const Dims& d) {
   AttnBwdWs w;
   AttnParams ap = {};
   attn_segments(d, &ap);
   w.n_split = tsp::attn_split_count(ap, &w.split_len);
+  {
+    AttnBwdParams bp = {};
+    bp.batch = d.B;
+    bp.heads = d.hs;
+    bp.n_seg = ap.n_seg;
+    for (int k = 0; k < 2; ++k) {
+      bp.seg_rows[k] = ap.seg_rows[k];
+      bp.seg_pos0[k] = ap.seg_pos0[k];
+    }
+    w.dq_split = tsp::attn_bwd_dq_split(bp, &w.dq_split_len);
+  }
   w.m_pad = (int)((d.M + 63) / 64 * 64);
   const size_t rows = (size_t)d.M * d.hs;
   const size_t qa = align_up(rows * d.d * 2), f = align_up(rows * 4);
@@ -170,7 +182,9 @@ AttnBwdWs attn_bwd_ws(const Dims& d) {
   w.dqt = w.at + tr;
   w.po = w.dqt + tr;
   w.pml = w.po + align_up(part * d.d * 4);
-  w.total = w.pml + align_up(part * 2 * 4);
+  w.dqp = w.pml + align_up(part * 2 * 4);
+  const size_t dq_part = w.dq_split > 1 ? (size_t)w.dq_split * rows * d.d * 4 : 0;
+  w.total = w.dqp + align_up(dq_part);
   return w;
 }
 // Attention backward, second stage: the transposed gradient of one shard's K or V rows,
@@ -556,6 +570,9 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     }
     bp.scale_log2 = ap.scale_log2;
     bp.scale = d.scale;
+    bp.dq_split = w.dq_split;
+    bp.dq_split_len = w.dq_split_len;
+    bp.dq_part = reinterpret_cast<float*>(ws + w.dqp);
     TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st, tsp::launch_attn_bwd_prep(bp, st));
     TSP_LAUNCH(TSP_KERNEL_ABWD_KV, st, tsp::launch_attn_bwd_dkdv(bp, st));
     TSP_LAUNCH(TSP_KERNEL_ABWD_Q, st, tsp::launch_attn_bwd_dq(bp, st));
