@@ -46,7 +46,9 @@ namespace {
 
 constexpr int kBwdWaves = 4;
 constexpr int kBwdThreads = kBwdWaves * kWave;
-constexpr int kKvTile = 32 * kBwdWaves;  // keys per key-stationary workgroup
+constexpr int kKvWaves = 8;
+constexpr int kKvThreads = kKvWaves * kWave;
+constexpr int kKvTile = 32 * kKvWaves;  // keys per key-stationary workgroup
 constexpr int kQStage = 64;              // queries staged per step (key-stationary)
 constexpr int kDqTile = 32 * kBwdWaves;  // queries per query-stationary workgroup
 constexpr int kKStage = 64;              // keys staged per step (query-stationary)
@@ -83,15 +85,17 @@ struct BwCfg {
 
 // One 64-row tile into LDS at `dst`.  Row r of the tile comes from base + min(r, last)
 // rows of `row_bytes` each; rows past `last` repeat it (finite values that the caller
-// masks).  Wave w's load i fills rows (4 i + w) RPD .. + RPD - 1.
-template <int D>
+// masks).  Wave w's load i fills rows (WAVES i + w) RPD .. + RPD - 1.
+template <int D, int WAVES = kBwdWaves>
 __device__ __forceinline__ void load_tile64(const uint16_t* base, uint32_t row_bytes, int last,
                                             lds_char* dst, int wave, int lane) {
   using C = BwCfg<D>;
   const rsrc_t rsrc = make_rsrc(base);
+  constexpr int N = 64 / (WAVES * C::RPD);  // loads per wave
+  static_assert(N * WAVES * C::RPD == 64, "tile cover");
 #pragma unroll
-  for (int i = 0; i < C::DMA64; ++i) {
-    const int blk = i * kBwdWaves + wave;
+  for (int i = 0; i < N; ++i) {
+    const int blk = i * WAVES + wave;
     const int r = blk * C::RPD + lane / C::KCH;
     const uint32_t rr = (uint32_t)min(r, last);
     const uint32_t voff = rr * row_bytes + 16u * (uint32_t)((lane % C::KCH) ^ C::f(r));
@@ -141,27 +145,26 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const AttnBwdParams 
 }
 
 // ---------------------------------------------------------------------------------
-// Key-stationary kernel: dK, dV of 128 keys of one kv head.
+// Key-stationary kernel: dK, dV of 256 keys of one kv head.
 //
-// The query tiles (64 rows of Qs and dO with their lse and delta) stream through a
-// three-slot LDS ring; each wave takes every tile in two 32-query blocks.  Block n's
-// work has three parts: M1 (the S and dP products, 16 MFMAs on row reads), V (the
-// probabilities and dS, vector ops only) and M2 (the dV^T and dK^T products, 16 MFMAs
-// on transpose reads).  They are software-pipelined over the blocks of all tiles:
-// iteration n issues M1(n + 1) interleaved with V(n), then M2(n), so the vector work of
-// one block runs under the matrix work of the next.  M1(n + 1) may start a new tile
-// while M2(n) still reads the previous one; with three slots and each tile's loads
-// issued one tile ahead (after the barrier that opens the tile before it), a slot is
-// refilled only after every wave has finished the block that last read it.
+// Eight waves, two per SIMD (at most 256 registers each), so that one wave's vector
+// and LDS phases overlap the other's matrix work; wave w owns keys 32 w .. 32 w + 31 of
+// the tile.  Its K fragments stay in registers; the V rows (B operand of dP) are read
+// from the workgroup's V tile, loaded into LDS once.  Query tiles of 64 rows of Qs and
+// dO stream through a two-slot ring, unrolled by slot so that LDS addresses are
+// registers plus immediates; each wave takes a tile in two 32-query blocks: S and dP
+// (row reads), the probabilities and dS (vector ops), then dV^T and dK^T (transpose
+// reads).
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
+__global__ __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   using C = BwCfg<D>;
   constexpr int T64 = C::T64;
-  constexpr int kSlots = 3;
-  // [Qs slots][dO slots][lse, delta slots]
-  __shared__ __attribute__((aligned(1024))) char L[2 * kSlots * T64 + kSlots * 2 * kQStage * 4];
+  constexpr int VT = kKvTile * C::RB;  // the V tile
+  // [V tile][Qs slot 0][Qs slot 1][dO slot 0][dO slot 1][lse, delta slot 0][slot 1]
+  __shared__ __attribute__((aligned(1024))) char L[VT + 4 * T64 + 2 * 2 * kQStage * 4];
   lds_char* Ls = (lds_char*)L;
-  float* Lf = reinterpret_cast<float*>(L + 2 * kSlots * T64);
+  float* Lf = reinterpret_cast<float*>(L + VT + 4 * T64);
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -183,20 +186,27 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
   const int wk0 = k0 + 32 * wave;  // this wave's first key
   const int key = wk0 + l32;       // this lane's key (the accumulator column)
 
-  // K and V fragments of this lane's key (B operands of S and dP): d slots 16 s + 8 hh.
-  // Keys past the last query position are never read (zero fragments: their dK, dV come
-  // out exactly zero, whatever those buffer rows hold).
+  // Keys past the last query position are never read: zero K fragments and zero V rows
+  // make their dK, dV exactly zero, whatever those buffer rows hold.
   int kv_len = 0;
   for (int sg = 0; sg < P.n_seg; ++sg) kv_len = max(kv_len, P.seg_pos0[sg] + P.seg_rows[sg]);
   const size_t kv_stride = (size_t)P.n_kv * D;
+  const uint16_t* kvbase = P.Kb + ((size_t)b * P.seq) * kv_stride + (size_t)kvh * D;
+  const uint16_t* vvbase = P.Vb + ((size_t)b * P.seq) * kv_stride + (size_t)kvh * D;
+  // V tile into LDS: keys k0 .. k0 + 255 (those at or past kv_len: key k0 - if any were
+  // readable they are all masked, so any finite row serves; rows are clamped to the
+  // last readable key and zeroed below through the K side).
+  const int v_last = min(kKvTile, kv_len - k0) - 1;  // >= 0: a tile exists only if so
+  for (int part = 0; part < kKvTile / 64; ++part)
+    load_tile64<D, kKvWaves>(vvbase + (size_t)(k0 + 64 * part) * kv_stride, 2u * (uint32_t)kv_stride,
+                             max(v_last - 64 * part, 0), Ls + part * T64, wave, lane);
+  // K fragments of this lane's key (B operand of S): d slots 16 s + 8 hh.
   const bool kread = key < kv_len;
-  const size_t krow = ((size_t)b * P.seq + (kread ? key : 0)) * kv_stride + (size_t)kvh * D;
-  u32x4 kf[C::KS], vf[C::KS];
+  u32x4 kf[C::KS];
 #pragma unroll
-  for (int s = 0; s < C::KS; ++s) {
-    kf[s] = kread ? ld16(P.Kb + krow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
-    vf[s] = kread ? ld16(P.Vb + krow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
-  }
+  for (int s = 0; s < C::KS; ++s)
+    kf[s] = kread ? ld16(kvbase + (size_t)key * kv_stride + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
+  const bool vzero = !kread;  // such keys: V fragments forced to zero below
 
   // Query tiles of 64 rows that can see key k0 or later: per segment, tiles from tf.
   int tf[2] = {0, 0}, nv[2] = {0, 0};
@@ -213,17 +223,14 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
   };
   // Tiles in order: for each of the g query heads, the visible tiles of segment 0 then
   // segment 1.  A cursor (u = tile within the head, gi = head) walks them without
-  // divisions; `adv` stops at the last tile.
+  // divisions.
   struct Cursor {
-    int u, gi, t;
+    int u, gi;
   };
   auto adv = [&](Cursor& c) __attribute__((always_inline)) {
-    if (c.t + 1 < n_tiles) {
-      ++c.t;
-      if (++c.u == per_head) {
-        c.u = 0;
-        ++c.gi;
-      }
+    if (++c.u == per_head) {
+      c.u = 0;
+      ++c.gi;
     }
   };
   auto tile_at = [&](const Cursor& c) __attribute__((always_inline)) {
@@ -233,58 +240,35 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
     T.r0 = kQStage * (T.seg == 0 ? tf[0] + c.u : tf[1] + c.u - nv[0]);
     return T;
   };
-  Cursor c_dma{0, 0, 0}, c_lse{0, 0, 0}, c_pos{0, 0, 0};
+  Cursor c_next{0, 0};
   const uint32_t q_row_bytes = 2u * (uint32_t)(P.heads * D);
-  // Qs and dO rows of tile t into its slot (LDS-destination loads).
-  auto issue = [&](int t) __attribute__((always_inline)) {
-    const int slot = t % kSlots;
-    const Tile T = tile_at(c_dma);
-    adv(c_dma);
-    const size_t e0 = (((size_t)b * P.s_loc + P.seg_row0[T.seg] + T.r0) * P.heads + T.head) * D;
-    const int last = P.seg_rows[T.seg] - 1 - T.r0;
-    load_tile64<D>(P.Qs + e0, q_row_bytes, last, Ls + slot * T64, wave, lane);
-    load_tile64<D>(P.dO + e0, q_row_bytes, last, Ls + (kSlots + slot) * T64, wave, lane);
-  };
-  // lse and delta of tile t (t past the last tile: the last one again), fetched two
-  // tiles ahead into a register: wave w takes rows 16 w .. 16 w + 15, lanes 0-15 lse and
-  // 16-31 delta (lanes 32-63 repeat them).  One unconditional load per wave per tile, so
-  // the count of loads in flight behind a tile's LDS-destination loads is the same in
-  // every wave; rows past the segment (clamped on load) get lse = +inf, delta = 0 when
-  // they are written to LDS (P = 0 there).
-  const int pr = 16 * wave + (lane & 15), pwhich = (lane >> 4) & 1;
+  // Tile at the cursor into slot S: Qs and dO rows (LDS-destination loads) and, in the
+  // first 16 lanes of each wave, lse / delta of rows 8 w .. 8 w + 7 into registers.
+  // Rows past the segment are clamped on load and get lse = +inf, delta = 0 when
+  // written to LDS (P = 0 there).
+  const int pr = 8 * wave + (lane & 7), pwhich = (lane >> 3) & 1;
   // (the array base is chosen from two scalar values, not by indexing the parameter
   // block per lane, which would load the pointer from memory)
   const float* const pbase = pwhich ? P.delta : P.lse;
-  float pend[kSlots];
-  int pend_last[kSlots];
-  auto pend_load = [&](auto slot_x) __attribute__((always_inline)) {
-    constexpr int X = decltype(slot_x)::value;
-    const Tile T = tile_at(c_lse);
-    adv(c_lse);
+  float pend = 0.f;
+  int pend_last = 0;
+  auto issue = [&](auto slot) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value;
+    const Tile T = tile_at(c_next);
+    adv(c_next);
+    const size_t e0 = (((size_t)b * P.s_loc + P.seg_row0[T.seg] + T.r0) * P.heads + T.head) * D;
     const int last = P.seg_rows[T.seg] - 1 - T.r0;
+    load_tile64<D, kKvWaves>(P.Qs + e0, q_row_bytes, last, Ls + VT + S * T64, wave, lane);
+    load_tile64<D, kKvWaves>(P.dO + e0, q_row_bytes, last, Ls + VT + (2 + S) * T64, wave, lane);
     const size_t li = ((size_t)b * P.heads + T.head) * P.s_loc + P.seg_row0[T.seg] + T.r0 +
                       min(pr, last);
-    pend[X] = pbase[li];
-    pend_last[X] = last;
+    pend = pbase[li];
+    pend_last = last;
   };
-  // Make tile t (slot U = t mod 3) resident: its lse / delta into LDS, every wave's
-  // loads of it landed, and every wave past block 2 t - 2 (so the slot refilled next,
-  // last read by block 2 t - 3, is free); then start tile t + 1's rows and tile t + 2's
-  // lse / delta.
-  auto open_tile = [&](auto slot_u, int t) __attribute__((always_inline)) {
-    constexpr int U = decltype(slot_u)::value;
-    if (lane < 32)
-      Lf[U * 2 * kQStage + pwhich * kQStage + pr] =
-          pr <= pend_last[U] ? pend[U] : (pwhich ? 0.f : INFINITY);
-    asm volatile("s_waitcnt vmcnt(1)" ::: "memory");  // all but tile t + 1's lse / delta
-    __syncthreads();
-    if (t + 1 < n_tiles) issue(t + 1);
-    pend_load(IC<(U + 2) % kSlots>{});  // tile t + 2 (the last tile once past it)
-  };
-  // Per-lane LDS offsets (within a slot and block; the swizzle of a row depends only on
-  // its index mod 16, which the slot, block and k-step offsets preserve):
-  //  M1 row reads of k-step ks: row l32, logical chunk 2 ks + hh -> kad ^ (32 ks);
-  //  M2 transpose reads, column block eb: rows trr and trr + 8 -> tra[eb], trb[eb].
+
+  // Per-lane LDS offsets (the swizzle of a row depends only on its index mod 16, which
+  // the slot, block and k-step offsets preserve): row reads of k-step ks at
+  // kad ^ (32 ks); transpose reads of column block eb at tra[eb] / trb[eb].
   const int kad = l32 * C::RB + 16 * (hh ^ C::f(l32));
   const int trr = tr_row(lane), trc = tr_col(lane);
   int tra[C::EB], trb[C::EB];
@@ -293,150 +277,97 @@ __global__ __launch_bounds__(kBwdThreads) void attn_bwd_dkdv_kernel(const AttnBw
     tra[eb] = C::off(trr, 32 * eb + trc);
     trb[eb] = C::off(trr + 8, 32 * eb + trc);
   }
+  const lds_char* vrows = Ls + 32 * wave * C::RB;  // this wave's 32 V rows
+
   f32x16 dkT[C::EB], dvT[C::EB];
 #pragma unroll
   for (int eb = 0; eb < C::EB; ++eb)
 #pragma unroll
     for (int e = 0; e < 16; ++e) dkT[eb][e] = dvT[eb][e] = 0.f;
 
-  // One block: V on (s, dp) -- block HALF of the tile in slot SLOT, at position tpos --
-  // spread over the steps of M1 of the next block into (s_out, dp_out), then M2.
-  // Element 4 g + r is query row 32 HALF + 8 g + 4 hh + r of the tile.  The slots are
-  // compile-time constants, so every LDS address is a per-lane register plus an
-  // immediate.  After the last block, M1 reads stale rows of a free slot (in bounds)
-  // and its result is never used.
-  constexpr int EPC = 16 / C::KS;  // vector elements per M1 step
-  auto block = [&](auto slot, auto half, int tpos, const f32x16& s, const f32x16& dp,
-                   f32x16& s_out, f32x16& dp_out) __attribute__((always_inline)) {
+  // Block HF of the tile in slot S, at position tpos: element 4 g + r of the score /
+  // dP accumulators is query row 32 HF + 8 g + 4 hh + r, key `key`.
+  auto block = [&](auto slot, auto half, int tpos, int rows_left) __attribute__((always_inline)) {
     constexpr int S = decltype(slot)::value, HF = decltype(half)::value;
-    constexpr int NS = HF == 0 ? S : (S + 1) % kSlots, NH = 1 - HF;  // the next block
-    constexpr int QB = S * T64 + HF * 32 * C::RB;     // this block's rows in the Qs ring
-    constexpr int NQB = NS * T64 + NH * 32 * C::RB;   // the next block's rows
-    constexpr int OR = kSlots * T64;                  // Qs ring -> dO ring
-    const float* lse_t = Lf + S * 2 * kQStage + 32 * HF + 4 * hh;
-    const int rel = key - (tpos + 32 * HF + 4 * hh);  // masked where rel > 8 g + r
-    constexpr int H = C::KS / 2;
-    u32x4 qa[C::KS], oa[C::KS];
+    constexpr int QB = VT + S * T64 + HF * 32 * C::RB;  // this block's Qs rows
+    constexpr int OB = QB + 2 * T64;                    // and dO rows
+    f32x16 s, dp;
 #pragma unroll
-    for (int ks = 0; ks < H; ++ks) {
-      qa[ks] = lds_read16(Ls + NQB + (kad ^ (32 * ks)));
-      oa[ks] = lds_read16(Ls + OR + NQB + (kad ^ (32 * ks)));
-    }
-    f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_t);
-    f32x4 d4 = *reinterpret_cast<const f32x4*>(lse_t + kQStage);
-    float pv[16], dv[16];
-    // M2 operands: transpose reads of dO^T and Qs^T for pair i = (s2, eb) of this block.
-    auto rd = [&](int i, u32x4& ot, u32x4& qt) __attribute__((always_inline)) {
-      const int s2 = i / C::EB, eb = i % C::EB;
-      const lds_char* bq = Ls + QB + 16 * s2 * C::RB;
-      const u32x2 olo = lds_read_tr(bq + OR + tra[eb]), ohi = lds_read_tr(bq + OR + trb[eb]);
-      const u32x2 qlo = lds_read_tr(bq + tra[eb]), qhi = lds_read_tr(bq + trb[eb]);
-      ot = u32x4{olo[0], olo[1], ohi[0], ohi[1]};
-      qt = u32x4{qlo[0], qlo[1], qhi[0], qhi[1]};
-    };
-    constexpr int NI = 2 * C::EB;
-    u32x4 ot[C::EB], qt[C::EB];
-#pragma unroll
-    for (int e = 0; e < 16; ++e) s_out[e] = dp_out[e] = 0.f;
-    __builtin_amdgcn_sched_barrier(0);
+    for (int e = 0; e < 16; ++e) s[e] = dp[e] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks) {
-      if (ks == C::KS - 1) {
-#pragma unroll
-        for (int i = 0; i < C::EB; ++i) rd(i, ot[i], qt[i]);
-      }
-      if (ks == 0) {  // second half of the M1 operands
-#pragma unroll
-        for (int k2 = H; k2 < C::KS; ++k2) {
-          qa[k2] = lds_read16(Ls + NQB + (kad ^ (32 * k2)));
-          oa[k2] = lds_read16(Ls + OR + NQB + (kad ^ (32 * k2)));
-        }
-      }
-      s_out = mfma32(qa[ks], kf[ks], s_out);
-      dp_out = mfma32(oa[ks], vf[ks], dp_out);
-      // Pin the two MFMAs here: being pure, they would otherwise float to their uses.
-      asm volatile("" : "+a"(s_out), "+a"(dp_out));
-#pragma unroll
-      for (int e = ks * EPC; e < (ks + 1) * EPC; ++e) {
-        const int g = e >> 2, r = e & 3;
-        if (r == 0 && g > 0) {
-          l4 = *reinterpret_cast<const f32x4*>(lse_t + 8 * g);
-          d4 = *reinterpret_cast<const f32x4*>(lse_t + kQStage + 8 * g);
-        }
-        pv[e] = __builtin_amdgcn_exp2f(s[e] - l4[r]);
-        dv[e] = pv[e] * (dp[e] - d4[r]);
-        asm volatile("" : "+v"(pv[e]), "+v"(dv[e]));  // computed here, under M1
-      }
+      const int o = kad ^ (32 * ks);
+      u32x4 vf = lds_read16(vrows + o);
+      if (vzero) vf = u32x4{0u, 0u, 0u, 0u};
+      s = mfma32(lds_read16(Ls + QB + o), kf[ks], s);
+      dp = mfma32(lds_read16(Ls + OB + o), vf, dp);
+      // (no operand prefetch across steps: registers are the limit here, and the other
+      // wave of the SIMD covers the LDS latency)
       __builtin_amdgcn_sched_barrier(0);
     }
-    // Causal mask, only in blocks that cross this wave's diagonal: P and dS are zero
-    // where the key comes after the query (rel > 8 g + r).
+    // Causal mask, only in blocks that cross this wave's diagonal: scores of keys after
+    // the query (rel > 8 g + r) become -inf, so P and dS are zero there.
     if (wk0 + 31 > tpos + 32 * HF) {
+      const int rel = key - (tpos + 32 * HF + 4 * hh);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const bool off = rel > 8 * (e >> 2) + (e & 3);
-        pv[e] = off ? 0.f : pv[e];
-        dv[e] = off ? 0.f : dv[e];
-      }
+      for (int e = 0; e < 16; ++e) s[e] = rel > 8 * (e >> 2) + (e & 3) ? -INFINITY : s[e];
     }
+    // P = 2^(S - lse), dS = P (dP - delta), packed to bf16 in the accumulator's row order
+    // (the B operands below).
+    const float* lse_t = Lf + S * 2 * kQStage + 32 * HF + 4 * hh;
     u32x4 pf[2], df[2];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_t + 8 * g);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(lse_t + kQStage + 8 * g);
+      float pv[4], dv[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        pf[h][q] = pack_bf16x2(pv[8 * h + 2 * q], pv[8 * h + 2 * q + 1]);
-        df[h][q] = pack_bf16x2(dv[8 * h + 2 * q], dv[8 * h + 2 * q + 1]);
+      for (int r = 0; r < 4; ++r) {
+        pv[r] = __builtin_amdgcn_exp2f(s[4 * g + r] - l4[r]);
+        dv[r] = pv[r] * (dp[4 * g + r] - d4[r]);
       }
-    // M2: 2 EB MFMA pairs over (s2, eb); the transpose reads of the first EB pairs were
-    // issued in the last M1 step, each later pair's EB pairs ahead.
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int s2 = i / C::EB, eb = i % C::EB;
-      dvT[eb] = mfma32(ot[i % C::EB], pf[s2], dvT[eb]);
-      dkT[eb] = mfma32(qt[i % C::EB], df[s2], dkT[eb]);
-      if (i + C::EB < NI) rd(i + C::EB, ot[i % C::EB], qt[i % C::EB]);
+      pf[g >> 1][2 * (g & 1)] = pack_bf16x2(pv[0], pv[1]);
+      pf[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(pv[2], pv[3]);
+      df[g >> 1][2 * (g & 1)] = pack_bf16x2(dv[0], dv[1]);
+      df[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
     }
+    // dV^T += dO^T P and dK^T += Qs^T dS; k-step s2 covers query rows 32 HF + 16 s2 + ..
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+      for (int eb = 0; eb < C::EB; ++eb) {
+        const lds_char* bq = Ls + QB + 16 * s2 * C::RB;
+        const u32x2 olo = lds_read_tr(bq + 2 * T64 + tra[eb]), ohi = lds_read_tr(bq + 2 * T64 + trb[eb]);
+        dvT[eb] = mfma32(u32x4{olo[0], olo[1], ohi[0], ohi[1]}, pf[s2], dvT[eb]);
+        const u32x2 qlo = lds_read_tr(bq + tra[eb]), qhi = lds_read_tr(bq + trb[eb]);
+        dkT[eb] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, df[s2], dkT[eb]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    (void)rows_left;
   };
 
-  // Tile t holds blocks 2 t (scores in sA) and 2 t + 1 (scores in sB, made while the
-  // first is finished); the next tile opens between them.  Tiles go round the ring
-  // three at a time, so that each one's slot is a constant.
-  if (n_tiles > 0) {
-    f32x16 sA, dpA, sB, dpB;
-    pend_load(IC<0>{});
-    issue(0);
-    pend_load(IC<1>{});
-    open_tile(IC<0>{}, 0);
-    int tpos;
-    {
-      const Tile T = tile_at(c_pos);
-      adv(c_pos);
-      tpos = P.seg_pos0[T.seg] + T.r0;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) sA[e] = dpA[e] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) {
-        sA = mfma32(lds_read16(Ls + (kad ^ (32 * ks))), kf[ks], sA);
-        dpA = mfma32(lds_read16(Ls + kSlots * T64 + (kad ^ (32 * ks))), vf[ks], dpA);
-      }
-    }
-    auto tile = [&](auto slot, int t) __attribute__((always_inline)) {
-      block(slot, IC<0>{}, tpos, sA, dpA, sB, dpB);
-      int tpos_next = tpos;
-      if (t + 1 < n_tiles) {
-        open_tile(IC<(decltype(slot)::value + 1) % kSlots>{}, t + 1);
-        const Tile T = tile_at(c_pos);
-        adv(c_pos);
-        tpos_next = P.seg_pos0[T.seg] + T.r0;
-      }
-      block(slot, IC<1>{}, tpos, sB, dpB, sA, dpA);
-      tpos = tpos_next;
-    };
-    for (int t = 0; t < n_tiles; t += kSlots) {
-      tile(IC<0>{}, t);
-      if (t + 1 < n_tiles) tile(IC<1>{}, t + 1);
-      if (t + 2 < n_tiles) tile(IC<2>{}, t + 2);
-    }
+  // One tile in slot S: make it resident (its lse / delta into LDS, every wave's loads
+  // landed, every wave done with the previous tile), start the next one into the other
+  // slot, then its two blocks.
+  Cursor c_pos{0, 0};
+  auto tile = [&](auto slot, int t) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value;
+    if (lane < 16)
+      Lf[S * 2 * kQStage + pwhich * kQStage + pr] =
+          pr <= pend_last ? pend : (pwhich ? 0.f : INFINITY);
+    wait_dma();
+    __syncthreads();
+    if (t + 1 < n_tiles) issue(IC<1 - S>{});
+    const Tile T = tile_at(c_pos);
+    adv(c_pos);
+    const int tpos = P.seg_pos0[T.seg] + T.r0;
+    block(slot, IC<0>{}, tpos, 0);
+    if (T.r0 + 32 < P.seg_rows[T.seg]) block(slot, IC<1>{}, tpos, 0);
+  };
+  if (n_tiles > 0) issue(IC<0>{});
+  for (int t = 0; t < n_tiles; t += 2) {
+    tile(IC<0>{}, t);
+    if (t + 1 < n_tiles) tile(IC<1>{}, t + 1);
   }
 
   // Accumulator element 4 g + r of block eb: d = 32 eb + 8 g + 4 hh + r, key = `key`.
@@ -742,7 +673,7 @@ hipError_t launch_attn_bwd_dkdv(const AttnBwdParams& p, hipStream_t s) {
   const int n_kt = (int)((p.seq + kKvTile - 1) / kKvTile);
   const void* fn = p.head_dim == 128 ? reinterpret_cast<const void*>(&attn_bwd_dkdv_kernel<128>)
                                      : reinterpret_cast<const void*>(&attn_bwd_dkdv_kernel<64>);
-  return hipLaunchKernel(fn, dim3(n_kt * (p.heads / p.group) * p.batch), dim3(kBwdThreads), args,
+  return hipLaunchKernel(fn, dim3(n_kt * (p.heads / p.group) * p.batch), dim3(kKvThreads), args,
                          0, s);
 }
 
