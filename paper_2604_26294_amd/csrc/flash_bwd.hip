@@ -207,6 +207,11 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   for (int s = 0; s < C::KS; ++s)
     kf[s] = kread ? ld16(kvbase + (size_t)key * kv_stride + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
   const bool vzero = !kread;  // such keys: V fragments forced to zero below
+  // Consume the K fragments here, before the loop: the compiler then waits for their
+  // loads once, instead of at a point inside the loop where the same wait would also
+  // cover the newest tile loads.
+#pragma unroll
+  for (int s = 0; s < C::KS; ++s) asm volatile("" ::"v"(kf[s]));
 
   // Query tiles of 64 rows that can see key k0 or later: per segment, tiles from tf.
   int tf[2] = {0, 0}, nv[2] = {0, 0};
@@ -250,8 +255,23 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   // (the array base is chosen from two scalar values, not by indexing the parameter
   // block per lane, which would load the pointer from memory)
   const float* const pbase = pwhich ? P.delta : P.lse;
-  float pend = 0.f;
-  int pend_last = 0;
+  // lse / delta run two tiles ahead of the rows (pend[S] holds those of the next tile
+  // to use slot S), with one unconditional load per wave per tile so that the number of
+  // loads behind a tile's rows is the same in every wave.
+  float pend[2] = {0.f, 0.f};
+  int pend_last[2] = {0, 0};
+  Cursor c_lse{0, 0};
+  int lse_left = n_tiles;
+  auto pend_load = [&](auto slot) __attribute__((always_inline)) {
+    constexpr int S = decltype(slot)::value;
+    const Tile T = tile_at(c_lse);
+    if (--lse_left > 0) adv(c_lse);  // past the last tile: reload the last one
+    const int last = P.seg_rows[T.seg] - 1 - T.r0;
+    const size_t li = ((size_t)b * P.heads + T.head) * P.s_loc + P.seg_row0[T.seg] + T.r0 +
+                      min(pr, last);
+    pend[S] = pbase[li];
+    pend_last[S] = last;
+  };
   auto issue = [&](auto slot) __attribute__((always_inline)) {
     constexpr int S = decltype(slot)::value;
     const Tile T = tile_at(c_next);
@@ -260,10 +280,6 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     const int last = P.seg_rows[T.seg] - 1 - T.r0;
     load_tile64<D, kKvWaves>(P.Qs + e0, q_row_bytes, last, Ls + VT + S * T64, wave, lane);
     load_tile64<D, kKvWaves>(P.dO + e0, q_row_bytes, last, Ls + VT + (2 + S) * T64, wave, lane);
-    const size_t li = ((size_t)b * P.heads + T.head) * P.s_loc + P.seg_row0[T.seg] + T.r0 +
-                      min(pr, last);
-    pend = pbase[li];
-    pend_last = last;
   };
 
   // Per-lane LDS offsets (the swizzle of a row depends only on its index mod 16, which
@@ -354,17 +370,22 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     constexpr int S = decltype(slot)::value;
     if (lane < 16)
       Lf[S * 2 * kQStage + pwhich * kQStage + pr] =
-          pr <= pend_last ? pend : (pwhich ? 0.f : INFINITY);
-    wait_dma();
+          pr <= pend_last[S] ? pend[S] : (pwhich ? 0.f : INFINITY);
+    asm volatile("s_waitcnt vmcnt(1)" ::: "memory");  // all but tile t + 1's lse / delta
     __syncthreads();
     if (t + 1 < n_tiles) issue(IC<1 - S>{});
+    pend_load(IC<S>{});  // tile t + 2
     const Tile T = tile_at(c_pos);
     adv(c_pos);
     const int tpos = P.seg_pos0[T.seg] + T.r0;
     block(slot, IC<0>{}, tpos, 0);
     if (T.r0 + 32 < P.seg_rows[T.seg]) block(slot, IC<1>{}, tpos, 0);
   };
-  if (n_tiles > 0) issue(IC<0>{});
+  if (n_tiles > 0) {
+    pend_load(IC<0>{});
+    issue(IC<0>{});
+    pend_load(IC<1>{});
+  }
   for (int t = 0; t < n_tiles; t += 2) {
     tile(IC<0>{}, t);
     if (t + 1 < n_tiles) tile(IC<1>{}, t + 1);
@@ -455,6 +476,11 @@ void attn_bwd_dq_kernel(const AttnBwdParams P) {
   const size_t li = ((size_t)b * P.heads + head) * P.s_loc + row0 + (qvalid ? qloc : 0);
   const float neg_lse = qvalid ? -P.lse[li] : -INFINITY;  // invalid query: P = 0
   const float neg_del = qvalid ? -P.delta[li] : 0.f;
+  // Consume these loads before the loop: the compiler then waits for them once, not at
+  // a point inside the loop where the same wait would also cover the newest key tiles.
+#pragma unroll
+  for (int s = 0; s < C::KS; ++s) asm volatile("" ::"v"(qf[s]), "v"(of[s]));
+  asm volatile("" ::"v"(neg_lse), "v"(neg_del));
 
   const size_t kv_stride = (size_t)P.n_kv * D;
   const uint32_t kv_row_bytes = 2u * (uint32_t)kv_stride;
