@@ -128,3 +128,22 @@ def test_two_stages_accumulate_into_one_dx():
     both = prob.attn_kv_bwd(dkl, dvl, accumulate=True)[0]
     torch.cuda.synchronize()
     assert torch.allclose(both, first + second_only, rtol=1e-5, atol=1e-6)
+
+
+def test_first_stage_accumulates():
+    """A second first-stage call with accumulate != 0 adds the same dX, weight-gradient
+    blocks and K/V-gradient contributions again (up to the fp32 summation order)."""
+    wl, p = MID_GQA64, 2
+    x_bits, w_bits, dy_bits = _inputs(wl)
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    prob.prefill_kv(include_self=True)
+    dy = to_device_bf16(local_rows(dy_bits, wl, p))
+    dx, dw, dk, dv = prob.attn_bwd(dy)
+    once = [dx.clone(), [t.clone() for t in dw], dk.clone(), dv.clone()]
+    prob.attn_bwd(dy, accumulate=True)
+    torch.cuda.synchronize()
+    assert torch.allclose(dx, 2 * once[0], rtol=1e-5, atol=1e-6)
+    for a, b in zip(dw, once[1]):
+        assert torch.allclose(a, 2 * b, rtol=1e-5, atol=1e-6)
+    assert torch.allclose(dk, 2 * once[2], rtol=1e-5, atol=1e-6)
+    assert torch.allclose(dv, 2 * once[3], rtol=1e-5, atol=1e-6)
