@@ -161,10 +161,12 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   using C = BwCfg<D>;
   constexpr int T64 = C::T64;
   constexpr int VT = kKvTile * C::RB;  // the V tile
-  // [V tile][Qs slot 0][Qs slot 1][dO slot 0][dO slot 1][lse, delta slot 0][slot 1]
-  __shared__ __attribute__((aligned(1024))) char L[VT + 4 * T64 + 2 * 2 * kQStage * 4];
+  constexpr int VO = 4 * T64 + 2 * 2 * kQStage * 4;  // its offset
+  // [Qs slot 0][Qs slot 1][dO slot 0][dO slot 1][lse, delta slot 0][slot 1][V tile]: the
+  // ring first, so that its offsets fit the 16-bit immediate of the LDS reads.
+  __shared__ __attribute__((aligned(1024))) char L[VO + VT];
   lds_char* Ls = (lds_char*)L;
-  float* Lf = reinterpret_cast<float*>(L + VT + 4 * T64);
+  float* Lf = reinterpret_cast<float*>(L + 4 * T64);
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -186,27 +188,28 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   const int wk0 = k0 + 32 * wave;  // this wave's first key
   const int key = wk0 + l32;       // this lane's key (the accumulator column)
 
-  // Keys past the last query position are never read: zero K fragments and zero V rows
-  // make their dK, dV exactly zero, whatever those buffer rows hold.
+  // Keys at or past kv_len (the last query position + 1) are never read: their K
+  // fragments are zero and their V rows repeat the last readable key; every query masks
+  // them, so their dK, dV come out exactly zero.
   int kv_len = 0;
   for (int sg = 0; sg < P.n_seg; ++sg) kv_len = max(kv_len, P.seg_pos0[sg] + P.seg_rows[sg]);
   const size_t kv_stride = (size_t)P.n_kv * D;
   const uint16_t* kvbase = P.Kb + ((size_t)b * P.seq) * kv_stride + (size_t)kvh * D;
   const uint16_t* vvbase = P.Vb + ((size_t)b * P.seq) * kv_stride + (size_t)kvh * D;
-  // V tile into LDS: keys k0 .. k0 + 255 (those at or past kv_len: key k0 - if any were
-  // readable they are all masked, so any finite row serves; rows are clamped to the
-  // last readable key and zeroed below through the K side).
-  const int v_last = min(kKvTile, kv_len - k0) - 1;  // >= 0: a tile exists only if so
-  for (int part = 0; part < kKvTile / 64; ++part)
-    load_tile64<D, kKvWaves>(vvbase + (size_t)(k0 + 64 * part) * kv_stride, 2u * (uint32_t)kv_stride,
-                             max(v_last - 64 * part, 0), Ls + part * T64, wave, lane);
+  // V tile into LDS: keys k0 .. k0 + 255, rows past the last readable key repeating it
+  // (a tile with no readable key has no query tile to visit either and loads nothing).
+  const int v_last = min(kKvTile, kv_len - k0) - 1;
+  if (v_last >= 0)
+    for (int part = 0; part < kKvTile / 64; ++part)
+      load_tile64<D, kKvWaves>(vvbase + (size_t)(k0 + 64 * part) * kv_stride,
+                               2u * (uint32_t)kv_stride, max(v_last - 64 * part, 0),
+                               Ls + VO + part * T64, wave, lane);
   // K fragments of this lane's key (B operand of S): d slots 16 s + 8 hh.
   const bool kread = key < kv_len;
   u32x4 kf[C::KS];
 #pragma unroll
   for (int s = 0; s < C::KS; ++s)
     kf[s] = kread ? ld16(kvbase + (size_t)key * kv_stride + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
-  const bool vzero = !kread;  // such keys: V fragments forced to zero below
   // Consume the K fragments here, before the loop: the compiler then waits for their
   // loads once, instead of at a point inside the loop where the same wait would also
   // cover the newest tile loads.
@@ -278,8 +281,8 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     adv(c_next);
     const size_t e0 = (((size_t)b * P.s_loc + P.seg_row0[T.seg] + T.r0) * P.heads + T.head) * D;
     const int last = P.seg_rows[T.seg] - 1 - T.r0;
-    load_tile64<D, kKvWaves>(P.Qs + e0, q_row_bytes, last, Ls + VT + S * T64, wave, lane);
-    load_tile64<D, kKvWaves>(P.dO + e0, q_row_bytes, last, Ls + VT + (2 + S) * T64, wave, lane);
+    load_tile64<D, kKvWaves>(P.Qs + e0, q_row_bytes, last, Ls + S * T64, wave, lane);
+    load_tile64<D, kKvWaves>(P.dO + e0, q_row_bytes, last, Ls + (2 + S) * T64, wave, lane);
   };
 
   // Per-lane LDS offsets (the swizzle of a row depends only on its index mod 16, which
@@ -293,7 +296,7 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     tra[eb] = C::off(trr, 32 * eb + trc);
     trb[eb] = C::off(trr + 8, 32 * eb + trc);
   }
-  const lds_char* vrows = Ls + 32 * wave * C::RB;  // this wave's 32 V rows
+  const lds_char* vrows = Ls + VO + 32 * wave * C::RB;  // this wave's 32 V rows
 
   f32x16 dkT[C::EB], dvT[C::EB];
 #pragma unroll
@@ -305,7 +308,7 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   // dP accumulators is query row 32 HF + 8 g + 4 hh + r, key `key`.
   auto block = [&](auto slot, auto half, int tpos, int rows_left) __attribute__((always_inline)) {
     constexpr int S = decltype(slot)::value, HF = decltype(half)::value;
-    constexpr int QB = VT + S * T64 + HF * 32 * C::RB;  // this block's Qs rows
+    constexpr int QB = S * T64 + HF * 32 * C::RB;  // this block's Qs rows
     constexpr int OB = QB + 2 * T64;                    // and dO rows
     f32x16 s, dp;
 #pragma unroll
@@ -313,8 +316,7 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks) {
       const int o = kad ^ (32 * ks);
-      u32x4 vf = lds_read16(vrows + o);
-      if (vzero) vf = u32x4{0u, 0u, 0u, 0u};
+      const u32x4 vf = lds_read16(vrows + o);
       s = mfma32(lds_read16(Ls + QB + o), kf[ks], s);
       dp = mfma32(lds_read16(Ls + OB + o), vf, dp);
       // (no operand prefetch across steps: registers are the limit here, and the other
