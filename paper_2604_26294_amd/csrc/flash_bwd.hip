@@ -252,8 +252,8 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   const uint32_t q_row_bytes = 2u * (uint32_t)(P.heads * D);
   // Tile at the cursor into slot S: Qs and dO rows (LDS-destination loads) and, in the
   // first 16 lanes of each wave, lse / delta of rows 8 w .. 8 w + 7 into registers.
-  // Rows past the segment are clamped on load and get lse = +inf, delta = 0 when
-  // written to LDS (P = 0 there).
+  // They are written to LDS negated; rows past the segment are clamped on load and get
+  // -lse = -inf, -delta = 0 there (P = 0).
   const int pr = 8 * wave + (lane & 7), pwhich = (lane >> 3) & 1;
   // (the array base is chosen from two scalar values, not by indexing the parameter
   // block per lane, which would load the pointer from memory)
@@ -310,9 +310,20 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     constexpr int S = decltype(slot)::value, HF = decltype(half)::value;
     constexpr int QB = S * T64 + HF * 32 * C::RB;  // this block's Qs rows
     constexpr int OB = QB + 2 * T64;                    // and dO rows
+    // The accumulators start at -lse and -delta of their query rows (held negated in
+    // LDS), so that they end as S - lse and dP - delta.
+    const float* nlse = Lf + S * 2 * kQStage + 32 * HF + 4 * hh;
     f32x16 s, dp;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) s[e] = dp[e] = 0.f;
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(nlse + 8 * g);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(nlse + kQStage + 8 * g);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s[4 * g + r] = l4[r];
+        dp[4 * g + r] = d4[r];
+      }
+    }
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks) {
       const int o = kad ^ (32 * ks);
@@ -332,17 +343,14 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     }
     // P = 2^(S - lse), dS = P (dP - delta), packed to bf16 in the accumulator's row order
     // (the B operands below).
-    const float* lse_t = Lf + S * 2 * kQStage + 32 * HF + 4 * hh;
     u32x4 pf[2], df[2];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_t + 8 * g);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(lse_t + kQStage + 8 * g);
       float pv[4], dv[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        pv[r] = __builtin_amdgcn_exp2f(s[4 * g + r] - l4[r]);
-        dv[r] = pv[r] * (dp[4 * g + r] - d4[r]);
+        pv[r] = __builtin_amdgcn_exp2f(s[4 * g + r]);
+        dv[r] = pv[r] * dp[4 * g + r];
       }
       pf[g >> 1][2 * (g & 1)] = pack_bf16x2(pv[0], pv[1]);
       pf[g >> 1][2 * (g & 1) + 1] = pack_bf16x2(pv[2], pv[3]);
@@ -372,7 +380,7 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     constexpr int S = decltype(slot)::value;
     if (lane < 16)
       Lf[S * 2 * kQStage + pwhich * kQStage + pr] =
-          pr <= pend_last[S] ? pend[S] : (pwhich ? 0.f : INFINITY);
+          pr <= pend_last[S] ? -pend[S] : (pwhich ? 0.f : -INFINITY);
     asm volatile("s_waitcnt vmcnt(1)" ::: "memory");  // all but tile t + 1's lse / delta
     __syncthreads();
     if (t + 1 < n_tiles) issue(IC<1 - S>{});
