@@ -97,7 +97,9 @@ typedef struct tsp_shape {
 /* Gated ring MLP of rank p (Algorithm 2):
  *   Y (+)= sum over t = 0..D-1, j = (p - t) mod D, of
  *          bf16( SiLU(X W_gate[j]^T) * (X W_up[j]^T) ) W_down[j]
- * with SiLU(z) = z * sigmoid(z), fp32 accumulation across shards in ring order.
+ * with SiLU(z) = z * sigmoid(z), fp32 accumulation across shards in ring order, the
+ * down projections of steps 2i and 2i+1 taken as one product over both shards (an odd
+ * last step alone): the same sum up to fp32 rounding order.
  *   x_loc      [B, S_loc, h] bf16       the rank's tokens
  *   w_gate[j]  [ffn/D, h]   bf16       W1 shard j
  *   w_up[j]    [ffn/D, h]   bf16       W3 shard j
@@ -154,7 +156,8 @@ tsp_status tsp_kv_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
  *       sees keys j <= pos(t) (layout 1: the two CausalAttn calls of Algorithm 1, the
  *       first half of the rows against keys [0, s1 = (p+1)*S_c), the second against
  *       [0, s2 = (2D-p)*S_c));
- *   Y (+)= Flatten(A) W_O^(r)^T   (fp32, shards accumulated in order r = 0..D-1).
+ *   Y (+)= Flatten(A) W_O^(r)^T   (fp32, shards accumulated in order r = 0..D-1, the
+ *       output projections of shards 2i and 2i+1 as one product over both).
  * Q, K, V, the softmax probabilities and A are rounded to bf16 for the matrix cores.
  *   x_loc, w_attn as for tsp_kv_rank_fwd;  k_buf, v_buf [B, S, n_kv, d] bf16: this
  *   rank's rows are written; every other row its queries can see must already hold

@@ -2,6 +2,8 @@
 //
 //   gate+up+SwiGLU  Hs = bf16( SiLU(X W1^T) * (X W3^T) )          Algorithm 2, gate/up
 //   down / O-proj   Y (+)= Hs W2   or   Y (+)= Flatten(A) W_O^T    Algorithm 2 / 1, "+="
+//                   (optionally over two shards at once: the contraction then runs over
+//                   [A A'] and [B; B'], two operand pairs held in separate buffers)
 //   SwiGLU backward G = X W1^T, U = X W3^T, dHs = dY W2^T in one pass; dG, dU and the
 //                   transposes of dG, dU, Hs for the weight-gradient products
 //   Q/K/V proj      Q = X W_Q^T -> workspace, K, V -> full-sequence buffers at the
@@ -164,11 +166,18 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
 
   auto dma_stage = [&](int stage, int k0) {
     lds_char* S = Ls + stage * C::STAGE;
+    if constexpr (NN) {
+      // (k0 is uniform: the part is chosen per stage, from scalar values)
+      const bool hi = P.A_hi != nullptr && k0 >= P.k_split;
+      const int kk = hi ? k0 - P.k_split : k0;
+      dma_nt<BM, C::WAVES>(S, hi ? P.A_hi : P.A, P.lda, m0, P.M, kk, wave, lane);
+      dma_nn<BN, C::WAVES>(S + C::A_BYTES, hi ? P.B_hi : P.B, P.ldb, kk,
+                           hi ? P.Kb_rows_hi : P.Kb_rows, n0, P.N, wave, lane);
+      return;
+    }
     dma_nt<BM, C::WAVES>(S, P.A, P.lda, m0, P.M, k0, wave, lane);
     if constexpr (C::BWD) dma_nt<BM, C::WAVES>(S + BM * BK * 2, P.A2, P.lda, m0, P.M, k0, wave, lane);
-    if constexpr (NN) {
-      dma_nn<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, k0, P.Kb_rows, n0, P.N, wave, lane);
-    } else if constexpr (EPI == EPI_SWIGLU || C::BWD) {
+    if constexpr (EPI == EPI_SWIGLU || C::BWD) {
       dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
       dma_nt<BN, C::WAVES>(S + C::A_BYTES + BN * BK * 2, P.B2, P.ldb, n0, P.N, k0, wave, lane);
       if constexpr (C::BWD)
@@ -421,6 +430,8 @@ hipError_t launch(const GemmParams& p, hipStream_t s) {
   using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   if (p.K <= 0 || p.K % BK != 0) return hipErrorInvalidValue;
+  if (p.A_hi && (!NN || p.k_split <= 0 || p.k_split >= p.K || p.k_split % BK != 0))
+    return hipErrorInvalidValue;
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   // hipLaunchKernel returns the status of this launch only (not an earlier error).
   void* args[] = {const_cast<GemmParams*>(&p)};

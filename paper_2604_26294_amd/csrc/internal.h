@@ -17,6 +17,14 @@ struct GemmParams {
   const uint16_t* B2;  // SwiGLU (both directions): the up-projection operand, layout of B
   int M, N, K;         // K: contraction length, a multiple of 64
   int Kb_rows;         // [K, N] operands: rows actually present (rows >= Kb_rows are clamped)
+  // Two-part contraction ([K, N] products only): contraction indices k >= k_split come
+  // from A_hi (columns k - k_split, row stride lda) and B_hi (rows k - k_split, clamped
+  // at Kb_rows_hi), the ones below from A and B.  k_split is a multiple of 64; A_hi ==
+  // nullptr means one part.
+  const uint16_t* A_hi;
+  const uint16_t* B_hi;
+  int k_split;
+  int Kb_rows_hi;
 
   // SwiGLU epilogue: H[m, n] = bf16( SiLU(C_gate) * C_up ) for n < N, and 0 for
   // N <= n < ldh (the zero padding that lets the down projection contract over ldh).

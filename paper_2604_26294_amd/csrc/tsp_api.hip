@@ -72,10 +72,20 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
 }
 
 // Workspace regions (each 256-byte aligned):
-//   MLP:   Hs [M, F/D rounded up to 64] bf16 (zero-padded columns)
-//   ATTN:  Q [M, H_s d] bf16, A [M, H_s d] bf16
+//   MLP:   Hs of two ring steps, [M, F/D rounded up to 64] bf16 each (zero-padded columns)
+//   ATTN:  Q [M, H_s d] bf16, A of two shard steps [M, H_s d] bf16 each
 //   LAYER: u [M, h] bf16, then max(MLP, ATTN)
-size_t ws_mlp(const Dims& d) { return align_up((size_t)d.M * d.fs_pad * 2); }
+// (with D = 1 there is one step and the second buffer is not used)
+//
+// The down and output projections run once per two steps, over both steps' operands
+// (Y += [Hs Hs'] [W2; W2'] = Hs W2 + Hs' W2'): Y is then read and written once per
+// pair instead of once per step.  The two shards involved are the current one and its
+// predecessor, which a streaming schedule holds anyway while the next one arrives; the
+// sum differs from the step-by-step one only in fp32 rounding order.
+constexpr int kPair = 2;
+size_t ws_mlp(const Dims& d) {
+  return (d.D > 1 ? kPair : 1) * align_up((size_t)d.M * d.fs_pad * 2);
+}
 // Attention workspace: Q of the current shard and the attention output A (bf16
 // [M, H_s d] each), then the key-range partials when the shard's attention is split.
 // The rank's query rows as segments of consecutive global positions (Algorithm 1):
@@ -105,7 +115,7 @@ void attn_segments(const Dims& d, AttnParams* ap) {
 }
 
 struct AttnWs {
-  size_t q, a, po, pml, total;  // byte offsets and total size
+  size_t q, a, a2, po, pml, total;  // byte offsets and total size
   int n_split, split_len;
 };
 AttnWs attn_ws(const Dims& d) {
@@ -117,7 +127,8 @@ AttnWs attn_ws(const Dims& d) {
   const size_t part = w.n_split > 1 ? (size_t)w.n_split * rows : 0;
   w.q = 0;
   w.a = align_up(rows * d.d * 2);
-  w.po = w.a + align_up(rows * d.d * 2);
+  w.a2 = w.a + align_up(rows * d.d * 2);
+  w.po = d.D > 1 ? w.a2 + align_up(rows * d.d * 2) : w.a2;
   w.pml = w.po + align_up(part * d.d * 4);
   w.total = w.pml + align_up(part * 2 * 4);
   return w;
@@ -279,12 +290,18 @@ void timer_end(int kind, long slot, hipStream_t st) {
 
 // ----------------------------------------------------------------- launch sequences
 
-// Algorithm 2 on an already validated problem.  Ring step t uses shard (p - t) mod D.
+// Algorithm 2 on an already validated problem.  Ring step t uses shard (p - t) mod D;
+// the down projections of steps 2i and 2i + 1 run as one product (Hs of step t in
+// buffer t mod 2), an odd last step on its own.
 tsp_status run_mlp(const Dims& d, const uint16_t* x, const uint16_t* const* wg,
                    const uint16_t* const* wu, const uint16_t* const* wd, float* y,
                    int accumulate, uint16_t* hs_ws, hipStream_t st) {
+  const size_t hs_elems = align_up((size_t)d.M * d.fs_pad * 2) / 2;
+  int j_prev = 0;
+  bool first_down = true;
   for (int t = 0; t < d.D; ++t) {
     const int j = ((d.p - t) % d.D + d.D) % d.D;
+    uint16_t* hs = hs_ws + (size_t)(t % kPair) * hs_elems;
     GemmParams up = {};
     up.A = x;
     up.lda = d.h;
@@ -294,23 +311,35 @@ tsp_status run_mlp(const Dims& d, const uint16_t* x, const uint16_t* const* wg,
     up.M = (int)d.M;
     up.N = d.fs;
     up.K = d.h;
-    up.H = hs_ws;
+    up.H = hs;
     up.ldh = d.fs_pad;
     TSP_LAUNCH(TSP_KERNEL_GATE_UP, st, tsp::launch_gemm_swiglu(up, st));
 
-    GemmParams dn = {};
-    dn.A = hs_ws;
-    dn.lda = d.fs_pad;
-    dn.B = wd[j];
-    dn.ldb = d.h;
-    dn.M = (int)d.M;
-    dn.N = d.h;
-    dn.K = d.fs_pad;  // padded columns of Hs are zero; W2 rows past fs are clamped
-    dn.Kb_rows = d.fs;
-    dn.Y = y;
-    dn.ldy = d.h;
-    dn.accumulate = (t > 0 || accumulate) ? 1 : 0;
-    TSP_LAUNCH(TSP_KERNEL_DOWN, st, tsp::launch_gemm_nn_acc(dn, st));
+    const bool second = t % kPair == 1;
+    if (second || t == d.D - 1) {
+      GemmParams dn = {};
+      dn.A = second ? hs_ws : hs;
+      dn.lda = d.fs_pad;
+      dn.B = wd[second ? j_prev : j];
+      dn.ldb = d.h;
+      dn.M = (int)d.M;
+      dn.N = d.h;
+      dn.K = d.fs_pad;  // padded columns of Hs are zero; W2 rows past fs are clamped
+      dn.Kb_rows = d.fs;
+      if (second) {
+        dn.A_hi = hs;
+        dn.B_hi = wd[j];
+        dn.k_split = d.fs_pad;
+        dn.Kb_rows_hi = d.fs;
+        dn.K = 2 * d.fs_pad;
+      }
+      dn.Y = y;
+      dn.ldy = d.h;
+      dn.accumulate = (!first_down || accumulate) ? 1 : 0;
+      first_down = false;
+      TSP_LAUNCH(TSP_KERNEL_DOWN, st, tsp::launch_gemm_nn_acc(dn, st));
+    }
+    j_prev = j;
   }
   return TSP_OK;
 }
@@ -429,8 +458,12 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
   const float log2e = 1.4426950408889634f;
   const AttnWs aw = attn_ws(d);
   uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + aw.q);
-  uint16_t* a_ws = reinterpret_cast<uint16_t*>(ws + aw.a);
+  // A of shard r in buffer r mod 2; the output projections of shards 2i and 2i + 1 run
+  // as one product, an odd last shard on its own.
+  uint16_t* a_buf[kPair] = {reinterpret_cast<uint16_t*>(ws + aw.a),
+                            reinterpret_cast<uint16_t*>(ws + aw.a2)};
   for (int r = 0; r < d.D; ++r) {
+    uint16_t* a_ws = a_buf[r % kPair];
     GemmParams g = qkv_params(d, x, wa[r], r, q_ws, kb, vb, true);
     TSP_LAUNCH(TSP_KERNEL_QKV, st, tsp::launch_gemm_qkv(g, st));
 
@@ -453,19 +486,30 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     ap.part_ml = reinterpret_cast<float*>(ws + aw.pml);
     TSP_LAUNCH(TSP_KERNEL_ATTN, st, tsp::launch_flash_attn(ap, st));
 
+    const bool second = r % kPair == 1;
+    if (!second && r != d.D - 1) continue;
+    const size_t wo = (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T block [H_s d, h]
     GemmParams o = {};
-    o.A = a_ws;
+    o.A = a_buf[0];
     o.lda = qd;
-    o.B = wa[r] + (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T block [H_s d, h]
+    o.B = wa[second ? r - 1 : r] + wo;
     o.ldb = d.h;
     o.M = (int)d.M;
     o.N = d.h;
     o.K = qd;
     o.Kb_rows = qd;
+    if (second) {
+      o.A_hi = a_buf[1];
+      o.B_hi = wa[r] + wo;
+      o.k_split = qd;
+      o.Kb_rows_hi = qd;
+      o.K = 2 * qd;
+    }
     o.Y = y;
     o.ldy = d.h;
-    o.accumulate = (r > 0 || accumulate) ? 1 : 0;
-    if (r == 0 && residual) {
+    const bool first_proj = r < kPair;
+    o.accumulate = (!first_proj || accumulate) ? 1 : 0;
+    if (first_proj && residual) {
       o.R = residual;
       o.ldr = d.h;
     }
@@ -818,7 +862,8 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
   char* base = static_cast<char*>(ws);
   uint16_t* u_ws = reinterpret_cast<uint16_t*>(base);
   char* rest = base + align_up((size_t)d.M * d.h * 2);
-  // u = x + Attn(x): Y starts from x at the first shard; the last shard also writes bf16(u).
+  // u = x + Attn(x): Y starts from x at the first output projection; the last one also
+  // writes bf16(u).
   TSP_TRY(run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, 0, x_loc, u_ws, rest, stream));
   // y = u + MLP(bf16 u): the MLP accumulates onto Y, which holds u.
   return run_mlp(d, u_ws, w_gate, w_up, w_down, y_loc, 1, reinterpret_cast<uint16_t*>(rest),

@@ -12,16 +12,16 @@ from paper_2604_26294_amd import inputs as I  # noqa: E402
 from paper_2604_26294_amd import tsp as T  # noqa: E402
 from paper_2604_26294_amd.harness import RankProblem  # noqa: E402
 from paper_2604_26294_amd.workloads import TINY  # noqa: E402
-from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, SINGLE, assert_close,  # noqa: E402
-                              f64, gen, oracle_blocks)
+from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, ODD3, SINGLE,  # noqa: E402
+                              assert_close, f64, gen, oracle_blocks)
 
 CASES = [(TINY, 0), (TINY, 1), (MID_GQA64, 0), (MID_GQA64, 2), (MID_GQA64, 3),
-         (MID_MHA128, 1), (MID_GQA8, 1), (SINGLE, 0),
+         (MID_MHA128, 1), (MID_GQA8, 1), (SINGLE, 0), (ODD3, 2), (ODD3, 0),
          # zigzag shards (Algorithm 1 as printed): two query segments, K/V rows written
          # at reordered positions, every other rank's rows visible
          (TINY.with_layout(1), 0), (TINY.with_layout(1), 1), (MID_GQA64.with_layout(1), 0),
          (MID_GQA64.with_layout(1), 3), (MID_MHA128.with_layout(1), 0),
-         (MID_GQA8.with_layout(1), 1), (SINGLE.with_layout(1), 0)]
+         (MID_GQA8.with_layout(1), 1), (SINGLE.with_layout(1), 0), (ODD3.with_layout(1), 1)]
 _IDS = [f"{w.name}-{w.layout_name}-r{p}" for w, p in CASES]
 _cache = {}
 
