@@ -66,7 +66,10 @@ def log(msg):
 
 
 def kernel_flops(wl):
-    """Algorithmic FLOPs of one launch of each kernel class (TSP_KERNEL_* order)."""
+    """Algorithmic FLOPs of each kernel class (TSP_KERNEL_* order) over one call of the
+    entry point that launches it (all D shard steps), whatever the number of launches:
+    the down and output projections of two steps share a launch, and so do the two dX
+    products of one MLP backward step."""
     from paper_2604_26294_amd.flops import step_attn_core_flops
     D = wl.degree
     m = wl.batch * wl.s_loc
@@ -74,20 +77,22 @@ def kernel_flops(wl):
     fs = wl.ffn // D
     qd = wl.n_heads // D * wl.head_dim
     kd = wl.n_kv_heads // D * wl.head_dim
-    return {"gate_up": 2.0 * m * 2 * fs * h, "down": 2.0 * m * h * fs,
-            "qkv": 2.0 * m * (qd + 2 * kd) * h, "attn": step_attn_core_flops(wl),
-            "oproj": 2.0 * m * qd * h,
-            # MLP backward: G, U and dHs in one pass; one dX product; one weight gradient
-            "bwd_gate": 2.0 * m * 3 * fs * h, "bwd_dx": 2.0 * m * fs * h,
-            "bwd_dw": 2.0 * m * fs * h,
-            # attention backward, first stage: the Q / dA products; the forward recomputation;
-            # dK/dV recomputes S and forms dP, dV, dK (4 of the forward's 2 products' cost
-            # each pair = 2x the core); dQ recomputes S, dP and forms dQ (1.5x); the
-            # stage's dX and weight-gradient products (second-stage launches are K_s/H_s
-            # of these)
-            "abwd_proj": 2.0 * m * qd * h, "abwd_fwd": step_attn_core_flops(wl),
-            "abwd_kv": 2.0 * step_attn_core_flops(wl), "abwd_q": 1.5 * step_attn_core_flops(wl),
-            "abwd_dx": 2.0 * m * qd * h, "abwd_dw": 2.0 * m * qd * h}
+    core = step_attn_core_flops(wl)
+    per_step = {"gate_up": 2.0 * m * 2 * fs * h, "down": 2.0 * m * h * fs,
+                "qkv": 2.0 * m * (qd + 2 * kd) * h, "attn": core,
+                "oproj": 2.0 * m * qd * h,
+                # MLP backward: G, U and dHs in one pass; dX = dG W1 + dU W3; the three
+                # weight gradients
+                "bwd_gate": 2.0 * m * 3 * fs * h, "bwd_dx": 2 * 2.0 * m * fs * h,
+                "bwd_dw": 3 * 2.0 * m * fs * h,
+                # attention backward, first stage: the Q and dA products; the forward
+                # recomputation; dK/dV recomputes S and forms dP, dV, dK (2x the core); dQ
+                # recomputes S, dP and forms dQ (1.5x); the dX product and the two
+                # weight-gradient products
+                "abwd_proj": 2 * 2.0 * m * qd * h, "abwd_fwd": core,
+                "abwd_kv": 2.0 * core, "abwd_q": 1.5 * core,
+                "abwd_dx": 2.0 * m * qd * h, "abwd_dw": 2 * 2.0 * m * qd * h}
+    return {k: D * v for k, v in per_step.items()}
 
 
 def cpu_baseline(wl, x_bits, w_bits, rows: int):
@@ -250,16 +255,17 @@ def main(argv=None):
             continue
         avg = tot / n
         kernels[name] = {"avg_ms": round(avg, 5), "launches_per_step": n // args.steps,
-                         "tflops": round(kf[name] / (avg * 1e-3) / 1e12, 2),
+                         "tflops": round(kf[name] / (tot / args.steps * 1e-3) / 1e12, 2),
                          "time_share": round(tot / args.steps / ms, 4)}
     dom = max(kernels, key=lambda n: kernels[n]["time_share"])
     dom_avg = kernels[dom]["avg_ms"]
-    achieved = kf[dom] / (dom_avg * 1e-3) / 1e12
+    dom_flops = kf[dom] / kernels[dom]["launches_per_step"]  # per launch
+    achieved = dom_flops / (dom_avg * 1e-3) / 1e12
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": measured_traffic(wl, dom),
-                "flops_per_launch": kf[dom], "avg_launch_ms": dom_avg}
+                "flops_per_launch": dom_flops, "avg_launch_ms": dom_avg}
 
     # The attention and MLP entry points on their own (same rank, same buffers).
     ms_attn = time_calls(prob.attn_fwd, args.steps, 2)
@@ -291,7 +297,8 @@ def main(argv=None):
         tot, n = T.tsp_profile_read(k)
         if n:
             bwd_kernels[name] = {"avg_ms": round(tot / n, 5), "launches": n // args.steps,
-                                 "tflops": round(kf[name] / (tot / n * 1e-3) / 1e12, 2)}
+                                 "tflops": round(kf[name] / (tot / args.steps * 1e-3) / 1e12,
+                                                 2)}
     blocks["mlp_bwd"] = {"ms": round(ms_bwd, 4), "flops": bwd_flops,
                          "tflops": round(bwd_flops / (ms_bwd * 1e-3) / 1e12, 2),
                          "flops_note": "16 M F h executed (G, U recomputed); 12 M F h without",
@@ -320,12 +327,12 @@ def main(argv=None):
             e = {"avg_ms": round(tot / n, 5), "launches": n // args.steps,
                  "time_share": round(tot / args.steps / ms_ab1, 4)}
             if name != "abwd_aux":
-                e["tflops"] = round(kf[name] / (tot / n * 1e-3) / 1e12, 2)
+                e["tflops"] = round(kf[name] / (tot / args.steps * 1e-3) / 1e12, 2)
             ab1_kernels[name] = e
     T.tsp_profile_enable(False)
     ms_ab2 = time_calls(lambda: prob.attn_kv_bwd(dkl, dvl), args.steps, 0)
-    core = kf["attn"]
     D = wl.degree
+    core = kf["attn"] / D
     qd = wl.n_heads // D * wl.head_dim
     kd = wl.n_kv_heads // D * wl.head_dim
     gemm1 = 5 * 2.0 * m_tok * qd * wl.hidden          # Q, dA, dX, dW_Q, dW_O^T per shard

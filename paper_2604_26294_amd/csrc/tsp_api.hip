@@ -380,20 +380,25 @@ tsp_status run_mlp_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     g.ldt = w.m_pad;
     TSP_LAUNCH(TSP_KERNEL_BWD_GATE, st, tsp::launch_gemm_swiglu_bwd(g, st));
 
-    // dX (+)= dG W_gate[j] + dU W_up[j]: [M, F/D] x [F/D, h], padded columns are zero.
-    for (int k = 0; k < 2; ++k) {
+    // dX (+)= dG W_gate[j] + dU W_up[j] = [dG dU] [W_gate[j]; W_up[j]] in one product
+    // ([M, F/D] x [F/D, h] twice; padded columns of dG, dU are zero).
+    {
       GemmParams p = {};
-      p.A = k == 0 ? dg : du;
+      p.A = dg;
       p.lda = d.fs_pad;
-      p.B = k == 0 ? wg[j] : wu[j];
+      p.B = wg[j];
       p.ldb = d.h;
+      p.Kb_rows = d.fs;
+      p.A_hi = du;
+      p.B_hi = wu[j];
+      p.k_split = d.fs_pad;
+      p.Kb_rows_hi = d.fs;
       p.M = (int)d.M;
       p.N = d.h;
-      p.K = d.fs_pad;
-      p.Kb_rows = d.fs;
+      p.K = 2 * d.fs_pad;
       p.Y = dx;
       p.ldy = d.h;
-      p.accumulate = (t > 0 || k > 0 || accumulate) ? 1 : 0;
+      p.accumulate = (t > 0 || accumulate) ? 1 : 0;
       TSP_LAUNCH(TSP_KERNEL_BWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
     }
     // dW (+)= (dG^T | dU^T | Hs^T) (X | X | dY): [F/D, M] x [M, h], padded rows are zero.
@@ -666,23 +671,31 @@ tsp_status run_attn_kv_bwd(const Dims& d, const uint16_t* x, const uint16_t* con
   const int qd = d.hs * d.d, kd = d.ks * d.d, ld = d.nkv * d.d;
   const int m_pad = (int)((d.M + 63) / 64 * 64);
   uint16_t* t_ws = reinterpret_cast<uint16_t*>(ws);
-  for (int r = 0; r < d.D; ++r)
-    for (int k = 0; k < 2; ++k) {
-      const uint16_t* g = (k == 0 ? dkl : dvl) + (size_t)r * kd;  // [M, K_s d], row stride ld
-      const size_t blk = (size_t)(qd + k * kd) * d.h;             // W_K or W_V block
-      GemmParams p = {};  // dX (+)= g W_{K|V}^(r)
-      p.A = g;
+  for (int r = 0; r < d.D; ++r) {
+    const uint16_t* gk = dkl + (size_t)r * kd;  // [M, K_s d], row stride ld
+    const uint16_t* gv = dvl + (size_t)r * kd;
+    {
+      GemmParams p = {};  // dX (+)= dK W_K^(r) + dV W_V^(r), one product over both
+      p.A = gk;
       p.lda = ld;
-      p.B = wa[r] + blk;
+      p.B = wa[r] + (size_t)qd * d.h;
       p.ldb = d.h;
+      p.Kb_rows = kd;
+      p.A_hi = gv;
+      p.B_hi = wa[r] + (size_t)(qd + kd) * d.h;
+      p.k_split = kd;
+      p.Kb_rows_hi = kd;
       p.M = (int)d.M;
       p.N = d.h;
-      p.K = kd;
-      p.Kb_rows = kd;
+      p.K = 2 * kd;
       p.Y = dx;
       p.ldy = d.h;
-      p.accumulate = (r > 0 || k > 0 || accumulate) ? 1 : 0;
+      p.accumulate = (r > 0 || accumulate) ? 1 : 0;
       TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+    }
+    for (int k = 0; k < 2; ++k) {
+      const uint16_t* g = k == 0 ? gk : gv;
+      const size_t blk = (size_t)(qd + k * kd) * d.h;  // W_K or W_V block
       TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
                  tsp::launch_transpose_bf16(g, ld, (int)d.M, kd, t_ws, m_pad, st));
       GemmParams q = {};  // block (+)= g^T X
@@ -699,6 +712,7 @@ tsp_status run_attn_kv_bwd(const Dims& d, const uint16_t* x, const uint16_t* con
       q.accumulate = accumulate ? 1 : 0;
       TSP_LAUNCH(TSP_KERNEL_ABWD_DW, st, tsp::launch_gemm_nn_acc_small(q, st));
     }
+  }
   return TSP_OK;
 }
 
