@@ -468,7 +468,13 @@ hipError_t launch_gemm_nn_acc_small(const GemmParams& p, hipStream_t s) {
   return launch<128, 128, 2, 4, true, EPI_ACC, 2>(p, s);
 }
 
+// Projections with few output tiles (the backward's Q and dA products, N = H_s d; GQA
+// shapes; short sequences) would leave CUs idle with 256 x 192 tiles: below one tile per
+// CU they take 128 x 128 tiles.
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s) {
+  constexpr long long kCus = 256;
+  const long long big = (long long)((p.M + 255) / 256) * ((p.N + 191) / 192);
+  if (big < kCus) return launch<128, 128, 2, 4, false, EPI_QKV, 2>(p, s);
   return launch<256, 192, 4, 2, false, EPI_QKV, 2>(p, s);
 }
 
