@@ -34,6 +34,8 @@
 // stored with its width padded to a multiple of 64 with zero columns (written by the
 // SwiGLU epilogue), and the matching W2 rows past F/D are clamped, so padded terms
 // contribute exact zeros.
+#include <climits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -138,8 +140,9 @@ __device__ __forceinline__ void dma_nn(lds_char* dst, const uint16_t* base, int 
   }
 }
 
+// One output tile (work index w) of the product P.
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
-__global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParams P) {
+__device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
   using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
   constexpr int TM = C::TM, TN = C::TN, TNB = C::TNB;
   __shared__ __attribute__((aligned(1024))) char L[C::LDS_BYTES];
@@ -151,8 +154,6 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
   const int l32 = lane & 31, hh = lane >> 5;
 
   const int tiles_n = (P.N + BN - 1) / BN;
-  const int tiles_m = (P.M + BM - 1) / BM;
-  const int w = xcd_work_index(blockIdx.x, tiles_m * tiles_n);
   const int m0 = (w / tiles_n) * BM;
   const int n0 = (w % tiles_n) * BN;
 
@@ -164,15 +165,26 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+  // The two parts of a two-part contraction as values (the asm keeps the compiler from
+  // turning the per-stage choice into a choice between field addresses, which would put
+  // the parameters in scratch memory).
+  const uint16_t* a_lo = P.A;
+  const uint16_t* a_hi = P.A_hi ? P.A_hi : P.A;
+  const uint16_t* b_lo = P.B;
+  const uint16_t* b_hi = P.A_hi ? P.B_hi : P.B;
+  int kr_lo = P.Kb_rows, kr_hi = P.Kb_rows_hi, k_split = P.A_hi ? P.k_split : INT_MAX;
+  if constexpr (NN)
+    asm volatile("" : "+s"(a_lo), "+s"(a_hi), "+s"(b_lo), "+s"(b_hi), "+s"(kr_lo), "+s"(kr_hi),
+                 "+s"(k_split));
   auto dma_stage = [&](int stage, int k0) {
     lds_char* S = Ls + stage * C::STAGE;
     if constexpr (NN) {
       // (k0 is uniform: the part is chosen per stage, from scalar values)
-      const bool hi = P.A_hi != nullptr && k0 >= P.k_split;
-      const int kk = hi ? k0 - P.k_split : k0;
-      dma_nt<BM, C::WAVES>(S, hi ? P.A_hi : P.A, P.lda, m0, P.M, kk, wave, lane);
-      dma_nn<BN, C::WAVES>(S + C::A_BYTES, hi ? P.B_hi : P.B, P.ldb, kk,
-                           hi ? P.Kb_rows_hi : P.Kb_rows, n0, P.N, wave, lane);
+      const bool hi = k0 >= k_split;
+      const int kk = hi ? k0 - k_split : k0;
+      dma_nt<BM, C::WAVES>(S, hi ? a_hi : a_lo, P.lda, m0, P.M, kk, wave, lane);
+      dma_nn<BN, C::WAVES>(S + C::A_BYTES, hi ? b_hi : b_lo, P.ldb, kk, hi ? kr_hi : kr_lo, n0,
+                           P.N, wave, lane);
       return;
     }
     dma_nt<BM, C::WAVES>(S, P.A, P.lda, m0, P.M, k0, wave, lane);
@@ -426,12 +438,67 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
 }
 
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
-hipError_t launch(const GemmParams& p, hipStream_t s) {
-  using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
-  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+__global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParams P) {
+  const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
+  gemm_tile<BM, BN, WGM, WGN, NN, EPI, STAGES>(P, xcd_work_index(blockIdx.x, tiles));
+}
+
+// Up to three independent products of one configuration in one launch: the tiles of
+// product i follow those of the products before it, so small products that would each
+// leave CUs idle fill the chip together.
+struct GemmGroup {
+  GemmParams p[kGemmGroupMax];
+  int n;
+};
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
+__global__ __launch_bounds__(kWave * WGM * WGN) void gemm_group_kernel(const GemmGroup G) {
+  int tiles[kGemmGroupMax], total = 0;
+#pragma unroll
+  for (int i = 0; i < kGemmGroupMax; ++i) {
+    tiles[i] = i < G.n ? ((G.p[i].M + BM - 1) / BM) * ((G.p[i].N + BN - 1) / BN) : 0;
+    total += tiles[i];
+  }
+  int w = xcd_work_index(blockIdx.x, total), i = 0;
+  while (i + 1 < G.n && w >= tiles[i]) w -= tiles[i++];  // uniform per workgroup
+  gemm_tile<BM, BN, WGM, WGN, NN, EPI, STAGES>(G.p[i], w);
+}
+
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
+hipError_t check_params(const GemmParams& p) {
   if (p.K <= 0 || p.K % BK != 0) return hipErrorInvalidValue;
   if (p.A_hi && (!NN || p.k_split <= 0 || p.k_split >= p.K || p.k_split % BK != 0))
     return hipErrorInvalidValue;
+  return hipSuccess;
+}
+
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
+hipError_t launch_group(const GemmParams* ps, int n, hipStream_t s) {
+  using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
+  if (n < 1 || n > kGemmGroupMax) return hipErrorInvalidValue;
+  GemmGroup g = {};
+  long long total = 0;
+  for (int i = 0; i < n; ++i) {
+    const GemmParams& p = ps[i];
+    if (p.M <= 0 || p.N <= 0) return hipErrorInvalidValue;
+    const hipError_t e = check_params<BM, BN, WGM, WGN, NN, EPI, STAGES>(p);
+    if (e != hipSuccess) return e;
+    g.p[i] = p;
+    total += (long long)((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  }
+  g.n = n;
+  if (total > INT32_MAX) return hipErrorInvalidValue;
+  void* args[] = {&g};
+  return hipLaunchKernel(
+      reinterpret_cast<const void*>(&gemm_group_kernel<BM, BN, WGM, WGN, NN, EPI, STAGES>),
+      dim3((unsigned)total), dim3(C::THREADS), args, 0, s);
+}
+
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
+hipError_t launch(const GemmParams& p, hipStream_t s) {
+  using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
+  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  const hipError_t e = check_params<BM, BN, WGM, WGN, NN, EPI, STAGES>(p);
+  if (e != hipSuccess) return e;
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   // hipLaunchKernel returns the status of this launch only (not an earlier error).
   void* args[] = {const_cast<GemmParams*>(&p)};
@@ -466,6 +533,11 @@ hipError_t launch_gemm_swiglu_bwd(const GemmParams& p, hipStream_t s) {
 // shape where 256 x 256 would make 96.
 hipError_t launch_gemm_nn_acc_small(const GemmParams& p, hipStream_t s) {
   return launch<128, 128, 2, 4, true, EPI_ACC, 2>(p, s);
+}
+
+// Several weight-gradient products in one launch (each with M = F/D or H_s d rows).
+hipError_t launch_gemm_nn_acc_small_group(const GemmParams* ps, int n, hipStream_t s) {
+  return launch_group<128, 128, 2, 4, true, EPI_ACC, 2>(ps, n, s);
 }
 
 // Projections with few output tiles (the backward's Q and dA products, N = H_s d; GQA

@@ -79,6 +79,10 @@ hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s);
 // The accumulate epilogue on 128 x 128 tiles, for products with few output tiles
 // (the weight gradients: F/D x h outputs).
 hipError_t launch_gemm_nn_acc_small(const GemmParams& p, hipStream_t s);
+// Up to kGemmGroupMax independent products of launch_gemm_nn_acc_small's form in one
+// launch (each must have M, N > 0).
+constexpr int kGemmGroupMax = 3;
+hipError_t launch_gemm_nn_acc_small_group(const GemmParams* ps, int n, hipStream_t s);
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s);
 
 // Causal flash attention of one rank's queries for the heads of one shard.

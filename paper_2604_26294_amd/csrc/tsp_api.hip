@@ -198,11 +198,11 @@ AttnBwdWs attn_bwd_ws(const Dims& d) {
   w.total = w.dqp + align_up(dq_part);
   return w;
 }
-// Attention backward, second stage: the transposed gradient of one shard's K or V rows,
-// [K_s d, M rounded up to 64] bf16.
+// Attention backward, second stage: the transposed gradients of one shard's K and V
+// rows, [K_s d, M rounded up to 64] bf16 each.
 size_t ws_attn_kv_bwd(const Dims& d) {
   const size_t m_pad = (size_t)((d.M + 63) / 64 * 64);
-  return align_up((size_t)d.ks * d.d * m_pad * 2);
+  return 2 * align_up((size_t)d.ks * d.d * m_pad * 2);
 }
 size_t ws_layer(const Dims& d) {
   const size_t a = ws_mlp(d), b = ws_attn(d);
@@ -401,22 +401,23 @@ tsp_status run_mlp_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
       p.accumulate = (t > 0 || accumulate) ? 1 : 0;
       TSP_LAUNCH(TSP_KERNEL_BWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
     }
-    // dW (+)= (dG^T | dU^T | Hs^T) (X | X | dY): [F/D, M] x [M, h], padded rows are zero.
+    // dW (+)= (dG^T | dU^T | Hs^T) (X | X | dY): [F/D, M] x [M, h], padded rows are zero;
+    // the three products in one launch.
+    GemmParams p[3] = {};
     for (int k = 0; k < 3; ++k) {
-      GemmParams p = {};
-      p.A = k == 0 ? dgt : (k == 1 ? dut : hst);
-      p.lda = w.m_pad;
-      p.B = k < 2 ? x : dy;
-      p.ldb = d.h;
-      p.M = d.fs;
-      p.N = d.h;
-      p.K = w.m_pad;
-      p.Kb_rows = (int)d.M;
-      p.Y = k == 0 ? dwg[j] : (k == 1 ? dwu[j] : dwd[j]);
-      p.ldy = d.h;
-      p.accumulate = accumulate ? 1 : 0;
-      TSP_LAUNCH(TSP_KERNEL_BWD_DW, st, tsp::launch_gemm_nn_acc_small(p, st));
+      p[k].A = k == 0 ? dgt : (k == 1 ? dut : hst);
+      p[k].lda = w.m_pad;
+      p[k].B = k < 2 ? x : dy;
+      p[k].ldb = d.h;
+      p[k].M = d.fs;
+      p[k].N = d.h;
+      p[k].K = w.m_pad;
+      p[k].Kb_rows = (int)d.M;
+      p[k].Y = k == 0 ? dwg[j] : (k == 1 ? dwu[j] : dwd[j]);
+      p[k].ldy = d.h;
+      p[k].accumulate = accumulate ? 1 : 0;
     }
+    TSP_LAUNCH(TSP_KERNEL_BWD_DW, st, tsp::launch_gemm_nn_acc_small_group(p, 3, st));
   }
   return TSP_OK;
 }
@@ -644,22 +645,22 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
                tsp::launch_transpose_bf16(dq_ws, qd, (int)d.M, qd, dqt_ws, w.m_pad, st));
     TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
                tsp::launch_transpose_bf16(a_ws, qd, (int)d.M, qd, at_ws, w.m_pad, st));
-    // W_Q block (+)= dQ^T X;  W_O^T block (+)= A^T dY: [H_s d, M] x [M, h].
+    // W_Q block (+)= dQ^T X;  W_O^T block (+)= A^T dY: [H_s d, M] x [M, h], one launch.
+    GemmParams q[2] = {};
     for (int k = 0; k < 2; ++k) {
-      GemmParams q = {};
-      q.A = k == 0 ? dqt_ws : at_ws;
-      q.lda = w.m_pad;
-      q.B = k == 0 ? x : dy;
-      q.ldb = d.h;
-      q.M = qd;
-      q.N = d.h;
-      q.K = w.m_pad;
-      q.Kb_rows = (int)d.M;
-      q.Y = dw[r] + (k == 0 ? (size_t)0 : (size_t)(qd + 2 * kd) * d.h);
-      q.ldy = d.h;
-      q.accumulate = accumulate ? 1 : 0;
-      TSP_LAUNCH(TSP_KERNEL_ABWD_DW, st, tsp::launch_gemm_nn_acc_small(q, st));
+      q[k].A = k == 0 ? dqt_ws : at_ws;
+      q[k].lda = w.m_pad;
+      q[k].B = k == 0 ? x : dy;
+      q[k].ldb = d.h;
+      q[k].M = qd;
+      q[k].N = d.h;
+      q[k].K = w.m_pad;
+      q[k].Kb_rows = (int)d.M;
+      q[k].Y = dw[r] + (k == 0 ? (size_t)0 : (size_t)(qd + 2 * kd) * d.h);
+      q[k].ldy = d.h;
+      q[k].accumulate = accumulate ? 1 : 0;
     }
+    TSP_LAUNCH(TSP_KERNEL_ABWD_DW, st, tsp::launch_gemm_nn_acc_small_group(q, 2, st));
   }
   return TSP_OK;
 }
@@ -671,6 +672,7 @@ tsp_status run_attn_kv_bwd(const Dims& d, const uint16_t* x, const uint16_t* con
   const int qd = d.hs * d.d, kd = d.ks * d.d, ld = d.nkv * d.d;
   const int m_pad = (int)((d.M + 63) / 64 * 64);
   uint16_t* t_ws = reinterpret_cast<uint16_t*>(ws);
+  const size_t t_elems = align_up((size_t)kd * m_pad * 2) / 2;
   for (int r = 0; r < d.D; ++r) {
     const uint16_t* gk = dkl + (size_t)r * kd;  // [M, K_s d], row stride ld
     const uint16_t* gv = dvl + (size_t)r * kd;
@@ -693,25 +695,26 @@ tsp_status run_attn_kv_bwd(const Dims& d, const uint16_t* x, const uint16_t* con
       p.accumulate = (r > 0 || accumulate) ? 1 : 0;
       TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
     }
+    // W_K block (+)= dK^T X;  W_V block (+)= dV^T X: [K_s d, M] x [M, h], one launch.
+    GemmParams q[2] = {};
     for (int k = 0; k < 2; ++k) {
       const uint16_t* g = k == 0 ? gk : gv;
-      const size_t blk = (size_t)(qd + k * kd) * d.h;  // W_K or W_V block
+      uint16_t* gt = t_ws + (size_t)k * t_elems;
       TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
-                 tsp::launch_transpose_bf16(g, ld, (int)d.M, kd, t_ws, m_pad, st));
-      GemmParams q = {};  // block (+)= g^T X
-      q.A = t_ws;
-      q.lda = m_pad;
-      q.B = x;
-      q.ldb = d.h;
-      q.M = kd;
-      q.N = d.h;
-      q.K = m_pad;
-      q.Kb_rows = (int)d.M;
-      q.Y = dw[r] + blk;
-      q.ldy = d.h;
-      q.accumulate = accumulate ? 1 : 0;
-      TSP_LAUNCH(TSP_KERNEL_ABWD_DW, st, tsp::launch_gemm_nn_acc_small(q, st));
+                 tsp::launch_transpose_bf16(g, ld, (int)d.M, kd, gt, m_pad, st));
+      q[k].A = gt;
+      q[k].lda = m_pad;
+      q[k].B = x;
+      q[k].ldb = d.h;
+      q[k].M = kd;
+      q[k].N = d.h;
+      q[k].K = m_pad;
+      q[k].Kb_rows = (int)d.M;
+      q[k].Y = dw[r] + (size_t)(qd + k * kd) * d.h;
+      q[k].ldy = d.h;
+      q[k].accumulate = accumulate ? 1 : 0;
     }
+    TSP_LAUNCH(TSP_KERNEL_ABWD_DW, st, tsp::launch_gemm_nn_acc_small_group(q, 2, st));
   }
   return TSP_OK;
 }
