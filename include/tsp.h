@@ -243,19 +243,21 @@ tsp_status tsp_workspace_bytes(const tsp_shape* shape, int op, size_t* bytes);
  * one class and returns the summed kernel time and the number of launches. */
 enum {
   TSP_KERNEL_GATE_UP = 0, /* gate + up projections with fused SwiGLU (Algorithm 2) */
-  TSP_KERNEL_DOWN = 1,    /* down projection + fp32 shard accumulate (Algorithm 2) */
+  TSP_KERNEL_DOWN = 1,    /* down projection + fp32 shard accumulate, two ring steps per
+                             launch (Algorithm 2) */
   TSP_KERNEL_QKV = 2,     /* Q/K/V projections with K/V scatter (Algorithm 1) */
   TSP_KERNEL_ATTN = 3,    /* causal flash attention of one shard step (Algorithm 1) */
-  TSP_KERNEL_OPROJ = 4,   /* output projection + fp32 shard accumulate (Algorithm 1) */
+  TSP_KERNEL_OPROJ = 4,   /* output projection + fp32 shard accumulate, two shards per
+                             launch (Algorithm 1) */
   TSP_KERNEL_BWD_GATE = 5, /* MLP backward: G, U, dHs products with the SwiGLU backward */
-  TSP_KERNEL_BWD_DX = 6,   /* MLP backward: dX accumulate */
-  TSP_KERNEL_BWD_DW = 7,   /* MLP backward: weight-gradient products */
+  TSP_KERNEL_BWD_DX = 6,   /* MLP backward: dX accumulate (dG and dU paths, one launch) */
+  TSP_KERNEL_BWD_DW = 7,   /* MLP backward: the three weight-gradient products, one launch */
   TSP_KERNEL_ABWD_PROJ = 8,  /* attention backward: Q and dA = dY W_O products */
   TSP_KERNEL_ABWD_FWD = 9,   /* attention backward: forward recomputation with lse */
   TSP_KERNEL_ABWD_KV = 10,   /* attention backward: dK / dV (key-stationary) */
   TSP_KERNEL_ABWD_Q = 11,    /* attention backward: dQ (query-stationary) */
   TSP_KERNEL_ABWD_DX = 12,   /* attention backward: dX accumulate (both stages) */
-  TSP_KERNEL_ABWD_DW = 13,   /* attention backward: weight-gradient products */
+  TSP_KERNEL_ABWD_DW = 13,   /* attention backward: weight-gradient products, two per launch */
   TSP_KERNEL_ABWD_AUX = 14,  /* attention backward: delta / scaled-Q prep, transposes */
   TSP_KERNEL_COUNT = 15
 };
