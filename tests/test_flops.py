@@ -84,3 +84,18 @@ def test_zigzag_pairs_brute_force_and_balance():
         assert total == seq * (seq + 1) // 2
     zz = TINY.with_layout(1)
     assert F.rank_flops(zz, 0).total == F.rank_flops(zz, 1).total
+
+
+@pytest.mark.parametrize("wl", ALL, ids=lambda w: w.name)
+def test_bench_kernel_classes_sum_to_rank_flops(wl):
+    """The benchmark's per-kernel-class FLOPs over one layer call (whatever the number of
+    launches that carry them) add up to the rank's algorithmic count."""
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    if root not in sys.path:
+        sys.path.insert(0, root)
+    import bench
+    kf = bench.kernel_flops(wl)
+    rf = F.rank_flops(wl)
+    assert kf["gate_up"] + kf["down"] == pytest.approx(rf.mlp, rel=1e-12)
+    assert kf["qkv"] + kf["oproj"] + kf["attn"] == pytest.approx(rf.attn, rel=1e-12)
