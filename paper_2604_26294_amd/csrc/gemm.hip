@@ -443,7 +443,7 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParam
   gemm_tile<BM, BN, WGM, WGN, NN, EPI, STAGES>(P, xcd_work_index(blockIdx.x, tiles));
 }
 
-// Up to three independent products of one configuration in one launch: the tiles of
+// Up to kGemmGroupMax independent products of one configuration in one launch: the tiles of
 // product i follow those of the products before it, so small products that would each
 // leave CUs idle fill the chip together.
 struct GemmGroup {

@@ -81,7 +81,7 @@ hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s);
 hipError_t launch_gemm_nn_acc_small(const GemmParams& p, hipStream_t s);
 // Up to kGemmGroupMax independent products of launch_gemm_nn_acc_small's form in one
 // launch (each must have M, N > 0).
-constexpr int kGemmGroupMax = 3;
+constexpr int kGemmGroupMax = 6;
 hipError_t launch_gemm_nn_acc_small_group(const GemmParams* ps, int n, hipStream_t s);
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s);
 

@@ -136,9 +136,10 @@ AttnWs attn_ws(const Dims& d) {
 size_t ws_attn(const Dims& d) { return attn_ws(d).total; }
 // MLP backward workspace: dG, dU [M, F/D rounded up to 64] bf16 (the A operands of the
 // dX products), then dG^T, dU^T, Hs^T [F/D, M rounded up to 64] bf16 (the A operands of
-// the weight-gradient products, zero-padded past M).
+// the weight-gradient products, zero-padded past M) of two ring steps (one when D = 1):
+// the weight gradients of steps 2i and 2i + 1 run as one grouped launch.
 struct MlpBwdWs {
-  size_t dg, du, dgt, dut, hst, total;
+  size_t dg, du, dgt, dut, hst, tr_set, total;
   int m_pad;
 };
 MlpBwdWs mlp_bwd_ws(const Dims& d) {
@@ -150,7 +151,8 @@ MlpBwdWs mlp_bwd_ws(const Dims& d) {
   w.dgt = 2 * rm;
   w.dut = 2 * rm + tr;
   w.hst = 2 * rm + 2 * tr;
-  w.total = 2 * rm + 3 * tr;
+  w.tr_set = 3 * tr;  // one step's three transposes; the second step's follow
+  w.total = 2 * rm + (d.D > 1 ? 2 : 1) * 3 * tr;
   return w;
 }
 // Attention backward, first stage: Q (recomputed, then scaled in place), A, dA, dQ
@@ -355,11 +357,14 @@ tsp_status run_mlp_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
   const MlpBwdWs w = mlp_bwd_ws(d);
   uint16_t* dg = reinterpret_cast<uint16_t*>(ws + w.dg);
   uint16_t* du = reinterpret_cast<uint16_t*>(ws + w.du);
-  uint16_t* dgt = reinterpret_cast<uint16_t*>(ws + w.dgt);
-  uint16_t* dut = reinterpret_cast<uint16_t*>(ws + w.dut);
-  uint16_t* hst = reinterpret_cast<uint16_t*>(ws + w.hst);
+  GemmParams dw[kPair * 3] = {};
+  int n_dw = 0;
   for (int t = 0; t < d.D; ++t) {
     const int j = ((d.p - t) % d.D + d.D) % d.D;
+    const size_t set = (size_t)(t % kPair) * w.tr_set;
+    uint16_t* dgt = reinterpret_cast<uint16_t*>(ws + w.dgt + set);
+    uint16_t* dut = reinterpret_cast<uint16_t*>(ws + w.dut + set);
+    uint16_t* hst = reinterpret_cast<uint16_t*>(ws + w.hst + set);
     GemmParams g = {};
     g.A = x;
     g.A2 = dy;
@@ -402,22 +407,26 @@ tsp_status run_mlp_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
       TSP_LAUNCH(TSP_KERNEL_BWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
     }
     // dW (+)= (dG^T | dU^T | Hs^T) (X | X | dY): [F/D, M] x [M, h], padded rows are zero;
-    // the three products in one launch.
-    GemmParams p[3] = {};
+    // the three products of steps 2i and 2i + 1 in one launch (an odd last step alone).
     for (int k = 0; k < 3; ++k) {
-      p[k].A = k == 0 ? dgt : (k == 1 ? dut : hst);
-      p[k].lda = w.m_pad;
-      p[k].B = k < 2 ? x : dy;
-      p[k].ldb = d.h;
-      p[k].M = d.fs;
-      p[k].N = d.h;
-      p[k].K = w.m_pad;
-      p[k].Kb_rows = (int)d.M;
-      p[k].Y = k == 0 ? dwg[j] : (k == 1 ? dwu[j] : dwd[j]);
-      p[k].ldy = d.h;
-      p[k].accumulate = accumulate ? 1 : 0;
+      GemmParams& q = dw[n_dw++];
+      q = GemmParams{};
+      q.A = k == 0 ? dgt : (k == 1 ? dut : hst);
+      q.lda = w.m_pad;
+      q.B = k < 2 ? x : dy;
+      q.ldb = d.h;
+      q.M = d.fs;
+      q.N = d.h;
+      q.K = w.m_pad;
+      q.Kb_rows = (int)d.M;
+      q.Y = k == 0 ? dwg[j] : (k == 1 ? dwu[j] : dwd[j]);
+      q.ldy = d.h;
+      q.accumulate = accumulate ? 1 : 0;
     }
-    TSP_LAUNCH(TSP_KERNEL_BWD_DW, st, tsp::launch_gemm_nn_acc_small_group(p, 3, st));
+    if (t % kPair == 1 || t == d.D - 1) {
+      TSP_LAUNCH(TSP_KERNEL_BWD_DW, st, tsp::launch_gemm_nn_acc_small_group(dw, n_dw, st));
+      n_dw = 0;
+    }
   }
   return TSP_OK;
 }

@@ -12,11 +12,12 @@ from oracle import tsp_oracle as O  # noqa: E402
 from paper_2604_26294_amd import inputs as I  # noqa: E402
 from paper_2604_26294_amd.harness import RankProblem, local_rows, to_device_bf16  # noqa: E402
 from paper_2604_26294_amd.workloads import TINY  # noqa: E402
-from tests.gpu_common import MID_GQA64, MID_MHA128, SINGLE, assert_close, f64  # noqa: E402
+from tests.gpu_common import MID_GQA64, MID_MHA128, ODD3, SINGLE, assert_close, f64  # noqa: E402
 
 # Ragged tails: M = B S_loc = 384 / 640 / 320 against 128-row tiles, F/D = 344 / 1384 /
 # 1024 against 128-column tiles and the 64-wide contraction step.
-CASES = [(TINY, 1), (MID_GQA64, 3), (MID_MHA128, 0), (SINGLE, 0), (MID_GQA64.with_layout(1), 2)]
+CASES = [(TINY, 1), (MID_GQA64, 3), (MID_MHA128, 0), (SINGLE, 0), (MID_GQA64.with_layout(1), 2),
+         (ODD3, 1)]  # odd D: the weight gradients of the last ring step run alone
 _cache = {}
 
 
