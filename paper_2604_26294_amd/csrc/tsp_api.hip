@@ -155,13 +155,13 @@ MlpBwdWs mlp_bwd_ws(const Dims& d) {
   w.total = 2 * rm + (d.D > 1 ? 2 : 1) * 3 * tr;
   return w;
 }
-// Attention backward, first stage: Q (recomputed, then scaled in place), A, dA, dQ
-// [M, H_s d] bf16; lse, delta [B, H_s, S_loc] fp32; A^T and dQ^T [H_s d, M rounded up
+// Attention backward, first stage: Q (recomputed, then scaled in place), A, dA, and dQ of
+// two shard steps [M, H_s d] bf16 (the dX products of shards 2i and 2i + 1 run as one); lse, delta [B, H_s, S_loc] fp32; A^T and dQ^T [H_s d, M rounded up
 // to 64] bf16 (the A operands of the weight-gradient products, zero past M); then the
 // forward recomputation's key-range partials, as for the forward, and the dQ kernel's
 // key-range partials.
 struct AttnBwdWs {
-  size_t q, a, da, dq, lse, delta, at, dqt, po, pml, dqp, total;
+  size_t q, a, da, dq, dq2, lse, delta, at, dqt, po, pml, dqp, total;
   int m_pad, n_split, split_len, dq_split, dq_split_len;
 };
 AttnBwdWs attn_bwd_ws(const Dims& d) {
@@ -189,7 +189,8 @@ AttnBwdWs attn_bwd_ws(const Dims& d) {
   w.a = qa;
   w.da = 2 * qa;
   w.dq = 3 * qa;
-  w.lse = 4 * qa;
+  w.dq2 = 4 * qa;  // dQ of the odd shard of a pair (unused when D = 1)
+  w.lse = (d.D > 1 ? 5 : 4) * qa;
   w.delta = w.lse + f;
   w.at = w.delta + f;
   w.dqt = w.at + tr;
@@ -566,7 +567,8 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
   uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + w.q);
   uint16_t* a_ws = reinterpret_cast<uint16_t*>(ws + w.a);
   uint16_t* da_ws = reinterpret_cast<uint16_t*>(ws + w.da);
-  uint16_t* dq_ws = reinterpret_cast<uint16_t*>(ws + w.dq);
+  uint16_t* dq_buf[kPair] = {reinterpret_cast<uint16_t*>(ws + w.dq),
+                             reinterpret_cast<uint16_t*>(ws + w.dq2)};
   uint16_t* at_ws = reinterpret_cast<uint16_t*>(ws + w.at);
   uint16_t* dqt_ws = reinterpret_cast<uint16_t*>(ws + w.dqt);
   float* lse = reinterpret_cast<float*>(ws + w.lse);
@@ -574,6 +576,7 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
   for (int r = 0; r < d.D; ++r) {
     const uint16_t* wq = wa[r];
     const uint16_t* wo_t = wa[r] + (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T [H_s d, h]
+    uint16_t* dq_ws = dq_buf[r % kPair];
     GemmParams g = nt_params(d, x, wq, qd, q_ws);
     TSP_LAUNCH(TSP_KERNEL_ABWD_PROJ, st, tsp::launch_gemm_qkv(g, st));
 
@@ -636,19 +639,31 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     TSP_LAUNCH(TSP_KERNEL_ABWD_KV, st, tsp::launch_attn_bwd_dkdv(bp, st));
     TSP_LAUNCH(TSP_KERNEL_ABWD_Q, st, tsp::launch_attn_bwd_dq(bp, st));
 
-    GemmParams p = {};  // dX (+)= dQ W_Q^(r): [M, H_s d] x [H_s d, h]
-    p.A = dq_ws;
-    p.lda = qd;
-    p.B = wq;
-    p.ldb = d.h;
-    p.M = (int)d.M;
-    p.N = d.h;
-    p.K = qd;
-    p.Kb_rows = qd;
-    p.Y = dx;
-    p.ldy = d.h;
-    p.accumulate = (r > 0 || accumulate) ? 1 : 0;
-    TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+    // dX (+)= dQ W_Q^(r): [M, H_s d] x [H_s d, h], shards 2i and 2i + 1 as one product
+    // ([dQ dQ'] [W_Q; W_Q']), an odd last shard alone.
+    const bool second = r % kPair == 1;
+    if (second || r == d.D - 1) {
+      GemmParams p = {};
+      p.A = dq_buf[0];
+      p.lda = qd;
+      p.B = second ? wa[r - 1] : wq;
+      p.ldb = d.h;
+      p.M = (int)d.M;
+      p.N = d.h;
+      p.K = qd;
+      p.Kb_rows = qd;
+      if (second) {
+        p.A_hi = dq_buf[1];
+        p.B_hi = wq;
+        p.k_split = qd;
+        p.Kb_rows_hi = qd;
+        p.K = 2 * qd;
+      }
+      p.Y = dx;
+      p.ldy = d.h;
+      p.accumulate = (r >= kPair || accumulate) ? 1 : 0;
+      TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+    }
 
     TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
                tsp::launch_transpose_bf16(dq_ws, qd, (int)d.M, qd, dqt_ws, w.m_pad, st));

@@ -18,13 +18,14 @@ from oracle import tsp_oracle as O  # noqa: E402
 from paper_2604_26294_amd import inputs as I  # noqa: E402
 from paper_2604_26294_amd.harness import RankProblem, local_rows, to_device_bf16  # noqa: E402
 from paper_2604_26294_amd.workloads import TINY  # noqa: E402
-from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, SINGLE, assert_close,  # noqa: E402
-                              f64)
+from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, ODD3, SINGLE,  # noqa: E402
+                              assert_close, f64)
 
 # Ragged tails: S_loc = 128 / 192 / 640 / 256 / 320 against the 64-query stage and
 # 128-query tile; the zigzag shard's two segments of 96 rows; GQA group 2 and 8.
 CASES = [(TINY, 1), (MID_GQA64, 3), (MID_GQA64, 0), (MID_MHA128, 1), (MID_GQA8, 1),
-         (SINGLE, 0), (MID_GQA64.with_layout(1), 2), (MID_MHA128.with_layout(1), 0)]
+         (SINGLE, 0), (MID_GQA64.with_layout(1), 2), (MID_MHA128.with_layout(1), 0),
+         (ODD3, 2)]  # odd D: the dX product of the last shard runs alone
 _cache = {}
 
 
