@@ -47,12 +47,24 @@ def gen(wl: Workload):
     return I.make_x_full(wl), I.make_weights(wl)
 
 
+def stress_inputs(wl: Workload, kind: str):
+    """Seeded inputs of wl; kind "peaky" multiplies W_Q by 8 (exact in bf16), which makes
+    the softmax rows peaky (the attention stress input)."""
+    x_bits, w_bits = gen(wl)
+    if kind == "peaky":
+        w_bits = dict(w_bits)
+        w_bits["wq"] = I.round_to_bf16_bits(I.bf16_bits_to_f32(w_bits["wq"]) * np.float32(8.0))
+    return x_bits, w_bits
+
+
 def f64(bits):
     return I.bf16_bits_to_f64(bits)
 
 
-def oracle_blocks(wl: Workload, x_bits, w_bits, p, blocks=("mlp", "attn", "layer")):
-    """fp64 outputs of rank p: the MLP and attention blocks on x, and the layer."""
+def oracle_blocks(wl: Workload, x_bits, w_bits, p, blocks=("mlp", "attn", "layer"),
+                  scale=None):
+    """fp64 outputs of rank p: the MLP and attention blocks on x, and the layer
+    (``scale``: softmax scale, None = 1/sqrt(d))."""
     x = f64(x_bits)
     w = {k: f64(v) for k, v in w_bits.items()}
     D = wl.degree
@@ -72,11 +84,13 @@ def oracle_blocks(wl: Workload, x_bits, w_bits, p, blocks=("mlp", "attn", "layer
         if zz:
             kv = [O.gather_kv_zigzag(chunks, attn_sh[r], hs, ks, d) for r in range(D)]
             out["attn"] = O.attn_rank_zigzag(chunks[p], attn_sh, kv, p, wl.n_heads,
-                                             wl.n_kv_heads, d)
+                                             wl.n_kv_heads, d, scale)
         else:
             kv = [O.gather_kv(chunks, attn_sh[r], hs, ks, d) for r in range(D)]
-            out["attn"] = O.attn_rank(chunks[p], attn_sh, kv, p, wl.n_heads, wl.n_kv_heads, d)
+            out["attn"] = O.attn_rank(chunks[p], attn_sh, kv, p, wl.n_heads, wl.n_kv_heads, d,
+                                      scale)
     if "layer" in blocks:
         fn = O.layer_rank_zigzag if zz else O.layer_rank
-        out["layer"] = fn(chunks, attn_sh, w1s, w3s, w2s, p, wl.n_heads, wl.n_kv_heads, d)["y"]
+        out["layer"] = fn(chunks, attn_sh, w1s, w3s, w2s, p, wl.n_heads, wl.n_kv_heads, d,
+                          scale)["y"]
     return out

@@ -34,8 +34,20 @@ def _data(wl):
 
 
 def _rows(s_loc):
-    # both ends of the local rows and of each half (the zigzag layout's two chunks)
-    return sorted({0, 1, 127, 128, s_loc // 2 - 1, s_loc // 2, s_loc // 2 + 7, s_loc - 1})
+    """Both ends of the local rows and of each half (the zigzag layout's two chunks),
+    and one row in every 128-row block at an offset that walks through the block (so
+    every 256-query attention tile, every 128- or 256-row GEMM tile and every wavefront
+    position within them is sampled somewhere)."""
+    ends = {0, 1, 127, 128, s_loc // 2 - 1, s_loc // 2, s_loc // 2 + 7, s_loc - 1}
+    blocks = {min(128 * i + (37 * i + 5) % 128, s_loc - 1) for i in range((s_loc + 127) // 128)}
+    return sorted(ends | blocks)
+
+
+def _attention_rows(x_b, wf, wl, pos, chunk=16):
+    """O.attention_rows over the positions in chunks (bounds the oracle's memory)."""
+    return np.concatenate([O.attention_rows(x_b, wf["wq"], wf["wk"], wf["wv"], wf["wo"],
+                                            wl.n_heads, wl.n_kv_heads, pos[i:i + chunk])
+                           for i in range(0, len(pos), chunk)], axis=0)
 
 
 @pytest.mark.parametrize("wl,p", CASES, ids=[f"{w.name}-{w.layout_name}-r{p}" for w, p in CASES])
@@ -56,8 +68,7 @@ def test_sampled_rows_match_unsharded_layer(wl, p):
         pos = [p * wl.s_loc + r for r in rows]
     for b in batches:
         x_b = I.bf16_bits_to_f64(x_bits[b, :max(pos) + 1])
-        attn = O.attention_rows(x_b, wf["wq"], wf["wk"], wf["wv"], wf["wo"], wl.n_heads,
-                                wl.n_kv_heads, pos)
+        attn = _attention_rows(x_b, wf, wl, list(pos))
         xr = x_b[pos]
         mlp_x = O.mlp_full(xr, wf["w1"], wf["w3"], wf["w2"])
         u = xr + attn

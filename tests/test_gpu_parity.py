@@ -145,9 +145,10 @@ def test_deterministic_and_linear():
 @pytest.mark.parametrize("wl,p", [(MID_GQA64, 2), (MID_GQA64.with_layout(1), 3), (MID_MHA128, 1)],
                          ids=["gqa64-contiguous-r2", "gqa64-zigzag-r3", "mha128-contiguous-r1"])
 def test_back_to_back_calls_are_bit_identical(wl, p):
-    """Each call overlaps its shard steps on two streams (double-buffered workspace);
-    every reduction is ordered, so repeated calls enqueued back to back, with the
-    entry points interleaved, must reproduce the first result bit for bit."""
+    """Calls enqueued back to back on one stream, with the three forward entry points
+    interleaved and sharing one workspace, reproduce the first result of each entry
+    point bit for bit (every reduction has a fixed order and nothing depends on what an
+    earlier call left in the workspace)."""
     print(f"[overlap] {wl.name} {wl.layout_name} rank {p}", flush=True)
     prob = RankProblem(wl, *_inputs(wl), p)
     prob.prefill_kv()

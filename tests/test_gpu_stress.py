@@ -1,0 +1,106 @@
+"""GPU parity under the attention stress inputs, element by element against the fp64
+oracle at the same tolerance as every other parity test, through the C ABI.
+
+* Peaky logits: W_Q scaled by 8 (exact in bf16).  The logits' spread grows eightfold
+  (a standard deviation of about 10 in log2 units at these shapes), so each softmax
+  row is dominated by a few keys and the running maximum of a row grows by many units
+  as later key tiles arrive: the online softmax has to move its reference repeatedly
+  (Algorithm 1's CausalAttn computed one key tile at a time).
+* An explicit softmax scale (tsp_shape.softmax_scale = 0.2 instead of 1/sqrt(d)), on
+  the forward and on the attention backward.
+
+The cases include a shape whose attention is split over key ranges (the partial
+results merged by the combine kernel), the zigzag layout's two query segments, GQA
+with g = 8 and head_dim 64.  W_Q x 8 together with scale 0.2 is not a case: at that
+logit spread (18 times the default) the bf16 rounding of Q and K alone, which both
+paths' inputs to the score products carry on the GPU, moves the output by more than
+the tolerance whatever the kernel does.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from oracle import tsp_oracle as O  # noqa: E402
+from paper_2604_26294_amd import inputs as I  # noqa: E402
+from paper_2604_26294_amd.harness import RankProblem, local_rows, to_device_bf16  # noqa: E402
+from paper_2604_26294_amd.workloads import TINY  # noqa: E402
+from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, assert_close, f64,  # noqa: E402
+                              oracle_blocks, stress_inputs)
+
+# MID_MHA128 rank 1 (contiguous) and rank 0 (zigzag) split their keys into 3 ranges.
+CASES = [(TINY, 1), (MID_MHA128, 1), (MID_MHA128.with_layout(1), 0), (MID_GQA64, 3),
+         (MID_GQA8, 1)]
+_IDS = [f"{w.name}-{w.layout_name}-r{p}" for w, p in CASES]
+SCALE = 0.2
+_cache = {}
+
+
+def _inputs(wl, kind):
+    key = (wl.name, kind)
+    if key not in _cache:
+        _cache[key] = stress_inputs(wl, kind)
+    return _cache[key]
+
+
+def _scale(kind):
+    return SCALE if kind == "scale" else None
+
+
+@pytest.mark.parametrize("wl,p", CASES, ids=_IDS)
+@pytest.mark.parametrize("kind", ["peaky", "scale"])
+def test_attention_and_layer_forward(wl, p, kind):
+    print(f"[stress fwd] {wl.name} {wl.layout_name} rank {p} {kind}", flush=True)
+    x_bits, w_bits = _inputs(wl, kind)
+    sc = _scale(kind)
+    prob = RankProblem(wl, x_bits, w_bits, p, softmax_scale=sc or 0.0)
+    prob.prefill_kv()
+    y_attn = prob.attn_fwd().double().cpu().numpy()
+    y_layer = prob.layer().double().cpu().numpy()
+    ref = oracle_blocks(wl, x_bits, w_bits, p, blocks=("attn", "layer"), scale=sc)
+    mr, cos = assert_close(y_attn, ref["attn"], f"{wl.name} r{p} {kind} attn")
+    print(f"  attn max_rel={mr:.3e} cos={cos:.6f}", flush=True)
+    assert_close(y_layer, ref["layer"], f"{wl.name} r{p} {kind} layer")
+
+
+BWD_CASES = [(TINY, 1, "peaky"), (MID_MHA128, 1, "peaky"), (MID_GQA64, 3, "scale"),
+             (MID_MHA128, 1, "scale"), (MID_GQA64.with_layout(1), 2, "scale")]
+
+
+@pytest.mark.parametrize("wl,p,kind", BWD_CASES,
+                         ids=[f"{w.name}-{w.layout_name}-r{p}-{k}" for w, p, k in BWD_CASES])
+def test_attention_backward_first_stage(wl, p, kind):
+    print(f"[stress bwd] {wl.name} {wl.layout_name} rank {p} {kind}", flush=True)
+    x_bits, w_bits = _inputs(wl, kind)
+    dy_bits = I.make_dy_full(wl)
+    sc = _scale(kind)
+    prob = RankProblem(wl, x_bits, w_bits, p, softmax_scale=sc or 0.0)
+    prob.prefill_kv(include_self=True)
+    dx, dw, dk, dv = prob.attn_bwd(to_device_bf16(local_rows(dy_bits, wl, p)))
+    torch.cuda.synchronize()
+    D = wl.degree
+    w = {k: f64(v) for k, v in w_bits.items()}
+    shards = [I.attn_shard_packed(w, r, D, wl.n_heads, wl.n_kv_heads, wl.head_dim)
+              for r in range(D)]
+    xs = [f64(local_rows(x_bits, wl, q)) for q in range(D)]
+    gather = O.gather_kv_zigzag if wl.layout == 1 else O.gather_kv
+    kv = [gather(xs, shards[r], wl.n_heads // D, wl.n_kv_heads // D, wl.head_dim)
+          for r in range(D)]
+    ref = O.attn_rank_bwd(xs[p], shards, kv, p, wl.n_heads, wl.n_kv_heads, wl.head_dim,
+                          f64(local_rows(dy_bits, wl, p)), scale=sc,
+                          layout="zigzag" if wl.layout == 1 else "contiguous")
+    qd = wl.n_heads // D * wl.head_dim
+    kd = wl.n_kv_heads // D * wl.head_dim
+    ks = wl.n_kv_heads // D
+    mr, cos = assert_close(dx.double().cpu().numpy(), ref["dx"], f"{wl.name} r{p} {kind} dX")
+    print(f"  dX max_rel={mr:.3e} cos={cos:.6f}", flush=True)
+    dk_all, dv_all = dk.double().cpu().numpy(), dv.double().cpu().numpy()
+    for r in range(D):
+        g = dw[r].double().cpu().numpy()
+        assert_close(g[:qd], ref["dwq"][r], f"{wl.name} r{p} {kind} dW_Q[{r}]")
+        assert_close(g[qd + 2 * kd:], ref["dwo_t"][r], f"{wl.name} r{p} {kind} dW_O^T[{r}]")
+        cols = slice(r * ks, (r + 1) * ks)
+        assert_close(dk_all[:, :, cols], ref["dk"][r], f"{wl.name} r{p} {kind} dK-hat[{r}]")
+        assert_close(dv_all[:, :, cols], ref["dv"][r], f"{wl.name} r{p} {kind} dV-hat[{r}]")
