@@ -145,22 +145,21 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   const int j0 = k_begin / kStepKeys;
   const int n_steps = k_end > k_begin ? (k_end - k_begin + kStepKeys - 1) / kStepKeys : 0;
 
-  // Q fragments (the B operand of S^T): lane holds Q[qloc][16 ks + 8 hh .. +7], scaled
-  // by c = softmax scale * log2(e) and rounded to bf16 once, so that the score MFMAs
-  // produce base-2 logits directly.
+  // Q fragments (the B operand of S^T): lane holds Q[qloc][16 ks + 8 hh .. +7].  Q
+  // arrives multiplied by softmax scale * log2(e) (and rounded once), so the score
+  // MFMAs produce base-2 logits directly.
   u32x4 qf[C::KS];
   {
-    const float c = P.scale_log2;
     const uint16_t* qrow =
         P.Q + (((size_t)b * P.s_loc + row0 + (qvalid ? qloc : 0)) * P.heads + head) * D;
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) {
-      const u32x4 raw = qvalid ? ld16(qrow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
+    for (int s = 0; s < C::KS; ++s)
+      qf[s] = qvalid ? ld16(qrow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
+    // Take the loads' wait here, before any tile load is issued: left to the compiler,
+    // the wait lands inside the key loop (ahead of the first score MFMA of every step),
+    // where vmcnt(0) would also wait for the next tile's loads.
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        qf[s][e] = pack_bf16x2(bf16_bits_to_f32(raw[e] & 0xffffu) * c,
-                               bf16_bits_to_f32(raw[e] >> 16) * c);
-    }
+    for (int s = 0; s < C::KS; ++s) asm volatile("" : "+v"(qf[s]));
   }
   const size_t kv_stride = (size_t)P.n_kv * D;  // elements between consecutive keys
   const uint16_t* kbase = P.Kb + (size_t)b * P.seq * kv_stride + (size_t)kvh * D;

@@ -14,10 +14,10 @@
 // streams the keys: dQ accumulates in registers).  Both recompute the scores; only
 // the query-stationary one needs dP's row sums, which delta already holds.
 //
-// The logits are formed exactly as the forward formed them: Q scaled by
-// scale * log2(e) and rounded to bf16 (Qs), so that P = 2^(Qs K^T - lse) reproduces
-// the forward's probabilities.  Since scale Q = Qs / log2(e) up to that rounding,
-// dK = ln(2) dS^T Qs.
+// The logits are formed exactly as the forward formed them, from the queries scaled by
+// scale * log2(e) and rounded to bf16 once (Qs, written so by the projection), so that
+// P = 2^(Qs K^T - lse) reproduces the forward's probabilities.  Since scale Q =
+// Qs / log2(e) up to that rounding, dK = ln(2) dS^T Qs.
 //
 // MFMA layouts (32 x 32 x 16).  Key-stationary: S = Qs K^T and dP = dO V^T with the
 // queries as rows (A operands read from LDS row by row, K and V fragments as B from
@@ -111,8 +111,8 @@ __device__ __forceinline__ int tr_row(int lane) { return (((lane >> 4) >> 1) << 
 __device__ __forceinline__ int tr_col(int lane) { return 16 * ((lane >> 4) & 1) + 4 * (lane & 3); }
 
 // ---------------------------------------------------------------------------------
-// delta = rowsum(dO * O) per (query, head) and Qs = bf16(c Q).  A group of D / 8
-// lanes handles one (row, head): 8 elements per lane, reduced across the group.
+// delta = rowsum(dO * O) per (query, head).  A group of D / 8 lanes handles one
+// (row, head): 8 elements per lane, reduced across the group.
 template <int D>
 __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const AttnBwdParams P) {
   constexpr int G = D / 8;
@@ -124,16 +124,12 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const AttnBwdParams 
   const size_t e0 = (size_t)(valid ? rh : 0) * D + 8 * part;
   float acc = 0.f;
   if (valid) {
-    const u32x4 o = ld16(P.O + e0), g = ld16(P.dO + e0), q = ld16(P.Qin + e0);
-    u32x4 qs;
+    const u32x4 o = ld16(P.O + e0), g = ld16(P.dO + e0);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       acc += bf16_bits_to_f32(o[e] & 0xffffu) * bf16_bits_to_f32(g[e] & 0xffffu);
       acc += bf16_bits_to_f32(o[e] >> 16) * bf16_bits_to_f32(g[e] >> 16);
-      qs[e] = pack_bf16x2(bf16_bits_to_f32(q[e] & 0xffffu) * P.scale_log2,
-                          bf16_bits_to_f32(q[e] >> 16) * P.scale_log2);
     }
-    st16(P.Qs + e0, qs);
   }
 #pragma unroll
   for (int m = 1; m < G; m <<= 1) acc += __shfl_xor(acc, m);

@@ -6,8 +6,9 @@
 //                   [A A'] and [B; B'], two operand pairs held in separate buffers)
 //   SwiGLU backward G = X W1^T, U = X W3^T, dHs = dY W2^T in one pass; dG, dU and the
 //                   transposes of dG, dU, Hs for the weight-gradient products
-//   Q/K/V proj      Q = X W_Q^T -> workspace, K, V -> full-sequence buffers at the
-//                   rows' sequence positions (zigzag reorder folded in)  Algorithm 1
+//   Q/K/V proj      Q = X W_Q^T (times a factor, then rounded) -> workspace, K, V ->
+//                   full-sequence buffers at the rows' sequence positions (zigzag
+//                   reorder folded in)  Algorithm 1
 //
 // One workgroup = WGM x WGN wavefronts (8 by default: two per SIMD); each wavefront owns
 // a (BM/WGM) x (BN/WGN) block of C as 32 x 32 MFMA tiles.  K advances in steps of 64.
@@ -417,8 +418,10 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
           *reinterpret_cast<u32x2*>(P.H + (size_t)mm[q] * P.ldh + nn[q]) = bits;
         } else {
           if (!ok[q]) continue;
-          const u32x2 bits{pack_bf16x2(v[q][0], v[q][1]), pack_bf16x2(v[q][2], v[q][3])};
           const int n = nn[q], m = mm[q];
+          const float f = n < P.nq ? P.q_scale : 1.f;  // the Q block is scaled, then rounded
+          const u32x2 bits{pack_bf16x2(f * v[q][0], f * v[q][1]),
+                           pack_bf16x2(f * v[q][2], f * v[q][3])};
           uint16_t* dst;
           if (n < P.nq) {
             dst = P.Q + (size_t)m * P.ldq + n;

@@ -54,13 +54,15 @@ struct GemmParams {
   uint16_t* U;
   int ldu;
 
-  // Q/K/V epilogue: columns [0, nq) -> Q[m, n]; [nq, nq+nkv) -> K buffer;
+  // Q/K/V epilogue: columns [0, nq) -> Q[m, n] = bf16(q_scale C[m, n]) (the factor
+  // applied to the fp32 product, so Q is rounded once); [nq, nq+nkv) -> K buffer;
   // [nq+nkv, nq+2nkv) -> V buffer.  Row m = b*rows_per_batch + t lands at sequence
   // position kv_pos0 + t of batch b if t < kv_seg, else at kv_pos1 + (t - kv_seg)
   // (the zigzag layout's second chunk); column c of the K (or V) block lands at
   // element kv_col0 + c of that position's row.
   uint16_t* Q;
   int ldq;
+  float q_scale;
   uint16_t* Kb;
   uint16_t* Vb;
   int nq, nkv;
@@ -86,7 +88,9 @@ hipError_t launch_gemm_nn_acc_small_group(const GemmParams* ps, int n, hipStream
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s);
 
 // Causal flash attention of one rank's queries for the heads of one shard.
-//   Q [B, S_loc, H_s, d] bf16;  K/V buffers [B, S, n_kv, d] bf16 (heads
+//   Q [B, S_loc, H_s, d] bf16, the queries times softmax scale * log2(e) (rounded to
+//   bf16 once, by the projection's epilogue), so that Q K^T are base-2 logits;
+//   K/V buffers [B, S, n_kv, d] bf16 (heads
 //   kv_head0 .. kv_head0 + H_s/g - 1 are this shard's);  O [B, S_loc, H_s, d] bf16.
 //   The local rows form n_seg segments of consecutive global positions: rows
 //   [seg_row0[k], seg_row0[k] + seg_rows[k]) sit at positions seg_pos0[k] + (row -
@@ -110,7 +114,6 @@ struct AttnParams {
   int seg_rows[2];
   int seg_pos0[2];
   int kv_len;       // number of readable keys: the last segment position + 1
-  float scale_log2; // softmax scale * log2(e)
   // Key-range split (attn_split_count): each query tile's keys [0, n) are processed in
   // ranges [c split_len, (c + 1) split_len), c < n_split.  With n_split > 1 the ranges
   // write partial results -- part_o [n_split][part_rows][d] fp32 (unnormalised O) and
@@ -121,8 +124,8 @@ struct AttnParams {
   long long part_rows;
   float* part_o;
   float* part_ml;
-  // Optional: the log-sum-exp of each query's base-2 logits (scores times scale_log2,
-  // with Q rounded to bf16 after scaling, as the kernel computes them), fp32
+  // Optional: the log-sum-exp of each query's base-2 logits (the products of the
+  // scaled bf16 queries with the keys, as the kernel computes them), fp32
   // [B, H_s, S_loc]; written when non-null.
   float* lse;
 };
@@ -139,17 +142,18 @@ int attn_split_count(const AttnParams& p, int* split_len);
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s);
 
 // Backward of launch_flash_attn for one shard's heads (same segments and buffers).
-//   Qin  [B, S_loc, H_s, d] bf16   the recomputed queries;
+//   Qs   [B, S_loc, H_s, d] bf16   the recomputed queries, scaled as for the forward
+//                                  (bf16(softmax scale * log2(e) * q));
 //   O    [B, S_loc, H_s, d] bf16   the recomputed attention output;
 //   dO   [B, S_loc, H_s, d] bf16   its upstream gradient;
 //   lse  [B, H_s, S_loc] fp32      base-2 log-sum-exp from the forward (AttnParams::lse).
-// Writes Qs = bf16(scale_log2 Qin) (may alias Qin), delta = rowsum(dO * O) [B, H_s, S_loc],
-// dQ [B, S_loc, H_s, d] bf16, and the contributions to the gradients of the gathered
+// Writes delta = rowsum(dO * O) [B, H_s, S_loc],
+// dQ [B, S_loc, H_s, d] bf16 (the gradient of the unscaled queries), and the
+// contributions to the gradients of the gathered
 // K / V: dK, dV [B, S, n_kv, d] fp32, columns of kv heads kv_head0 .. + H_s/g - 1, every
 // one of the S rows (overwritten, or added to if accumulate).
 struct AttnBwdParams {
-  const uint16_t* Qin;
-  uint16_t* Qs;
+  const uint16_t* Qs;
   const uint16_t* O;
   const uint16_t* dO;
   const uint16_t* Kb;
@@ -172,7 +176,6 @@ struct AttnBwdParams {
   int seg_row0[2];
   int seg_rows[2];
   int seg_pos0[2];
-  float scale_log2;  // softmax scale * log2(e)
   float scale;       // softmax scale
   // dQ key-range split (attn_bwd_dq_split): with dq_split > 1 each query tile's keys
   // [c dq_split_len, (c + 1) dq_split_len) write fp32 partials dq_part
@@ -186,7 +189,7 @@ struct AttnBwdParams {
 // stage, in *split_len); depends on the shape only.
 int attn_bwd_dq_split(const AttnBwdParams& p, int* split_len);
 
-// The three kernels of the backward, in this order: delta and Qs; dK / dV; dQ.
+// The three kernels of the backward, in this order: delta; dK / dV; dQ.
 hipError_t launch_attn_bwd_prep(const AttnBwdParams& p, hipStream_t s);
 hipError_t launch_attn_bwd_dkdv(const AttnBwdParams& p, hipStream_t s);
 hipError_t launch_attn_bwd_dq(const AttnBwdParams& p, hipStream_t s);

@@ -432,6 +432,8 @@ tsp_status run_mlp_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
   return TSP_OK;
 }
 
+constexpr float kLog2e = 1.4426950408889634f;
+
 GemmParams qkv_params(const Dims& d, const uint16_t* x, const uint16_t* shard, int r,
                       uint16_t* q_ws, uint16_t* kb, uint16_t* vb, bool with_q) {
   GemmParams g = {};
@@ -445,6 +447,7 @@ GemmParams qkv_params(const Dims& d, const uint16_t* x, const uint16_t* shard, i
   g.K = d.h;
   g.Q = q_ws;
   g.ldq = qd;
+  g.q_scale = d.scale * kLog2e;  // the attention kernels take base-2-logit queries
   g.Kb = kb;
   g.Vb = vb;
   g.nq = with_q ? qd : 0;
@@ -471,7 +474,6 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
                     uint16_t* kb, uint16_t* vb, float* y, int accumulate,
                     const uint16_t* residual, uint16_t* u_out, char* ws, hipStream_t st) {
   const int qd = d.hs * d.d, kd = d.ks * d.d;
-  const float log2e = 1.4426950408889634f;
   const AttnWs aw = attn_ws(d);
   uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + aw.q);
   // A of shard r in buffer r mod 2; the output projections of shards 2i and 2i + 1 run
@@ -494,7 +496,6 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     ap.seq = d.S;
     ap.n_kv = d.nkv;
     ap.kv_head0 = r * d.ks;
-    ap.scale_log2 = d.scale * log2e;
     ap.n_split = aw.n_split;
     ap.split_len = aw.split_len;
     ap.part_rows = (long long)d.M * d.hs;
@@ -538,10 +539,12 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
   return TSP_OK;
 }
 
-// C[M, n] = A[M, h] B[n, h]^T, bf16 out (the Q epilogue of the projection kernel with
+// C[M, n] = f A[M, h] B[n, h]^T, bf16 out (the Q epilogue of the projection kernel with
 // every column in the Q block).
-GemmParams nt_params(const Dims& d, const uint16_t* a, const uint16_t* b, int n, uint16_t* out) {
+GemmParams nt_params(const Dims& d, const uint16_t* a, const uint16_t* b, int n, uint16_t* out,
+                     float f) {
   GemmParams g = {};
+  g.q_scale = f;
   g.A = a;
   g.lda = d.h;
   g.B = b;
@@ -562,7 +565,6 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
                         float* dx, int accumulate, float* const* dw, float* dk, float* dv,
                         char* ws, hipStream_t st) {
   const int qd = d.hs * d.d, kd = d.ks * d.d;
-  const float log2e = 1.4426950408889634f;
   const AttnBwdWs w = attn_bwd_ws(d);
   uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + w.q);
   uint16_t* a_ws = reinterpret_cast<uint16_t*>(ws + w.a);
@@ -577,7 +579,8 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     const uint16_t* wq = wa[r];
     const uint16_t* wo_t = wa[r] + (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T [H_s d, h]
     uint16_t* dq_ws = dq_buf[r % kPair];
-    GemmParams g = nt_params(d, x, wq, qd, q_ws);
+    // Q times scale * log2(e), as the attention kernels take it
+    GemmParams g = nt_params(d, x, wq, qd, q_ws, d.scale * kLog2e);
     TSP_LAUNCH(TSP_KERNEL_ABWD_PROJ, st, tsp::launch_gemm_qkv(g, st));
 
     AttnParams ap = {};
@@ -591,7 +594,6 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     ap.seq = d.S;
     ap.n_kv = d.nkv;
     ap.kv_head0 = r * d.ks;
-    ap.scale_log2 = d.scale * log2e;
     ap.n_split = w.n_split;
     ap.split_len = w.split_len;
     ap.part_rows = (long long)d.M * d.hs;
@@ -600,11 +602,10 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     ap.lse = lse;
     TSP_LAUNCH(TSP_KERNEL_ABWD_FWD, st, tsp::launch_flash_attn(ap, st));
 
-    g = nt_params(d, dy, wo_t, qd, da_ws);  // dA = dY W_O^(r)
+    g = nt_params(d, dy, wo_t, qd, da_ws, 1.f);  // dA = dY W_O^(r)
     TSP_LAUNCH(TSP_KERNEL_ABWD_PROJ, st, tsp::launch_gemm_qkv(g, st));
 
     AttnBwdParams bp = {};
-    bp.Qin = q_ws;
     bp.Qs = q_ws;
     bp.O = a_ws;
     bp.dO = da_ws;
@@ -630,7 +631,6 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
       bp.seg_rows[k] = ap.seg_rows[k];
       bp.seg_pos0[k] = ap.seg_pos0[k];
     }
-    bp.scale_log2 = ap.scale_log2;
     bp.scale = d.scale;
     bp.dq_split = w.dq_split;
     bp.dq_split_len = w.dq_split_len;
