@@ -36,8 +36,10 @@
  *   - Every device pointer must be 16-byte aligned.
  *   - The caller owns every buffer.  The library never allocates or frees device
  *     memory and keeps no state between calls (apart from the opt-in kernel timing
- *     records of tsp_profile_enable and the per-thread code of the last HIP failure);
- *     scratch space is the caller's workspace, sized by tsp_workspace_bytes.
+ *     records of tsp_profile_enable, the per-thread code of the last HIP failure and
+ *     the fixed scratch array of tsp_layer_rank_fwd_noalloc); scratch space is the
+ *     caller's workspace, sized by tsp_workspace_bytes (tsp_layer_rank_fwd_noalloc
+ *     excepted).
  *   - Calls only enqueue work on `stream` (NULL = the default stream) and never
  *     synchronise.  Calls on different streams must use different workspaces and
  *     must not write the same outputs.
@@ -223,6 +225,32 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                               const uint16_t* const* w_up, const uint16_t* const* w_down,
                               uint16_t* k_buf, uint16_t* v_buf, float* y_loc, void* ws,
                               size_t ws_bytes, hipStream_t stream);
+
+/* Scratch size available to tsp_layer_rank_fwd_noalloc on each device (64 MiB). */
+#define TSP_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* tsp_layer_rank_fwd for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  Same arguments
+ * and results, minus the workspace: the scratch space comes from a fixed array of
+ * TSP_NOALLOC_SCRATCH_BYTES per device, part of the library's device code (resident on
+ * every device the library has run on, until the process ends), used on the calling
+ * thread's current HIP device, which must be the device of `stream`.  The call neither
+ * allocates nor frees anything.
+ *   - A shape whose layer workspace (tsp_workspace_bytes(shape, TSP_OP_LAYER)) exceeds
+ *     TSP_NOALLOC_SCRATCH_BYTES returns TSP_ERR_WORKSPACE before anything is enqueued
+ *     (the 7B-class layer at S = 8192, D = 8 needs 27 MiB and fits; at S = 65536 it
+ *     needs 121 MiB and does not).
+ *   - All calls on one device share its array: calls that can overlap in time on one
+ *     device (different streams, or different host threads without ordering) race on
+ *     it and must not be made; calls ordered on one stream are fine.
+ *   - The array keeps whatever the last call left; no call needs it cleared.
+ *   - The first call on a device looks up the array's device address (no kernel). */
+tsp_status tsp_layer_rank_fwd_noalloc(const tsp_shape* shape, const uint16_t* x_loc,
+                                      const uint16_t* const* w_attn,
+                                      const uint16_t* const* w_gate,
+                                      const uint16_t* const* w_up,
+                                      const uint16_t* const* w_down, uint16_t* k_buf,
+                                      uint16_t* v_buf, float* y_loc, hipStream_t stream);
 
 enum {
   TSP_OP_MLP = 0,

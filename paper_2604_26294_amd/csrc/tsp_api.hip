@@ -743,6 +743,70 @@ tsp_status run_attn_kv_bwd(const Dims& d, const uint16_t* x, const uint16_t* con
   return TSP_OK;
 }
 
+// ------------------------------------------------------------ allocation-free layer call
+// Scratch space of tsp_layer_rank_fwd_noalloc: one fixed array per GPU, part of this
+// file's device code object (the runtime places it in each device's memory when the
+// code object is loaded there, and it stays until the process ends).  In host code the
+// name `scratch` is only a stand-in; its device address comes from hipGetSymbolAddress,
+// taken once per device with that device current, and only that address is used.
+//
+// Nothing in it needs clearing: every kernel writes each scratch element it later reads
+// in the same call (Q, A, the gated product including its zero padding, bf16(u), and
+// the attention key-range partials, which every (range, query tile) workgroup writes
+// even when none of its keys is visible).
+static __device__ __align__(256) char scratch[TSP_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array.
+tsp_status scratch_of_current_device(void** out) {
+  int dev = 0;
+  TSP_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return TSP_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    TSP_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) return TSP_ERR_HIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return TSP_OK;
+}
+
+tsp_status check_layer_args(const tsp_shape* shape, const uint16_t* x_loc,
+                            const uint16_t* const* w_attn, const uint16_t* const* w_gate,
+                            const uint16_t* const* w_up, const uint16_t* const* w_down,
+                            uint16_t* k_buf, uint16_t* v_buf, float* y_loc, Dims* d) {
+  TSP_TRY(check_shape(shape, d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_shards(w_attn, d->D));
+  TSP_TRY(check_shards(w_gate, d->D));
+  TSP_TRY(check_shards(w_up, d->D));
+  TSP_TRY(check_shards(w_down, d->D));
+  TSP_TRY(check_ptr(k_buf));
+  TSP_TRY(check_ptr(v_buf));
+  TSP_TRY(check_ptr(y_loc));
+  return TSP_OK;
+}
+
+// The layer on a validated problem, with scratch space `ws` (at least ws_layer(d) bytes).
+tsp_status run_layer(const Dims& d, const uint16_t* x_loc, const uint16_t* const* w_attn,
+                     const uint16_t* const* w_gate, const uint16_t* const* w_up,
+                     const uint16_t* const* w_down, uint16_t* k_buf, uint16_t* v_buf,
+                     float* y_loc, char* ws, hipStream_t stream) {
+  uint16_t* u_ws = reinterpret_cast<uint16_t*>(ws);
+  char* rest = ws + align_up((size_t)d.M * d.h * 2);
+  // u = x + Attn(x): Y starts from x at the first output projection; the last one also
+  // writes bf16(u).
+  TSP_TRY(run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, 0, x_loc, u_ws, rest, stream));
+  // y = u + MLP(bf16 u): the MLP accumulates onto Y, which holds u.
+  return run_mlp(d, u_ws, w_gate, w_up, w_down, y_loc, 1, reinterpret_cast<uint16_t*>(rest),
+                 stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -888,27 +952,28 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                               uint16_t* k_buf, uint16_t* v_buf, float* y_loc, void* ws,
                               size_t ws_bytes, hipStream_t stream) {
   Dims d;
-  TSP_TRY(check_shape(shape, &d));
-  TSP_TRY(check_ptr(x_loc));
-  TSP_TRY(check_shards(w_attn, d.D));
-  TSP_TRY(check_shards(w_gate, d.D));
-  TSP_TRY(check_shards(w_up, d.D));
-  TSP_TRY(check_shards(w_down, d.D));
-  TSP_TRY(check_ptr(k_buf));
-  TSP_TRY(check_ptr(v_buf));
-  TSP_TRY(check_ptr(y_loc));
+  TSP_TRY(check_layer_args(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf, y_loc, &d));
   TSP_TRY(check_ptr(ws));
   if (ws_bytes < ws_layer(d)) return TSP_ERR_WORKSPACE;
   if (d.M == 0) return TSP_OK;
-  char* base = static_cast<char*>(ws);
-  uint16_t* u_ws = reinterpret_cast<uint16_t*>(base);
-  char* rest = base + align_up((size_t)d.M * d.h * 2);
-  // u = x + Attn(x): Y starts from x at the first output projection; the last one also
-  // writes bf16(u).
-  TSP_TRY(run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, 0, x_loc, u_ws, rest, stream));
-  // y = u + MLP(bf16 u): the MLP accumulates onto Y, which holds u.
-  return run_mlp(d, u_ws, w_gate, w_up, w_down, y_loc, 1, reinterpret_cast<uint16_t*>(rest),
-                 stream);
+  return run_layer(d, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf, y_loc,
+                   static_cast<char*>(ws), stream);
+}
+
+tsp_status tsp_layer_rank_fwd_noalloc(const tsp_shape* shape, const uint16_t* x_loc,
+                                      const uint16_t* const* w_attn,
+                                      const uint16_t* const* w_gate,
+                                      const uint16_t* const* w_up,
+                                      const uint16_t* const* w_down, uint16_t* k_buf,
+                                      uint16_t* v_buf, float* y_loc, hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_layer_args(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf, y_loc, &d));
+  if (ws_layer(d) > (size_t)TSP_NOALLOC_SCRATCH_BYTES) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  void* ws = nullptr;
+  TSP_TRY(scratch_of_current_device(&ws));
+  return run_layer(d, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf, y_loc,
+                   static_cast<char*>(ws), stream);
 }
 
 tsp_status tsp_profile_enable(int enable) {

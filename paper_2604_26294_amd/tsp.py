@@ -66,6 +66,7 @@ def _load() -> ctypes.CDLL:
         "tsp_attn_kv_rank_bwd": [SH, P, PP, P, P, P, I, PP, VP, SZ, VP],
         "tsp_attn_rank_fwd": [SH, P, PP, P, P, P, I, VP, SZ, VP],
         "tsp_layer_rank_fwd": [SH, P, PP, PP, PP, PP, P, P, P, VP, SZ, VP],
+        "tsp_layer_rank_fwd_noalloc": [SH, P, PP, PP, PP, PP, P, P, P, VP],
         "tsp_workspace_bytes": [SH, I, ctypes.POINTER(ctypes.c_size_t)],
         "tsp_status_str": [I],
         "tsp_abi_version": [],
@@ -198,6 +199,20 @@ def tsp_layer_rank_fwd(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf,
     _check(lib.tsp_layer_rank_fwd(ctypes.byref(shape), _ptr(x_loc), a, g, u, d, _ptr(k_buf),
                                   _ptr(v_buf), _ptr(y_loc), _ptr(ws), _nbytes(ws),
                                   _stream(stream)), "tsp_layer_rank_fwd")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TSP_NOALLOC_SCRATCH_BYTES
+
+
+def tsp_layer_rank_fwd_noalloc(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf, y_loc,
+                               stream=None):
+    a, _a = _ptrs(w_attn)
+    g, _g = _ptrs(w_gate)
+    u, _u = _ptrs(w_up)
+    d, _d = _ptrs(w_down)
+    _check(lib.tsp_layer_rank_fwd_noalloc(ctypes.byref(shape), _ptr(x_loc), a, g, u, d,
+                                          _ptr(k_buf), _ptr(v_buf), _ptr(y_loc),
+                                          _stream(stream)), "tsp_layer_rank_fwd_noalloc")
 
 
 def tsp_profile_enable(enable: bool = True):

@@ -12,7 +12,7 @@ import re
 import pytest
 
 from paper_2604_26294_amd import tsp as T
-from paper_2604_26294_amd.workloads import ALL, TINY
+from paper_2604_26294_amd.workloads import ALL, BY_NAME, TINY
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "tsp.h")
 FAKE = 0x7F0000000000  # 16-byte aligned stand-in for a device address
@@ -215,3 +215,35 @@ def test_one_hip_runtime_whatever_the_import_order():
                          cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
     assert out.returncode == 0, out.stderr
     assert out.stdout.split()[0] == "1", out.stdout
+
+
+def test_noalloc_layer_validates_before_touching_the_gpu():
+    """tsp_layer_rank_fwd_noalloc rejects bad arguments, and shapes whose layer
+    workspace exceeds its fixed scratch array, before any HIP call; the Python constant
+    matches the header's."""
+    src = open(HEADER).read()
+    m = re.search(r"#define TSP_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", src)
+    assert m and int(m.group(1)) << int(m.group(2)) == T.NOALLOC_SCRATCH_BYTES
+    L = T.lib
+    good, _k1 = _arr(2)
+    nul, _k2 = _arr(2, 0)
+    sh = _shape()
+    args = [ctypes.byref(sh), FAKE, good, good, good, good, FAKE, FAKE, FAKE, None]
+    for pos, val, code in [(0, None, 1), (1, None, 1), (2, nul, 1), (5, None, 1),
+                           (6, FAKE + 2, 4), (8, None, 1)]:
+        a = list(args)
+        a[pos] = val
+        assert L.tsp_layer_rank_fwd_noalloc(*a) == code, (pos, code)
+    a = list(args)
+    a[0] = ctypes.byref(_shape(rank=4))
+    assert L.tsp_layer_rank_fwd_noalloc(*a) == 3
+    big = T.shape_of(BY_NAME["7b-h4096-S65536-D8"])
+    assert T.workspace_bytes(big, T.OP_LAYER) > T.NOALLOC_SCRATCH_BYTES
+    g8, _k3 = _arr(8)
+    assert L.tsp_layer_rank_fwd_noalloc(ctypes.byref(big), FAKE, g8, g8, g8, g8, FAKE, FAKE,
+                                        FAKE, None) == 5
+    empty = _shape(batch=0)
+    assert L.tsp_layer_rank_fwd_noalloc(ctypes.byref(empty), FAKE, good, good, good, good, FAKE,
+                                        FAKE, FAKE, None) == 0
+    fits = T.shape_of(BY_NAME["7b-h4096-S8192-D8"])
+    assert T.workspace_bytes(fits, T.OP_LAYER) <= T.NOALLOC_SCRATCH_BYTES
