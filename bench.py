@@ -2,11 +2,14 @@
 """Throughput of one rank's TSP layer forward (attention + gated MLP) on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--rank P]
-                    [--layout contiguous|zigzag] [--no-cpu-baseline] [--rank-sweep]
+                    [--layout contiguous|zigzag] [--group-steps G] [--no-cpu-baseline]
+                    [--rank-sweep]
 
 A step is one ``tsp_layer_rank_fwd`` call: all D attention shard steps (Q/K/V
 projection, causal flash attention, output projection) and all D ring MLP steps
-(gate+up with SwiGLU, down projection) for the rank's S/D tokens.  Inputs, weight
+(gate+up with SwiGLU, down projection) for the rank's S/D tokens, the shard steps taken
+in groups of G (tsp_shape.group_steps; 0 = the library default, all D steps when
+D <= 8, since every shard is resident).  Inputs, weight
 shards and the K/V rows of the earlier ranks (the modelled all-gather) are resident
 in HBM before timing starts.  Prints one JSON line on stdout; progress goes to stderr.
 
@@ -68,7 +71,7 @@ def log(msg):
 def kernel_flops(wl):
     """Algorithmic FLOPs of each kernel class (TSP_KERNEL_* order) over one call of the
     entry point that launches it (all D shard steps), whatever the number of launches:
-    the down and output projections of two steps share a launch, and so do the two dX
+    the forward's products of one group of steps share a launch, and so do the two dX
     products of one MLP backward step."""
     from paper_2604_26294_amd.flops import step_attn_core_flops
     D = wl.degree
@@ -173,7 +176,7 @@ def time_calls(fn, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
-def rank_sweep(wl, x_bits, w_bits, steps, warmup):
+def rank_sweep(wl, x_bits, w_bits, steps, warmup, group_steps=0):
     """Layer time of every rank of the group (each with its own K/V prefix pre-filled)."""
     import torch
 
@@ -182,7 +185,7 @@ def rank_sweep(wl, x_bits, w_bits, steps, warmup):
     rows = []
     for p in range(wl.degree):
         w = wl.at_rank(p)
-        prob = RankProblem(w, x_bits, w_bits, p)
+        prob = RankProblem(w, x_bits, w_bits, p, group_steps=group_steps)
         prob.prefill_kv()
         torch.cuda.synchronize()
         ms = time_calls(prob.layer, steps, warmup)
@@ -206,7 +209,11 @@ def main(argv=None):
     ap.add_argument("--rank", type=int, default=None)
     ap.add_argument("--layout", default="contiguous", choices=["contiguous", "zigzag"],
                     help="sequence layout of the ranks (zigzag: Algorithm 1 as printed)")
+    ap.add_argument("--group-steps", type=int, default=0,
+                    help="forward shard steps per grouped launch (0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--forward-only", action="store_true",
+                    help="skip the backward blocks (for short profiling runs)")
     ap.add_argument("--cpu-rows", type=int, default=128)
     ap.add_argument("--rank-sweep", action="store_true",
                     help="also time the layer of every rank of the group")
@@ -234,7 +241,8 @@ def main(argv=None):
     log(f"workload {wl.name} rank {wl.rank}: generating seeded inputs")
     x_bits = I.make_x_full(wl)
     w_bits = I.make_weights(wl)
-    prob = RankProblem(wl, x_bits, w_bits)
+    prob = RankProblem(wl, x_bits, w_bits, group_steps=args.group_steps)
+    group = min(args.group_steps or T.GROUP_STEPS_MAX, wl.degree)
     log("pre-filling the K/V rows of earlier ranks (the modelled all-gather, untimed)")
     prob.prefill_kv()
     torch.cuda.synchronize()
@@ -309,6 +317,9 @@ def main(argv=None):
         "mlp": {"ms": round(ms_mlp, 4), "flops": rf.mlp,
                 "tflops": round(rf.mlp / (ms_mlp * 1e-3) / 1e12, 2)},
     }
+    if args.forward_only:
+        return finish(args, wl, x_bits, w_bits, ms, ms_prof, rf, tflops, roofline, kernels,
+                      blocks)
     # The per-rank MLP backward on the same rank: dX and this rank's contribution to
     # every shard's weight gradients, for a synthetic upstream gradient.  Executed
     # products: G, U (recomputed) and dHs, dX (two), the three weight gradients = 16 M F h
@@ -383,7 +394,14 @@ def main(argv=None):
                       "core); backward: 2.5x the forward core plus the gradient products",
         "kernels": ab1_kernels}
     del dy, dkl, dvl
+    return finish(args, wl, x_bits, w_bits, ms, ms_prof, rf, tflops, roofline, kernels, blocks)
 
+
+def finish(args, wl, x_bits, w_bits, ms, ms_prof, rf, tflops, roofline, kernels, blocks):
+    """Prints the JSON line (with the rank sweep and the CPU baseline when asked for)."""
+    from paper_2604_26294_amd import tsp as T
+    from paper_2604_26294_amd.flops import paper_layer_flops, rank_algorithmic_bytes
+    group = min(args.group_steps or T.GROUP_STEPS_MAX, wl.degree)
     nbytes = rank_algorithmic_bytes(wl)
     hbm = {"algorithmic_bytes": nbytes, "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
            "frac_of_peak": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
@@ -397,7 +415,7 @@ def main(argv=None):
         "config": {"workload": wl.name, "batch": wl.batch, "seq": wl.seq, "hidden": wl.hidden,
                    "ffn": wl.ffn, "n_heads": wl.n_heads, "n_kv_heads": wl.n_kv_heads,
                    "head_dim": wl.head_dim, "degree": wl.degree, "rank": wl.rank,
-                   "layout": wl.layout_name},
+                   "layout": wl.layout_name, "group_steps": group},
         "pct_of_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "flops_per_step": rf.total,
         "paper_flops_per_rank_noncausal": paper_layer_flops(wl) / wl.degree,
@@ -409,7 +427,8 @@ def main(argv=None):
         "cpu_baseline": None,
     }
     if args.rank_sweep:
-        out["rank_sweep"] = rank_sweep(wl, x_bits, w_bits, max(3, args.steps // 4), 2)
+        out["rank_sweep"] = rank_sweep(wl, x_bits, w_bits, max(3, args.steps // 4), 2,
+                                       args.group_steps)
     if not args.no_cpu_baseline and wl.layout == 0:  # the sampled oracle leg is contiguous-only
         out["cpu_baseline"] = cpu_baseline(wl, x_bits, w_bits, args.cpu_rows)
     print(json.dumps(out), flush=True)

@@ -64,7 +64,7 @@
 extern "C" {
 #endif
 
-#define TSP_ABI_VERSION 1
+#define TSP_ABI_VERSION 2
 
 typedef enum tsp_status {
   TSP_OK = 0,
@@ -94,14 +94,29 @@ typedef struct tsp_shape {
   int32_t rank;         /* p: this rank */
   int32_t layout;       /* 0 = contiguous chunks, 1 = zigzag (see the top of this file) */
   float softmax_scale;  /* <= 0 selects 1/sqrt(head_dim) */
+  int32_t group_steps;  /* forward shard steps per grouped launch, 0..TSP_GROUP_STEPS_MAX
+                           (0 = TSP_GROUP_STEPS_MAX; values above D act as D; negative:
+                           TSP_ERR_SHAPE, above the maximum: TSP_ERR_UNSUPPORTED) */
 } tsp_shape;
+
+/* Forward shard-step grouping.  tsp_mlp_rank_fwd, tsp_attn_rank_fwd and the layer calls
+ * take their D shard steps in groups of G = min(group_steps, D) consecutive steps of
+ * the schedule's order (the last group holds the remainder).  A group's products run as
+ * one launch each: its gate+up (Q/K/V) products as one grouped launch, its down (output)
+ * projection as ONE product whose contraction runs over the group's shards in order
+ * (Y += [Hs_1 .. Hs_G] [W_down_1; ..; W_down_G]), and its attention over the group's
+ * G n_h/D heads at once.  The result is the step-by-step sum up to fp32 rounding order.
+ * In a streaming schedule G is the number of weight shards held at once; with every
+ * shard resident (one GPU) the default takes all D steps together (D <= the maximum).
+ * The backward calls take their steps one (or two) at a time and ignore it. */
+#define TSP_GROUP_STEPS_MAX 8
 
 /* Gated ring MLP of rank p (Algorithm 2):
  *   Y (+)= sum over t = 0..D-1, j = (p - t) mod D, of
  *          bf16( SiLU(X W_gate[j]^T) * (X W_up[j]^T) ) W_down[j]
  * with SiLU(z) = z * sigmoid(z), fp32 accumulation across shards in ring order, the
- * down projections of steps 2i and 2i+1 taken as one product over both shards (an odd
- * last step alone): the same sum up to fp32 rounding order.
+ * steps grouped as tsp_shape.group_steps says (the down projections of a group's
+ * steps one product over its shards): the same sum up to fp32 rounding order.
  *   x_loc      [B, S_loc, h] bf16       the rank's tokens
  *   w_gate[j]  [ffn/D, h]   bf16       W1 shard j
  *   w_up[j]    [ffn/D, h]   bf16       W3 shard j
@@ -158,8 +173,9 @@ tsp_status tsp_kv_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
  *       sees keys j <= pos(t) (layout 1: the two CausalAttn calls of Algorithm 1, the
  *       first half of the rows against keys [0, s1 = (p+1)*S_c), the second against
  *       [0, s2 = (2D-p)*S_c));
- *   Y (+)= Flatten(A) W_O^(r)^T   (fp32, shards accumulated in order r = 0..D-1, the
- *       output projections of shards 2i and 2i+1 as one product over both).
+ *   Y (+)= Flatten(A) W_O^(r)^T   (fp32, shards accumulated in order r = 0..D-1,
+ *       grouped as tsp_shape.group_steps says: the output projections of a group's
+ *       shards one product over them).
  * Q, K, V, the softmax probabilities and A are rounded to bf16 for the matrix cores.
  *   x_loc, w_attn as for tsp_kv_rank_fwd;  k_buf, v_buf [B, S, n_kv, d] bf16: this
  *   rank's rows are written; every other row its queries can see must already hold
@@ -226,8 +242,8 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                               uint16_t* k_buf, uint16_t* v_buf, float* y_loc, void* ws,
                               size_t ws_bytes, hipStream_t stream);
 
-/* Scratch size available to tsp_layer_rank_fwd_noalloc on each device (64 MiB). */
-#define TSP_NOALLOC_SCRATCH_BYTES (64u << 20)
+/* Scratch size available to tsp_layer_rank_fwd_noalloc on each device (128 MiB). */
+#define TSP_NOALLOC_SCRATCH_BYTES (128u << 20)
 
 /* tsp_layer_rank_fwd for callers that cannot allocate device memory: code under HIP
  * graph capture, tight serving loops, harnesses that forbid allocation.  Same arguments
@@ -238,8 +254,8 @@ tsp_status tsp_layer_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
  * allocates nor frees anything.
  *   - A shape whose layer workspace (tsp_workspace_bytes(shape, TSP_OP_LAYER)) exceeds
  *     TSP_NOALLOC_SCRATCH_BYTES returns TSP_ERR_WORKSPACE before anything is enqueued
- *     (the 7B-class layer at S = 8192, D = 8 needs 27 MiB and fits; at S = 65536 it
- *     needs 121 MiB and does not).
+ *     (the 7B-class layer at S = 8192, D = 8 needs 94 MiB and fits; at S = 65536 it
+ *     needs 240 MiB and does not).
  *   - All calls on one device share its array: calls that can overlap in time on one
  *     device (different streams, or different host threads without ordering) race on
  *     it and must not be made; calls ordered on one stream are fine.

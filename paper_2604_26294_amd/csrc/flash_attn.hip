@@ -42,7 +42,11 @@
 // LDS read address is (per-lane base XOR a constant) + an immediate offset.
 #include <math.h>
 
+#include <functional>
+#include <mutex>
+#include <queue>
 #include <type_traits>
+#include <vector>
 
 #include "common.h"
 #include "internal.h"
@@ -536,7 +540,9 @@ long long split_makespan(const int* tile_keys, int n_qt, long long bh, int n, in
   const long long q = total / kXcds, rem = total % kXcds;
   long long worst = 0;
   for (int x = 0; x < kXcds; ++x) {
-    long long finish[kCusPerXcd] = {};
+    // finish times of the XCD's CUs; the earliest-free one takes the next item
+    std::priority_queue<long long, std::vector<long long>, std::greater<long long>> finish(
+        std::greater<long long>(), std::vector<long long>(kCusPerXcd, 0));
     const long long w0 = x * q + (x < rem ? x : rem), w1 = w0 + q + (x < rem ? 1 : 0);
     for (long long w = w0; w < w1; ++w) {
       const int t = (int)(w % n_qt);
@@ -544,19 +550,68 @@ long long split_makespan(const int* tile_keys, int n_qt, long long bh, int n, in
       const long long keys = min(max((long long)tile_keys[t] - (long long)split * len, 0LL),
                                  (long long)len);
       const long long cost = keys > 0 ? keys + kPieceCost : kEmptyCost;
-      int c = 0;
-      for (int i = 1; i < kCusPerXcd; ++i)
-        if (finish[i] < finish[c]) c = i;
-      finish[c] += cost;
+      const long long f = finish.top() + cost;
+      finish.pop();
+      finish.push(f);
     }
-    for (int i = 0; i < kCusPerXcd; ++i) worst = max(worst, finish[i]);
+    while (!finish.empty()) {
+      worst = max(worst, finish.top());
+      finish.pop();
+    }
   }
   return worst;
 }
 
+// Shapes already priced (the choice depends on these fields only); callers ask for the
+// same shape several times per entry point call.
+struct SplitKey {
+  int batch, heads, head_dim, n_seg, seg_rows[2], seg_pos0[2];
+  bool operator==(const SplitKey& o) const {
+    return batch == o.batch && heads == o.heads && head_dim == o.head_dim && n_seg == o.n_seg &&
+           seg_rows[0] == o.seg_rows[0] && seg_rows[1] == o.seg_rows[1] &&
+           seg_pos0[0] == o.seg_pos0[0] && seg_pos0[1] == o.seg_pos0[1];
+  }
+};
+struct SplitChoice {
+  SplitKey key;
+  int n, len;
+};
+std::mutex g_split_mu;
+std::vector<SplitChoice> g_split_cache;
+constexpr size_t kSplitCacheMax = 64;
+
+int attn_split_count_uncached(const AttnParams& p, int* split_len);
+
 }  // namespace
 
 int attn_split_count(const AttnParams& p, int* split_len) {
+  SplitKey key = {p.batch, p.heads, p.head_dim, p.n_seg, {0, 0}, {0, 0}};
+  for (int k = 0; k < p.n_seg && k < 2; ++k) {
+    key.seg_rows[k] = p.seg_rows[k];
+    key.seg_pos0[k] = p.seg_pos0[k];
+  }
+  {
+    std::lock_guard<std::mutex> lock(g_split_mu);
+    for (const SplitChoice& c : g_split_cache)
+      if (c.key == key) {
+        if (split_len) *split_len = c.len;
+        return c.n;
+      }
+  }
+  int len = 0;
+  const int n = attn_split_count_uncached(p, &len);
+  {
+    std::lock_guard<std::mutex> lock(g_split_mu);
+    if (g_split_cache.size() >= kSplitCacheMax) g_split_cache.erase(g_split_cache.begin());
+    g_split_cache.push_back({key, n, len});
+  }
+  if (split_len) *split_len = len;
+  return n;
+}
+
+namespace {
+
+int attn_split_count_uncached(const AttnParams& p, int* split_len) {
   // Keys of each query tile, in the kernel's order (last segment first, last tile first).
   constexpr int kMaxTiles = 1024;
   int tile_keys[kMaxTiles];
@@ -578,10 +633,16 @@ int attn_split_count(const AttnParams& p, int* split_len) {
   int best_n = 1;
   if (bh > 0 && n_qt <= kMaxTiles) {
     // Candidate range counts 1..8, at least 4 key tiles per range.  Estimated time =
-    // simulated makespan x the time a workgroup spends per key (~30 ns at d = 128, from
-    // the measured step rate) + the partials' HBM traffic (written, read back and
-    // merged, at ~4 TB/s); the smallest wins, ties going to fewer ranges.
-    const double t_key = 30e-9 * p.head_dim / 128.0, bw = 4e12;
+    // simulated makespan x the time a workgroup spends per key + the partials' HBM
+    // traffic (written, read back and merged); the smallest wins, ties going to fewer
+    // ranges.  Per key a workgroup executes 4 kQTile d FLOPs (its Q K^T and P V rows),
+    // at the fraction of one CU's bf16 MFMA peak (2516.6 / 256 TFLOP/s) this kernel
+    // reaches (0.44 measured at 7B, S = 65536: ~30 ns per key at d = 128); the partials
+    // move at about half the HBM peak (8 TB/s).  Only the ratio of the two terms
+    // matters, so the constants need refitting only when that fraction moves a lot.
+    constexpr double kCuPeak = 2516.6e12 / 256, kPeakFraction = 0.44, kPartialBw = 4e12;
+    const double t_key = 4.0 * kQTile * p.head_dim / (kPeakFraction * kCuPeak);
+    const double bw = kPartialBw;
     const double rows = (double)bh * p.s_loc;
     double best = -1.0;
     for (int n = 1; n <= 8; ++n) {
@@ -600,6 +661,8 @@ int attn_split_count(const AttnParams& p, int* split_len) {
   if (split_len) *split_len = len_of(best_n);
   return best_n;
 }
+
+}  // namespace
 
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
   if (p.batch <= 0 || p.s_loc <= 0 || p.heads <= 0) return hipSuccess;

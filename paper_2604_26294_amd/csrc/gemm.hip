@@ -36,6 +36,7 @@
 // SwiGLU epilogue), and the matching W2 rows past F/D are clamped, so padded terms
 // contribute exact zeros.
 #include <climits>
+#include <type_traits>
 
 #include "common.h"
 #include "internal.h"
@@ -141,155 +142,16 @@ __device__ __forceinline__ void dma_nn(lds_char* dst, const uint16_t* base, int 
   }
 }
 
-// One output tile (work index w) of the product P.
-template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
-__device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
-  using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
-  constexpr int TM = C::TM, TN = C::TN, TNB = C::TNB;
-  __shared__ __attribute__((aligned(1024))) char L[C::LDS_BYTES];
-  lds_char* Ls = (lds_char*)L;
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / WGN, wn = wave % WGN;
+// Epilogue of one C tile (configuration C: WAVES, WM, WN, TM, TN, TNB, LDS_BYTES, BWD)
+// from the accumulators of each wavefront, staged through the workgroup's LDS (free:
+// every operand read has completed).
+template <class C, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)[C::TM][C::TNB],
+                                              char* L, const int wave, const int lane,
+                                              const int m0, const int n0, const int wm,
+                                              const int wn, const int split = 0) {
+  constexpr int TM = C::TM, TN = C::TN;
   const int l32 = lane & 31, hh = lane >> 5;
-
-  const int tiles_n = (P.N + BN - 1) / BN;
-  const int m0 = (w / tiles_n) * BM;
-  const int n0 = (w % tiles_n) * BN;
-
-  f32x16 acc[TM][TNB];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TNB; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  // The two parts of a two-part contraction as values (the asm keeps the compiler from
-  // turning the per-stage choice into a choice between field addresses, which would put
-  // the parameters in scratch memory).
-  const uint16_t* a_lo = P.A;
-  const uint16_t* a_hi = P.A_hi ? P.A_hi : P.A;
-  const uint16_t* b_lo = P.B;
-  const uint16_t* b_hi = P.A_hi ? P.B_hi : P.B;
-  int kr_lo = P.Kb_rows, kr_hi = P.Kb_rows_hi, k_split = P.A_hi ? P.k_split : INT_MAX;
-  if constexpr (NN)
-    asm volatile("" : "+s"(a_lo), "+s"(a_hi), "+s"(b_lo), "+s"(b_hi), "+s"(kr_lo), "+s"(kr_hi),
-                 "+s"(k_split));
-  auto dma_stage = [&](int stage, int k0) {
-    lds_char* S = Ls + stage * C::STAGE;
-    if constexpr (NN) {
-      // (k0 is uniform: the part is chosen per stage, from scalar values)
-      const bool hi = k0 >= k_split;
-      const int kk = hi ? k0 - k_split : k0;
-      dma_nt<BM, C::WAVES>(S, hi ? a_hi : a_lo, P.lda, m0, P.M, kk, wave, lane);
-      dma_nn<BN, C::WAVES>(S + C::A_BYTES, hi ? b_hi : b_lo, P.ldb, kk, hi ? kr_hi : kr_lo, n0,
-                           P.N, wave, lane);
-      return;
-    }
-    dma_nt<BM, C::WAVES>(S, P.A, P.lda, m0, P.M, k0, wave, lane);
-    if constexpr (C::BWD) dma_nt<BM, C::WAVES>(S + BM * BK * 2, P.A2, P.lda, m0, P.M, k0, wave, lane);
-    if constexpr (EPI == EPI_SWIGLU || C::BWD) {
-      dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
-      dma_nt<BN, C::WAVES>(S + C::A_BYTES + BN * BK * 2, P.B2, P.ldb, n0, P.N, k0, wave, lane);
-      if constexpr (C::BWD)
-        dma_nt<BN, C::WAVES>(S + C::A_BYTES + 2 * BN * BK * 2, P.B3, P.ldb, n0, P.N, k0, wave,
-                             lane);
-    } else {
-      dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
-    }
-  };
-
-  // Operand addressing (see the header): A / NT-B row R, chunk 2 s + hh ->
-  //   R_base * 128 + (opa ^ 32 s),  opa = l32 * 128 + 16 (hh ^ nt_swz(l32)).
-  const int opa = l32 * 128 + 16 * (hh ^ nt_swz(l32));
-  // NN-B transpose reads for output column block j: rows 16 s + 8 hh + t/4 (+4), columns
-  // wn WN + 32 j + 16 (g mod 2) + 4 (t mod 4)  ->  16 s NN_RB + (nb ^ 2 (wn WN + 32 j)).
-  int nb_lo = 0, nb_hi = 0;
-  if constexpr (NN) {
-    const int t = lane & 15, g = lane >> 4;
-    const int cl = 2 * (g & 1) + ((t & 3) >> 1), half8 = 8 * (t & 1);
-    const int r_lo = 8 * (g >> 1) + (t >> 2), r_hi = r_lo + 4;
-    nb_lo = r_lo * C::NN_RB + 16 * (cl ^ nn_swz(r_lo)) + half8;
-    nb_hi = r_hi * C::NN_RB + 16 * (cl ^ nn_swz(r_hi)) + half8;
-  }
-
-  // STAGES-deep ring: stage k lives in slot k mod STAGES.  Step kt waits for stage kt
-  // (the loads of up to STAGES - 2 later stages stay in flight), then refills the slot
-  // that step kt - 1 read with stage kt + STAGES - 1.
-  const int nk = P.K / BK;
-#pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st)
-    if (st < nk) dma_stage(st, st * BK);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int ahead = min(STAGES - 2, nk - 1 - kt);  // later stages already issued
-    if constexpr (STAGES >= 4) {
-      if (ahead >= 2) wait_dma<C::LOADS * 2>();
-      else if (ahead == 1) wait_dma<C::LOADS>();
-      else wait_dma<0>();
-    } else if constexpr (STAGES == 3) {
-      if (ahead >= 1) wait_dma<C::LOADS>();
-      else wait_dma<0>();
-    } else {
-      wait_dma<0>();
-    }
-    __syncthreads();  // stage kt resident; every wave is past step kt-1
-    if (kt + STAGES - 1 < nk) dma_stage((kt + STAGES - 1) % STAGES, (kt + STAGES - 1) * BK);
-    const lds_char* SA = Ls + (kt % STAGES) * C::STAGE;
-    const lds_char* SB = SA + C::A_BYTES;
-#pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      u32x4 a[TM], a2[TM], b[TNB];
-      const int xo = opa ^ (32 * s);
-#pragma unroll
-      for (int i = 0; i < TM; ++i) a[i] = lds_read16(SA + (wm * C::WM + 32 * i) * 128 + xo);
-      if constexpr (C::BWD) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          a2[i] = lds_read16(SA + BM * BK * 2 + (wm * C::WM + 32 * i) * 128 + xo);
-      }
-#pragma unroll
-      for (int j = 0; j < TNB; ++j) {
-        if constexpr (NN) {
-          const int cx = 2 * (wn * C::WN + 32 * j);
-          const u32x2 lo = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_lo ^ cx));
-          const u32x2 hi = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_hi ^ cx));
-          b[j] = u32x4{lo[0], lo[1], hi[0], hi[1]};
-        } else {
-          const int brow = (j / TN) * BN + wn * C::WN + 32 * (j % TN);  // panel j / TN
-          b[j] = lds_read16(SB + brow * 128 + xo);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TNB; ++j)
-          acc[i][j] = mfma32(C::BWD && j >= 2 * TN ? a2[i] : a[i], b[j], acc[i][j]);
-    }
-    // Issue order: the operand reads of k-substep s+1 are spread between the MFMAs of
-    // substep s (R / M per MFMA, one more for the first R mod M), so LDS latency hides
-    // behind matrix work.
-    {
-      constexpr int R = C::NAP * TM + (NN ? 2 : 1) * TNB;  // LDS reads per substep
-      constexpr int M = TM * TNB;                          // MFMAs per substep
-      constexpr int RM = R / M;
-      __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
-#pragma unroll
-      for (int s = 0; s < BK / 16; ++s)
-#pragma unroll
-        for (int i = 0; i < M; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          if (s + 1 < BK / 16) {
-            if (i < R % M) __builtin_amdgcn_sched_group_barrier(0x100, RM + 1, 0);
-            else if (RM > 0) __builtin_amdgcn_sched_group_barrier(0x100, RM, 0);
-          }
-        }
-    }
-  }
-  __syncthreads();  // operand stages are free for the epilogue
-
-  // ---------------------------------------------------------------- epilogue
   // Each wavefront stages one 32-row block of its C tile in LDS as fp32, then writes it
   // out in 4-column chunks: consecutive lanes cover consecutive columns, every global
   // access is 16 bytes (fp32) or 8 bytes (bf16), and all loads of a block are in flight
@@ -383,6 +245,14 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
       ok[q] = mm[q] < P.M && nn[q] < P.N;
     }
     if constexpr (EPI == EPI_ACC) {
+      if (P.k_splits > 1) {  // a partial product of one contraction range
+        float* dst = P.part + (size_t)split * P.M * P.N;
+#pragma unroll
+        for (int q = 0; q < PER_LANE; ++q)
+          if (ok[q]) *reinterpret_cast<f32x4*>(dst + (size_t)mm[q] * P.N + nn[q]) = v[q];
+        __syncthreads();
+        continue;
+      }
       f32x4 base[PER_LANE];
 #pragma unroll
       for (int q = 0; q < PER_LANE; ++q) {
@@ -410,8 +280,8 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
 #pragma unroll
       for (int q = 0; q < PER_LANE; ++q) {
         if constexpr (EPI == EPI_SWIGLU) {
-          // Columns [N, ldh) are the zero padding of the gated product.
-          if (mm[q] >= P.M || nn[q] >= P.ldh) continue;
+          // Columns [N, h_cols) are the zero padding of the gated product.
+          if (mm[q] >= P.M || nn[q] >= (P.h_cols > 0 ? P.h_cols : P.ldh)) continue;
           const u32x2 bits = nn[q] < P.N ? u32x2{pack_bf16x2(v[q][0], v[q][1]),
                                                  pack_bf16x2(v[q][2], v[q][3])}
                                          : u32x2{0u, 0u};
@@ -440,10 +310,426 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
   }
 }
 
+// One output tile (work index w) of the product P.
+template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
+__device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
+  using C = Cfg<BM, BN, WGM, WGN, NN, EPI, STAGES>;
+  constexpr int TM = C::TM, TN = C::TN, TNB = C::TNB;
+  __shared__ __attribute__((aligned(1024))) char L[C::LDS_BYTES];
+  lds_char* Ls = (lds_char*)L;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int l32 = lane & 31, hh = lane >> 5;
+
+  const int tiles_n = (P.N + BN - 1) / BN;
+  // Work index -> (contraction range, output tile): ranges outermost.
+  int split = 0, wt = w;
+  if (EPI == EPI_ACC && P.k_splits > 1) {
+    const int tiles = ((P.M + BM - 1) / BM) * tiles_n;
+    split = w / tiles;
+    wt = w - split * tiles;
+  }
+  const int m0 = (wt / tiles_n) * BM;
+  const int n0 = (wt % tiles_n) * BN;
+
+  f32x16 acc[TM][TNB];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TNB; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // The operand pairs of a multi-part contraction, read once into scalar registers (the
+  // asm keeps them there: the per-stage choice is then a chain of scalar selects, not an
+  // indexed access, which would put the parameters in scratch memory).
+  const uint16_t* ap[kGemmPartsMax];
+  const uint16_t* bp[kGemmPartsMax];
+  int k_part = INT_MAX;
+  if constexpr (NN) {
+    const bool multi = P.n_parts > 1;
+#pragma unroll
+    for (int i = 0; i < kGemmPartsMax; ++i) {
+      ap[i] = multi && i < P.n_parts ? P.A_part[i] : P.A;
+      bp[i] = multi && i < P.n_parts ? P.B_part[i] : P.B;
+      asm volatile("" : "+s"(ap[i]), "+s"(bp[i]));
+    }
+    if (multi) k_part = P.k_part;
+    asm volatile("" : "+s"(k_part));
+  }
+  auto dma_stage = [&](int stage, int k0) {
+    lds_char* S = Ls + stage * C::STAGE;
+    if constexpr (NN) {
+      // (k0 is uniform: the part is chosen per stage, from scalar values)
+      const int part = k0 / k_part, kk = k0 - part * k_part;
+      const uint16_t* a = ap[0];
+      const uint16_t* b = bp[0];
+#pragma unroll
+      for (int i = 1; i < kGemmPartsMax; ++i) {
+        a = part == i ? ap[i] : a;
+        b = part == i ? bp[i] : b;
+      }
+      dma_nt<BM, C::WAVES>(S, a, P.lda, m0, P.M, kk, wave, lane);
+      dma_nn<BN, C::WAVES>(S + C::A_BYTES, b, P.ldb, kk, P.Kb_rows, n0, P.N, wave, lane);
+      return;
+    }
+    dma_nt<BM, C::WAVES>(S, P.A, P.lda, m0, P.M, k0, wave, lane);
+    if constexpr (C::BWD) dma_nt<BM, C::WAVES>(S + BM * BK * 2, P.A2, P.lda, m0, P.M, k0, wave, lane);
+    if constexpr (EPI == EPI_SWIGLU || C::BWD) {
+      dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
+      dma_nt<BN, C::WAVES>(S + C::A_BYTES + BN * BK * 2, P.B2, P.ldb, n0, P.N, k0, wave, lane);
+      if constexpr (C::BWD)
+        dma_nt<BN, C::WAVES>(S + C::A_BYTES + 2 * BN * BK * 2, P.B3, P.ldb, n0, P.N, k0, wave,
+                             lane);
+    } else {
+      dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
+    }
+  };
+
+  // Operand addressing (see the header): A / NT-B row R, chunk 2 s + hh ->
+  //   R_base * 128 + (opa ^ 32 s),  opa = l32 * 128 + 16 (hh ^ nt_swz(l32)).
+  const int opa = l32 * 128 + 16 * (hh ^ nt_swz(l32));
+  // NN-B transpose reads for output column block j: rows 16 s + 8 hh + t/4 (+4), columns
+  // wn WN + 32 j + 16 (g mod 2) + 4 (t mod 4)  ->  16 s NN_RB + (nb ^ 2 (wn WN + 32 j)).
+  int nb_lo = 0, nb_hi = 0;
+  if constexpr (NN) {
+    const int t = lane & 15, g = lane >> 4;
+    const int cl = 2 * (g & 1) + ((t & 3) >> 1), half8 = 8 * (t & 1);
+    const int r_lo = 8 * (g >> 1) + (t >> 2), r_hi = r_lo + 4;
+    nb_lo = r_lo * C::NN_RB + 16 * (cl ^ nn_swz(r_lo)) + half8;
+    nb_hi = r_hi * C::NN_RB + 16 * (cl ^ nn_swz(r_hi)) + half8;
+  }
+
+  // STAGES-deep ring: stage k lives in slot k mod STAGES.  Step kt waits for stage kt
+  // (the loads of up to STAGES - 2 later stages stay in flight), then refills the slot
+  // that step kt - 1 read with stage kt + STAGES - 1.
+  // Contraction steps [kb, kb + nk) (all of them unless the contraction is split); step
+  // kb + kt lives in ring slot kt mod STAGES.
+  int kb = 0, nk = P.K / BK;
+  if (EPI == EPI_ACC && P.k_splits > 1) {
+    const int all = nk;
+    kb = split * all / P.k_splits;
+    nk = (split + 1) * all / P.k_splits - kb;
+  }
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < nk) dma_stage(st, (kb + st) * BK);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int ahead = min(STAGES - 2, nk - 1 - kt);  // later stages already issued
+    if constexpr (STAGES >= 4) {
+      if (ahead >= 2) wait_dma<C::LOADS * 2>();
+      else if (ahead == 1) wait_dma<C::LOADS>();
+      else wait_dma<0>();
+    } else if constexpr (STAGES == 3) {
+      if (ahead >= 1) wait_dma<C::LOADS>();
+      else wait_dma<0>();
+    } else {
+      wait_dma<0>();
+    }
+    __syncthreads();  // stage kt resident; every wave is past step kt-1
+    if (kt + STAGES - 1 < nk)
+      dma_stage((kt + STAGES - 1) % STAGES, (kb + kt + STAGES - 1) * BK);
+    const lds_char* SA = Ls + (kt % STAGES) * C::STAGE;
+    const lds_char* SB = SA + C::A_BYTES;
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      u32x4 a[TM], a2[TM], b[TNB];
+      const int xo = opa ^ (32 * s);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) a[i] = lds_read16(SA + (wm * C::WM + 32 * i) * 128 + xo);
+      if constexpr (C::BWD) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          a2[i] = lds_read16(SA + BM * BK * 2 + (wm * C::WM + 32 * i) * 128 + xo);
+      }
+#pragma unroll
+      for (int j = 0; j < TNB; ++j) {
+        if constexpr (NN) {
+          const int cx = 2 * (wn * C::WN + 32 * j);
+          const u32x2 lo = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_lo ^ cx));
+          const u32x2 hi = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_hi ^ cx));
+          b[j] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        } else {
+          const int brow = (j / TN) * BN + wn * C::WN + 32 * (j % TN);  // panel j / TN
+          b[j] = lds_read16(SB + brow * 128 + xo);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TNB; ++j)
+          acc[i][j] = mfma32(C::BWD && j >= 2 * TN ? a2[i] : a[i], b[j], acc[i][j]);
+    }
+    // Issue order: the operand reads of k-substep s+1 are spread between the MFMAs of
+    // substep s (R / M per MFMA, one more for the first R mod M), so LDS latency hides
+    // behind matrix work.
+    {
+      constexpr int R = C::NAP * TM + (NN ? 2 : 1) * TNB;  // LDS reads per substep
+      constexpr int M = TM * TNB;                          // MFMAs per substep
+      constexpr int RM = R / M;
+      __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+#pragma unroll
+      for (int s = 0; s < BK / 16; ++s)
+#pragma unroll
+        for (int i = 0; i < M; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if (s + 1 < BK / 16) {
+            if (i < R % M) __builtin_amdgcn_sched_group_barrier(0x100, RM + 1, 0);
+            else if (RM > 0) __builtin_amdgcn_sched_group_barrier(0x100, RM, 0);
+          }
+        }
+    }
+  }
+  __syncthreads();  // operand stages are free for the epilogue
+
+  gemm_epilogue<C, EPI>(P, acc, L, wave, lane, m0, n0, wm, wn, split);
+}
+
+// ---------------------------------------------------------------- deep-ring tiles
+// Products with [N, K] operands (both contraction-contiguous).  One wavefront per SIMD:
+// 4 per workgroup (2 x 2), each owning a (BM/2) x (BN/2) block of C (with the SwiGLU
+// epilogue: BN/2 gate and BN/2 up columns) as 32 x 32 MFMA tiles, 16 of them at BM = 256,
+// BN = 128 + 128: 256 fp32 accumulators per lane, held in the accumulation registers.  Per 16-deep substep a wavefront reads 8 operand fragments from LDS for 16
+// MFMAs (the two-wavefront-per-SIMD tiles above read 6 for 8), which halves the LDS
+// read traffic per MFMA.  K advances in stages of 32, through a ring of STAGES slots of
+// 32 KB: loads of stages kt+2 .. kt+STAGES stay in flight while stage kt is consumed
+// (about three stages of matrix work hide the load latency where a ring of two 64-deep
+// stages hides one).  Each stage has ONE workgroup barrier, placed among the MFMAs of
+// its second substep: every wavefront has by then received all of the stage's operands
+// (its slot may be refilled) and waited for its own loads of the next stage (which the
+// barrier makes visible to all), so the next stage's first operands are read while the
+// stage's last MFMAs still run.
+//
+// LDS layout.  Operand panels are rows of 32 bf16 (64 bytes, four 16-byte chunks),
+// physical chunk = logical chunk XOR ((row / 4) mod 4), so the 16 rows x one chunk of a
+// 16-lane group of an operand read cover all 64 banks.
+//
+// Measured against the two-wavefront tiles above on the 7B shapes: faster for gate+up
+// (1146 vs 1014 TFLOP/s), slower for the [K, N] products (whose transpose reads double
+// the LDS instructions per substep) and for Q/K/V, which keep the tiles above.
+template <int BM, int BN, int EPI, int STAGES>
+struct DrCfg {
+  static constexpr int WAVES = 4, THREADS = kWave * WAVES;
+  static constexpr int BKS = 32;  // contraction indices per stage
+  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int TM = WM / 32, TN = WN / 32;
+  static constexpr bool BWD = false;
+  static constexpr int NBP = EPI == EPI_SWIGLU ? 2 : 1;  // B panels
+  static constexpr int TNB = NBP * TN;
+  static constexpr int NB = NBP * BN;
+  static constexpr int A_BYTES = BM * BKS * 2;
+  static constexpr int B_BYTES = NB * BKS * 2;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int LDS_BYTES = STAGES * STAGE;
+  static constexpr int A_LOADS = A_BYTES / 1024 / WAVES;  // per wavefront and stage
+  static constexpr int B_LOADS = B_BYTES / 1024 / WAVES;
+  static constexpr int LOADS = A_LOADS + B_LOADS;
+  static_assert(STAGES >= 3 && LDS_BYTES <= 160 * 1024, "LDS ring");
+  static_assert(LOADS * (STAGES - 1) < 64, "vmcnt range");
+  static_assert(A_LOADS * 1024 * WAVES == A_BYTES && B_LOADS * 1024 * WAVES == B_BYTES,
+                "DMA cover");
+  static_assert(EPI == EPI_SWIGLU || EPI == EPI_QKV, "[N, K] operand products");
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
+};
+
+__device__ __forceinline__ int dr_swz(int row) { return (row >> 2) & 3; }
+
+// Rows [row0, row0 + ROWS) x k [k0, k0 + 32) of a row-major [nrows, ld] matrix into LDS
+// (64-byte rows).  Instruction i of wave w fills rows 16 (i W + w) .. +15.
+template <int ROWS, int WAVES>
+__device__ __forceinline__ void dma_nt32(lds_char* dst, const uint16_t* base, int ld, int row0,
+                                         int nrows, int k0, int wave, int lane) {
+  const int rsub = lane >> 2, pc = lane & 3;
+#pragma unroll
+  for (int i = 0; i < ROWS / 16 / WAVES; ++i) {
+    const int blk = i * WAVES + wave;
+    const int r = 16 * blk + rsub;
+    const int grow = min(row0 + r, nrows - 1);
+    dma16(base + (size_t)grow * ld + k0 + 8 * (pc ^ dr_swz(r)), dst + blk * 1024);
+  }
+}
+
+template <int BM, int BN, int EPI, int STAGES>
+__device__ __forceinline__ void gemm_tile_dr(const GemmParams& P, const int w) {
+  using C = DrCfg<BM, BN, EPI, STAGES>;
+  constexpr int TM = C::TM, TN = C::TN, TNB = C::TNB, BKS = C::BKS;
+  __shared__ __attribute__((aligned(1024))) char L[C::LDS_BYTES];
+  lds_char* Ls = (lds_char*)L;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31, hh = lane >> 5;
+
+  const int tiles_n = (P.N + BN - 1) / BN;
+  const int m0 = (w / tiles_n) * BM;
+  const int n0 = (w % tiles_n) * BN;
+
+  f32x16 acc[TM][TNB];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TNB; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // Sources of stage k (contraction indices [k BKS, (k + 1) BKS)).
+  struct Src {
+    const uint16_t* a;
+    const uint16_t* b;
+    int kk;
+  };
+  auto stage_src = [&](int k) { return Src{P.A, P.B, k * BKS}; };
+  // Load instruction `piece` (0 .. LOADS-1) of this wavefront for a stage into `slot`:
+  // A rows first, then the B panels (16 rows of 64 bytes per instruction).
+  auto dma_piece = [&](int slot, const Src& src, int piece) {
+    lds_char* S = Ls + slot * C::STAGE;
+    if (piece < C::A_LOADS) {
+      const int blk = piece * C::WAVES + wave, r = 16 * blk + (lane >> 2);
+      const int grow = min(m0 + r, P.M - 1);
+      dma16(src.a + (size_t)grow * P.lda + src.kk + 8 * ((lane & 3) ^ dr_swz(r)), S + blk * 1024);
+      return;
+    }
+    constexpr int PER_PANEL = C::B_LOADS / C::NBP;
+    const int pb = piece - C::A_LOADS, panel = pb / PER_PANEL;
+    const int blk = (pb % PER_PANEL) * C::WAVES + wave, r = 16 * blk + (lane >> 2);
+    const int grow = min(n0 + r, P.N - 1);
+    const uint16_t* b = panel == 0 ? src.b : P.B2;
+    dma16(b + (size_t)grow * P.ldb + src.kk + 8 * ((lane & 3) ^ dr_swz(r)),
+          S + C::A_BYTES + panel * BN * BKS * 2 + blk * 1024);
+  };
+
+  // Operand of 32-row block R_base, substep s: R_base * 64 + (opa ^ 32 s).
+  const int opa = l32 * 64 + 16 * (hh ^ dr_swz(l32));
+  // Operand read `idx` (0 .. R-1: the TM A fragments, then the TNB B fragments) of
+  // substep s of the stage in `slot`.
+  auto read_one = [&](int slot, int s, int idx, u32x4 (&a)[TM], u32x4 (&b)[TNB]) {
+    const lds_char* SA = Ls + slot * C::STAGE;
+    const lds_char* SB = SA + C::A_BYTES;
+    const int xo = opa ^ (32 * s);
+    if (idx < TM) {
+      a[idx] = lds_read16(SA + (wm * C::WM + 32 * idx) * 64 + xo);
+      return;
+    }
+    const int j = idx - TM;
+    const int brow = (j / TN) * BN + wn * C::WN + 32 * (j % TN);  // panel j / TN
+    b[j] = lds_read16(SB + brow * 64 + xo);
+  };
+  constexpr int R = TM + TNB;         // operand fragments per substep
+  constexpr int MF = TM * TNB;        // MFMAs per substep
+  constexpr int FIRST = TNB;          // substep-1 MFMAs before the barrier
+  constexpr int ITEMS = R + C::LOADS; // reads and loads spread over the other MFMAs
+  constexpr int SLOTS = MF - FIRST;
+
+  const int nk = P.K / BKS;  // >= 2 (K is a multiple of 64)
+  // Stage k goes to slot k mod STAGES.  Stage indices past the last re-load the last
+  // stage into slots nothing reads again, so that every step has the same number of
+  // loads in flight (one fixed wait count).
+#pragma unroll
+  for (int st = 0; st < STAGES; ++st) {
+    const Src src = stage_src(min(st, nk - 1));
+#pragma unroll
+    for (int i = 0; i < C::LOADS; ++i) dma_piece(st, src, i);
+  }
+  wait_dma<C::LOADS * (STAGES - 1)>();
+  __syncthreads();
+  u32x4 a0[TM], b0[TNB], a1[TM], b1[TNB];
+#pragma unroll
+  for (int i = 0; i < R; ++i) read_one(0, 0, i, a0, b0);
+
+  auto step = [&](const int kt, auto last) {
+    const int slot = kt % STAGES;
+    // substep 0: MFMAs on (a0, b0), the reads of substep 1 spread over the first of them
+#pragma unroll
+    for (int i = 0; i < R; ++i) read_one(slot, 1, i, a1, b1);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TNB; ++j) acc[i][j] = mfma32(a0[i], b0[j], acc[i][j]);
+#pragma unroll
+    for (int i = 0; i < MF; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (2 * i + 1 < R) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      else if (2 * i < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // substep 1: its first MFMAs (after which every read of stage kt has returned) ...
+#pragma unroll
+    for (int q = 0; q < FIRST; ++q)
+      acc[q / TNB][q % TNB] = mfma32(a1[q / TNB], b1[q % TNB], acc[q / TNB][q % TNB]);
+    if constexpr (!decltype(last)::value) {
+      const Src src = stage_src(min(kt + STAGES, nk - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      // ... stage kt+1 resident (own loads waited for, everyone's through the barrier,
+      // which also ends every wavefront's reads of stage kt), then the rest of the
+      // MFMAs, with stage kt+1's first operand reads and the loads of stage kt+STAGES
+      // into slot kt spread between them.
+      wait_dma<C::LOADS * (STAGES - 2)>();
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __syncthreads();
+      const int next = (kt + 1) % STAGES;
+#pragma unroll
+      for (int q = 0; q < SLOTS; ++q) {
+        const int qq = FIRST + q;
+        acc[qq / TNB][qq % TNB] = mfma32(a1[qq / TNB], b1[qq % TNB], acc[qq / TNB][qq % TNB]);
+#pragma unroll
+        for (int it = q * ITEMS / SLOTS; it < (q + 1) * ITEMS / SLOTS; ++it) {
+          if (it < R) read_one(next, 0, it, a0, b0);
+          else dma_piece(slot, src, it - R);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int q = FIRST; q < MF; ++q)
+        acc[q / TNB][q % TNB] = mfma32(a1[q / TNB], b1[q % TNB], acc[q / TNB][q % TNB]);
+    }
+  };
+  for (int kt = 0; kt + 1 < nk; ++kt) step(kt, std::false_type{});
+  step(nk - 1, std::true_type{});
+  wait_dma<0>();   // the re-loads of the last stages
+  __syncthreads();  // operand slots are free for the epilogue
+  gemm_epilogue<C, EPI>(P, acc, L, wave, lane, m0, n0, wm, wn);
+}
+
+template <int BM, int BN, int EPI, int STAGES>
+__global__ __launch_bounds__(256) void gemm_dr_kernel(const GemmParams P) {
+  const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
+  gemm_tile_dr<BM, BN, EPI, STAGES>(P, xcd_work_index(blockIdx.x, tiles));
+}
+
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
 __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParams P) {
   const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
-  gemm_tile<BM, BN, WGM, WGN, NN, EPI, STAGES>(P, xcd_work_index(blockIdx.x, tiles));
+  const int items = EPI == EPI_ACC && P.k_splits > 1 ? tiles * P.k_splits : tiles;
+  gemm_tile<BM, BN, WGM, WGN, NN, EPI, STAGES>(P, xcd_work_index(blockIdx.x, items));
+}
+
+// Y = base + sum of the k_splits partial products in range order (base and U as in the
+// accumulate epilogue); 4 consecutive columns per thread.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmParams P) {
+  const int c4 = P.N / 4;
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)P.M * c4) return;
+  const int m = (int)(i / c4), n = 4 * (int)(i - (long long)m * c4);
+  const size_t mn = (size_t)P.M * P.N, at = (size_t)m * P.N + n;
+  f32x4 sum = *reinterpret_cast<const f32x4*>(P.part + at);
+  for (int c = 1; c < P.k_splits; ++c) sum += *reinterpret_cast<const f32x4*>(P.part + c * mn + at);
+  f32x4 base = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (P.R) {
+    const u32x2 r = *reinterpret_cast<const u32x2*>(P.R + (size_t)m * P.ldr + n);
+    base = f32x4{bf16_bits_to_f32(r[0] & 0xffffu), bf16_bits_to_f32(r[0] >> 16),
+                 bf16_bits_to_f32(r[1] & 0xffffu), bf16_bits_to_f32(r[1] >> 16)};
+  } else if (P.accumulate) {
+    base = *reinterpret_cast<const f32x4*>(P.Y + (size_t)m * P.ldy + n);
+  }
+  const f32x4 out = sum + base;
+  *reinterpret_cast<f32x4*>(P.Y + (size_t)m * P.ldy + n) = out;
+  if (P.U)
+    *reinterpret_cast<u32x2*>(P.U + (size_t)m * P.ldu + n) =
+        u32x2{pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3])};
 }
 
 // Up to kGemmGroupMax independent products of one configuration in one launch: the tiles of
@@ -453,6 +739,7 @@ struct GemmGroup {
   GemmParams p[kGemmGroupMax];
   int n;
 };
+static_assert(sizeof(GemmGroup) <= 4096, "kernel argument size limit");
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
 __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_group_kernel(const GemmGroup G) {
   int tiles[kGemmGroupMax], total = 0;
@@ -469,8 +756,15 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_group_kernel(const Gem
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
 hipError_t check_params(const GemmParams& p) {
   if (p.K <= 0 || p.K % BK != 0) return hipErrorInvalidValue;
-  if (p.A_hi && (!NN || p.k_split <= 0 || p.k_split >= p.K || p.k_split % BK != 0))
+  if (p.k_splits > 1 && (EPI != EPI_ACC || !p.part || p.N % 4 != 0 || p.k_splits > p.K / BK))
     return hipErrorInvalidValue;
+  if (p.n_parts > 1) {
+    if (!NN || p.n_parts > kGemmPartsMax || p.k_part <= 0 || p.k_part % BK != 0 ||
+        (long long)p.n_parts * p.k_part != p.K)
+      return hipErrorInvalidValue;
+    for (int i = 0; i < p.n_parts; ++i)
+      if (!p.A_part[i] || !p.B_part[i]) return hipErrorInvalidValue;
+  }
   return hipSuccess;
 }
 
@@ -502,27 +796,125 @@ hipError_t launch(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   const hipError_t e = check_params<BM, BN, WGM, WGN, NN, EPI, STAGES>(p);
   if (e != hipSuccess) return e;
-  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  long long tiles = (long long)((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  if (EPI == EPI_ACC && p.k_splits > 1) tiles *= p.k_splits;
+  if (tiles > INT32_MAX) return hipErrorInvalidValue;
   // hipLaunchKernel returns the status of this launch only (not an earlier error).
   void* args[] = {const_cast<GemmParams*>(&p)};
   return hipLaunchKernel(reinterpret_cast<const void*>(&gemm_kernel<BM, BN, WGM, WGN, NN, EPI, STAGES>),
-                         dim3(tiles), dim3(C::THREADS), args, 0, s);
+                         dim3((unsigned)tiles), dim3(C::THREADS), args, 0, s);
+}
+
+template <int BM, int BN, int EPI, int STAGES>
+__global__ __launch_bounds__(256) void gemm_dr_group_kernel(const GemmGroup G) {
+  int tiles[kGemmGroupMax], total = 0;
+#pragma unroll
+  for (int i = 0; i < kGemmGroupMax; ++i) {
+    tiles[i] = i < G.n ? ((G.p[i].M + BM - 1) / BM) * ((G.p[i].N + BN - 1) / BN) : 0;
+    total += tiles[i];
+  }
+  int w = xcd_work_index(blockIdx.x, total), i = 0;
+  while (i + 1 < G.n && w >= tiles[i]) w -= tiles[i++];  // uniform per workgroup
+  gemm_tile_dr<BM, BN, EPI, STAGES>(G.p[i], w);
+}
+
+template <int BM, int BN, int EPI, int STAGES>
+hipError_t launch_dr(const GemmParams& p, hipStream_t s) {
+  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  if (p.k_splits > 1) return hipErrorInvalidValue;
+  const hipError_t e = check_params<BM, BN, 2, 2, false, EPI, STAGES>(p);
+  if (e != hipSuccess) return e;
+  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  void* args[] = {const_cast<GemmParams*>(&p)};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&gemm_dr_kernel<BM, BN, EPI, STAGES>),
+                         dim3(tiles), dim3(256), args, 0, s);
+}
+
+template <int BM, int BN, int EPI, int STAGES>
+hipError_t launch_dr_group(const GemmParams* ps, int n, hipStream_t s) {
+  if (n == 1) return launch_dr<BM, BN, EPI, STAGES>(ps[0], s);
+  if (n < 1 || n > kGemmGroupMax) return hipErrorInvalidValue;
+  GemmGroup g = {};
+  long long total = 0;
+  for (int i = 0; i < n; ++i) {
+    const GemmParams& p = ps[i];
+    if (p.M <= 0 || p.N <= 0) return hipErrorInvalidValue;
+    const hipError_t e = check_params<BM, BN, 2, 2, false, EPI, STAGES>(p);
+    if (e != hipSuccess) return e;
+    g.p[i] = p;
+    total += (long long)((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  }
+  g.n = n;
+  if (total > INT32_MAX) return hipErrorInvalidValue;
+  void* args[] = {&g};
+  return hipLaunchKernel(
+      reinterpret_cast<const void*>(&gemm_dr_group_kernel<BM, BN, EPI, STAGES>),
+      dim3((unsigned)total), dim3(256), args, 0, s);
+}
+
+long long tiles_of(const GemmParams* ps, int n, int bm, int bn) {
+  long long t = 0;
+  for (int i = 0; i < n && i < kGemmGroupMax; ++i)
+    t += (long long)((ps[i].M + bm - 1) / bm) * ((ps[i].N + bn - 1) / bn);
+  return t;
 }
 
 }  // namespace
 
-// Tile shapes are chosen for the shard products of the 7B-class layer on 256 CUs
-// (one workgroup per CU): gate+up (M = S_loc, N = F/D = 1376) in 128 x 128 tiles makes
-// 704 tiles, 2.75 full rounds instead of 1.4 with 256 x 128 (measured 5 % slower
-// despite the lower L2 traffic), with a 3-slot ring (144 KB) because its 48 KB per
-// K step of operands otherwise arrive late; Q/K/V (N = 3 d H_s = 1536) in 256 x 192
-// tiles makes exactly 256; down / O-proj (N = h = 4096) in 256 x 256 tiles makes 512.
+// Tile shapes are chosen for the grouped shard products of the 7B-class layer on 256
+// CUs (one workgroup per CU).  Gate+up (M = S_loc, N = F/D = 1376 per shard, 8 shards
+// per launch) takes the deep-ring 256 x 128 tiles when they make at least 4 rounds
+// (S_loc = 8192: 2816 tiles), else 128 x 128 two-wavefront tiles with a 3-slot ring;
+// Q/K/V (N = 3 d H_s = 1536 per shard) 256 x 192 tiles; down / O-proj (N = h = 4096)
+// 256 x 256 tiles (512 at S_loc = 8192), their contraction split when that makes fewer
+// tiles than CUs.
+constexpr long long kCus = 256;
+
 hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s) {
-  return launch<128, 128, 2, 4, false, EPI_SWIGLU, 3>(p, s);
+  return launch_gemm_swiglu_group(&p, 1, s);
 }
 
-hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s) {
-  return launch<256, 256, 2, 4, true, EPI_ACC, 2>(p, s);
+hipError_t launch_gemm_swiglu_group(const GemmParams* ps, int n, hipStream_t s) {
+  if (tiles_of(ps, n, 256, 128) >= 4 * kCus) return launch_dr_group<256, 128, EPI_SWIGLU, 4>(ps, n, s);
+  if (n == 1) return launch<128, 128, 2, 4, false, EPI_SWIGLU, 3>(ps[0], s);
+  return launch_group<128, 128, 2, 4, false, EPI_SWIGLU, 3>(ps, n, s);
+}
+
+// Below one 256 x 256 output tile per CU (short sequences: M = S_loc = 1024 and N = h =
+// 4096 make 64) the contraction is split into ranges, enough (tile, range) items for
+// every CU with at least 16 steps of 64 per range; the partial products go through an
+// fp32 workspace and a reduction kernel that applies the epilogue.
+int gemm_nn_acc_splits(int M, int N, int K) {
+  const long long tiles = (long long)((M + 255) / 256) * ((N + 255) / 256);
+  if (tiles <= 0 || tiles >= kCus || N % 4 != 0) return 1;
+  int splits = (int)((kCus + tiles - 1) / tiles);
+  const int max_splits = K / BK / 16;
+  if (splits > max_splits) splits = max_splits;
+  return splits > 1 ? splits : 1;
+}
+
+hipError_t launch_gemm_nn_acc(const GemmParams& p, float* part, hipStream_t s) {
+  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  const int splits = gemm_nn_acc_splits(p.M, p.N, p.K);
+  if (splits == 1) {
+    GemmParams q = p;
+    q.k_splits = 1;
+    return launch<256, 256, 2, 4, true, EPI_ACC, 2>(q, s);
+  }
+  if (!part) {  // no workspace: the whole contraction per tile, on 128 x 128 tiles
+    GemmParams q = p;
+    q.k_splits = 1;
+    return launch<128, 128, 2, 4, true, EPI_ACC, 2>(q, s);
+  }
+  GemmParams q = p;
+  q.k_splits = splits;
+  q.part = part;
+  hipError_t e = launch<256, 256, 2, 4, true, EPI_ACC, 2>(q, s);
+  if (e != hipSuccess) return e;
+  const long long threads = (long long)p.M * (p.N / 4);
+  void* args[] = {&q};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&splitk_reduce_kernel),
+                         dim3((unsigned)((threads + 255) / 256)), dim3(256), args, 0, s);
 }
 
 // SwiGLU backward (M = S_loc, N = F/D): 128 x 128 tiles with five 16 KB operand panels
@@ -547,10 +939,17 @@ hipError_t launch_gemm_nn_acc_small_group(const GemmParams* ps, int n, hipStream
 // shapes; short sequences) would leave CUs idle with 256 x 192 tiles: below one tile per
 // CU they take 128 x 128 tiles.
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s) {
-  constexpr long long kCus = 256;
-  const long long big = (long long)((p.M + 255) / 256) * ((p.N + 191) / 192);
-  if (big < kCus) return launch<128, 128, 2, 4, false, EPI_QKV, 2>(p, s);
-  return launch<256, 192, 4, 2, false, EPI_QKV, 2>(p, s);
+  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  return launch_gemm_qkv_group(&p, 1, s);
+}
+
+hipError_t launch_gemm_qkv_group(const GemmParams* ps, int n, hipStream_t s) {
+  if (tiles_of(ps, n, 256, 192) < kCus) {
+    if (n == 1) return launch<128, 128, 2, 4, false, EPI_QKV, 2>(ps[0], s);
+    return launch_group<128, 128, 2, 4, false, EPI_QKV, 2>(ps, n, s);
+  }
+  if (n == 1) return launch<256, 192, 4, 2, false, EPI_QKV, 2>(ps[0], s);
+  return launch_group<256, 192, 4, 2, false, EPI_QKV, 2>(ps, n, s);
 }
 
 }  // namespace tsp

@@ -6,6 +6,11 @@
 
 namespace tsp {
 
+// Most operand pairs of one multi-part contraction, and most products of one grouped
+// launch (launch_gemm_*_group).
+constexpr int kGemmPartsMax = 8;
+constexpr int kGemmGroupMax = 8;
+
 // Parameters of the bf16 MFMA GEMM family: C[M, N] = A[M, K] * B, fp32 accumulation.
 // B is [N, K] row-major ("NT", both operands contraction-contiguous) or [K, N]
 // row-major ("NN").  The epilogue decides what C becomes.
@@ -17,19 +22,22 @@ struct GemmParams {
   const uint16_t* B2;  // SwiGLU (both directions): the up-projection operand, layout of B
   int M, N, K;         // K: contraction length, a multiple of 64
   int Kb_rows;         // [K, N] operands: rows actually present (rows >= Kb_rows are clamped)
-  // Two-part contraction ([K, N] products only): contraction indices k >= k_split come
-  // from A_hi (columns k - k_split, row stride lda) and B_hi (rows k - k_split, clamped
-  // at Kb_rows_hi), the ones below from A and B.  k_split is a multiple of 64; A_hi ==
-  // nullptr means one part.
-  const uint16_t* A_hi;
-  const uint16_t* B_hi;
-  int k_split;
-  int Kb_rows_hi;
+  // Multi-part contraction ([K, N] products only): with n_parts >= 2 the contraction
+  // indices form n_parts consecutive ranges of k_part each (k_part a multiple of 64,
+  // K = n_parts k_part); index k of range i = k / k_part reads column k - i k_part of
+  // A_part[i] (row stride lda) and row k - i k_part of B_part[i] (row stride ldb, rows
+  // >= Kb_rows clamped).  n_parts <= 1: one part, A and B.
+  int n_parts;
+  int k_part;
+  const uint16_t* A_part[kGemmPartsMax];
+  const uint16_t* B_part[kGemmPartsMax];
 
   // SwiGLU epilogue: H[m, n] = bf16( SiLU(C_gate) * C_up ) for n < N, and 0 for
-  // N <= n < ldh (the zero padding that lets the down projection contract over ldh).
+  // N <= n < h_cols (the zero padding that lets the down projection contract over
+  // h_cols), row stride ldh; h_cols == 0 means h_cols = ldh.
   uint16_t* H;
   int ldh;
+  int h_cols;
 
   // SwiGLU backward (fused products G = A B^T, U = A B2^T and dHs = A2 B3^T, all NT
   // with the same K): with s = SiLU(G), s' its derivative,
@@ -53,6 +61,13 @@ struct GemmParams {
   int ldr;
   uint16_t* U;
   int ldu;
+  // Split contraction (accumulate products of launch_gemm_nn_acc): with k_splits > 1
+  // the K/64 contraction steps are cut into k_splits consecutive ranges (range c: steps
+  // [c nk / k_splits, (c + 1) nk / k_splits)), each written as an fp32 partial product to
+  // part + c M N (row stride N); a second kernel then forms Y = base + the partials
+  // summed in range order (and U), as above.  Set by launch_gemm_nn_acc.
+  int k_splits;
+  float* part;
 
   // Q/K/V epilogue: columns [0, nq) -> Q[m, n] = bf16(q_scale C[m, n]) (the factor
   // applied to the fp32 product, so Q is rounded once); [nq, nq+nkv) -> K buffer;
@@ -76,16 +91,25 @@ struct GemmParams {
 };
 
 hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s);
+// Up to kGemmGroupMax independent products of launch_gemm_swiglu's form in one launch
+// (each must have M, N > 0; the tiles of product i follow those of the ones before it).
+hipError_t launch_gemm_swiglu_group(const GemmParams* ps, int n, hipStream_t s);
 hipError_t launch_gemm_swiglu_bwd(const GemmParams& p, hipStream_t s);
-hipError_t launch_gemm_nn_acc(const GemmParams& p, hipStream_t s);
+// The accumulate epilogue over [K, N] operands.  Products with fewer 256 x 256 output
+// tiles than CUs split their contraction (gemm_nn_acc_splits ranges) through an fp32
+// workspace `part` of at least splits * M * N floats (unused when splits == 1); without
+// one (part == nullptr) they run unsplit on 128 x 128 tiles.
+hipError_t launch_gemm_nn_acc(const GemmParams& p, float* part, hipStream_t s);
+int gemm_nn_acc_splits(int M, int N, int K);
 // The accumulate epilogue on 128 x 128 tiles, for products with few output tiles
 // (the weight gradients: F/D x h outputs).
 hipError_t launch_gemm_nn_acc_small(const GemmParams& p, hipStream_t s);
 // Up to kGemmGroupMax independent products of launch_gemm_nn_acc_small's form in one
 // launch (each must have M, N > 0).
-constexpr int kGemmGroupMax = 6;
 hipError_t launch_gemm_nn_acc_small_group(const GemmParams* ps, int n, hipStream_t s);
 hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s);
+// Up to kGemmGroupMax products of launch_gemm_qkv's form in one launch.
+hipError_t launch_gemm_qkv_group(const GemmParams* ps, int n, hipStream_t s);
 
 // Causal flash attention of one rank's queries for the heads of one shard.
 //   Q [B, S_loc, H_s, d] bf16, the queries times softmax scale * log2(e) (rounded to

@@ -30,7 +30,13 @@ struct Dims {
   float scale;
   bool zz;     // zigzag layout: local rows = [chunk p; chunk 2D-1-p] of S/(2D) tokens each
   int s_c;     // S_loc / 2 (zigzag chunk length)
+  int G;       // forward shard steps per grouped launch (1 .. min(D, kGroupMax))
 };
+
+// Most shard steps of one grouped launch (the number of operand pairs one product's
+// multi-part contraction, and one grouped launch, can hold).
+constexpr int kGroupMax = tsp::kGemmGroupMax < tsp::kGemmPartsMax ? tsp::kGemmGroupMax
+                                                                  : tsp::kGemmPartsMax;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -47,6 +53,8 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
   if (s->layout != 0 && s->layout != 1) return TSP_ERR_UNSUPPORTED;
   if (s->layout == 1 && s->seq % (2 * s->degree) != 0) return TSP_ERR_SHAPE;
   if (s->head_dim != 64 && s->head_dim != 128) return TSP_ERR_UNSUPPORTED;
+  if (s->group_steps < 0) return TSP_ERR_SHAPE;
+  if (s->group_steps > kGroupMax) return TSP_ERR_UNSUPPORTED;
   if (s->hidden % 8 != 0 || (s->ffn / s->degree) % 8 != 0) return TSP_ERR_UNSUPPORTED;
   o->B = s->batch;
   o->S = s->seq;
@@ -68,24 +76,43 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
   o->scale = s->softmax_scale > 0.f ? s->softmax_scale : 1.0f / sqrtf((float)s->head_dim);
   o->zz = s->layout == 1;
   o->s_c = o->s_loc / 2;
+  o->G = s->group_steps > 0 ? s->group_steps : kGroupMax;
+  if (o->G > o->D) o->G = o->D;
   return TSP_OK;
 }
 
-// Workspace regions (each 256-byte aligned):
-//   MLP:   Hs of two ring steps, [M, F/D rounded up to 64] bf16 each (zero-padded columns)
-//   ATTN:  Q [M, H_s d] bf16, A of two shard steps [M, H_s d] bf16 each
+// Forward workspace regions (each 256-byte aligned), for groups of G shard steps:
+//   MLP:   Hs of the G ring steps of a group side by side, [M, G x (F/D rounded up to
+//          64)] bf16 (zero-padded columns), then the down projection's fp32 partial
+//          products when its contraction is split (short sequences)
+//   ATTN:  Q and A of the G shard steps of a group, [M, G H_s d] bf16 each, then the
+//          attention's key-range partials, then the output projection's partials
 //   LAYER: u [M, h] bf16, then max(MLP, ATTN)
-// (with D = 1 there is one step and the second buffer is not used)
 //
-// The down and output projections run once per two steps, over both steps' operands
-// (Y += [Hs Hs'] [W2; W2'] = Hs W2 + Hs' W2'): Y is then read and written once per
-// pair instead of once per step.  The two shards involved are the current one and its
-// predecessor, which a streaming schedule holds anyway while the next one arrives; the
-// sum differs from the step-by-step one only in fp32 rounding order.
-constexpr int kPair = 2;
-size_t ws_mlp(const Dims& d) {
-  return (d.D > 1 ? kPair : 1) * align_up((size_t)d.M * d.fs_pad * 2);
+// A group's products run as one launch each: the gate+up (and Q/K/V) products of its
+// G shards as one grouped launch, and the down (output) projection as one product over
+// the G shards' operands (Y += [Hs_1 .. Hs_G] [W2_1; ..; W2_G] = sum of Hs_i W2_i), so Y
+// is read and written once per group instead of once per step, and the attention of
+// the group's G H_s heads as one launch.  The steps of a group are consecutive in the
+// schedule's order and their operand pairs are laid out in that order along the
+// contraction; the sum differs from the step-by-step one only in fp32 rounding order.
+// In a streaming schedule G is the number of shards held at once; with every shard
+// resident (one GPU), the default groups min(D, kGroupMax) steps.
+constexpr int kPair = 2;  // the backward's weight and dX products of two steps at once
+// fp32 partial products of a split down (output) projection over groups of n steps of
+// k_step contraction columns each, for the group sizes that occur.
+size_t split_part_bytes(const Dims& d, int k_step) {
+  size_t most = 0;
+  for (const int n : {d.G, d.D % d.G}) {
+    if (n == 0) continue;
+    const int splits = tsp::gemm_nn_acc_splits((int)d.M, d.h, n * k_step);
+    const size_t b = splits > 1 ? (size_t)splits * d.M * d.h * 4 : 0;
+    if (b > most) most = b;
+  }
+  return align_up(most);
 }
+size_t ws_mlp_hs(const Dims& d) { return align_up((size_t)d.M * d.G * d.fs_pad * 2); }
+size_t ws_mlp(const Dims& d) { return ws_mlp_hs(d) + split_part_bytes(d, d.fs_pad); }
 // Attention workspace: Q of the current shard and the attention output A (bf16
 // [M, H_s d] each), then the key-range partials when the shard's attention is split.
 // The rank's query rows as segments of consecutive global positions (Algorithm 1):
@@ -114,23 +141,39 @@ void attn_segments(const Dims& d, AttnParams* ap) {
   }
 }
 
+// Key ranges of the forward attention over the n H_s heads of a group of n shards.
+int attn_group_split(const Dims& d, int n, int* split_len) {
+  AttnParams ap = {};
+  attn_segments(d, &ap);
+  ap.heads = n * d.hs;
+  return tsp::attn_split_count(ap, split_len);
+}
 struct AttnWs {
-  size_t q, a, a2, po, pml, total;  // byte offsets and total size
-  int n_split, split_len;
+  size_t q, a, po, pml, proj, total;  // byte offsets and total size
 };
 AttnWs attn_ws(const Dims& d) {
   AttnWs w;
-  AttnParams ap = {};
-  attn_segments(d, &ap);
-  w.n_split = tsp::attn_split_count(ap, &w.split_len);
-  const size_t rows = (size_t)d.M * d.hs;
-  const size_t part = w.n_split > 1 ? (size_t)w.n_split * rows : 0;
+  // Partials for the widest need among the group sizes that occur (G, and D mod G for
+  // a last, smaller group).
+  size_t part = 0;
+  for (const int n : {d.G, d.D % d.G}) {
+    if (n == 0) continue;
+    int len = 0;
+    const int ns = attn_group_split(d, n, &len);
+    const size_t p = ns > 1 ? (size_t)ns * d.M * n * d.hs : 0;
+    if (p > part) part = p;
+  }
+  const size_t qa = align_up((size_t)d.M * d.G * d.hs * d.d * 2);
   w.q = 0;
-  w.a = align_up(rows * d.d * 2);
-  w.a2 = w.a + align_up(rows * d.d * 2);
-  w.po = d.D > 1 ? w.a2 + align_up(rows * d.d * 2) : w.a2;
+  w.a = qa;
+  w.po = 2 * qa;
   w.pml = w.po + align_up(part * d.d * 4);
-  w.total = w.pml + align_up(part * 2 * 4);
+  // The output projection's partials reuse the key-range partials' space: the combine
+  // kernel has consumed those before the projection starts (same stream).
+  w.proj = w.po;
+  const size_t after_attn = w.pml + align_up(part * 2 * 4);
+  const size_t after_proj = w.proj + split_part_bytes(d, d.hs * d.d);
+  w.total = after_attn > after_proj ? after_attn : after_proj;
   return w;
 }
 size_t ws_attn(const Dims& d) { return attn_ws(d).total; }
@@ -294,57 +337,68 @@ void timer_end(int kind, long slot, hipStream_t st) {
 // ----------------------------------------------------------------- launch sequences
 
 // Algorithm 2 on an already validated problem.  Ring step t uses shard (p - t) mod D;
-// the down projections of steps 2i and 2i + 1 run as one product (Hs of step t in
-// buffer t mod 2), an odd last step on its own.
+// the steps run in groups of G consecutive ones (the last group may be smaller): the
+// group's gate+up products as one grouped launch (Hs of its i-th step in columns
+// [i F/D_pad, (i + 1) F/D_pad) of the workspace), then one down projection over the
+// group's shards.
 tsp_status run_mlp(const Dims& d, const uint16_t* x, const uint16_t* const* wg,
                    const uint16_t* const* wu, const uint16_t* const* wd, float* y,
-                   int accumulate, uint16_t* hs_ws, hipStream_t st) {
-  const size_t hs_elems = align_up((size_t)d.M * d.fs_pad * 2) / 2;
-  int j_prev = 0;
-  bool first_down = true;
-  for (int t = 0; t < d.D; ++t) {
-    const int j = ((d.p - t) % d.D + d.D) % d.D;
-    uint16_t* hs = hs_ws + (size_t)(t % kPair) * hs_elems;
-    GemmParams up = {};
-    up.A = x;
-    up.lda = d.h;
-    up.B = wg[j];
-    up.B2 = wu[j];
-    up.ldb = d.h;
-    up.M = (int)d.M;
-    up.N = d.fs;
-    up.K = d.h;
-    up.H = hs;
-    up.ldh = d.fs_pad;
-    TSP_LAUNCH(TSP_KERNEL_GATE_UP, st, tsp::launch_gemm_swiglu(up, st));
-
-    const bool second = t % kPair == 1;
-    if (second || t == d.D - 1) {
-      GemmParams dn = {};
-      dn.A = second ? hs_ws : hs;
-      dn.lda = d.fs_pad;
-      dn.B = wd[second ? j_prev : j];
-      dn.ldb = d.h;
-      dn.M = (int)d.M;
-      dn.N = d.h;
-      dn.K = d.fs_pad;  // padded columns of Hs are zero; W2 rows past fs are clamped
-      dn.Kb_rows = d.fs;
-      if (second) {
-        dn.A_hi = hs;
-        dn.B_hi = wd[j];
-        dn.k_split = d.fs_pad;
-        dn.Kb_rows_hi = d.fs;
-        dn.K = 2 * d.fs_pad;
-      }
-      dn.Y = y;
-      dn.ldy = d.h;
-      dn.accumulate = (!first_down || accumulate) ? 1 : 0;
-      first_down = false;
-      TSP_LAUNCH(TSP_KERNEL_DOWN, st, tsp::launch_gemm_nn_acc(dn, st));
+                   int accumulate, char* ws, hipStream_t st) {
+  uint16_t* hs_ws = reinterpret_cast<uint16_t*>(ws);
+  float* part = reinterpret_cast<float*>(ws + ws_mlp_hs(d));
+  for (int t0 = 0; t0 < d.D; t0 += d.G) {
+    const int n = d.D - t0 < d.G ? d.D - t0 : d.G;
+    GemmParams up[tsp::kGemmGroupMax] = {};
+    GemmParams dn = {};
+    for (int i = 0; i < n; ++i) {
+      const int t = t0 + i, j = ((d.p - t) % d.D + d.D) % d.D;
+      GemmParams& u = up[i];
+      u.A = x;
+      u.lda = d.h;
+      u.B = wg[j];
+      u.B2 = wu[j];
+      u.ldb = d.h;
+      u.M = (int)d.M;
+      u.N = d.fs;
+      u.K = d.h;
+      u.H = hs_ws + (size_t)i * d.fs_pad;
+      u.ldh = n * d.fs_pad;
+      u.h_cols = d.fs_pad;
+      dn.A_part[i] = u.H;
+      dn.B_part[i] = wd[j];
     }
-    j_prev = j;
+    TSP_LAUNCH(TSP_KERNEL_GATE_UP, st, tsp::launch_gemm_swiglu_group(up, n, st));
+    dn.A = hs_ws;
+    dn.lda = n * d.fs_pad;
+    dn.B = dn.B_part[0];
+    dn.ldb = d.h;
+    dn.M = (int)d.M;
+    dn.N = d.h;
+    dn.K = n * d.fs_pad;  // padded columns of Hs are zero; W2 rows past fs are clamped
+    dn.Kb_rows = d.fs;
+    dn.n_parts = n;
+    dn.k_part = d.fs_pad;
+    dn.Y = y;
+    dn.ldy = d.h;
+    dn.accumulate = (t0 > 0 || accumulate) ? 1 : 0;
+    TSP_LAUNCH(TSP_KERNEL_DOWN, st, tsp::launch_gemm_nn_acc(dn, part, st));
   }
   return TSP_OK;
+}
+
+// Two-part contraction [A0 A1] [B0; B1] (row strides lda, ldb; B rows >= kb_rows of each
+// part clamped), each part k_part wide.
+void set_two_parts(GemmParams* p, const uint16_t* a0, const uint16_t* b0, const uint16_t* a1,
+                   const uint16_t* b1, int k_part) {
+  p->A = a0;
+  p->B = b0;
+  p->A_part[0] = a0;
+  p->B_part[0] = b0;
+  p->A_part[1] = a1;
+  p->B_part[1] = b1;
+  p->n_parts = 2;
+  p->k_part = k_part;
+  p->K = 2 * k_part;
 }
 
 // Backward of run_mlp (same ring order).  Per shard: one fused GEMM for G, U, dHs and
@@ -390,22 +444,16 @@ tsp_status run_mlp_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     // ([M, F/D] x [F/D, h] twice; padded columns of dG, dU are zero).
     {
       GemmParams p = {};
-      p.A = dg;
+      set_two_parts(&p, dg, wg[j], du, wu[j], d.fs_pad);
       p.lda = d.fs_pad;
-      p.B = wg[j];
       p.ldb = d.h;
       p.Kb_rows = d.fs;
-      p.A_hi = du;
-      p.B_hi = wu[j];
-      p.k_split = d.fs_pad;
-      p.Kb_rows_hi = d.fs;
       p.M = (int)d.M;
       p.N = d.h;
-      p.K = 2 * d.fs_pad;
       p.Y = dx;
       p.ldy = d.h;
       p.accumulate = (t > 0 || accumulate) ? 1 : 0;
-      TSP_LAUNCH(TSP_KERNEL_BWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+      TSP_LAUNCH(TSP_KERNEL_BWD_DX, st, tsp::launch_gemm_nn_acc(p, nullptr, st));
     }
     // dW (+)= (dG^T | dU^T | Hs^T) (X | X | dY): [F/D, M] x [M, h], padded rows are zero;
     // the three products of steps 2i and 2i + 1 in one launch (an odd last step alone).
@@ -468,22 +516,32 @@ GemmParams qkv_params(const Dims& d, const uint16_t* x, const uint16_t* shard, i
   return g;
 }
 
-// Algorithm 1 (contiguous chunks).  `residual` (bf16 [M, h]) initialises Y at the
-// first shard instead of zero / the old Y; `u_out` receives bf16(Y) after the last.
+// Algorithm 1 on a validated problem.  `residual` (bf16 [M, h]) initialises Y at the
+// first output projection instead of zero / the old Y; `u_out` receives bf16(Y) after
+// the last.  The shards run in groups of G consecutive ones (the last may be smaller):
+// per group one grouped Q/K/V launch (Q of its i-th shard in columns [i H_s d,
+// (i + 1) H_s d) of the workspace, i.e. [M, n H_s, d] for a group of n), one attention
+// launch over the group's n H_s heads (kv heads r0 K_s .. (r0 + n) K_s - 1), and one
+// output projection over the group's shards.
 tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
                     uint16_t* kb, uint16_t* vb, float* y, int accumulate,
                     const uint16_t* residual, uint16_t* u_out, char* ws, hipStream_t st) {
   const int qd = d.hs * d.d, kd = d.ks * d.d;
+  const size_t wo = (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T block [H_s d, h] of a shard
   const AttnWs aw = attn_ws(d);
   uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + aw.q);
-  // A of shard r in buffer r mod 2; the output projections of shards 2i and 2i + 1 run
-  // as one product, an odd last shard on its own.
-  uint16_t* a_buf[kPair] = {reinterpret_cast<uint16_t*>(ws + aw.a),
-                            reinterpret_cast<uint16_t*>(ws + aw.a2)};
-  for (int r = 0; r < d.D; ++r) {
-    uint16_t* a_ws = a_buf[r % kPair];
-    GemmParams g = qkv_params(d, x, wa[r], r, q_ws, kb, vb, true);
-    TSP_LAUNCH(TSP_KERNEL_QKV, st, tsp::launch_gemm_qkv(g, st));
+  uint16_t* a_ws = reinterpret_cast<uint16_t*>(ws + aw.a);
+  for (int r0 = 0; r0 < d.D; r0 += d.G) {
+    const int n = d.D - r0 < d.G ? d.D - r0 : d.G;
+    GemmParams g[tsp::kGemmGroupMax] = {};
+    GemmParams o = {};
+    for (int i = 0; i < n; ++i) {
+      g[i] = qkv_params(d, x, wa[r0 + i], r0 + i, q_ws + (size_t)i * qd, kb, vb, true);
+      g[i].ldq = n * qd;
+      o.A_part[i] = a_ws + (size_t)i * qd;
+      o.B_part[i] = wa[r0 + i] + wo;
+    }
+    TSP_LAUNCH(TSP_KERNEL_QKV, st, tsp::launch_gemm_qkv_group(g, n, st));
 
     AttnParams ap = {};
     ap.Q = q_ws;
@@ -491,50 +549,42 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     ap.Vb = vb;
     ap.O = a_ws;
     attn_segments(d, &ap);
+    ap.heads = n * d.hs;
     ap.group = d.g;
     ap.head_dim = d.d;
     ap.seq = d.S;
     ap.n_kv = d.nkv;
-    ap.kv_head0 = r * d.ks;
-    ap.n_split = aw.n_split;
-    ap.split_len = aw.split_len;
-    ap.part_rows = (long long)d.M * d.hs;
+    ap.kv_head0 = r0 * d.ks;
+    ap.n_split = attn_group_split(d, n, &ap.split_len);
+    ap.part_rows = (long long)d.M * ap.heads;
     ap.part_o = reinterpret_cast<float*>(ws + aw.po);
     ap.part_ml = reinterpret_cast<float*>(ws + aw.pml);
     TSP_LAUNCH(TSP_KERNEL_ATTN, st, tsp::launch_flash_attn(ap, st));
 
-    const bool second = r % kPair == 1;
-    if (!second && r != d.D - 1) continue;
-    const size_t wo = (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T block [H_s d, h]
-    GemmParams o = {};
-    o.A = a_buf[0];
-    o.lda = qd;
-    o.B = wa[second ? r - 1 : r] + wo;
+    o.A = a_ws;
+    o.lda = n * qd;
+    o.B = o.B_part[0];
     o.ldb = d.h;
     o.M = (int)d.M;
     o.N = d.h;
-    o.K = qd;
+    o.K = n * qd;
     o.Kb_rows = qd;
-    if (second) {
-      o.A_hi = a_buf[1];
-      o.B_hi = wa[r] + wo;
-      o.k_split = qd;
-      o.Kb_rows_hi = qd;
-      o.K = 2 * qd;
-    }
+    o.n_parts = n;
+    o.k_part = qd;
     o.Y = y;
     o.ldy = d.h;
-    const bool first_proj = r < kPair;
-    o.accumulate = (!first_proj || accumulate) ? 1 : 0;
-    if (first_proj && residual) {
+    const bool first = r0 == 0, last = r0 + n == d.D;
+    o.accumulate = (!first || accumulate) ? 1 : 0;
+    if (first && residual) {
       o.R = residual;
       o.ldr = d.h;
     }
-    if (r == d.D - 1 && u_out) {
+    if (last && u_out) {
       o.U = u_out;
       o.ldu = d.h;
     }
-    TSP_LAUNCH(TSP_KERNEL_OPROJ, st, tsp::launch_gemm_nn_acc(o, st));
+    TSP_LAUNCH(TSP_KERNEL_OPROJ, st,
+               tsp::launch_gemm_nn_acc(o, reinterpret_cast<float*>(ws + aw.proj), st));
   }
   return TSP_OK;
 }
@@ -652,17 +702,11 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
       p.N = d.h;
       p.K = qd;
       p.Kb_rows = qd;
-      if (second) {
-        p.A_hi = dq_buf[1];
-        p.B_hi = wq;
-        p.k_split = qd;
-        p.Kb_rows_hi = qd;
-        p.K = 2 * qd;
-      }
+      if (second) set_two_parts(&p, dq_buf[0], wa[r - 1], dq_buf[1], wq, qd);
       p.Y = dx;
       p.ldy = d.h;
       p.accumulate = (r >= kPair || accumulate) ? 1 : 0;
-      TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+      TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, nullptr, st));
     }
 
     TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
@@ -702,22 +746,16 @@ tsp_status run_attn_kv_bwd(const Dims& d, const uint16_t* x, const uint16_t* con
     const uint16_t* gv = dvl + (size_t)r * kd;
     {
       GemmParams p = {};  // dX (+)= dK W_K^(r) + dV W_V^(r), one product over both
-      p.A = gk;
+      set_two_parts(&p, gk, wa[r] + (size_t)qd * d.h, gv, wa[r] + (size_t)(qd + kd) * d.h, kd);
       p.lda = ld;
-      p.B = wa[r] + (size_t)qd * d.h;
       p.ldb = d.h;
       p.Kb_rows = kd;
-      p.A_hi = gv;
-      p.B_hi = wa[r] + (size_t)(qd + kd) * d.h;
-      p.k_split = kd;
-      p.Kb_rows_hi = kd;
       p.M = (int)d.M;
       p.N = d.h;
-      p.K = 2 * kd;
       p.Y = dx;
       p.ldy = d.h;
       p.accumulate = (r > 0 || accumulate) ? 1 : 0;
-      TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, st));
+      TSP_LAUNCH(TSP_KERNEL_ABWD_DX, st, tsp::launch_gemm_nn_acc(p, nullptr, st));
     }
     // W_K block (+)= dK^T X;  W_V block (+)= dV^T X: [K_s d, M] x [M, h], one launch.
     GemmParams q[2] = {};
@@ -751,9 +789,10 @@ tsp_status run_attn_kv_bwd(const Dims& d, const uint16_t* x, const uint16_t* con
 // taken once per device with that device current, and only that address is used.
 //
 // Nothing in it needs clearing: every kernel writes each scratch element it later reads
-// in the same call (Q, A, the gated product including its zero padding, bf16(u), and
-// the attention key-range partials, which every (range, query tile) workgroup writes
-// even when none of its keys is visible).
+// in the same call (Q, A, the gated product including its zero padding, bf16(u), the
+// attention key-range partials, which every (range, query tile) workgroup writes even
+// when none of its keys is visible, and the split projections' partial products, which
+// every (range, output tile) workgroup writes in full).
 static __device__ __align__(256) char scratch[TSP_NOALLOC_SCRATCH_BYTES];
 
 constexpr int kMaxDevices = 64;
@@ -803,8 +842,7 @@ tsp_status run_layer(const Dims& d, const uint16_t* x_loc, const uint16_t* const
   // writes bf16(u).
   TSP_TRY(run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, 0, x_loc, u_ws, rest, stream));
   // y = u + MLP(bf16 u): the MLP accumulates onto Y, which holds u.
-  return run_mlp(d, u_ws, w_gate, w_up, w_down, y_loc, 1, reinterpret_cast<uint16_t*>(rest),
-                 stream);
+  return run_mlp(d, u_ws, w_gate, w_up, w_down, y_loc, 1, rest, stream);
 }
 
 }  // namespace
@@ -840,8 +878,8 @@ tsp_status tsp_mlp_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
   TSP_TRY(check_ptr(ws));
   if (ws_bytes < ws_mlp(d)) return TSP_ERR_WORKSPACE;
   if (d.M == 0) return TSP_OK;
-  return run_mlp(d, x_loc, w_gate, w_up, w_down, y_loc, accumulate,
-                 static_cast<uint16_t*>(ws), stream);
+  return run_mlp(d, x_loc, w_gate, w_up, w_down, y_loc, accumulate, static_cast<char*>(ws),
+                 stream);
 }
 
 tsp_status tsp_mlp_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,

@@ -46,17 +46,19 @@ class RankProblem:
 
     ``x_full`` / ``w`` are the bf16 bit patterns of the whole-sequence input and the
     full weights (see :func:`inputs.make_x_full`, :func:`inputs.make_weights`).
-    ``softmax_scale`` is passed to every attention call (0 = the default 1/sqrt(d)).
+    ``softmax_scale`` is passed to every attention call (0 = the default 1/sqrt(d)),
+    ``group_steps`` to every forward call (0 = the library's default grouping).
     """
 
     def __init__(self, wl: Workload, x_full: np.ndarray, w: dict, p: int | None = None,
-                 device="cuda", kv_fill: float | None = 0.0, softmax_scale: float = 0.0):
+                 device="cuda", kv_fill: float | None = 0.0, softmax_scale: float = 0.0,
+                 group_steps: int = 0):
         self.wl = wl
         self.p = wl.rank if p is None else p
         self.device = device
         D = wl.degree
         # softmax_scale <= 0 selects 1/sqrt(head_dim) (tsp_shape)
-        self.shape = T.shape_of(wl, self.p, softmax_scale)
+        self.shape = T.shape_of(wl, self.p, softmax_scale, group_steps)
         # ranks whose K/V rows this rank's queries can see: the earlier ones for
         # contiguous chunks, every one for a zigzag shard
         self.kv_ranks = list(range(self.p)) if wl.layout == 0 else \

@@ -43,7 +43,7 @@ class tsp_shape(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("degree", ctypes.c_int32),
                 ("rank", ctypes.c_int32), ("layout", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float)]
+                ("softmax_scale", ctypes.c_float), ("group_steps", ctypes.c_int32)]
 
 
 def _load() -> ctypes.CDLL:
@@ -88,16 +88,16 @@ lib = _load()
 
 
 def make_shape(batch, seq, hidden, ffn, n_heads, n_kv_heads, head_dim, degree, rank,
-               layout=0, softmax_scale=0.0) -> tsp_shape:
+               layout=0, softmax_scale=0.0, group_steps=0) -> tsp_shape:
     return tsp_shape(batch, seq, hidden, ffn, n_heads, n_kv_heads, head_dim, degree, rank,
-                     layout, softmax_scale)
+                     layout, softmax_scale, group_steps)
 
 
-def shape_of(wl, rank=None, softmax_scale=0.0) -> tsp_shape:
+def shape_of(wl, rank=None, softmax_scale=0.0, group_steps=0) -> tsp_shape:
     """tsp_shape of a :class:`~paper_2604_26294_amd.workloads.Workload`."""
     return make_shape(wl.batch, wl.seq, wl.hidden, wl.ffn, wl.n_heads, wl.n_kv_heads,
                       wl.head_dim, wl.degree, wl.rank if rank is None else rank, wl.layout,
-                      softmax_scale)
+                      softmax_scale, group_steps)
 
 
 def _ptr(t) -> int | None:
@@ -201,7 +201,8 @@ def tsp_layer_rank_fwd(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf,
                                   _stream(stream)), "tsp_layer_rank_fwd")
 
 
-NOALLOC_SCRATCH_BYTES = 64 << 20  # TSP_NOALLOC_SCRATCH_BYTES
+NOALLOC_SCRATCH_BYTES = 128 << 20  # TSP_NOALLOC_SCRATCH_BYTES
+GROUP_STEPS_MAX = 8  # TSP_GROUP_STEPS_MAX
 
 
 def tsp_layer_rank_fwd_noalloc(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf, v_buf, y_loc,

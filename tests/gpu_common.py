@@ -22,9 +22,10 @@ MID_GQA64 = Workload("mid-gqa-d64", 2, 768, 512, 1376, 8, 4, 64, 4, 0, w_std=0.0
 MID_MHA128 = Workload("mid-mha-d128", 1, 1280, 1024, 2768, 8, 8, 128, 2, 1, w_std=0.03)
 MID_GQA8 = Workload("mid-gqa8-d128", 1, 512, 2048, 5504, 16, 2, 128, 2, 1, w_std=0.02)
 SINGLE = Workload("single-rank-d1", 1, 320, 512, 1024, 4, 2, 128, 1, 0, w_std=0.04)
-# An odd degree: the down and output projections run over pairs of steps, the last
-# step on its own.
+# An odd degree: grouped two steps at a time, the last step forms a group on its own.
 ODD3 = Workload("odd-degree-d3", 1, 768, 384, 1152, 6, 3, 64, 3, 2, w_std=0.05)
+# More shards than one grouped launch holds: the default grouping makes two groups of 8.
+DEG16 = Workload("degree-d16", 1, 1024, 1024, 2048, 16, 16, 64, 16, 13, w_std=0.04)
 
 
 def metrics(got, ref):

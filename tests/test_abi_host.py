@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_version_and_status_strings():
-    assert T.lib.tsp_abi_version() == 1
+    assert T.lib.tsp_abi_version() == 2
     for code, name in T.STATUS_NAMES.items():
         assert T.lib.tsp_status_str(code).decode().startswith(name)
     assert T.lib.tsp_status_str(99).decode() == "TSP_ERR_UNKNOWN"
@@ -64,6 +64,15 @@ def test_workspace_covers_intermediates(wl):
     assert akv >= kd * m_pad * 2                        # one transposed K or V gradient
     for v in (mlp, attn, layer, bwd, abwd, akv):
         assert v % 256 == 0
+    # the default groups min(D, TSP_GROUP_STEPS_MAX) steps: the gated products, Q and A of
+    # a whole group are held at once; one step at a time needs a single step's share
+    g = min(wl.degree, T.GROUP_STEPS_MAX)
+    assert mlp >= g * m * fs * 2
+    assert attn >= 2 * g * m * qd * 2
+    one = T.shape_of(wl, group_steps=1)
+    assert T.workspace_bytes(one, T.OP_MLP) < m * (fs + 64) * 2 + 256
+    assert T.workspace_bytes(one, T.OP_MLP) <= mlp
+    assert T.workspace_bytes(one, T.OP_ATTN) <= attn
 
 
 def _shape(**kw):
@@ -80,6 +89,8 @@ def _shape(**kw):
     (dict(ffn=687), 2), (dict(degree=0, rank=0), 2), (dict(batch=-1), 2),
     (dict(layout=2), 6), (dict(layout=-1), 6), (dict(layout=1, seq=258), 2),
     (dict(layout=1), 0), (dict(head_dim=32, n_heads=8), 6), (dict(ffn=680), 6),
+    (dict(group_steps=-1), 2), (dict(group_steps=T.GROUP_STEPS_MAX + 1), 6),
+    (dict(group_steps=T.GROUP_STEPS_MAX), 0), (dict(group_steps=1), 0),
 ])
 def test_shape_validation(kw, code):
     out = ctypes.c_size_t(0)
