@@ -45,11 +45,11 @@ PEAK_HBM_GBS = 8000.0
 # copy (FETCH x 2.0, WRITE x 1.0).  A record only applies to the kernel source it was taken
 # on (sha256 prefix); after any change to that source the traffic is reported as null.
 MEASURED_TRAFFIC = {
-    # flash_fwd_kernel<128, false> (73 865.1 / 34 816.0 KiB) + attn_combine_kernel<128, false>
-    # (16 910.5 / 8 192.0)
+    # flash_fwd_kernel<128, false>: one launch over 2 shards' 8 heads (4 per layer step),
+    # no key-range split (139 476.4 / 16 384.0 KiB)
     ("7b-h4096-S65536-D8", 7, "attn"): {
-        "source": "flash_attn.hip", "sha256": "656857387a5df5db",
-        "fetch_kib": 90775.6, "fetch_scale": 2.0, "write_kib": 43008.0, "write_scale": 1.0},
+        "source": "flash_attn.hip", "sha256": "00fcf5f26666c8f9",
+        "fetch_kib": 139476.4, "fetch_scale": 2.0, "write_kib": 16384.0, "write_scale": 1.0},
 }
 
 

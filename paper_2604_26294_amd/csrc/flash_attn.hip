@@ -58,6 +58,7 @@ namespace {
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kQTile = 32 * kWaves;  // queries per workgroup
+static_assert(kQTile == kAttnQueryTile, "query tile");
 constexpr int kStepKeys = 128;       // keys staged per step
 constexpr int kHalfKeys = 64;        // keys per sub-step
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (exp2 units)
@@ -135,6 +136,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   const int q0 = qt * kQTile;                    // first query of the tile, within its segment
   const int seg_rows = P.seg_rows[seg], row0 = P.seg_row0[seg], pos0 = P.seg_pos0[seg];
   const int kvh = P.kv_head0 + head / P.group;
+  const size_t ld = P.ld > 0 ? (size_t)P.ld : (size_t)P.heads * D;  // Q / O token row stride
 
   const int qloc = q0 + 32 * wave + l32;         // within the segment
   const bool qvalid = qloc < seg_rows;
@@ -155,7 +157,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   u32x4 qf[C::KS];
   {
     const uint16_t* qrow =
-        P.Q + (((size_t)b * P.s_loc + row0 + (qvalid ? qloc : 0)) * P.heads + head) * D;
+        P.Q + ((size_t)b * P.s_loc + row0 + (qvalid ? qloc : 0)) * ld + (size_t)head * D;
 #pragma unroll
     for (int s = 0; s < C::KS; ++s)
       qf[s] = qvalid ? ld16(qrow + 16 * s + 8 * hh) : u32x4{0u, 0u, 0u, 0u};
@@ -454,7 +456,8 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
 
   l_run = sum_with_partner(l_run);
   if (!qvalid) return;
-  const size_t row = ((size_t)b * P.s_loc + row0 + qloc) * P.heads + head;
+  const size_t trow = (size_t)b * P.s_loc + row0 + qloc;  // token row
+  const size_t row = trow * P.heads + head;                // (token, head) row of partials
   if (P.n_split == 1) {
     // Whole key range: normalise and write bf16 O (key 0 is visible to every query,
     // so l > 0).
@@ -464,7 +467,7 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
         P.lse[((size_t)b * P.heads + head) * P.s_loc + row0 + qloc] =
             mref + __builtin_amdgcn_logf(l_run);
     }
-    uint16_t* orow = P.O + row * D;
+    uint16_t* orow = P.O + trow * ld + (size_t)head * D;
 #pragma unroll
     for (int eb = 0; eb < C::EB; ++eb)
 #pragma unroll
@@ -520,7 +523,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams P) {
       P.lse[((size_t)b * P.heads + head) * P.s_loc + t] = m + __builtin_amdgcn_logf(l);
     }
   }
-  *reinterpret_cast<u32x2*>(P.O + row * D + 4 * c4) =
+  const long long ld = P.ld > 0 ? P.ld : (long long)P.heads * D;
+  *reinterpret_cast<u32x2*>(P.O + (row / P.heads) * ld + (row % P.heads) * D + 4 * c4) =
       u32x2{pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
 }
 
@@ -676,6 +680,7 @@ hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
     rows += p.seg_rows[k];
     n_qt += (p.seg_rows[k] + kQTile - 1) / kQTile;
   }
+  if (p.ld != 0 && (p.ld < p.heads * p.head_dim || p.ld % 8 != 0)) return hipErrorInvalidValue;
   if (rows != p.s_loc || p.n_split < 1 || p.split_len <= 0 || p.split_len % kStepKeys != 0 ||
       (p.n_split > 1 && (!p.part_o || !p.part_ml)))
     return hipErrorInvalidValue;

@@ -526,6 +526,9 @@ struct DrCfg {
   static constexpr int A_LOADS = A_BYTES / 1024 / WAVES;  // per wavefront and stage
   static constexpr int B_LOADS = B_BYTES / 1024 / WAVES;
   static constexpr int LOADS = A_LOADS + B_LOADS;
+  // Workgroups per CU the LDS ring allows (2 when it fits twice in 160 KB): with two,
+  // each SIMD interleaves two wavefronts, which must then fit in half the registers.
+  static constexpr int WAVES_PER_EU = 2 * LDS_BYTES <= 160 * 1024 ? 2 : 1;
   static_assert(STAGES >= 3 && LDS_BYTES <= 160 * 1024, "LDS ring");
   static_assert(LOADS * (STAGES - 1) < 64, "vmcnt range");
   static_assert(A_LOADS * 1024 * WAVES == A_BYTES && B_LOADS * 1024 * WAVES == B_BYTES,
@@ -695,7 +698,8 @@ __device__ __forceinline__ void gemm_tile_dr(const GemmParams& P, const int w) {
 }
 
 template <int BM, int BN, int EPI, int STAGES>
-__global__ __launch_bounds__(256) void gemm_dr_kernel(const GemmParams P) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
+    DrCfg<BM, BN, EPI, STAGES>::WAVES_PER_EU))) void gemm_dr_kernel(const GemmParams P) {
   const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
   gemm_tile_dr<BM, BN, EPI, STAGES>(P, xcd_work_index(blockIdx.x, tiles));
 }
@@ -806,7 +810,8 @@ hipError_t launch(const GemmParams& p, hipStream_t s) {
 }
 
 template <int BM, int BN, int EPI, int STAGES>
-__global__ __launch_bounds__(256) void gemm_dr_group_kernel(const GemmGroup G) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
+    DrCfg<BM, BN, EPI, STAGES>::WAVES_PER_EU))) void gemm_dr_group_kernel(const GemmGroup G) {
   int tiles[kGemmGroupMax], total = 0;
 #pragma unroll
   for (int i = 0; i < kGemmGroupMax; ++i) {

@@ -116,6 +116,8 @@ hipError_t launch_gemm_qkv_group(const GemmParams* ps, int n, hipStream_t s);
 //   bf16 once, by the projection's epilogue), so that Q K^T are base-2 logits;
 //   K/V buffers [B, S, n_kv, d] bf16 (heads
 //   kv_head0 .. kv_head0 + H_s/g - 1 are this shard's);  O [B, S_loc, H_s, d] bf16.
+//   Q and O rows may be wider than H_s d (a launch over some of the heads of a wider
+//   buffer): token row t starts ld elements after row t - 1.
 //   The local rows form n_seg segments of consecutive global positions: rows
 //   [seg_row0[k], seg_row0[k] + seg_rows[k]) sit at positions seg_pos0[k] + (row -
 //   seg_row0[k]) (one segment for contiguous chunks, two for a zigzag shard).  A query
@@ -138,6 +140,7 @@ struct AttnParams {
   int seg_rows[2];
   int seg_pos0[2];
   int kv_len;       // number of readable keys: the last segment position + 1
+  int ld;           // elements between consecutive token rows of Q and O (0: H_s d)
   // Key-range split (attn_split_count): each query tile's keys [0, n) are processed in
   // ranges [c split_len, (c + 1) split_len), c < n_split.  With n_split > 1 the ranges
   // write partial results -- part_o [n_split][part_rows][d] fp32 (unnormalised O) and
@@ -156,6 +159,8 @@ struct AttnParams {
 
 // Workgroups the attention kernel aims to launch: one per CU of an MI355X.
 constexpr int kAttnTargetWorkgroups = 256;
+// Queries per attention workgroup (one query tile).
+constexpr int kAttnQueryTile = 256;
 
 // Number of key ranges (and their length, a multiple of the key tile, in *split_len)
 // for one rank's attention (uses batch, heads and the segments of p): enough (query

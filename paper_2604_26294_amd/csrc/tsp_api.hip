@@ -141,27 +141,47 @@ void attn_segments(const Dims& d, AttnParams* ap) {
   }
 }
 
-// Key ranges of the forward attention over the n H_s heads of a group of n shards.
+// Key ranges of the forward attention over the n H_s heads of n shards.
 int attn_group_split(const Dims& d, int n, int* split_len) {
   AttnParams ap = {};
   attn_segments(d, &ap);
   ap.heads = n * d.hs;
   return tsp::attn_split_count(ap, split_len);
 }
+// Shards whose heads one attention launch of a group of n takes: the fewest whose
+// (query tile, head, batch) work items fill the GPU once (so that the workgroups on an
+// XCD start together and stream the same keys of the same head through its L2; a launch
+// of several rounds drifts out of step, as the query tiles' key counts differ, and
+// re-reads K/V), at most n.
+int attn_shards_per_launch(const Dims& d, int n) {
+  AttnParams ap = {};
+  attn_segments(d, &ap);
+  long long tiles = 0;
+  for (int k = 0; k < ap.n_seg; ++k) tiles += (ap.seg_rows[k] + tsp::kAttnQueryTile - 1) / tsp::kAttnQueryTile;
+  const long long per_shard = tiles * d.hs * d.B;
+  if (per_shard <= 0) return n;
+  const long long need = (tsp::kAttnTargetWorkgroups + per_shard - 1) / per_shard;
+  return (int)(need < n ? need : n);
+}
 struct AttnWs {
   size_t q, a, po, pml, proj, total;  // byte offsets and total size
 };
 AttnWs attn_ws(const Dims& d) {
   AttnWs w;
-  // Partials for the widest need among the group sizes that occur (G, and D mod G for
-  // a last, smaller group).
+  // Partials for the widest need among the attention launches that occur: groups of G
+  // (and D mod G for a last, smaller group), each in launches of attn_shards_per_launch
+  // shards (and a remainder).
   size_t part = 0;
   for (const int n : {d.G, d.D % d.G}) {
     if (n == 0) continue;
-    int len = 0;
-    const int ns = attn_group_split(d, n, &len);
-    const size_t p = ns > 1 ? (size_t)ns * d.M * n * d.hs : 0;
-    if (p > part) part = p;
+    const int sub = attn_shards_per_launch(d, n);
+    for (const int w : {sub, n % sub}) {
+      if (w == 0) continue;
+      int len = 0;
+      const int ns = attn_group_split(d, w, &len);
+      const size_t p = ns > 1 ? (size_t)ns * d.M * w * d.hs : 0;
+      if (p > part) part = p;
+    }
   }
   const size_t qa = align_up((size_t)d.M * d.G * d.hs * d.d * 2);
   w.q = 0;
@@ -543,23 +563,30 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     }
     TSP_LAUNCH(TSP_KERNEL_QKV, st, tsp::launch_gemm_qkv_group(g, n, st));
 
-    AttnParams ap = {};
-    ap.Q = q_ws;
-    ap.Kb = kb;
-    ap.Vb = vb;
-    ap.O = a_ws;
-    attn_segments(d, &ap);
-    ap.heads = n * d.hs;
-    ap.group = d.g;
-    ap.head_dim = d.d;
-    ap.seq = d.S;
-    ap.n_kv = d.nkv;
-    ap.kv_head0 = r0 * d.ks;
-    ap.n_split = attn_group_split(d, n, &ap.split_len);
-    ap.part_rows = (long long)d.M * ap.heads;
-    ap.part_o = reinterpret_cast<float*>(ws + aw.po);
-    ap.part_ml = reinterpret_cast<float*>(ws + aw.pml);
-    TSP_LAUNCH(TSP_KERNEL_ATTN, st, tsp::launch_flash_attn(ap, st));
+    // Attention over the group's heads, attn_shards_per_launch shards per launch (the
+    // columns of those shards within the group's Q and A).
+    const int sub = attn_shards_per_launch(d, n);
+    for (int i = 0; i < n; i += sub) {
+      const int w = n - i < sub ? n - i : sub;
+      AttnParams ap = {};
+      ap.Q = q_ws + (size_t)i * qd;
+      ap.Kb = kb;
+      ap.Vb = vb;
+      ap.O = a_ws + (size_t)i * qd;
+      attn_segments(d, &ap);
+      ap.heads = w * d.hs;
+      ap.ld = n * qd;
+      ap.group = d.g;
+      ap.head_dim = d.d;
+      ap.seq = d.S;
+      ap.n_kv = d.nkv;
+      ap.kv_head0 = (r0 + i) * d.ks;
+      ap.n_split = attn_group_split(d, w, &ap.split_len);
+      ap.part_rows = (long long)d.M * ap.heads;
+      ap.part_o = reinterpret_cast<float*>(ws + aw.po);
+      ap.part_ml = reinterpret_cast<float*>(ws + aw.pml);
+      TSP_LAUNCH(TSP_KERNEL_ATTN, st, tsp::launch_flash_attn(ap, st));
+    }
 
     o.A = a_ws;
     o.lda = n * qd;

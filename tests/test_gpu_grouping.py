@@ -12,8 +12,8 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 from paper_2604_26294_amd.harness import RankProblem  # noqa: E402
-from tests.gpu_common import (DEG16, MID_GQA64, MID_MHA128, ODD3, assert_close, gen,  # noqa: E402
-                              oracle_blocks)
+from tests.gpu_common import (DEG16, MID_GQA64, MID_MHA128, ODD3, SUBL, assert_close,  # noqa: E402
+                              gen, oracle_blocks)
 
 # (workload, rank, group_steps values); 0 is the library default, min(D, 8)
 CASES = [(MID_GQA64, 3, (1, 2, 3)), (MID_GQA64.with_layout(1), 1, (1, 3)),
@@ -53,3 +53,19 @@ def test_grouping_parity(wl, p, groups, block):
     scale = np.max(np.abs(base))
     for g, y in outs.items():
         assert np.max(np.abs(y - base)) <= 1e-2 * scale, f"G={g} vs default"
+
+
+@pytest.mark.parametrize("wl,p", [(SUBL, 2), (SUBL.with_layout(1), 1)],
+                         ids=["sub-launch-contiguous-r2", "sub-launch-zigzag-r1"])
+@pytest.mark.parametrize("block", ["attn", "layer"])
+def test_attention_launches_over_part_of_a_group(wl, p, block):
+    """A group's attention split over several launches, each over a few of the group's
+    shards (their heads' columns inside the group-wide Q and A rows)."""
+    print(f"[grouping] {wl.name} {wl.layout_name} rank {p} {block}", flush=True)
+    x_bits, w_bits = _inputs(wl)
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    prob.prefill_kv()
+    y = {"attn": prob.attn_fwd, "layer": prob.layer}[block]()
+    torch.cuda.synchronize()
+    ref = oracle_blocks(wl, x_bits, w_bits, p, blocks=(block,))[block]
+    assert_close(y.double().cpu().numpy(), ref, f"{wl.name} r{p} {block}")
