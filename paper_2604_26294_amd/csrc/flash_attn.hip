@@ -58,8 +58,8 @@ namespace {
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kQTile = 32 * kWaves;  // queries per workgroup
-static_assert(kQTile == kAttnQueryTile, "query tile");
 constexpr int kStepKeys = 128;       // keys staged per step
+static_assert(kQTile == kAttnQueryTile && kStepKeys == kAttnKeyStep, "tile sizes");
 constexpr int kHalfKeys = 64;        // keys per sub-step
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (exp2 units)
 
@@ -105,34 +105,21 @@ __device__ __forceinline__ float sum_with_partner(float x) {
   return a + b;
 }
 
+// One query tile of the kernel: tile `order` in the kernel's tile order (see
+// flash_fwd_kernel), key range `split`, query head `head` of batch entry `b`; K/V slots
+// in Ls.  Returns with every wavefront done reading Ls only after a barrier that follows
+// its last tile load (the caller's next tile may refill the slots after a barrier).
 template <int D, bool LSE>
-__global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
+__device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, const int nt0,
+                                           const int nt1, const int order, const int split,
+                                           const int head, const int b) {
   using C = FaCfg<D>;
   constexpr int KCH = C::KCH, RB = C::ROW_BYTES, TB = C::TILE_BYTES;
-  // [K slot 0][K slot 1][V slot 0][V slot 1]
-  __shared__ __attribute__((aligned(1024))) char L[4 * TB];
-  lds_char* Ls = (lds_char*)L;
-
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-
-  // Work item -> (batch, head, key range, query tile), query tile fastest, so the
-  // workgroups that share an XCD (contiguous work indices) stream the same keys of the
-  // same head through that XCD's L2.  Query tiles run over the segments' rows, last
-  // segment (latest positions, most keys) first and, within one, last tile first.
-  const int nt0 = (P.seg_rows[0] + kQTile - 1) / kQTile;
-  const int nt1 = P.n_seg > 1 ? (P.seg_rows[1] + kQTile - 1) / kQTile : 0;
-  const int n_qt = nt0 + nt1;
-  const int w = xcd_work_index(blockIdx.x, n_qt * P.n_split * P.heads * P.batch);
-  const int order = w % n_qt;
   const int seg = order < nt1 ? 1 : 0;
   const int qt = seg == 1 ? nt1 - 1 - order : nt0 - 1 - (order - nt1);
-  int rest = w / n_qt;
-  const int split = rest % P.n_split;
-  rest /= P.n_split;
-  const int head = rest % P.heads;
-  const int b = rest / P.heads;
   const int q0 = qt * kQTile;                    // first query of the tile, within its segment
   const int seg_rows = P.seg_rows[seg], row0 = P.seg_row0[seg], pos0 = P.seg_pos0[seg];
   const int kvh = P.kv_head0 + head / P.group;
@@ -492,6 +479,38 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   }
 }
 
+
+template <int D, bool LSE>
+__global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
+  using C = FaCfg<D>;
+  // [K slot 0][K slot 1][V slot 0][V slot 1]
+  __shared__ __attribute__((aligned(1024))) char L[4 * C::TILE_BYTES];
+  lds_char* Ls = (lds_char*)L;
+  // Work item -> (batch, head, key range, query tile), query tile fastest, so the
+  // workgroups that share an XCD (contiguous work indices) stream the same keys of the
+  // same head through that XCD's L2.  Query tiles run over the segments' rows, last
+  // segment (latest positions, most keys) first and, within one, last tile first.  With
+  // pair_tiles, work item i of a head takes tiles i and n_qt - 1 - i one after the other
+  // (the most and the fewest keys, the second most and second fewest, ...), so that all
+  // items cost about the same and the workgroups of a launch finish together.
+  const int nt0 = (P.seg_rows[0] + kQTile - 1) / kQTile;
+  const int nt1 = P.n_seg > 1 ? (P.seg_rows[1] + kQTile - 1) / kQTile : 0;
+  const int n_qt = nt0 + nt1;
+  const int n_items = P.pair_tiles ? (n_qt + 1) / 2 : n_qt;
+  const int w = xcd_work_index(blockIdx.x, n_items * P.n_split * P.heads * P.batch);
+  const int item = w % n_items;
+  int rest = w / n_items;
+  const int split = rest % P.n_split;
+  rest /= P.n_split;
+  const int head = rest % P.heads;
+  const int b = rest / P.heads;
+  flash_tile<D, LSE>(P, Ls, nt0, nt1, item, split, head, b);
+  if (P.pair_tiles && n_qt - 1 - item != item) {
+    __syncthreads();  // every wavefront is done with the first tile's K/V slots
+    flash_tile<D, LSE>(P, Ls, nt0, nt1, n_qt - 1 - item, split, head, b);
+  }
+}
+
 // Merges the n_split partial results of each (batch, query, head) row: with
 // M = max_c m_c, O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as bf16.
 // One thread per 4 consecutive head-dim columns of a row.
@@ -532,15 +551,12 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams P) {
 
 namespace {
 
-// Makespan, in keys visited by one workgroup plus fixed costs, of dispatching the work
-// items of a split into n key ranges of `len` keys: the kernel's work order, each XCD
-// taking its contiguous share of work indices and giving each next item to its first
-// free CU.  tile_keys lists the keys of the query tiles in the kernel's tile order.
-long long split_makespan(const int* tile_keys, int n_qt, long long bh, int n, int len) {
+// Makespan, in keys visited by one workgroup plus fixed costs, of dispatching `total`
+// work items of costs cost(w) (w in the kernel's work order): each XCD takes its
+// contiguous share of work indices and gives each next item to its first free CU.
+template <class Cost>
+long long dispatch_makespan(long long total, Cost cost) {
   constexpr int kCusPerXcd = kAttnTargetWorkgroups / kXcds;
-  constexpr long long kPieceCost = kStepKeys;      // setup and partial write: ~one step
-  constexpr long long kEmptyCost = kStepKeys / 8;  // a workgroup with no keys to visit
-  const long long total = bh * n_qt * n;
   const long long q = total / kXcds, rem = total % kXcds;
   long long worst = 0;
   for (int x = 0; x < kXcds; ++x) {
@@ -549,12 +565,7 @@ long long split_makespan(const int* tile_keys, int n_qt, long long bh, int n, in
         std::greater<long long>(), std::vector<long long>(kCusPerXcd, 0));
     const long long w0 = x * q + (x < rem ? x : rem), w1 = w0 + q + (x < rem ? 1 : 0);
     for (long long w = w0; w < w1; ++w) {
-      const int t = (int)(w % n_qt);
-      const int split = (int)((w / n_qt) % n);
-      const long long keys = min(max((long long)tile_keys[t] - (long long)split * len, 0LL),
-                                 (long long)len);
-      const long long cost = keys > 0 ? keys + kPieceCost : kEmptyCost;
-      const long long f = finish.top() + cost;
+      const long long f = finish.top() + cost(w);
       finish.pop();
       finish.push(f);
     }
@@ -566,56 +577,16 @@ long long split_makespan(const int* tile_keys, int n_qt, long long bh, int n, in
   return worst;
 }
 
-// Shapes already priced (the choice depends on these fields only); callers ask for the
-// same shape several times per entry point call.
-struct SplitKey {
-  int batch, heads, head_dim, n_seg, seg_rows[2], seg_pos0[2];
-  bool operator==(const SplitKey& o) const {
-    return batch == o.batch && heads == o.heads && head_dim == o.head_dim && n_seg == o.n_seg &&
-           seg_rows[0] == o.seg_rows[0] && seg_rows[1] == o.seg_rows[1] &&
-           seg_pos0[0] == o.seg_pos0[0] && seg_pos0[1] == o.seg_pos0[1];
-  }
+// The launch plan of a shape: key ranges (and their length) without pairing, and the
+// estimated seconds of that plan and of paired tiles without ranges.
+struct AttnPlan {
+  int n_split, split_len;
+  double sec_split, sec_pair;
 };
-struct SplitChoice {
-  SplitKey key;
-  int n, len;
-};
-std::mutex g_split_mu;
-std::vector<SplitChoice> g_split_cache;
-constexpr size_t kSplitCacheMax = 64;
 
-int attn_split_count_uncached(const AttnParams& p, int* split_len);
-
-}  // namespace
-
-int attn_split_count(const AttnParams& p, int* split_len) {
-  SplitKey key = {p.batch, p.heads, p.head_dim, p.n_seg, {0, 0}, {0, 0}};
-  for (int k = 0; k < p.n_seg && k < 2; ++k) {
-    key.seg_rows[k] = p.seg_rows[k];
-    key.seg_pos0[k] = p.seg_pos0[k];
-  }
-  {
-    std::lock_guard<std::mutex> lock(g_split_mu);
-    for (const SplitChoice& c : g_split_cache)
-      if (c.key == key) {
-        if (split_len) *split_len = c.len;
-        return c.n;
-      }
-  }
-  int len = 0;
-  const int n = attn_split_count_uncached(p, &len);
-  {
-    std::lock_guard<std::mutex> lock(g_split_mu);
-    if (g_split_cache.size() >= kSplitCacheMax) g_split_cache.erase(g_split_cache.begin());
-    g_split_cache.push_back({key, n, len});
-  }
-  if (split_len) *split_len = len;
-  return n;
-}
-
-namespace {
-
-int attn_split_count_uncached(const AttnParams& p, int* split_len) {
+AttnPlan attn_plan_uncached(const AttnParams& p) {
+  constexpr long long kPieceCost = kStepKeys;      // setup and output write: ~one step
+  constexpr long long kEmptyCost = kStepKeys / 8;  // a workgroup with no keys to visit
   // Keys of each query tile, in the kernel's order (last segment first, last tile first).
   constexpr int kMaxTiles = 1024;
   int tile_keys[kMaxTiles];
@@ -634,39 +605,94 @@ int attn_split_count_uncached(const AttnParams& p, int* split_len) {
     return (len + kStepKeys - 1) / kStepKeys * kStepKeys;
   };
   const long long bh = (long long)p.batch * p.heads;
-  int best_n = 1;
-  if (bh > 0 && n_qt <= kMaxTiles) {
-    // Candidate range counts 1..8, at least 4 key tiles per range.  Estimated time =
-    // simulated makespan x the time a workgroup spends per key + the partials' HBM
-    // traffic (written, read back and merged); the smallest wins, ties going to fewer
-    // ranges.  Per key a workgroup executes 4 kQTile d FLOPs (its Q K^T and P V rows),
-    // at the fraction of one CU's bf16 MFMA peak (2516.6 / 256 TFLOP/s) this kernel
-    // reaches (0.44 measured at 7B, S = 65536: ~30 ns per key at d = 128); the partials
-    // move at about half the HBM peak (8 TB/s).  Only the ratio of the two terms
-    // matters, so the constants need refitting only when that fraction moves a lot.
-    constexpr double kCuPeak = 2516.6e12 / 256, kPeakFraction = 0.44, kPartialBw = 4e12;
-    const double t_key = 4.0 * kQTile * p.head_dim / (kPeakFraction * kCuPeak);
-    const double bw = kPartialBw;
-    const double rows = (double)bh * p.s_loc;
-    double best = -1.0;
-    for (int n = 1; n <= 8; ++n) {
-      const int len = len_of(n);
-      if (n > 1 && len < 4 * kStepKeys) break;
-      if ((max_keys + len - 1) / len != n) continue;  // same ranges as a smaller n
-      const double traffic =
-          n > 1 ? (2.0 * n * rows * (p.head_dim + 2) * 4 + rows * p.head_dim * 2) / bw : 0.0;
-      const double t = split_makespan(tile_keys, n_qt, bh, n, len) * t_key + traffic;
-      if (best < 0 || t < best) {
-        best = t;
-        best_n = n;
-      }
+  AttnPlan plan = {1, len_of(1), 0.0, 0.0};
+  if (bh <= 0 || n_qt > kMaxTiles) return plan;
+  // Time per key of a workgroup: 4 kQTile d FLOPs (its Q K^T and P V rows) at the
+  // fraction of one CU's bf16 MFMA peak (2516.6 / 256 TFLOP/s) this kernel reaches (0.44
+  // measured at 7B, S = 65536: ~30 ns per key at d = 128).  Key-range partials move at
+  // about half the HBM peak (8 TB/s).  Only the ratio of the two matters, so the
+  // constants need refitting only when that fraction moves a lot.
+  constexpr double kCuPeak = 2516.6e12 / 256, kPeakFraction = 0.44, kPartialBw = 4e12;
+  const double t_key = 4.0 * kQTile * p.head_dim / (kPeakFraction * kCuPeak);
+  const double rows = (double)bh * p.s_loc;
+  // Key ranges: candidate counts 1..8, at least 4 key tiles per range; estimated time =
+  // simulated makespan x t_key + the partials' traffic (written, read back, merged); the
+  // smallest wins, ties going to fewer ranges.
+  double best = -1.0;
+  for (int n = 1; n <= 8; ++n) {
+    const int len = len_of(n);
+    if (n > 1 && len < 4 * kStepKeys) break;
+    if ((max_keys + len - 1) / len != n) continue;  // same ranges as a smaller n
+    const double traffic =
+        n > 1 ? (2.0 * n * rows * (p.head_dim + 2) * 4 + rows * p.head_dim * 2) / kPartialBw : 0.0;
+    const long long span = dispatch_makespan(bh * n_qt * n, [&](long long w) {
+      const int t = (int)(w % n_qt), split = (int)((w / n_qt) % n);
+      const long long keys =
+          min(max((long long)tile_keys[t] - (long long)split * len, 0LL), (long long)len);
+      return keys > 0 ? keys + kPieceCost : kEmptyCost;
+    });
+    const double sec = span * t_key + traffic;
+    if (best < 0 || sec < best) {
+      best = sec;
+      plan.n_split = n;
+      plan.split_len = len;
     }
   }
-  if (split_len) *split_len = len_of(best_n);
-  return best_n;
+  plan.sec_split = best;
+  // Paired tiles: item i takes tiles i and n_qt - 1 - i (one tile if they coincide).
+  const int n_items = (n_qt + 1) / 2;
+  const long long span = dispatch_makespan(bh * n_items, [&](long long w) {
+    const int i = (int)(w % n_items), j = n_qt - 1 - i;
+    return tile_keys[i] + kPieceCost + (j != i ? tile_keys[j] + kPieceCost : 0LL);
+  });
+  plan.sec_pair = span * t_key;
+  return plan;
+}
+
+// Shapes already planned (the plan depends on these fields only); callers ask for the
+// same shape several times per entry point call.
+struct PlanKey {
+  int batch, heads, head_dim, n_seg, seg_rows[2], seg_pos0[2];
+  bool operator==(const PlanKey& o) const {
+    return batch == o.batch && heads == o.heads && head_dim == o.head_dim && n_seg == o.n_seg &&
+           seg_rows[0] == o.seg_rows[0] && seg_rows[1] == o.seg_rows[1] &&
+           seg_pos0[0] == o.seg_pos0[0] && seg_pos0[1] == o.seg_pos0[1];
+  }
+};
+std::mutex g_plan_mu;
+std::vector<std::pair<PlanKey, AttnPlan>> g_plan_cache;
+constexpr size_t kPlanCacheMax = 64;
+
+AttnPlan attn_plan(const AttnParams& p) {
+  PlanKey key = {p.batch, p.heads, p.head_dim, p.n_seg, {0, 0}, {0, 0}};
+  for (int k = 0; k < p.n_seg && k < 2; ++k) {
+    key.seg_rows[k] = p.seg_rows[k];
+    key.seg_pos0[k] = p.seg_pos0[k];
+  }
+  {
+    std::lock_guard<std::mutex> lock(g_plan_mu);
+    for (const auto& c : g_plan_cache)
+      if (c.first == key) return c.second;
+  }
+  const AttnPlan plan = attn_plan_uncached(p);
+  std::lock_guard<std::mutex> lock(g_plan_mu);
+  if (g_plan_cache.size() >= kPlanCacheMax) g_plan_cache.erase(g_plan_cache.begin());
+  g_plan_cache.push_back({key, plan});
+  return plan;
 }
 
 }  // namespace
+
+int attn_split_count(const AttnParams& p, int* split_len) {
+  const AttnPlan plan = attn_plan(p);
+  if (split_len) *split_len = plan.split_len;
+  return plan.n_split;
+}
+
+double attn_launch_seconds(const AttnParams& p, bool pair) {
+  const AttnPlan plan = attn_plan(p);
+  return pair ? plan.sec_pair : plan.sec_split;
+}
 
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
   if (p.batch <= 0 || p.s_loc <= 0 || p.heads <= 0) return hipSuccess;
@@ -681,10 +707,12 @@ hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
     n_qt += (p.seg_rows[k] + kQTile - 1) / kQTile;
   }
   if (p.ld != 0 && (p.ld < p.heads * p.head_dim || p.ld % 8 != 0)) return hipErrorInvalidValue;
+  if (p.pair_tiles && p.n_split != 1) return hipErrorInvalidValue;
   if (rows != p.s_loc || p.n_split < 1 || p.split_len <= 0 || p.split_len % kStepKeys != 0 ||
       (p.n_split > 1 && (!p.part_o || !p.part_ml)))
     return hipErrorInvalidValue;
-  const dim3 grid(n_qt * p.n_split * p.heads * p.batch);
+  const int n_items = p.pair_tiles ? (n_qt + 1) / 2 : n_qt;
+  const dim3 grid(n_items * p.n_split * p.heads * p.batch);
   const void* fn;
   const void* combine;
   if (p.head_dim == 128) {

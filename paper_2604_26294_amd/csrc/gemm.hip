@@ -106,6 +106,18 @@ struct Cfg {
   static_assert(!NN || (BK * NN_RB / 1024) % WAVES == 0, "NN DMA cover");
 };
 
+// Output tile t of a tiles_m x tiles_n grid in the work order: blocks of kTileGroupM
+// consecutive row tiles, column tiles in order within a block and the rows of a block
+// fastest, so that the 32 consecutive tiles an XCD runs at a time span about as many row
+// as column tiles and its L2 serves each operand panel to several of them.
+constexpr int kTileGroupM = 4;
+__device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int* tm, int* tn) {
+  const int blk = t / (kTileGroupM * tiles_n), in = t - blk * kTileGroupM * tiles_n;
+  const int rows = min(kTileGroupM, tiles_m - blk * kTileGroupM);
+  *tm = blk * kTileGroupM + in % rows;
+  *tn = in / rows;
+}
+
 // Chunk swizzles of the NT and NN panels (physical chunk = logical chunk XOR swz(row)).
 __device__ __forceinline__ int nt_swz(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ int nn_swz(int row) { return 4 * (row & 3); }
@@ -331,8 +343,9 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
     split = w / tiles;
     wt = w - split * tiles;
   }
-  const int m0 = (wt / tiles_n) * BM;
-  const int n0 = (wt % tiles_n) * BN;
+  int tm, tn;
+  tile_coords(wt, (P.M + BM - 1) / BM, tiles_n, &tm, &tn);
+  const int m0 = tm * BM, n0 = tn * BN;
 
   f32x16 acc[TM][TNB];
 #pragma unroll
@@ -567,8 +580,9 @@ __device__ __forceinline__ void gemm_tile_dr(const GemmParams& P, const int w) {
   const int l32 = lane & 31, hh = lane >> 5;
 
   const int tiles_n = (P.N + BN - 1) / BN;
-  const int m0 = (w / tiles_n) * BM;
-  const int n0 = (w % tiles_n) * BN;
+  int tm, tn;
+  tile_coords(w, (P.M + BM - 1) / BM, tiles_n, &tm, &tn);
+  const int m0 = tm * BM, n0 = tn * BN;
 
   f32x16 acc[TM][TNB];
 #pragma unroll

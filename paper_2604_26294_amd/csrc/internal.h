@@ -148,6 +148,9 @@ struct AttnParams {
   // -- which a second kernel merges into O.
   int n_split;
   int split_len;
+  // With n_split = 1: each workgroup takes two query tiles of one head, the i-th most
+  // and the i-th fewest keys (equal work per workgroup).
+  int pair_tiles;
   long long part_rows;
   float* part_o;
   float* part_ml;
@@ -159,14 +162,19 @@ struct AttnParams {
 
 // Workgroups the attention kernel aims to launch: one per CU of an MI355X.
 constexpr int kAttnTargetWorkgroups = 256;
-// Queries per attention workgroup (one query tile).
+// Queries per attention workgroup (one query tile), and keys per tile step (key-range
+// lengths are multiples of it).
 constexpr int kAttnQueryTile = 256;
+constexpr int kAttnKeyStep = 128;
 
 // Number of key ranges (and their length, a multiple of the key tile, in *split_len)
 // for one rank's attention (uses batch, heads and the segments of p): enough (query
 // tile, head, batch, range) work items to fill the GPU.  Depends on the shape only, so
 // workspace sizes are known up front.
 int attn_split_count(const AttnParams& p, int* split_len);
+// Estimated seconds of one attention launch over p's heads: with the split that
+// attn_split_count chooses (pair = false), or with paired query tiles and no split.
+double attn_launch_seconds(const AttnParams& p, bool pair);
 
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s);
 

@@ -148,20 +148,47 @@ int attn_group_split(const Dims& d, int n, int* split_len) {
   ap.heads = n * d.hs;
   return tsp::attn_split_count(ap, split_len);
 }
-// Shards whose heads one attention launch of a group of n takes: the fewest whose
-// (query tile, head, batch) work items fill the GPU once (so that the workgroups on an
-// XCD start together and stream the same keys of the same head through its L2; a launch
-// of several rounds drifts out of step, as the query tiles' key counts differ, and
-// re-reads K/V), at most n.
-int attn_shards_per_launch(const Dims& d, int n) {
+// Key-range length covering every key of a launch in one range (paired tiles).
+int attn_full_len(const AttnParams& ap) {
+  const int keys = ap.seg_pos0[ap.n_seg - 1] + ap.seg_rows[ap.n_seg - 1];
+  return (keys + tsp::kAttnKeyStep - 1) / tsp::kAttnKeyStep * tsp::kAttnKeyStep;
+}
+// How a group of n shards runs its attention: launches over `width` shards each (the
+// last over the remainder), with paired query tiles or with key ranges.  A launch takes
+// the fewest shards whose work items fill the GPU once: the workgroups on an XCD then
+// start together and stream the same keys of the same head through its L2 (a launch of
+// several rounds drifts out of step, as the query tiles' key counts differ, and re-reads
+// K/V).  Pairing (tile i with tile n_qt - 1 - i: equal work per workgroup) halves the
+// work items; whichever plan the dispatch simulation of the attention launches
+// (tsp::attn_launch_seconds) prices lower for the whole group is taken.
+struct AttnLaunchPlan {
+  int width;
+  bool pair;
+};
+AttnLaunchPlan attn_launch_plan(const Dims& d, int n) {
   AttnParams ap = {};
   attn_segments(d, &ap);
   long long tiles = 0;
-  for (int k = 0; k < ap.n_seg; ++k) tiles += (ap.seg_rows[k] + tsp::kAttnQueryTile - 1) / tsp::kAttnQueryTile;
-  const long long per_shard = tiles * d.hs * d.B;
-  if (per_shard <= 0) return n;
-  const long long need = (tsp::kAttnTargetWorkgroups + per_shard - 1) / per_shard;
-  return (int)(need < n ? need : n);
+  for (int k = 0; k < ap.n_seg; ++k)
+    tiles += (ap.seg_rows[k] + tsp::kAttnQueryTile - 1) / tsp::kAttnQueryTile;
+  auto width_for = [&](long long items_per_shard) {
+    if (items_per_shard <= 0) return n;
+    const long long need = (tsp::kAttnTargetWorkgroups + items_per_shard - 1) / items_per_shard;
+    return (int)(need < n ? need : n);
+  };
+  auto group_seconds = [&](int width, bool pair) {
+    double sec = 0.0;
+    for (int i = 0; i < n; i += width) {
+      AttnParams q = ap;
+      q.heads = (n - i < width ? n - i : width) * d.hs;
+      sec += tsp::attn_launch_seconds(q, pair);
+    }
+    return sec;
+  };
+  const AttnLaunchPlan plain = {width_for(tiles * d.hs * d.B), false};
+  if (tiles < 2) return plain;
+  const AttnLaunchPlan paired = {width_for((tiles + 1) / 2 * d.hs * d.B), true};
+  return group_seconds(paired.width, true) < group_seconds(plain.width, false) ? paired : plain;
 }
 struct AttnWs {
   size_t q, a, po, pml, proj, total;  // byte offsets and total size
@@ -174,7 +201,9 @@ AttnWs attn_ws(const Dims& d) {
   size_t part = 0;
   for (const int n : {d.G, d.D % d.G}) {
     if (n == 0) continue;
-    const int sub = attn_shards_per_launch(d, n);
+    const AttnLaunchPlan lp = attn_launch_plan(d, n);
+    if (lp.pair) continue;  // no key ranges
+    const int sub = lp.width;
     for (const int w : {sub, n % sub}) {
       if (w == 0) continue;
       int len = 0;
@@ -563,9 +592,10 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     }
     TSP_LAUNCH(TSP_KERNEL_QKV, st, tsp::launch_gemm_qkv_group(g, n, st));
 
-    // Attention over the group's heads, attn_shards_per_launch shards per launch (the
-    // columns of those shards within the group's Q and A).
-    const int sub = attn_shards_per_launch(d, n);
+    // Attention over the group's heads, lp.width shards per launch (the columns of those
+    // shards within the group's Q and A).
+    const AttnLaunchPlan lp = attn_launch_plan(d, n);
+    const int sub = lp.width;
     for (int i = 0; i < n; i += sub) {
       const int w = n - i < sub ? n - i : sub;
       AttnParams ap = {};
@@ -581,7 +611,13 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
       ap.seq = d.S;
       ap.n_kv = d.nkv;
       ap.kv_head0 = (r0 + i) * d.ks;
-      ap.n_split = attn_group_split(d, w, &ap.split_len);
+      ap.pair_tiles = lp.pair ? 1 : 0;
+      if (lp.pair) {
+        ap.n_split = 1;
+        ap.split_len = attn_full_len(ap);
+      } else {
+        ap.n_split = attn_group_split(d, w, &ap.split_len);
+      }
       ap.part_rows = (long long)d.M * ap.heads;
       ap.part_o = reinterpret_cast<float*>(ws + aw.po);
       ap.part_ml = reinterpret_cast<float*>(ws + aw.pml);

@@ -26,9 +26,9 @@ SINGLE = Workload("single-rank-d1", 1, 320, 512, 1024, 4, 2, 128, 1, 0, w_std=0.
 ODD3 = Workload("odd-degree-d3", 1, 768, 384, 1152, 6, 3, 64, 3, 2, w_std=0.05)
 # More shards than one grouped launch holds: the default grouping makes two groups of 8.
 DEG16 = Workload("degree-d16", 1, 1024, 1024, 2048, 16, 16, 64, 16, 13, w_std=0.04)
-# 100 attention work items (5 query tiles x 2 heads x 10 batch entries) per shard: the
-# group of 4 shards runs its attention as a launch over 3 shards and one over 1 (each
-# launch just fills the GPU), inside Q / A rows 4 shards wide; GQA g = 2.
+# Many attention work items per shard (5 query tiles x 2 heads x 10 batch entries): the
+# launch plan pairs query tiles (5 tiles: pairs (0, 4), (1, 3) and tile 2 alone; in the
+# zigzag layout 6 tiles, pairs across the two segments); GQA g = 2.
 SUBL = Workload("sub-launch-b10", 10, 5120, 512, 1024, 8, 4, 64, 4, 2, w_std=0.05)
 
 

@@ -56,11 +56,13 @@ def test_grouping_parity(wl, p, groups, block):
 
 
 @pytest.mark.parametrize("wl,p", [(SUBL, 2), (SUBL.with_layout(1), 1)],
-                         ids=["sub-launch-contiguous-r2", "sub-launch-zigzag-r1"])
+                         ids=["paired-contiguous-r2", "paired-zigzag-r1"])
 @pytest.mark.parametrize("block", ["attn", "layer"])
-def test_attention_launches_over_part_of_a_group(wl, p, block):
-    """A group's attention split over several launches, each over a few of the group's
-    shards (their heads' columns inside the group-wide Q and A rows)."""
+def test_attention_with_paired_query_tiles(wl, p, block):
+    """A group's attention with two query tiles per workgroup (the i-th most and the i-th
+    fewest keys), as the launch plan takes it for shapes with many work items per shard;
+    launches over part of a group's shards (heads' columns inside group-wide Q and A rows)
+    are covered at full size (7B S=65536, 70B: 4 of 8 shards per launch; 13B: 1 of 4)."""
     print(f"[grouping] {wl.name} {wl.layout_name} rank {p} {block}", flush=True)
     x_bits, w_bits = _inputs(wl)
     prob = RankProblem(wl, x_bits, w_bits, p)
