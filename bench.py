@@ -45,11 +45,11 @@ PEAK_HBM_GBS = 8000.0
 # copy (FETCH x 2.0, WRITE x 1.0).  A record only applies to the kernel source it was taken
 # on (sha256 prefix); after any change to that source the traffic is reported as null.
 MEASURED_TRAFFIC = {
-    # flash_fwd_kernel<128, false>: one launch over 2 shards' 8 heads (4 per layer step),
-    # no key-range split (139 476.4 / 16 384.0 KiB)
+    # flash_fwd_kernel<128, false>: one launch over 4 shards' 16 heads with paired query
+    # tiles (2 per layer step), no key-range split (544 705.5 / 32 768.0 KiB)
     ("7b-h4096-S65536-D8", 7, "attn"): {
-        "source": "flash_attn.hip", "sha256": "00fcf5f26666c8f9",
-        "fetch_kib": 139476.4, "fetch_scale": 2.0, "write_kib": 16384.0, "write_scale": 1.0},
+        "source": "flash_attn.hip", "sha256": "7b1395ff1acd95fd",
+        "fetch_kib": 544705.5, "fetch_scale": 2.0, "write_kib": 32768.0, "write_scale": 1.0},
 }
 
 
