@@ -38,33 +38,43 @@ def silu(z: np.ndarray) -> np.ndarray:
         return z / (1.0 + np.exp(-z))
 
 
-def causal_probs(q: np.ndarray, k: np.ndarray, q_offset: int, scale: float) -> np.ndarray:
-    """Softmax probabilities P[i, j] of query row i (global position q_offset + i)
-    over keys j, with keys j > q_offset + i masked out.  q [Lq, d], k [Lk, d]."""
+def _positions(q_pos, lq: int) -> np.ndarray:
+    """Global positions of Lq query rows: q_pos itself (one per row), or, for an
+    integer, the consecutive positions q_pos, q_pos + 1, ..."""
+    if np.ndim(q_pos) == 0:
+        return int(q_pos) + np.arange(lq)
+    return np.asarray(q_pos)
+
+
+def causal_probs(q: np.ndarray, k: np.ndarray, q_pos, scale: float) -> np.ndarray:
+    """Softmax probabilities P[i, j] of query row i over keys j (key j at position j),
+    with the keys after the row's global position masked out; q_pos gives the rows'
+    positions (or the first of consecutive ones).  q [Lq, d], k [Lk, d]."""
     s = (q @ k.T) * scale
     lq, lk = s.shape
-    allowed = np.arange(lk)[None, :] <= (q_offset + np.arange(lq))[:, None]
+    allowed = np.arange(lk)[None, :] <= _positions(q_pos, lq)[:, None]
     s = np.where(allowed, s, -np.inf)
     s = s - s.max(axis=1, keepdims=True)
     e = np.exp(s)
     return e / e.sum(axis=1, keepdims=True)
 
 
-def causal_attention_core(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_offset: int,
+def causal_attention_core(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos,
                           scale: float) -> np.ndarray:
     """o_i = sum_j P[i, j] v_j for one head; q [Lq, d], k/v [Lk, d] -> [Lq, d].
 
-    The query block starts at global position q_offset, so this is the
-    bottom-right-aligned causal attention a rank runs for its chunk against the
-    gathered prefix (Algorithm 1, the CausalAttn call).  Queries are processed in
-    chunks only to bound memory.
+    Query row i sits at global position q_pos[i] (or q_pos + i for an integer) and sees
+    the keys at positions j <= that position: causal attention of any set of query rows
+    against keys held in sequence order (Algorithm 1's CausalAttn with its alignment).
+    Queries are processed in chunks only to bound memory.
     """
     lq = q.shape[0]
+    pos = _positions(q_pos, lq)
     out = np.empty((lq, v.shape[1]), dtype=np.float64)
     for lo in range(0, lq, _Q_CHUNK):
         hi = min(lq, lo + _Q_CHUNK)
-        kmax = min(k.shape[0], q_offset + hi)  # later keys are all masked for this chunk
-        p = causal_probs(q[lo:hi], k[:kmax], q_offset + lo, scale)
+        kmax = min(k.shape[0], int(pos[lo:hi].max()) + 1)  # later keys are masked for the chunk
+        p = causal_probs(q[lo:hi], k[:kmax], pos[lo:hi], scale)
         out[lo:hi] = p @ v[:kmax]
     return out
 
@@ -112,24 +122,27 @@ def layer_full(x, w, n_heads, n_kv_heads, scale=None):
 
 
 # ---------------------------------------------------------------------------
-# O2 -- the folded per-rank schedule, following Algorithms 1 and 2 step by step.
+# O2 -- the folded per-rank computation (Algorithms 1 and 2), from the definitions:
+# a rank's block output is the sum over all weight shards of that shard's term for the
+# rank's own tokens.
 # ---------------------------------------------------------------------------
 
-def mlp_rank(x_loc, w1_shards, w3_shards, w2_shards, p):
-    """TSP gated ring MLP on rank p (Algorithm 2).
+def ring_order(p, degree):
+    """The order in which rank p applies the MLP shards (Algorithm 2): the shard that
+    started on rank j reaches rank p after (p - j) mod D hand-offs to the right."""
+    return [(p - t) % degree for t in range(degree)]
 
-    Y starts at zero; at ring step t the rank holds the shard that started on
-    rank (p - t) mod D (each step receives from the left neighbour) and adds
-    (SiLU(X W1_j^T) * (X W3_j^T)) W2_j for its own tokens.  x_loc [B, S_loc, h].
+
+def mlp_rank(x_loc, w1_shards, w3_shards, w2_shards, p):
+    """Rank p's output of the folded gated MLP (Algorithm 2), x_loc [B, S_loc, h].
+
+    The MLP acts on each token separately and shard j holds rows j F/D .. (j+1) F/D - 1
+    of W1, W3 and W2, so the MLP of the rank's tokens is the sum over the shards of
+    (SiLU(X W1_j^T) * (X W3_j^T)) W2_j, here added in ring_order(p, D).
     """
-    degree = len(w1_shards)
-    y = np.zeros_like(x_loc, dtype=np.float64)
-    for t in range(degree):
-        j = (p - t) % degree
-        g = silu(x_loc @ w1_shards[j].T)
-        hh = x_loc @ w3_shards[j].T
-        y += (g * hh) @ w2_shards[j]
-    return y
+    terms = ((silu(x_loc @ w1_shards[j].T) * (x_loc @ w3_shards[j].T)) @ w2_shards[j]
+             for j in ring_order(p, len(w1_shards)))
+    return sum(terms, np.zeros_like(x_loc, dtype=np.float64))
 
 
 # ---------------------------------------------------------------------------
@@ -230,17 +243,17 @@ def gather_kv(x_chunks, packed, heads_per_shard, kv_heads_per_shard, head_dim):
 
 
 def attn_rank(x_loc, shards, kv_gathered, p, n_heads, n_kv_heads, head_dim, scale=None,
-              rows=None):
-    """TSP attention on rank p (Algorithm 1) with contiguous sequence chunks.
+              rows=None, positions=None):
+    """Rank p's output of the folded attention block (Algorithm 1), x_loc [B, S_loc, h].
 
-    For r = 0 .. D-1: unpack shard r, project the local Q, take the gathered
-    full-sequence K, V of shard r (``kv_gathered[r]``, from :func:`gather_kv`),
-    attend causally from the local chunk against the prefix of length (p+1) S_loc
-    -- bottom-right aligned, so local row i sits at global position p S_loc + i --
-    and accumulate Flatten(A) W_O^(r)^T into Y, which starts at zero.
-
-    ``rows`` optionally restricts the computation to some local query rows
-    (every row of the output depends only on its own query).
+    Shard r holds query heads r H_s .. (r+1) H_s - 1 (their W_Q rows and W_O columns) and
+    kv heads r K_s .. (r+1) K_s - 1, whose keys and values for the whole sequence are
+    ``kv_gathered[r]`` (the all-gather, in sequence order: :func:`gather_kv` or
+    :func:`gather_kv_zigzag`).  The block output of a token is the sum over the shards of
+    Flatten(A_r) W_O^(r)^T, A_r the causal attention of the shard's query heads of that
+    token, at its global position, over the shard's keys.  The rank's local row t sits at
+    ``positions[t]`` (default p S_loc + t: contiguous chunks).  ``rows`` optionally
+    restricts the computation to some local rows (a row depends only on its own query).
     """
     degree = len(shards)
     hs_heads = n_heads // degree
@@ -249,27 +262,20 @@ def attn_rank(x_loc, shards, kv_gathered, p, n_heads, n_kv_heads, head_dim, scal
     d = head_dim
     sc = default_scale(d, scale)
     b_, s_loc, h = x_loc.shape
-    xq = x_loc if rows is None else x_loc[:, rows]
-    lq = xq.shape[1]
-    row_pos = np.arange(s_loc) if rows is None else np.asarray(rows)
-    s1 = (p + 1) * s_loc
+    pos = p * s_loc + np.arange(s_loc) if positions is None else np.asarray(positions)
+    if rows is not None:
+        x_loc, pos = x_loc[:, rows], pos[np.asarray(rows)]
+    lq = x_loc.shape[1]
     y = np.zeros((b_, lq, h), dtype=np.float64)
     for r in range(degree):
         wq, _, _, wo_t = unpack_attn_shard(shards[r], hs_heads, ks_heads, d)
-        q = (xq @ wq.T).reshape(b_, lq, hs_heads, d)
+        q = (x_loc @ wq.T).reshape(b_, lq, hs_heads, d)
         k_hat, v_hat = kv_gathered[r]
         a = np.empty((b_, lq, hs_heads, d), dtype=np.float64)
         for b in range(b_):
             for i in range(hs_heads):
-                kh = i // g
-                if rows is None:
-                    a[b, :, i] = causal_attention_core(q[b, :, i], k_hat[b, :s1, kh],
-                                                       v_hat[b, :s1, kh], p * s_loc, sc)
-                else:
-                    for n, t in enumerate(row_pos):
-                        a[b, n:n + 1, i] = causal_attention_core(
-                            q[b, n:n + 1, i], k_hat[b, :s1, kh], v_hat[b, :s1, kh],
-                            p * s_loc + int(t), sc)
+                a[b, :, i] = causal_attention_core(q[b, :, i], k_hat[b, :, i // g],
+                                                   v_hat[b, :, i // g], pos, sc)
         y += a.reshape(b_, lq, hs_heads * d) @ wo_t
     return y
 
@@ -292,7 +298,7 @@ def layer_rank(x_chunks, attn_shards, w1_shards, w3_shards, w2_shards, p, n_head
 
 
 # ---------------------------------------------------------------------------
-# O2, zigzag layout: Algorithm 1 as printed (load-balanced causal partition).
+# O2, zigzag layout (Algorithm 1's load-balanced causal partition).
 # ---------------------------------------------------------------------------
 
 def zigzag_positions(seq, degree, p):
@@ -327,42 +333,15 @@ def gather_kv_zigzag(x_shards, packed, heads_per_shard, kv_heads_per_shard, head
 
 def attn_rank_zigzag(x_loc, shards, kv_gathered, p, n_heads, n_kv_heads, head_dim,
                      scale=None):
-    """TSP attention on rank p with zigzag shards (Algorithm 1 as printed).
-
-    For r = 0 .. D-1: unpack shard r and project the local Q; with S_c = S_loc / 2,
-    s1 = (p+1) S_c and s2 = (2D - p) S_c, split Q along the sequence into its two
-    halves, attend causally from the first half to the first s1 gathered keys and
-    from the second half to the first s2 (each query block bottom-right aligned to
-    its key block), concatenate the two outputs along the sequence into A, and
-    accumulate Flatten(A) W_O^(r)^T into Y, which starts at zero.
-    """
-    degree = len(shards)
-    hs_heads = n_heads // degree
-    ks_heads = n_kv_heads // degree
-    g = n_heads // n_kv_heads
-    d = head_dim
-    sc = default_scale(d, scale)
-    b_, s_loc, h = x_loc.shape
-    s_c = s_loc // 2
-    s1 = (p + 1) * s_c
-    s2 = (2 * degree - p) * s_c
-    y = np.zeros((b_, s_loc, h), dtype=np.float64)
-    for r in range(degree):
-        wq, _, _, wo_t = unpack_attn_shard(shards[r], hs_heads, ks_heads, d)
-        q = (x_loc @ wq.T).reshape(b_, s_loc, hs_heads, d)
-        k_hat, v_hat = kv_gathered[r]
-        a = np.empty((b_, s_loc, hs_heads, d), dtype=np.float64)
-        for b in range(b_):
-            for i in range(hs_heads):
-                kh = i // g
-                q1, q2 = q[b, :s_c, i], q[b, s_c:, i]
-                o1 = causal_attention_core(q1, k_hat[b, :s1, kh], v_hat[b, :s1, kh],
-                                           s1 - s_c, sc)
-                o2 = causal_attention_core(q2, k_hat[b, :s2, kh], v_hat[b, :s2, kh],
-                                           s2 - s_c, sc)
-                a[b, :, i] = np.concatenate([o1, o2], axis=0)
-        y += a.reshape(b_, s_loc, hs_heads * d) @ wo_t
-    return y
+    """Rank p's output of the folded attention block with zigzag shards (Algorithm 1):
+    :func:`attn_rank` with the local rows at ``zigzag_positions(S, D, p)`` and the
+    gathered keys in sequence order (:func:`gather_kv_zigzag`).  Algorithm 1's two
+    CausalAttn calls, the first half of the rows against the first s1 = (p+1) S_c keys
+    and the second against the first s2 = (2D - p) S_c, are this per-row causal rule:
+    the last row of each half sits at position s1 - 1 and s2 - 1."""
+    seq = kv_gathered[0][0].shape[1]
+    return attn_rank(x_loc, shards, kv_gathered, p, n_heads, n_kv_heads, head_dim, scale,
+                     positions=zigzag_positions(seq, len(shards), p))
 
 
 def layer_rank_zigzag(x_shards, attn_shards, w1_shards, w3_shards, w2_shards, p, n_heads,

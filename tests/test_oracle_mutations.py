@@ -51,11 +51,12 @@ def _mlp_full_gate_up_swapped(u, w1, w3, w2):
     return (O.silu(u @ w3.T) * (u @ w1.T)) @ w2
 
 
-def _attn_rank_zero_offset(x_loc, shards, kv, p, n_heads, n_kv, d, scale=None, rows=None):
-    # forgets the rank's query offset: every chunk treated as if it started at 0
-    y = _orig_attn_rank(x_loc, shards, [(k[:, p * x_loc.shape[1]:], v[:, p * x_loc.shape[1]:])
-                                        for k, v in kv], 0, n_heads, n_kv, d, scale, rows)
-    return y
+def _attn_rank_zero_offset(x_loc, shards, kv, p, n_heads, n_kv, d, scale=None, rows=None,
+                           positions=None):
+    # forgets the rank's query offset: the local rows taken to start at position 0
+    pos = np.arange(x_loc.shape[1]) if positions is None else \
+        np.asarray(positions) - np.asarray(positions)[0]
+    return _orig_attn_rank(x_loc, shards, kv, p, n_heads, n_kv, d, scale, rows, positions=pos)
 
 
 _orig_attn_rank = O.attn_rank
