@@ -16,8 +16,9 @@ in HBM before timing starts.  Prints one JSON line on stdout; progress goes to s
 Besides the layer call the line reports the attention-only and MLP-only entry points
 timed separately ("blocks"), the per-rank MLP backward (``tsp_mlp_rank_bwd``, with its
 kernel classes) on the same rank ("blocks.mlp_bwd"), the two-stage attention backward
-(``tsp_attn_rank_bwd`` and ``tsp_attn_kv_rank_bwd``, "blocks.attn_bwd"), the algorithmic
-HBM bytes of a step
+("blocks.attn_bwd": ``tsp_attn_rank_bwd_saved`` from the activations a
+``tsp_attn_rank_fwd_train`` call kept, then ``tsp_attn_kv_rank_bwd``; the recomputing
+``tsp_attn_rank_bwd`` beside it), the algorithmic HBM bytes of a step
 and the bandwidth they imply ("hbm"), the paper's non-causal F_layer / D for reference,
 and with --rank-sweep the layer time of every rank of the group and the max/min
 imbalance.
@@ -348,20 +349,24 @@ def main(argv=None):
                          "flops_note": "16 M F h executed (G, U recomputed); 12 M F h without",
                          "kernels": bwd_kernels}
 
-    # The per-rank attention backward: first stage (all D shards: recomputation, dA, the
-    # flash backward, dX query path, dW_Q and dW_O^T contributions, this rank's dK/dV
-    # contributions for every key) and second stage (K/V projection backward on the
-    # rank's rows, fed with synthetic reduce-scattered gradients).
+    # The per-rank attention backward: first stage (all D shards: dA, the flash backward,
+    # dX query path, dW_Q and dW_O^T contributions, this rank's dK/dV contributions for
+    # every key) and second stage (K/V projection backward on the rank's rows, fed with
+    # synthetic reduce-scattered gradients).  The training path takes A and the
+    # log-sum-exp kept by the forward (tsp_attn_rank_fwd_train, run once untimed); the
+    # recomputing entry point (tsp_attn_rank_bwd) is timed beside it.
     prob.prefill_kv(include_self=True)
     dk_bits, dv_bits = I.make_dkv_own(wl, wl.rank)
     dkl, dvl = to_device_bf16(dk_bits), to_device_bf16(dv_bits)
     del dk_bits, dv_bits
+    prob.attn_fwd_train()
     for _ in range(2):
+        prob.attn_bwd_saved(dy)
         prob.attn_bwd(dy)
         prob.attn_kv_bwd(dkl, dvl)
     torch.cuda.synchronize()
     T.tsp_profile_enable(True)
-    ms_ab1 = time_calls(lambda: prob.attn_bwd(dy), args.steps, 0)
+    ms_ab1 = time_calls(lambda: prob.attn_bwd_saved(dy), args.steps, 0)
     ab1_kernels = {}
     for k, name in enumerate(T.KERNELS):
         if not name.startswith("abwd_"):
@@ -374,13 +379,15 @@ def main(argv=None):
                 e["tflops"] = round(kf[name] / (tot / args.steps * 1e-3) / 1e12, 2)
             ab1_kernels[name] = e
     T.tsp_profile_enable(False)
+    ms_ab1_re = time_calls(lambda: prob.attn_bwd(dy), args.steps, 0)
     ms_ab2 = time_calls(lambda: prob.attn_kv_bwd(dkl, dvl), args.steps, 0)
     D = wl.degree
     core = kf["attn"] / D
     qd = wl.n_heads // D * wl.head_dim
     kd = wl.n_kv_heads // D * wl.head_dim
     gemm1 = 5 * 2.0 * m_tok * qd * wl.hidden          # Q, dA, dX, dW_Q, dW_O^T per shard
-    exec1 = D * (gemm1 + (1 + 2 + 1.5) * core)
+    exec1 = D * (gemm1 + (2 + 1.5) * core)            # with the kept A and lse
+    exec1_re = exec1 + D * core                        # plus the forward recomputation
     alg1 = D * (4 * 2.0 * m_tok * qd * wl.hidden + 2.5 * core)  # without Q, S, A recompute
     flops2 = D * 4 * 2.0 * m_tok * kd * wl.hidden      # dX (K, V) and dW_K, dW_V per shard
     blocks["attn_bwd"] = {
@@ -389,9 +396,17 @@ def main(argv=None):
         "flops_executed": exec1 + flops2, "flops_backward": alg1 + flops2,
         "tflops_executed": round((exec1 + flops2) / ((ms_ab1 + ms_ab2) * 1e-3) / 1e12, 2),
         "tflops_backward": round((alg1 + flops2) / ((ms_ab1 + ms_ab2) * 1e-3) / 1e12, 2),
-        "flops_note": "executed: with the Q / attention recomputation and the two flash "
-                      "backward kernels' repeated score and dP products (4.5x the forward "
-                      "core); backward: 2.5x the forward core plus the gradient products",
+        "flops_note": "stage one from the forward's kept A and log-sum-exp "
+                      "(tsp_attn_rank_bwd_saved); executed: with the Q recomputation and the "
+                      "two flash backward kernels' repeated score and dP products (3.5x the "
+                      "forward core); backward: 2.5x the forward core plus the gradient "
+                      "products",
+        "recompute": {"stage1_ms": round(ms_ab1_re, 4), "ms": round(ms_ab1_re + ms_ab2, 4),
+                      "tflops_executed": round((exec1_re + flops2) /
+                                               ((ms_ab1_re + ms_ab2) * 1e-3) / 1e12, 2),
+                      "tflops_backward": round((alg1 + flops2) /
+                                               ((ms_ab1_re + ms_ab2) * 1e-3) / 1e12, 2),
+                      "note": "tsp_attn_rank_bwd: A and the log-sum-exp recomputed (4.5x)"},
         "kernels": ab1_kernels}
     del dy, dkl, dvl
     return finish(args, wl, x_bits, w_bits, ms, ms_prof, rf, tflops, roofline, kernels, blocks)

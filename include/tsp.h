@@ -186,6 +186,22 @@ tsp_status tsp_attn_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                              float* y_loc, int accumulate, void* ws, size_t ws_bytes,
                              hipStream_t stream);
 
+/* tsp_attn_rank_fwd that also keeps what the backward needs (training): the attention
+ * output A of every shard and the log-sum-exp of every query's logits, so that
+ * tsp_attn_rank_bwd_saved need not recompute them (the forward in Algorithm 1's order,
+ * grouped as tsp_shape.group_steps says; results as tsp_attn_rank_fwd's).
+ *   a_out    [B, S_loc, n_h, d] bf16   A of all shards side by side: shard r's heads at
+ *                                     columns r*n_h/D*d ..; written
+ *   lse_out  [B, n_h, S_loc] fp32      log2 of the softmax denominator of each query's
+ *                                     base-2 logits (scale * log2(e) * q k, with q rounded
+ *                                     to bf16 as the kernels use it); written
+ * Other arguments as tsp_attn_rank_fwd (same workspace size, TSP_OP_ATTN). */
+tsp_status tsp_attn_rank_fwd_train(const tsp_shape* shape, const uint16_t* x_loc,
+                                   const uint16_t* const* w_attn, uint16_t* k_buf,
+                                   uint16_t* v_buf, float* y_loc, int accumulate,
+                                   uint16_t* a_out, float* lse_out, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
+
 /* Backward of tsp_attn_rank_fwd on rank p, first stage.  As for the MLP, the paper
  * costs the backward (Section 4) without printing it; these are the chain-rule
  * gradients of Algorithm 1.  The forward's K/V all-gather becomes a reduce-scatter of
@@ -216,6 +232,19 @@ tsp_status tsp_attn_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
                              const uint16_t* k_buf, const uint16_t* v_buf, float* dx_loc,
                              int accumulate, float* const* dw_attn, float* dk_buf,
                              float* dv_buf, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* tsp_attn_rank_bwd with A and the log-sum-exp taken from tsp_attn_rank_fwd_train
+ * (a_saved, lse_saved in its a_out / lse_out layouts, from the same inputs) instead of
+ * recomputed: the same gradients (Q is still recomputed from x, with the forward's single
+ * rounding), without the forward attention pass.  Workspace as tsp_attn_rank_bwd
+ * (TSP_OP_ATTN_BWD); other arguments as there. */
+tsp_status tsp_attn_rank_bwd_saved(const tsp_shape* shape, const uint16_t* x_loc,
+                                   const uint16_t* dy_loc, const uint16_t* const* w_attn,
+                                   const uint16_t* k_buf, const uint16_t* v_buf,
+                                   const uint16_t* a_saved, const float* lse_saved,
+                                   float* dx_loc, int accumulate, float* const* dw_attn,
+                                   float* dk_buf, float* dv_buf, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
 
 /* Backward of the rank's K/V projections, second stage of the attention backward:
  * with dK, dV the reduce-scattered gradients of this rank's rows of every shard's

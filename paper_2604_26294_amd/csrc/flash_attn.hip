@@ -451,10 +451,12 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     const float inv = 1.f / l_run;
     if constexpr (LSE) {
       if (hh == 0)
-        P.lse[((size_t)b * P.heads + head) * P.s_loc + row0 + qloc] =
+        P.lse[((size_t)b * (P.lse_heads > 0 ? P.lse_heads : P.heads) + P.lse_head0 + head) *
+                  P.s_loc + row0 + qloc] =
             mref + __builtin_amdgcn_logf(l_run);
     }
-    uint16_t* orow = P.O + trow * ld + (size_t)head * D;
+    const size_t ld_o = P.ld_o > 0 ? (size_t)P.ld_o : ld;
+    uint16_t* orow = P.O + trow * ld_o + (size_t)head * D;
 #pragma unroll
     for (int eb = 0; eb < C::EB; ++eb)
 #pragma unroll
@@ -539,10 +541,11 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams P) {
       // row = (b S_loc + t) H_s + head  ->  the [B, H_s, S_loc] log-sum-exp layout
       const long long bt = row / P.heads, b = bt / P.s_loc;
       const int head = (int)(row - bt * P.heads), t = (int)(bt - b * P.s_loc);
-      P.lse[((size_t)b * P.heads + head) * P.s_loc + t] = m + __builtin_amdgcn_logf(l);
+      const int lh = P.lse_heads > 0 ? P.lse_heads : P.heads;
+      P.lse[((size_t)b * lh + P.lse_head0 + head) * P.s_loc + t] = m + __builtin_amdgcn_logf(l);
     }
   }
-  const long long ld = P.ld > 0 ? P.ld : (long long)P.heads * D;
+  const long long ld = P.ld_o > 0 ? P.ld_o : (P.ld > 0 ? P.ld : (long long)P.heads * D);
   *reinterpret_cast<u32x2*>(P.O + (row / P.heads) * ld + (row % P.heads) * D + 4 * c4) =
       u32x2{pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
 }
@@ -707,6 +710,7 @@ hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
     n_qt += (p.seg_rows[k] + kQTile - 1) / kQTile;
   }
   if (p.ld != 0 && (p.ld < p.heads * p.head_dim || p.ld % 8 != 0)) return hipErrorInvalidValue;
+  if (p.ld_o != 0 && (p.ld_o < p.heads * p.head_dim || p.ld_o % 8 != 0)) return hipErrorInvalidValue;
   if (p.pair_tiles && p.n_split != 1) return hipErrorInvalidValue;
   if (rows != p.s_loc || p.n_split < 1 || p.split_len <= 0 || p.split_len % kStepKeys != 0 ||
       (p.n_split > 1 && (!p.part_o || !p.part_ml)))

@@ -122,9 +122,14 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const AttnBwdParams 
   const long long n_rows = (long long)P.batch * P.s_loc * P.heads;
   const bool valid = rh < n_rows;
   const size_t e0 = (size_t)(valid ? rh : 0) * D + 8 * part;
+  // O may sit in a wider buffer (token rows o_ld elements apart)
+  const long long bt_o = (valid ? rh : 0) / P.heads;
+  const size_t eo = P.o_ld > 0 ? (size_t)bt_o * P.o_ld + (size_t)((valid ? rh : 0) - bt_o * P.heads) * D +
+                                     8 * part
+                               : e0;
   float acc = 0.f;
   if (valid) {
-    const u32x4 o = ld16(P.O + e0), g = ld16(P.dO + e0);
+    const u32x4 o = ld16(P.O + eo), g = ld16(P.dO + e0);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       acc += bf16_bits_to_f32(o[e] & 0xffffu) * bf16_bits_to_f32(g[e] & 0xffffu);
@@ -254,6 +259,7 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   // (the array base is chosen from two scalar values, not by indexing the parameter
   // block per lane, which would load the pointer from memory)
   const float* const pbase = pwhich ? P.delta : P.lse;
+  const int lse_rows = P.lse_heads > 0 ? P.lse_heads : P.heads;
   // lse / delta run two tiles ahead of the rows (pend[S] holds those of the next tile
   // to use slot S), with one unconditional load per wave per tile so that the number of
   // loads behind a tile's rows is the same in every wave.
@@ -266,8 +272,10 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     const Tile T = tile_at(c_lse);
     if (--lse_left > 0) adv(c_lse);  // past the last tile: reload the last one
     const int last = P.seg_rows[T.seg] - 1 - T.r0;
-    const size_t li = ((size_t)b * P.heads + T.head) * P.s_loc + P.seg_row0[T.seg] + T.r0 +
-                      min(pr, last);
+    const size_t t_row = (size_t)P.seg_row0[T.seg] + T.r0 + min(pr, last);
+    // delta: [B, H_s, S_loc]; lse: [B, lse_heads, S_loc] from row lse_head0
+    const size_t li = pwhich ? ((size_t)b * P.heads + T.head) * P.s_loc + t_row
+                             : ((size_t)b * lse_rows + P.lse_head0 + T.head) * P.s_loc + t_row;
     pend[S] = pbase[li];
     pend_last[S] = last;
   };
@@ -480,7 +488,9 @@ void attn_bwd_dq_kernel(const AttnBwdParams P) {
     of[s] = ld16(P.dO + qrow + 16 * s + 8 * hh);
   }
   const size_t li = ((size_t)b * P.heads + head) * P.s_loc + row0 + (qvalid ? qloc : 0);
-  const float neg_lse = qvalid ? -P.lse[li] : -INFINITY;  // invalid query: P = 0
+  const size_t li_lse = ((size_t)b * (P.lse_heads > 0 ? P.lse_heads : P.heads) + P.lse_head0 +
+                         head) * P.s_loc + row0 + (qvalid ? qloc : 0);
+  const float neg_lse = qvalid ? -P.lse[li_lse] : -INFINITY;  // invalid query: P = 0
   const float neg_del = qvalid ? -P.delta[li] : 0.f;
   // Consume these loads before the loop: the compiler then waits for them once, not at
   // a point inside the loop where the same wait would also cover the newest key tiles.

@@ -117,7 +117,7 @@ hipError_t launch_gemm_qkv_group(const GemmParams* ps, int n, hipStream_t s);
 //   K/V buffers [B, S, n_kv, d] bf16 (heads
 //   kv_head0 .. kv_head0 + H_s/g - 1 are this shard's);  O [B, S_loc, H_s, d] bf16.
 //   Q and O rows may be wider than H_s d (a launch over some of the heads of a wider
-//   buffer): token row t starts ld elements after row t - 1.
+//   buffer): token row t of Q starts ld elements after row t - 1, of O ld_o.
 //   The local rows form n_seg segments of consecutive global positions: rows
 //   [seg_row0[k], seg_row0[k] + seg_rows[k]) sit at positions seg_pos0[k] + (row -
 //   seg_row0[k]) (one segment for contiguous chunks, two for a zigzag shard).  A query
@@ -140,7 +140,8 @@ struct AttnParams {
   int seg_rows[2];
   int seg_pos0[2];
   int kv_len;       // number of readable keys: the last segment position + 1
-  int ld;           // elements between consecutive token rows of Q and O (0: H_s d)
+  int ld;           // elements between consecutive token rows of Q (0: H_s d)
+  int ld_o;         // ... and of O (0: as Q)
   // Key-range split (attn_split_count): each query tile's keys [0, n) are processed in
   // ranges [c split_len, (c + 1) split_len), c < n_split.  With n_split > 1 the ranges
   // write partial results -- part_o [n_split][part_rows][d] fp32 (unnormalised O) and
@@ -156,8 +157,11 @@ struct AttnParams {
   float* part_ml;
   // Optional: the log-sum-exp of each query's base-2 logits (the products of the
   // scaled bf16 queries with the keys, as the kernel computes them), fp32
-  // [B, H_s, S_loc]; written when non-null.
+  // [B, lse_heads, S_loc] with this launch's heads at rows lse_head0 .. lse_head0 + H_s - 1
+  // (lse_heads = 0: H_s rows from 0); written when non-null.
   float* lse;
+  int lse_head0;
+  int lse_heads;
 };
 
 // Workgroups the attention kernel aims to launch: one per CU of an MI355X.
@@ -220,6 +224,12 @@ struct AttnBwdParams {
   int dq_split;
   int dq_split_len;
   float* dq_part;
+  // Row strides and head placement of inputs that come from a wider buffer (a saved
+  // forward): O's token rows o_ld elements apart (0: H_s d); lse rows of this launch's
+  // heads at lse_head0 .. of [B, lse_heads, S_loc] (lse_heads = 0: H_s rows from 0).
+  long long o_ld;
+  int lse_head0;
+  int lse_heads;
 };
 
 // Number of key ranges for the dQ kernel (and their length, a multiple of the key

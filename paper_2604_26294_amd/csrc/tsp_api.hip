@@ -574,14 +574,18 @@ GemmParams qkv_params(const Dims& d, const uint16_t* x, const uint16_t* shard, i
 // output projection over the group's shards.
 tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
                     uint16_t* kb, uint16_t* vb, float* y, int accumulate,
-                    const uint16_t* residual, uint16_t* u_out, char* ws, hipStream_t st) {
+                    const uint16_t* residual, uint16_t* u_out, char* ws, hipStream_t st,
+                    uint16_t* a_out = nullptr, float* lse_out = nullptr) {
   const int qd = d.hs * d.d, kd = d.ks * d.d;
   const size_t wo = (size_t)(qd + 2 * kd) * d.h;  // W_O^(r)^T block [H_s d, h] of a shard
   const AttnWs aw = attn_ws(d);
   uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + aw.q);
-  uint16_t* a_ws = reinterpret_cast<uint16_t*>(ws + aw.a);
   for (int r0 = 0; r0 < d.D; r0 += d.G) {
     const int n = d.D - r0 < d.G ? d.D - r0 : d.G;
+    // A of the group: the workspace ([M, n H_s d]), or the caller's [M, n_h d] buffer at
+    // the group's columns (kept for the backward)
+    uint16_t* a_ws = a_out ? a_out + (size_t)r0 * qd : reinterpret_cast<uint16_t*>(ws + aw.a);
+    const int a_ld = a_out ? d.D * qd : n * qd;
     GemmParams g[tsp::kGemmGroupMax] = {};
     GemmParams o = {};
     for (int i = 0; i < n; ++i) {
@@ -605,7 +609,11 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
       ap.O = a_ws + (size_t)i * qd;
       attn_segments(d, &ap);
       ap.heads = w * d.hs;
-      ap.ld = n * qd;
+      ap.ld = n * qd;     // Q: the group's workspace rows
+      ap.ld_o = a_ld;     // A: the workspace's, or the caller's wider rows
+      ap.lse = lse_out;
+      ap.lse_head0 = (r0 + i) * d.hs;
+      ap.lse_heads = d.nh;
       ap.group = d.g;
       ap.head_dim = d.d;
       ap.seq = d.S;
@@ -625,7 +633,7 @@ tsp_status run_attn(const Dims& d, const uint16_t* x, const uint16_t* const* wa,
     }
 
     o.A = a_ws;
-    o.lda = n * qd;
+    o.lda = a_ld;
     o.B = o.B_part[0];
     o.ldb = d.h;
     o.M = (int)d.M;
@@ -676,7 +684,8 @@ GemmParams nt_params(const Dims& d, const uint16_t* a, const uint16_t* b, int n,
 tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
                         const uint16_t* const* wa, const uint16_t* kb, const uint16_t* vb,
                         float* dx, int accumulate, float* const* dw, float* dk, float* dv,
-                        char* ws, hipStream_t st) {
+                        char* ws, hipStream_t st, const uint16_t* a_saved = nullptr,
+                        const float* lse_saved = nullptr) {
   const int qd = d.hs * d.d, kd = d.ks * d.d;
   const AttnBwdWs w = attn_bwd_ws(d);
   uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + w.q);
@@ -697,34 +706,45 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     TSP_LAUNCH(TSP_KERNEL_ABWD_PROJ, st, tsp::launch_gemm_qkv(g, st));
 
     AttnParams ap = {};
-    ap.Q = q_ws;
-    ap.Kb = kb;
-    ap.Vb = vb;
-    ap.O = a_ws;
     attn_segments(d, &ap);
-    ap.group = d.g;
-    ap.head_dim = d.d;
-    ap.seq = d.S;
-    ap.n_kv = d.nkv;
-    ap.kv_head0 = r * d.ks;
-    ap.n_split = w.n_split;
-    ap.split_len = w.split_len;
-    ap.part_rows = (long long)d.M * d.hs;
-    ap.part_o = reinterpret_cast<float*>(ws + w.po);
-    ap.part_ml = reinterpret_cast<float*>(ws + w.pml);
-    ap.lse = lse;
-    TSP_LAUNCH(TSP_KERNEL_ABWD_FWD, st, tsp::launch_flash_attn(ap, st));
+    // A and the log-sum-exp: the forward's, kept by tsp_attn_rank_fwd_train (shard r's
+    // columns of [M, n_h d] and rows of [B, n_h, S_loc]), or recomputed into the workspace
+    const uint16_t* a_src = a_saved ? a_saved + (size_t)r * qd : a_ws;
+    const int a_ld = a_saved ? d.nh * d.d : qd;
+    if (!a_saved) {
+      ap.Q = q_ws;
+      ap.Kb = kb;
+      ap.Vb = vb;
+      ap.O = a_ws;
+      ap.group = d.g;
+      ap.head_dim = d.d;
+      ap.seq = d.S;
+      ap.n_kv = d.nkv;
+      ap.kv_head0 = r * d.ks;
+      ap.n_split = w.n_split;
+      ap.split_len = w.split_len;
+      ap.part_rows = (long long)d.M * d.hs;
+      ap.part_o = reinterpret_cast<float*>(ws + w.po);
+      ap.part_ml = reinterpret_cast<float*>(ws + w.pml);
+      ap.lse = lse;
+      TSP_LAUNCH(TSP_KERNEL_ABWD_FWD, st, tsp::launch_flash_attn(ap, st));
+    }
 
     g = nt_params(d, dy, wo_t, qd, da_ws, 1.f);  // dA = dY W_O^(r)
     TSP_LAUNCH(TSP_KERNEL_ABWD_PROJ, st, tsp::launch_gemm_qkv(g, st));
 
     AttnBwdParams bp = {};
     bp.Qs = q_ws;
-    bp.O = a_ws;
+    bp.O = a_src;
+    bp.o_ld = a_ld;
     bp.dO = da_ws;
     bp.Kb = kb;
     bp.Vb = vb;
-    bp.lse = lse;
+    bp.lse = lse_saved ? lse_saved : lse;
+    if (lse_saved) {
+      bp.lse_head0 = r * d.hs;
+      bp.lse_heads = d.nh;
+    }
     bp.delta = delta;
     bp.dQ = dq_ws;
     bp.dK = dk;
@@ -775,7 +795,7 @@ tsp_status run_attn_bwd(const Dims& d, const uint16_t* x, const uint16_t* dy,
     TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
                tsp::launch_transpose_bf16(dq_ws, qd, (int)d.M, qd, dqt_ws, w.m_pad, st));
     TSP_LAUNCH(TSP_KERNEL_ABWD_AUX, st,
-               tsp::launch_transpose_bf16(a_ws, qd, (int)d.M, qd, at_ws, w.m_pad, st));
+               tsp::launch_transpose_bf16(a_src, a_ld, (int)d.M, qd, at_ws, w.m_pad, st));
     // W_Q block (+)= dQ^T X;  W_O^T block (+)= A^T dY: [H_s d, M] x [M, h], one launch.
     GemmParams q[2] = {};
     for (int k = 0; k < 2; ++k) {
@@ -1004,6 +1024,27 @@ tsp_status tsp_attn_rank_fwd(const tsp_shape* shape, const uint16_t* x_loc,
                   static_cast<char*>(ws), stream);
 }
 
+tsp_status tsp_attn_rank_fwd_train(const tsp_shape* shape, const uint16_t* x_loc,
+                                   const uint16_t* const* w_attn, uint16_t* k_buf,
+                                   uint16_t* v_buf, float* y_loc, int accumulate,
+                                   uint16_t* a_out, float* lse_out, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_shards(w_attn, d.D));
+  TSP_TRY(check_ptr(k_buf));
+  TSP_TRY(check_ptr(v_buf));
+  TSP_TRY(check_ptr(y_loc));
+  TSP_TRY(check_ptr(a_out));
+  TSP_TRY(check_ptr(lse_out));
+  TSP_TRY(check_ptr(ws));
+  if (ws_bytes < ws_attn(d)) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  return run_attn(d, x_loc, w_attn, k_buf, v_buf, y_loc, accumulate, nullptr, nullptr,
+                  static_cast<char*>(ws), stream, a_out, lse_out);
+}
+
 tsp_status tsp_attn_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
                              const uint16_t* dy_loc, const uint16_t* const* w_attn,
                              const uint16_t* k_buf, const uint16_t* v_buf, float* dx_loc,
@@ -1025,6 +1066,33 @@ tsp_status tsp_attn_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,
   if (d.M == 0) return TSP_OK;
   return run_attn_bwd(d, x_loc, dy_loc, w_attn, k_buf, v_buf, dx_loc, accumulate, dw_attn,
                       dk_buf, dv_buf, static_cast<char*>(ws), stream);
+}
+
+tsp_status tsp_attn_rank_bwd_saved(const tsp_shape* shape, const uint16_t* x_loc,
+                                   const uint16_t* dy_loc, const uint16_t* const* w_attn,
+                                   const uint16_t* k_buf, const uint16_t* v_buf,
+                                   const uint16_t* a_saved, const float* lse_saved,
+                                   float* dx_loc, int accumulate, float* const* dw_attn,
+                                   float* dk_buf, float* dv_buf, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  Dims d;
+  TSP_TRY(check_shape(shape, &d));
+  TSP_TRY(check_ptr(x_loc));
+  TSP_TRY(check_ptr(dy_loc));
+  TSP_TRY(check_shards(w_attn, d.D));
+  TSP_TRY(check_ptr(k_buf));
+  TSP_TRY(check_ptr(v_buf));
+  TSP_TRY(check_ptr(a_saved));
+  TSP_TRY(check_ptr(lse_saved));
+  TSP_TRY(check_ptr(dx_loc));
+  TSP_TRY(check_shards(dw_attn, d.D));
+  TSP_TRY(check_ptr(dk_buf));
+  TSP_TRY(check_ptr(dv_buf));
+  TSP_TRY(check_ptr(ws));
+  if (ws_bytes < attn_bwd_ws(d).total) return TSP_ERR_WORKSPACE;
+  if (d.M == 0) return TSP_OK;
+  return run_attn_bwd(d, x_loc, dy_loc, w_attn, k_buf, v_buf, dx_loc, accumulate, dw_attn,
+                      dk_buf, dv_buf, static_cast<char*>(ws), stream, a_saved, lse_saved);
 }
 
 tsp_status tsp_attn_kv_rank_bwd(const tsp_shape* shape, const uint16_t* x_loc,

@@ -114,6 +114,27 @@ class RankProblem:
                             self.adx, accumulate, self.adw, self.dk_buf, self.dv_buf, self.ws_abwd)
         return self.adx, self.adw, self.dk_buf, self.dv_buf
 
+    def attn_fwd_train(self, accumulate=False):
+        """The attention block forward that keeps A [B, S_loc, n_h, d] bf16 and the
+        base-2 log-sum-exp [B, n_h, S_loc] fp32 for attn_bwd_saved.  Returns (y, a, lse)."""
+        wl = self.wl
+        if not hasattr(self, "a_saved"):
+            self.a_saved = torch.empty((wl.batch, wl.s_loc, wl.n_heads, wl.head_dim),
+                                       dtype=torch.bfloat16, device=self.device)
+            self.lse_saved = torch.empty((wl.batch, wl.n_heads, wl.s_loc), dtype=torch.float32,
+                                         device=self.device)
+        T.tsp_attn_rank_fwd_train(self.shape, self.x_loc, self.attn, self.k_buf, self.v_buf,
+                                  self.y, accumulate, self.a_saved, self.lse_saved, self.ws)
+        return self.y, self.a_saved, self.lse_saved
+
+    def attn_bwd_saved(self, dy_loc, accumulate=False):
+        """attn_bwd with A and the log-sum-exp of the last attn_fwd_train call."""
+        self._attn_grads()
+        T.tsp_attn_rank_bwd_saved(self.shape, self.x_loc, dy_loc, self.attn, self.k_buf,
+                                  self.v_buf, self.a_saved, self.lse_saved, self.adx, accumulate,
+                                  self.adw, self.dk_buf, self.dv_buf, self.ws_abwd)
+        return self.adx, self.adw, self.dk_buf, self.dv_buf
+
     def attn_kv_bwd(self, dk_loc, dv_loc, accumulate=True):
         """Second stage: the K/V projection backward for the bf16 reduce-scattered
         gradients of this rank's rows [B, S_loc, n_kv, d].  Returns (dx, dw_attn list)."""

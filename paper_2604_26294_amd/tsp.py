@@ -65,6 +65,8 @@ def _load() -> ctypes.CDLL:
         "tsp_attn_rank_bwd": [SH, P, P, PP, P, P, P, I, PP, P, P, VP, SZ, VP],
         "tsp_attn_kv_rank_bwd": [SH, P, PP, P, P, P, I, PP, VP, SZ, VP],
         "tsp_attn_rank_fwd": [SH, P, PP, P, P, P, I, VP, SZ, VP],
+        "tsp_attn_rank_fwd_train": [SH, P, PP, P, P, P, I, P, P, VP, SZ, VP],
+        "tsp_attn_rank_bwd_saved": [SH, P, P, PP, P, P, P, P, P, I, PP, P, P, VP, SZ, VP],
         "tsp_layer_rank_fwd": [SH, P, PP, PP, PP, PP, P, P, P, VP, SZ, VP],
         "tsp_layer_rank_fwd_noalloc": [SH, P, PP, PP, PP, PP, P, P, P, VP],
         "tsp_workspace_bytes": [SH, I, ctypes.POINTER(ctypes.c_size_t)],
@@ -179,6 +181,26 @@ def tsp_attn_rank_bwd(shape, x_loc, dy_loc, w_attn, k_buf, v_buf, dx_loc, accumu
                                  _ptr(v_buf), _ptr(dx_loc), int(accumulate), dw, _ptr(dk_buf),
                                  _ptr(dv_buf), _ptr(ws), _nbytes(ws), _stream(stream)),
            "tsp_attn_rank_bwd")
+
+
+def tsp_attn_rank_fwd_train(shape, x_loc, w_attn, k_buf, v_buf, y_loc, accumulate, a_out, lse_out,
+                            ws, stream=None):
+    a, _a = _ptrs(w_attn)
+    _check(lib.tsp_attn_rank_fwd_train(ctypes.byref(shape), _ptr(x_loc), a, _ptr(k_buf),
+                                       _ptr(v_buf), _ptr(y_loc), int(accumulate), _ptr(a_out),
+                                       _ptr(lse_out), _ptr(ws), _nbytes(ws), _stream(stream)),
+           "tsp_attn_rank_fwd_train")
+
+
+def tsp_attn_rank_bwd_saved(shape, x_loc, dy_loc, w_attn, k_buf, v_buf, a_saved, lse_saved,
+                            dx_loc, accumulate, dw_attn, dk_buf, dv_buf, ws, stream=None):
+    a, _a = _ptrs(w_attn)
+    dw, _dw = _ptrs(dw_attn)
+    _check(lib.tsp_attn_rank_bwd_saved(ctypes.byref(shape), _ptr(x_loc), _ptr(dy_loc), a,
+                                       _ptr(k_buf), _ptr(v_buf), _ptr(a_saved), _ptr(lse_saved),
+                                       _ptr(dx_loc), int(accumulate), dw, _ptr(dk_buf),
+                                       _ptr(dv_buf), _ptr(ws), _nbytes(ws), _stream(stream)),
+           "tsp_attn_rank_bwd_saved")
 
 
 def tsp_attn_kv_rank_bwd(shape, x_loc, w_attn, dk_loc, dv_loc, dx_loc, accumulate, dw_attn, ws,
