@@ -258,3 +258,33 @@ def test_noalloc_layer_validates_before_touching_the_gpu():
                                         FAKE, FAKE, None) == 0
     fits = T.shape_of(BY_NAME["7b-h4096-S8192-D8"])
     assert T.workspace_bytes(fits, T.OP_LAYER) <= T.NOALLOC_SCRATCH_BYTES
+
+
+def test_training_pair_rejects_bad_arguments():
+    """tsp_attn_rank_fwd_train and tsp_attn_rank_bwd_saved validate every argument,
+    including the kept A / log-sum-exp buffers, before anything is enqueued."""
+    sh = _shape()
+    L = T.lib
+    good, _k1 = _arr(2)
+    nul, _k2 = _arr(2, 0)
+    fwd_need = T.workspace_bytes(sh, T.OP_ATTN)
+    fwd = [ctypes.byref(sh), FAKE, good, FAKE, FAKE, FAKE, 0, FAKE, FAKE, FAKE, fwd_need, None]
+    for pos, val, code in [(1, None, 1), (2, nul, 1), (5, None, 1), (7, None, 1),
+                           (7, FAKE + 2, 4), (8, None, 1), (8, FAKE + 4, 4), (9, None, 1),
+                           (10, fwd_need - 1, 5)]:
+        a = list(fwd)
+        a[pos] = val
+        assert L.tsp_attn_rank_fwd_train(*a) == code, ("fwd", pos, code)
+    bwd_need = T.workspace_bytes(sh, T.OP_ATTN_BWD)
+    bwd = [ctypes.byref(sh), FAKE, FAKE, good, FAKE, FAKE, FAKE, FAKE, FAKE, 0, good, FAKE, FAKE,
+           FAKE, bwd_need, None]
+    for pos, val, code in [(1, None, 1), (2, None, 1), (6, None, 1), (6, FAKE + 8, 4),
+                           (7, None, 1), (7, FAKE + 4, 4), (8, None, 1), (10, nul, 1),
+                           (13, None, 1), (14, bwd_need - 1, 5)]:
+        a = list(bwd)
+        a[pos] = val
+        assert L.tsp_attn_rank_bwd_saved(*a) == code, ("bwd", pos, code)
+    bad = _shape(rank=4)
+    a = list(bwd)
+    a[0] = ctypes.byref(bad)
+    assert L.tsp_attn_rank_bwd_saved(*a) == 3
