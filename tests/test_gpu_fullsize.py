@@ -143,34 +143,51 @@ def test_mlp_backward_sampled_rows(wl, p):
 @pytest.mark.parametrize("wl,p", BWD_CASES, ids=[f"{w.name}-r{p}" for w, p in BWD_CASES])
 def test_attention_backward_full_size(wl, p):
     """The attention backward's first stage at full size, in the benchmark's launch
-    configuration: sampled rows of dX's query path (every head), and for the first head
-    of the last shard every token's contribution to its W_Q and W_O^T gradient rows and,
-    with one query head per kv head, every key's dK-hat / dV-hat, from the oracle's
-    per-head attention backward in fp64."""
+    configuration, on both paths (recomputing the forward, and from the A and log-sum-exp
+    that the training forward kept): sampled rows of dX's query path (every head), and for
+    the first head of the last shard every token's contribution to its W_Q and W_O^T
+    gradient rows and, with one query head per kv head, every key's dK-hat / dV-hat, from
+    the oracle's per-head attention backward in fp64."""
     from paper_2604_26294_amd.harness import to_device_bf16
     print(f"[fullsize attn bwd] {wl.name} rank {p}", flush=True)
     assert wl.layout == 0 and wl.batch == 1
     x_bits, w_bits, wf = _data(wl)
     dy_bits = I.gaussian_bf16(wl.seed, I.TENSOR_ID["dy"], (wl.batch, wl.s_loc, wl.hidden),
                               wl.x_std)
-    prob = RankProblem(wl, x_bits, w_bits, p)
-    prob.prefill_kv(include_self=True)
-    dx, dw, dk, dv = prob.attn_bwd(to_device_bf16(dy_bits))
-    torch.cuda.synchronize()
     D, d, s_loc = wl.degree, wl.head_dim, wl.s_loc
     kv_len = (p + 1) * s_loc
-    x_b = I.bf16_bits_to_f64(x_bits[0, :kv_len])
-    dy_loc = I.bf16_bits_to_f64(dy_bits[0])
-    rows = [0, 127, s_loc // 2, s_loc - 1]
-    ref = O.attention_bwd_rows(x_b, wf["wq"], wf["wk"], wf["wv"], wf["wo"], wl.n_heads,
-                               wl.n_kv_heads, [p * s_loc + r for r in rows], dy_loc[rows])
-    assert_close(dx[0, rows].double().cpu().numpy(), ref, f"{wl.name} dX query-path rows")
-
     g = wl.n_heads // wl.n_kv_heads
     hs, qd, kd = wl.n_heads // D, wl.n_heads // D * d, wl.n_kv_heads // D * d
     r, i = D - 1, 0
     gh = r * hs + i
     kvh = gh // g
+    o0 = qd + 2 * kd
+    rows = [0, 127, s_loc // 2, s_loc - 1]
+
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    prob.prefill_kv(include_self=True)
+    dy = to_device_bf16(dy_bits)
+    got = {}
+    for path in ("recompute", "saved"):
+        if path == "recompute":
+            dx, dw, dk, dv = prob.attn_bwd(dy)
+        else:
+            prob.attn_fwd_train()
+            dx, dw, dk, dv = prob.attn_bwd_saved(dy)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(dk).all()) and bool(torch.isfinite(dv).all()), path
+        got[path] = {"dx": dx[0, rows].double().cpu().numpy(),
+                     "dwq": dw[r][i * d:(i + 1) * d].double().cpu().numpy(),
+                     "dwo": dw[r][o0 + i * d:o0 + (i + 1) * d].double().cpu().numpy(),
+                     "dk": dk[0, :kv_len, kvh].double().cpu().numpy(),
+                     "dv": dv[0, :kv_len, kvh].double().cpu().numpy()}
+    del prob, dx, dw, dk, dv
+    torch.cuda.empty_cache()
+
+    x_b = I.bf16_bits_to_f64(x_bits[0, :kv_len])
+    dy_loc = I.bf16_bits_to_f64(dy_bits[0])
+    ref_dx = O.attention_bwd_rows(x_b, wf["wq"], wf["wk"], wf["wv"], wf["wo"], wl.n_heads,
+                                  wl.n_kv_heads, [p * s_loc + r_ for r_ in rows], dy_loc[rows])
     x_loc = x_b[p * s_loc:]
     q = x_loc @ wf["wq"][gh * d:(gh + 1) * d].T
     k = x_b @ wf["wk"][kvh * d:(kvh + 1) * d].T
@@ -179,18 +196,15 @@ def test_attention_backward_full_size(wl, p):
     sc = 1.0 / np.sqrt(d)
     a = O.causal_attention_core(q, k, v, p * s_loc, sc)
     dq, dk_ref, dv_ref = O.causal_attention_core_bwd(q, k, v, da, p * s_loc, sc)
-    got = dw[r].double().cpu().numpy()
-    assert_close(got[i * d:(i + 1) * d], dq.T @ x_loc, f"{wl.name} dW_Q head {gh}")
-    o0 = qd + 2 * kd
-    assert_close(got[o0 + i * d:o0 + (i + 1) * d], a.T @ dy_loc, f"{wl.name} dW_O^T head {gh}")
-    if g == 1:
-        assert_close(dk[0, :kv_len, kvh].double().cpu().numpy(), dk_ref,
-                     f"{wl.name} dK-hat kv head {kvh}")
-        assert_close(dv[0, :kv_len, kvh].double().cpu().numpy(), dv_ref,
-                     f"{wl.name} dV-hat kv head {kvh}")
-    assert bool(torch.isfinite(dk).all()) and bool(torch.isfinite(dv).all())
-    del prob, dx, dw, dk, dv
-    torch.cuda.empty_cache()
+    for path, t in got.items():
+        assert_close(t["dx"], ref_dx, f"{wl.name} {path} dX query-path rows")
+        assert_close(t["dwq"], dq.T @ x_loc, f"{wl.name} {path} dW_Q head {gh}")
+        assert_close(t["dwo"], a.T @ dy_loc, f"{wl.name} {path} dW_O^T head {gh}")
+        if g == 1:
+            assert_close(t["dk"], dk_ref, f"{wl.name} {path} dK-hat kv head {kvh}")
+            assert_close(t["dv"], dv_ref, f"{wl.name} {path} dV-hat kv head {kvh}")
+    for key in got["saved"]:
+        assert_close(got["saved"][key], got["recompute"][key], f"{wl.name} saved vs recompute {key}")
 
 
 def test_long_context_layer_output_is_finite_everywhere():

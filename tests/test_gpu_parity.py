@@ -166,6 +166,25 @@ def test_back_to_back_calls_are_bit_identical(wl, p):
     assert_close(first["layer"].double().cpu().numpy(), ref, f"{wl.name} r{p} layer")
 
 
+@pytest.mark.parametrize("wl,p", [(MID_GQA8, 1), (MID_MHA128, 0)], ids=["gqa8-r1", "mha128-r0"])
+def test_workspace_contents_do_not_matter(wl, p):
+    """A workspace filled with 0xff bytes (every float a NaN) gives the same output bit
+    for bit as a zeroed one: each call writes every workspace element it reads (these
+    shapes split the down and output projections' contraction through fp32 partials
+    there, next to the gated product with its zero padding, Q and A)."""
+    print(f"[dirty ws] {wl.name} rank {p}", flush=True)
+    prob = RankProblem(wl, *_inputs(wl), p)
+    prob.prefill_kv()
+    prob.ws.zero_()
+    ref = {"layer": prob.layer().clone(), "mlp": prob.mlp().clone(),
+           "attn": prob.attn_fwd().clone()}
+    for name, run in (("layer", prob.layer), ("mlp", prob.mlp), ("attn", prob.attn_fwd)):
+        prob.ws.fill_(255)
+        got = run().clone()
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref[name]), name
+
+
 def test_accumulate_flag_adds_to_existing_output():
     wl, p = TINY, 1
     x_bits, w_bits = _inputs(wl)
