@@ -27,9 +27,13 @@
 //
 // Schedule.  Per step every wavefront takes the 128-key tile j in two 64-key halves
 // (scores, softmax, P V each), while tile j+1 of K and V streams into the other slot
-// of the two-slot rings.  (Variants that delay P V by a step so the two wavefronts of
-// a SIMD alternate matrix and vector phases measured slower, as did deeper rings and
-// loads spread across the step.)
+// of the two-slot rings.  The first tile of a key range also forms each half's row
+// maximum (the online softmax's reference); later tiles skip it unless a half's
+// probabilities outgrow the reference (see the softmax state below): with two
+// wavefronts per SIMD the kernel is bound by instruction issue, so the vector work
+// per score is what sets its speed.  (Variants that delay P V by a step so the two
+// wavefronts of a SIMD alternate matrix and vector phases measured slower, as did
+// deeper rings and loads spread across the step.)
 //
 // Data movement.  K and V tiles go from HBM straight into LDS (buffer loads with an
 // LDS destination, no register staging) in their natural [key][d] layout, 16-byte
@@ -62,6 +66,11 @@ constexpr int kStepKeys = 128;       // keys staged per step
 static_assert(kQTile == kAttnQueryTile && kStepKeys == kAttnKeyStep, "tile sizes");
 constexpr int kHalfKeys = 64;        // keys per sub-step
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (exp2 units)
+// After a query's first key tile its reference is left in place while every probability of
+// a 64-key half stays below this bound (checked on the half's sum, which also catches an
+// overflow to inf): the normalised result does not depend on the reference, only the
+// range of the fp32 / bf16 values does.
+constexpr float kSumLimit = 0x1p40f;
 
 template <int D>
 struct FaCfg {
@@ -229,11 +238,14 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
 
   // Online-softmax state of this lane's query (shared with its partner lane l ^ 32).
   // Scores are produced relative to the reference mref (the score MFMAs start from the
-  // accumulator value -mref), so o = sum 2^(s - mref) v and l = sum 2^(s - mref).
-  // mref follows the running maximum lazily: it moves only when a score exceeds it by
-  // more than kRescaleLog2, or to the first visible score of the query; in between,
-  // every probability is bounded by 2^kRescaleLog2 and numerator and denominator share
-  // the stale reference, so the normalised result is unchanged.
+  // accumulator value -mref), so o = sum 2^(s - mref) v and l = sum 2^(s - mref); the
+  // normalised result o / l does not depend on mref, which only has to keep the values
+  // in range.  In the first key tile of the range (which holds the first key every query
+  // of the range sees) mref is set from the row maximum: it moves to the first visible
+  // score and whenever a score exceeds it by more than kRescaleLog2.  After that the row
+  // maximum is not formed: a 64-key half whose probabilities sum below kSumLimit (so
+  // every one of them is below it, and none overflowed) keeps mref; otherwise the half
+  // takes the first tile's path and its probabilities are formed again.
   f32x16 o[C::EB];
 #pragma unroll
   for (int eb = 0; eb < C::EB; ++eb)
@@ -293,7 +305,10 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   };
   // Lazy reference update for half H with row max mx (relative to mref).  Must follow
   // every P V product already issued: it rescales o.
-  auto rescale = [&](auto half, float mx) __attribute__((always_inline)) {
+  // With shift_other, the other half's scores (already formed against the old
+  // reference) move along.
+  auto rescale = [&](auto half, float mx, bool shift_other = false)
+                     __attribute__((always_inline)) {
     constexpr int H = decltype(half)::value;
     const bool visible = mx != -INFINITY;
     const bool move = mx > kRescaleLog2 || (!seen && visible);
@@ -311,6 +326,12 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
       for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) sc[H][bb][e] -= shift;
+      if (shift_other) {
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sc[1 - H][bb][e] -= shift;
+      }
 #pragma unroll
       for (int e = 0; e < 16; ++e) negm[e] = -mref;
     }
@@ -417,6 +438,81 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     pv(slot, h1);
     order_probs_pv();
   };
+  // Probabilities of half H (bf16, into pf as probs does) with their row sum in four
+  // partial sums started from zero; returns the lane's sum.
+  auto probs_sum = [&](auto half) __attribute__((always_inline)) {
+    constexpr int H = decltype(half)::value;
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
+    float ls[4];
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t pk = pack_bf16x2(__builtin_amdgcn_exp2f(sc[H][bb][8 * s2 + 2 * q]),
+                                          __builtin_amdgcn_exp2f(sc[H][bb][8 * s2 + 2 * q + 1]));
+          pf[H][bb][s2][q] = pk;
+          ls[q] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk), ones,
+                                                  bb == 0 && s2 == 0 ? 0.f : ls[q], false);
+        }
+    return (ls[0] + ls[1]) + (ls[2] + ls[3]);
+  };
+  // The half's probabilities are final unless one of them reached kSumLimit (then the
+  // reference moves as in the first tile, and they are formed again); adds the sum.
+  // Half 0 settles after half 1's scores were formed: those move with the reference.
+  auto settle = [&](auto half, float sum) __attribute__((always_inline)) {
+    constexpr int H = decltype(half)::value;
+    if (__any(!(sum < kSumLimit))) {
+      rescale(half, rowmax(half), H == 0);
+      sum = probs_sum(half);
+    }
+    l_run += sum;
+  };
+  // Both halves of tile j after the query's first tile: no row maximum unless settle
+  // finds one needed.
+  //   scores(0) | scores(1) + probs(0) | settle(0) | P V(0) + probs(1) | settle(1) | P V(1)
+  auto both_halves_fast = [&](auto slot, int j) __attribute__((always_inline)) {
+    constexpr IC<0> h0{};
+    constexpr IC<1> h1{};
+    const int kt0 = j * kStepKeys, kt1 = kt0 + kHalfKeys;
+    scores(slot, h0);
+    order_scores();
+    mask(h0, kt0);
+    scores(slot, h1);
+    const float s0 = probs_sum(h0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 2);
+#pragma unroll
+    for (int i = 0; i < C::KS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 2);
+      if (i + 2 < C::KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 2);
+      __builtin_amdgcn_sched_group_barrier(0x002, 64 / C::KS, 2);
+    }
+    settle(h0, s0);
+    mask(h1, kt1);
+    pv(slot, h0);
+    const float s1 = probs_sum(h1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 3);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int eb = 0; eb < C::EB; ++eb) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 3);
+        if (k < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 3);
+        __builtin_amdgcn_sched_group_barrier(0x002, 64 / (4 * C::EB), 3);
+      }
+    settle(h1, s1);
+    pv(slot, h1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 4);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int eb = 0; eb < C::EB; ++eb) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 4);
+        if (k < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 4);
+      }
+  };
   // One step: tile j (resident in slot SLOT once every wave's DMA has landed) is
   // consumed while tile j + 1 streams into the other slot.
   auto step = [&](auto slot, int j) __attribute__((always_inline)) {
@@ -429,16 +525,20 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     }
     // A half past every query of the wavefront (only in its last tile) is fully masked
     // and leaves the softmax state unchanged, so one code path serves every tile.
-    if (half_active(j, 0)) both_halves(slot, j);
+    if (half_active(j, 0)) {
+      if (j == j0) both_halves(slot, j);
+      else both_halves_fast(slot, j);
+    }
   };
 
   if (n_steps > 0) {
     dma_tile(kbase, dma_off_k, dma_col_k, j0, 0);
     dma_tile(vbase, dma_off_v, dma_col_v, j0, 2 * TB);
   }
-  for (int t = 0; t < n_steps; t += 2) {
-    step(IC<0>{}, j0 + t);
-    if (t + 1 < n_steps) step(IC<1>{}, j0 + t + 1);
+  if (n_steps > 0) step(IC<0>{}, j0);
+  for (int t = 1; t < n_steps; t += 2) {
+    step(IC<1>{}, j0 + t);
+    if (t + 1 < n_steps) step(IC<0>{}, j0 + t + 1);
   }
 
   l_run = sum_with_partner(l_run);

@@ -52,13 +52,23 @@ def gen(wl: Workload):
     return I.make_x_full(wl), I.make_weights(wl)
 
 
+RISING_ROWS = 128  # the first key tile of the attention kernel
+
+
 def stress_inputs(wl: Workload, kind: str):
     """Seeded inputs of wl; kind "peaky" multiplies W_Q by 8 (exact in bf16), which makes
-    the softmax rows peaky (the attention stress input)."""
+    the softmax rows peaky (the attention stress input); "rising" also divides the
+    token rows at sequence positions below RISING_ROWS by 16 (exact), so that the logits
+    of the first keys are small and a row's maximum grows by tens of log2 units after
+    its first key tile."""
     x_bits, w_bits = gen(wl)
-    if kind == "peaky":
+    if kind in ("peaky", "rising"):
         w_bits = dict(w_bits)
         w_bits["wq"] = I.round_to_bf16_bits(I.bf16_bits_to_f32(w_bits["wq"]) * np.float32(8.0))
+    if kind == "rising":
+        x_bits = x_bits.copy()
+        x_bits[:, :RISING_ROWS] = I.round_to_bf16_bits(
+            I.bf16_bits_to_f32(x_bits[:, :RISING_ROWS]) * np.float32(0.0625))
     return x_bits, w_bits
 
 

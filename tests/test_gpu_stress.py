@@ -6,6 +6,11 @@ oracle at the same tolerance as every other parity test, through the C ABI.
   row is dominated by a few keys and the running maximum of a row grows by many units
   as later key tiles arrive: the online softmax has to move its reference repeatedly
   (Algorithm 1's CausalAttn computed one key tile at a time).
+* Rising logits: the peaky input with the token rows of the first key tile (positions
+  below 128) divided by 16, so that a row's largest logit grows by 30-70 log2 units
+  after the first tile: the reference the kernel took from that tile no longer bounds
+  the probabilities (their sum over a 64-key half passes 2^40 or overflows), and the
+  half has to be formed again against a moved reference.
 * An explicit softmax scale (tsp_shape.softmax_scale = 0.2 instead of 1/sqrt(d)), on
   the forward and on the attention backward.
 
@@ -50,7 +55,7 @@ def _scale(kind):
 
 
 @pytest.mark.parametrize("wl,p", CASES, ids=_IDS)
-@pytest.mark.parametrize("kind", ["peaky", "scale"])
+@pytest.mark.parametrize("kind", ["peaky", "rising", "scale"])
 def test_attention_and_layer_forward(wl, p, kind):
     print(f"[stress fwd] {wl.name} {wl.layout_name} rank {p} {kind}", flush=True)
     x_bits, w_bits = _inputs(wl, kind)
@@ -66,7 +71,8 @@ def test_attention_and_layer_forward(wl, p, kind):
 
 
 BWD_CASES = [(TINY, 1, "peaky"), (MID_MHA128, 1, "peaky"), (MID_GQA64, 3, "scale"),
-             (MID_MHA128, 1, "scale"), (MID_GQA64.with_layout(1), 2, "scale")]
+             (MID_MHA128, 1, "scale"), (MID_GQA64.with_layout(1), 2, "scale"),
+             (MID_MHA128, 1, "rising")]
 
 
 @pytest.mark.parametrize("wl,p,kind", BWD_CASES,
