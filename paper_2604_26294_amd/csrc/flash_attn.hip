@@ -66,10 +66,9 @@ constexpr int kStepKeys = 128;       // keys staged per step
 static_assert(kQTile == kAttnQueryTile && kStepKeys == kAttnKeyStep, "tile sizes");
 constexpr int kHalfKeys = 64;        // keys per sub-step
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (exp2 units)
-// After a query's first key tile its reference is left in place while every probability of
-// a 64-key half stays below this bound (checked on the half's sum, which also catches an
-// overflow to inf): the normalised result does not depend on the reference, only the
-// range of the fp32 / bf16 values does.
+// After a query's first key tile its reference is left in place while the row sum stays
+// below this bound (which also catches an overflow to inf): the normalised result does not
+// depend on the reference, only the range of the fp32 / bf16 values does.
 constexpr float kSumLimit = 0x1p40f;
 
 template <int D>
@@ -243,9 +242,9 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   // in range.  In the first key tile of the range (which holds the first key every query
   // of the range sees) mref is set from the row maximum: it moves to the first visible
   // score and whenever a score exceeds it by more than kRescaleLog2.  After that the row
-  // maximum is not formed: a 64-key half whose probabilities sum below kSumLimit (so
-  // every one of them is below it, and none overflowed) keeps mref; otherwise the half
-  // takes the first tile's path and its probabilities are formed again.
+  // maximum is not formed: while the row sum stays below kSumLimit (so every probability
+  // since mref last moved is below it, and none overflowed) mref stays; a 64-key half
+  // that takes the sum past it takes the first tile's path instead and is formed again.
   f32x16 o[C::EB];
 #pragma unroll
   for (int eb = 0; eb < C::EB; ++eb)
@@ -438,37 +437,25 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     pv(slot, h1);
     order_probs_pv();
   };
-  // Probabilities of half H (bf16, into pf as probs does) with their row sum in four
-  // partial sums started from zero; returns the lane's sum.
-  auto probs_sum = [&](auto half) __attribute__((always_inline)) {
-    constexpr int H = decltype(half)::value;
-    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-    const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
-    float ls[4];
-#pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t pk = pack_bf16x2(__builtin_amdgcn_exp2f(sc[H][bb][8 * s2 + 2 * q]),
-                                          __builtin_amdgcn_exp2f(sc[H][bb][8 * s2 + 2 * q + 1]));
-          pf[H][bb][s2][q] = pk;
-          ls[q] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk), ones,
-                                                  bb == 0 && s2 == 0 ? 0.f : ls[q], false);
-        }
-    return (ls[0] + ls[1]) + (ls[2] + ls[3]);
+  // Probabilities of half H (bf16, into pf) added to the row sum, as probs does; the
+  // sum before the half is kept in l_prev.
+  float l_prev = 0.f;
+  auto probs_run = [&](auto half) __attribute__((always_inline)) {
+    l_prev = l_run;
+    probs(half);
   };
-  // The half's probabilities are final unless one of them reached kSumLimit (then the
-  // reference moves as in the first tile, and they are formed again); adds the sum.
-  // Half 0 settles after half 1's scores were formed: those move with the reference.
-  auto settle = [&](auto half, float sum) __attribute__((always_inline)) {
+  // The half's probabilities are final while the row sum stays below kSumLimit (then so
+  // does every probability since the reference last moved, and none overflowed).
+  // Otherwise the sum goes back to its value before the half, the reference moves as in
+  // the first tile and the half is formed again.  Half 0 settles after half 1's scores
+  // were formed: those move with the reference.
+  auto settle = [&](auto half) __attribute__((always_inline)) {
     constexpr int H = decltype(half)::value;
-    if (__any(!(sum < kSumLimit))) {
+    if (__any(!(l_run < kSumLimit))) {
+      l_run = l_prev;
       rescale(half, rowmax(half), H == 0);
-      sum = probs_sum(half);
+      probs(half);
     }
-    l_run += sum;
   };
   // Both halves of tile j after the query's first tile: no row maximum unless settle
   // finds one needed.
@@ -481,7 +468,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     order_scores();
     mask(h0, kt0);
     scores(slot, h1);
-    const float s0 = probs_sum(h0);
+    probs_run(h0);
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 2);
 #pragma unroll
     for (int i = 0; i < C::KS; ++i) {
@@ -489,10 +476,10 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
       if (i + 2 < C::KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 2);
       __builtin_amdgcn_sched_group_barrier(0x002, 64 / C::KS, 2);
     }
-    settle(h0, s0);
+    settle(h0);
     mask(h1, kt1);
     pv(slot, h0);
-    const float s1 = probs_sum(h1);
+    probs_run(h1);
     __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 3);
 #pragma unroll
     for (int k = 0; k < 4; ++k)
@@ -502,7 +489,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
         if (k < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 3);
         __builtin_amdgcn_sched_group_barrier(0x002, 64 / (4 * C::EB), 3);
       }
-    settle(h1, s1);
+    settle(h1);
     pv(slot, h1);
     __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 4);
 #pragma unroll
