@@ -31,9 +31,14 @@
 // maximum (the online softmax's reference); later tiles skip it unless a half's
 // probabilities outgrow the reference (see the softmax state below): with two
 // wavefronts per SIMD the kernel is bound by instruction issue, so the vector work
-// per score is what sets its speed.  (Variants that delay P V by a step so the two
-// wavefronts of a SIMD alternate matrix and vector phases measured slower, as did
-// deeper rings and loads spread across the step.)
+// per score is what sets its speed.  The slots are handed over through counters in
+// LDS rather than a workgroup barrier per step: the older wavefront of each SIMD
+// (the one the arbiter favours, which also issues the tile loads) may then run up to
+// about half a step ahead of the younger one instead of waiting for it every step.
+// (Variants that delay P V by a step so the two wavefronts of a SIMD alternate matrix
+// and vector phases measured slower, as did deeper rings, loads spread across the
+// step, and separate K and V counters that let the older wavefront run a whole step
+// ahead.)
 //
 // Data movement.  K and V tiles go from HBM straight into LDS (buffer loads with an
 // LDS destination, no register staging) in their natural [key][d] layout, 16-byte
@@ -113,10 +118,33 @@ __device__ __forceinline__ float sum_with_partner(float x) {
   return a + b;
 }
 
+// Per-slot synchronisation of the K/V ring through counters in LDS (instead of a
+// workgroup barrier per step).  The counters only grow within a query tile: slot s's
+// "full" count gains one per loader wavefront whose share of the slot's tile has landed,
+// its "empty" count one per wavefront done reading the slot.  A wait spins on the count
+// with s_sleep and gives up after kSpinMax polls, so an error in the protocol shows as
+// a wrong result, never as a hang.
+typedef __attribute__((address_space(3))) int lds_int;
+constexpr int kSpinMax = 4096;
+constexpr int kLoaders = kWaves / 2;  // the older wavefront of each SIMD loads the tiles
+__device__ __forceinline__ void lds_signal(lds_int* p) {
+  if ((threadIdx.x & 63) == 0)
+    asm volatile("ds_add_u32 %0, %1" ::"v"((uint32_t)(uintptr_t)p), "v"(1u) : "memory");
+}
+__device__ __forceinline__ void lds_wait_ge(lds_int* p, int target) {
+  for (int i = 0; i < kSpinMax; ++i) {
+    int v;
+    asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+                 : "=v"(v) : "v"((uint32_t)(uintptr_t)p) : "memory");
+    if (__builtin_amdgcn_readfirstlane(v) >= target) return;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
 // One query tile of the kernel: tile `order` in the kernel's tile order (see
 // flash_fwd_kernel), key range `split`, query head `head` of batch entry `b`; K/V slots
-// in Ls.  Returns with every wavefront done reading Ls only after a barrier that follows
-// its last tile load (the caller's next tile may refill the slots after a barrier).
+// in Ls.  A wavefront may return while others still read the slots: the caller's next
+// tile may refill them only after a barrier.
 template <int D, bool LSE>
 __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, const int nt0,
                                            const int nt1, const int order, const int split,
@@ -171,7 +199,12 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   // (the swizzle depends on the row only through bits that are the same for every i).
   // A full tile's source is (scalar tile base) + (scalar i * row step) + (per-lane 32-bit
   // offset), so its loads need no vector arithmetic.
+  // The loader wavefront w (w < kLoaders) issues the instructions of shares w and
+  // w + kLoaders; share w + kLoaders's rows are kShareRows further on and have the same
+  // swizzle (which depends on the row only through (row / RPW) mod KCH).
   constexpr int kRowStep = kWaves * C::ROWS_PER_DMA;  // rows between instructions
+  constexpr int kShareRows = kLoaders * C::ROWS_PER_DMA;
+  static_assert(kShareRows % (C::RPW * KCH) == 0, "shares w and w + kLoaders swizzle alike");
   const int dma_row0 = wave * C::ROWS_PER_DMA + lane / KCH;
   const int dma_col_k = 8 * ((lane % KCH) ^ C::fk(dma_row0));
   const int dma_col_v = 8 * ((lane % KCH) ^ C::fv(dma_row0));
@@ -183,24 +216,36 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   // rows at or past k_end are clamped to its last key: the range either ends at a
   // multiple of the tile size or at n_keys, and keys >= n_keys are past every query
   // of this workgroup, so those rows are always masked and merely need to be finite.
-  auto dma_tile = [&](const uint16_t* base, uint32_t lane_off, int col, int tile,
-                      int slot_off) __attribute__((always_inline)) {
+  auto dma_share = [&](const uint16_t* base, uint32_t lane_off, int col, int v, int tile,
+                       int slot_off) __attribute__((always_inline)) {
     const int key0 = tile * kStepKeys;
     const rsrc_t rsrc = make_rsrc(base + (size_t)key0 * kv_stride);
-    lds_char* dst = Ls + slot_off + wave * (kWave * 16);
+    lds_char* dst = Ls + slot_off + (wave + v * kLoaders) * (kWave * 16);
+    const uint32_t share_off = (uint32_t)(v * kShareRows) * row_bytes;
     if (key0 + kStepKeys <= k_end) {
 #pragma unroll
       for (int i = 0; i < C::DMA_PER_LANE; ++i)
-        dma16(rsrc, lane_off, i * dma_step, dst + i * kWaves * (kWave * 16));
+        dma16(rsrc, lane_off, share_off + i * dma_step, dst + i * kWaves * (kWave * 16));
     } else {
       const int last = k_end - 1 - key0;
 #pragma unroll
       for (int i = 0; i < C::DMA_PER_LANE; ++i) {
-        const uint32_t row = (uint32_t)min(dma_row0 + i * kRowStep, last);
+        const uint32_t row = (uint32_t)min(dma_row0 + v * kShareRows + i * kRowStep, last);
         dma16(rsrc, row * row_bytes + 2u * col, 0u, dst + i * kWaves * (kWave * 16));
       }
     }
   };
+  // K and V of tile `tile` into slot S: the calling loader's two shares.
+  auto load_tile = [&](int tile, int S) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      dma_share(kbase, dma_off_k, dma_col_k, v, tile, S * TB);
+      dma_share(vbase, dma_off_v, dma_col_v, v, tile, (2 + S) * TB);
+    }
+  };
+  lds_int* const ctr_full = reinterpret_cast<lds_int*>(Ls + 4 * TB);
+  lds_int* const ctr_empty = ctr_full + 2;
+  const bool loader = wave < kLoaders;
 
   // LDS read addresses.  Slot offsets and block strides are compile-time immediates;
   // the per-lane parts below are computed once.
@@ -394,7 +439,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   // independent matrix phase to overlap with:
   //   scores(0) | max(0) | rescale(0) | scores(1) + probs(0) | mask(1) |
   //   P V(0) + max(1) | rescale(1) | probs(1) + P V(1)
-  auto both_halves = [&](auto slot, int j) __attribute__((always_inline)) {
+  auto both_halves_a = [&](auto slot, int j) __attribute__((always_inline)) {
     constexpr IC<0> h0{};
     constexpr IC<1> h1{};
     const int kt0 = j * kStepKeys, kt1 = kt0 + kHalfKeys;
@@ -420,6 +465,10 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
       for (int s2 = 0; s2 < 2; ++s2) asm volatile("" ::"v"(pf[0][bb][s2]));
     asm volatile("" ::"v"(l_run));
     mask(h1, kt1);
+  };
+  auto both_halves_b = [&](auto slot) __attribute__((always_inline)) {
+    constexpr IC<0> h0{};
+    constexpr IC<1> h1{};
     pv(slot, h0);
     const float mx1 = rowmax(h1);
     // P V(0): its V^T reads run a k-step ahead; the row max of half 1 fills in.
@@ -460,7 +509,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   // Both halves of tile j after the query's first tile: no row maximum unless settle
   // finds one needed.
   //   scores(0) | scores(1) + probs(0) | settle(0) | P V(0) + probs(1) | settle(1) | P V(1)
-  auto both_halves_fast = [&](auto slot, int j) __attribute__((always_inline)) {
+  auto both_halves_fast_a = [&](auto slot, int j) __attribute__((always_inline)) {
     constexpr IC<0> h0{};
     constexpr IC<1> h1{};
     const int kt0 = j * kStepKeys, kt1 = kt0 + kHalfKeys;
@@ -478,6 +527,10 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     }
     settle(h0);
     mask(h1, kt1);
+  };
+  auto both_halves_fast_b = [&](auto slot) __attribute__((always_inline)) {
+    constexpr IC<0> h0{};
+    constexpr IC<1> h1{};
     pv(slot, h0);
     probs_run(h1);
     __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 3);
@@ -500,28 +553,40 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
         if (k < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 4);
       }
   };
-  // One step: tile j (resident in slot SLOT once every wave's DMA has landed) is
-  // consumed while tile j + 1 streams into the other slot.
+  // One step: tile j in slot SLOT.  The loaders' shares of tile j were issued during
+  // step j - 1; tile j + 1 goes into the other slot in the middle of this step, once
+  // every wavefront is done with tile j - 1 there.  The older wavefront of a SIMD can so
+  // run up to about half a step ahead of the younger one instead of waiting for it at a
+  // barrier every step.
   auto step = [&](auto slot, int j) __attribute__((always_inline)) {
     constexpr int S = decltype(slot)::value;
-    wait_dma();
-    __syncthreads();  // K and V tile j resident; every wave is past step j-1
-    if (j + 1 < j0 + n_steps) {
-      dma_tile(kbase, dma_off_k, dma_col_k, j + 1, (1 - S) * TB);
-      dma_tile(vbase, dma_off_v, dma_col_v, j + 1, (3 - S) * TB);
+    const int use = (j - j0) >> 1;  // earlier tiles in this slot
+    if (loader) {
+      wait_dma();
+      lds_signal(ctr_full + S);
     }
+    lds_wait_ge(ctr_full + S, kLoaders * (use + 1));  // K and V tile j resident
     // A half past every query of the wavefront (only in its last tile) is fully masked
     // and leaves the softmax state unchanged, so one code path serves every tile.
-    if (half_active(j, 0)) {
-      if (j == j0) both_halves(slot, j);
-      else both_halves_fast(slot, j);
+    const bool active = half_active(j, 0);
+    if (active) {
+      if (j == j0) both_halves_a(slot, j);
+      else both_halves_fast_a(slot, j);
     }
+    if (loader && j + 1 < j0 + n_steps) {
+      if (j > j0) lds_wait_ge(ctr_empty + (1 - S), kWaves * (((j - 1 - j0) >> 1) + 1));
+      load_tile(j + 1, 1 - S);
+    }
+    if (active) {
+      if (j == j0) both_halves_b(slot);
+      else both_halves_fast_b(slot);
+    }
+    lds_signal(ctr_empty + S);  // done with slot S (LDS operations complete in order)
   };
 
-  if (n_steps > 0) {
-    dma_tile(kbase, dma_off_k, dma_col_k, j0, 0);
-    dma_tile(vbase, dma_off_v, dma_col_v, j0, 2 * TB);
-  }
+  if (tid < 4) ctr_full[tid] = 0;  // full[0..1], empty[0..1]
+  __syncthreads();
+  if (n_steps > 0 && loader) load_tile(j0, 0);
   if (n_steps > 0) step(IC<0>{}, j0);
   for (int t = 1; t < n_steps; t += 2) {
     step(IC<1>{}, j0 + t);
@@ -572,8 +637,8 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
 template <int D, bool LSE>
 __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
   using C = FaCfg<D>;
-  // [K slot 0][K slot 1][V slot 0][V slot 1]
-  __shared__ __attribute__((aligned(1024))) char L[4 * C::TILE_BYTES];
+  // [K slot 0][K slot 1][V slot 0][V slot 1][slot counters]
+  __shared__ __attribute__((aligned(1024))) char L[4 * C::TILE_BYTES + 64];
   lds_char* Ls = (lds_char*)L;
   // Work item -> (batch, head, key range, query tile), query tile fastest, so the
   // workgroups that share an XCD (contiguous work indices) stream the same keys of the

@@ -23,8 +23,9 @@ __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" :
 // the next LDS read it cannot prove disjoint, which would stall every step of a
 // pipelined loop on the load of the NEXT tile.  Hidden in asm, the load is ordered only
 // by the kernel's own waits: a kernel using it reads a slot only after a vmcnt(0) wait
-// and a barrier that follow the slot's loads, and refills a slot only after a barrier
-// that follows its last read.  The compiler's own waits stay correct because loads
+// that follows the slot's loads and a barrier (or an LDS counter that every loading
+// wavefront raises after that wait), and refills a slot only after a barrier (or a
+// counter that every reader raises after its last read) that follows its last read.  The compiler's own waits stay correct because loads
 // complete in issue order.  Kernels using this helper use M0 nowhere else (a reserved
 // register the compiler does not track through asm).
 typedef u32x4 rsrc_t;
