@@ -884,7 +884,9 @@ long long tiles_of(const GemmParams* ps, int n, int bm, int bn) {
 // CUs (one workgroup per CU).  Gate+up (M = S_loc, N = F/D = 1376 per shard, 8 shards
 // per launch) takes the deep-ring 256 x 128 tiles when they make at least 4 rounds
 // (S_loc = 8192: 2816 tiles), else 128 x 128 two-wavefront tiles with a 3-slot ring;
-// Q/K/V (N = 3 d H_s = 1536 per shard) 256 x 192 tiles; down / O-proj (N = h = 4096)
+// Q/K/V (N = 3 d H_s = 1536 per shard) 256 x 256 tiles when they make two rounds or more
+// (S_loc = 8192: 1536 tiles), else 256 x 192 (S_loc = 1024: 256 tiles, one per CU) or,
+// below one tile per CU, 128 x 128; down / O-proj (N = h = 4096)
 // 256 x 256 tiles (512 at S_loc = 8192), their contraction split when that makes fewer
 // tiles than CUs.
 constexpr long long kCus = 256;
@@ -963,6 +965,10 @@ hipError_t launch_gemm_qkv(const GemmParams& p, hipStream_t s) {
 }
 
 hipError_t launch_gemm_qkv_group(const GemmParams* ps, int n, hipStream_t s) {
+  if (tiles_of(ps, n, 256, 256) >= 2 * kCus) {
+    if (n == 1) return launch<256, 256, 2, 4, false, EPI_QKV, 2>(ps[0], s);
+    return launch_group<256, 256, 2, 4, false, EPI_QKV, 2>(ps, n, s);
+  }
   if (tiles_of(ps, n, 256, 192) < kCus) {
     if (n == 1) return launch<128, 128, 2, 4, false, EPI_QKV, 2>(ps[0], s);
     return launch_group<128, 128, 2, 4, false, EPI_QKV, 2>(ps, n, s);
