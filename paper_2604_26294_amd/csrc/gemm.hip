@@ -500,224 +500,6 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
   gemm_epilogue<C, EPI>(P, acc, L, wave, lane, m0, n0, wm, wn, split);
 }
 
-// ---------------------------------------------------------------- deep-ring tiles
-// Products with [N, K] operands (both contraction-contiguous).  One wavefront per SIMD:
-// 4 per workgroup (2 x 2), each owning a (BM/2) x (BN/2) block of C (with the SwiGLU
-// epilogue: BN/2 gate and BN/2 up columns) as 32 x 32 MFMA tiles, 16 of them at BM = 256,
-// BN = 128 + 128: 256 fp32 accumulators per lane, held in the accumulation registers.  Per 16-deep substep a wavefront reads 8 operand fragments from LDS for 16
-// MFMAs (the two-wavefront-per-SIMD tiles above read 6 for 8), which halves the LDS
-// read traffic per MFMA.  K advances in stages of 32, through a ring of STAGES slots of
-// 32 KB: loads of stages kt+2 .. kt+STAGES stay in flight while stage kt is consumed
-// (about three stages of matrix work hide the load latency where a ring of two 64-deep
-// stages hides one).  Each stage has ONE workgroup barrier, placed among the MFMAs of
-// its second substep: every wavefront has by then received all of the stage's operands
-// (its slot may be refilled) and waited for its own loads of the next stage (which the
-// barrier makes visible to all), so the next stage's first operands are read while the
-// stage's last MFMAs still run.
-//
-// LDS layout.  Operand panels are rows of 32 bf16 (64 bytes, four 16-byte chunks),
-// physical chunk = logical chunk XOR ((row / 4) mod 4), so the 16 rows x one chunk of a
-// 16-lane group of an operand read cover all 64 banks.
-//
-// Measured against the two-wavefront tiles above on the 7B shapes: faster for gate+up
-// (1146 vs 1014 TFLOP/s), slower for the [K, N] products (whose transpose reads double
-// the LDS instructions per substep) and for Q/K/V, which keep the tiles above.
-template <int BM, int BN, int EPI, int STAGES>
-struct DrCfg {
-  static constexpr int WAVES = 4, THREADS = kWave * WAVES;
-  static constexpr int BKS = 32;  // contraction indices per stage
-  static constexpr int WM = BM / 2, WN = BN / 2;
-  static constexpr int TM = WM / 32, TN = WN / 32;
-  static constexpr bool BWD = false;
-  static constexpr int NBP = EPI == EPI_SWIGLU ? 2 : 1;  // B panels
-  static constexpr int TNB = NBP * TN;
-  static constexpr int NB = NBP * BN;
-  static constexpr int A_BYTES = BM * BKS * 2;
-  static constexpr int B_BYTES = NB * BKS * 2;
-  static constexpr int STAGE = A_BYTES + B_BYTES;
-  static constexpr int LDS_BYTES = STAGES * STAGE;
-  static constexpr int A_LOADS = A_BYTES / 1024 / WAVES;  // per wavefront and stage
-  static constexpr int B_LOADS = B_BYTES / 1024 / WAVES;
-  static constexpr int LOADS = A_LOADS + B_LOADS;
-  // Workgroups per CU the LDS ring allows (2 when it fits twice in 160 KB): with two,
-  // each SIMD interleaves two wavefronts, which must then fit in half the registers.
-  static constexpr int WAVES_PER_EU = 2 * LDS_BYTES <= 160 * 1024 ? 2 : 1;
-  static_assert(STAGES >= 3 && LDS_BYTES <= 160 * 1024, "LDS ring");
-  static_assert(LOADS * (STAGES - 1) < 64, "vmcnt range");
-  static_assert(A_LOADS * 1024 * WAVES == A_BYTES && B_LOADS * 1024 * WAVES == B_BYTES,
-                "DMA cover");
-  static_assert(EPI == EPI_SWIGLU || EPI == EPI_QKV, "[N, K] operand products");
-  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
-};
-
-__device__ __forceinline__ int dr_swz(int row) { return (row >> 2) & 3; }
-
-// Rows [row0, row0 + ROWS) x k [k0, k0 + 32) of a row-major [nrows, ld] matrix into LDS
-// (64-byte rows).  Instruction i of wave w fills rows 16 (i W + w) .. +15.
-template <int ROWS, int WAVES>
-__device__ __forceinline__ void dma_nt32(lds_char* dst, const uint16_t* base, int ld, int row0,
-                                         int nrows, int k0, int wave, int lane) {
-  const int rsub = lane >> 2, pc = lane & 3;
-#pragma unroll
-  for (int i = 0; i < ROWS / 16 / WAVES; ++i) {
-    const int blk = i * WAVES + wave;
-    const int r = 16 * blk + rsub;
-    const int grow = min(row0 + r, nrows - 1);
-    dma16(base + (size_t)grow * ld + k0 + 8 * (pc ^ dr_swz(r)), dst + blk * 1024);
-  }
-}
-
-template <int BM, int BN, int EPI, int STAGES>
-__device__ __forceinline__ void gemm_tile_dr(const GemmParams& P, const int w) {
-  using C = DrCfg<BM, BN, EPI, STAGES>;
-  constexpr int TM = C::TM, TN = C::TN, TNB = C::TNB, BKS = C::BKS;
-  __shared__ __attribute__((aligned(1024))) char L[C::LDS_BYTES];
-  lds_char* Ls = (lds_char*)L;
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int l32 = lane & 31, hh = lane >> 5;
-
-  const int tiles_n = (P.N + BN - 1) / BN;
-  int tm, tn;
-  tile_coords(w, (P.M + BM - 1) / BM, tiles_n, &tm, &tn);
-  const int m0 = tm * BM, n0 = tn * BN;
-
-  f32x16 acc[TM][TNB];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TNB; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  // Sources of stage k (contraction indices [k BKS, (k + 1) BKS)).
-  struct Src {
-    const uint16_t* a;
-    const uint16_t* b;
-    int kk;
-  };
-  auto stage_src = [&](int k) { return Src{P.A, P.B, k * BKS}; };
-  // Load instruction `piece` (0 .. LOADS-1) of this wavefront for a stage into `slot`:
-  // A rows first, then the B panels (16 rows of 64 bytes per instruction).
-  auto dma_piece = [&](int slot, const Src& src, int piece) {
-    lds_char* S = Ls + slot * C::STAGE;
-    if (piece < C::A_LOADS) {
-      const int blk = piece * C::WAVES + wave, r = 16 * blk + (lane >> 2);
-      const int grow = min(m0 + r, P.M - 1);
-      dma16(src.a + (size_t)grow * P.lda + src.kk + 8 * ((lane & 3) ^ dr_swz(r)), S + blk * 1024);
-      return;
-    }
-    constexpr int PER_PANEL = C::B_LOADS / C::NBP;
-    const int pb = piece - C::A_LOADS, panel = pb / PER_PANEL;
-    const int blk = (pb % PER_PANEL) * C::WAVES + wave, r = 16 * blk + (lane >> 2);
-    const int grow = min(n0 + r, P.N - 1);
-    const uint16_t* b = panel == 0 ? src.b : P.B2;
-    dma16(b + (size_t)grow * P.ldb + src.kk + 8 * ((lane & 3) ^ dr_swz(r)),
-          S + C::A_BYTES + panel * BN * BKS * 2 + blk * 1024);
-  };
-
-  // Operand of 32-row block R_base, substep s: R_base * 64 + (opa ^ 32 s).
-  const int opa = l32 * 64 + 16 * (hh ^ dr_swz(l32));
-  // Operand read `idx` (0 .. R-1: the TM A fragments, then the TNB B fragments) of
-  // substep s of the stage in `slot`.
-  auto read_one = [&](int slot, int s, int idx, u32x4 (&a)[TM], u32x4 (&b)[TNB]) {
-    const lds_char* SA = Ls + slot * C::STAGE;
-    const lds_char* SB = SA + C::A_BYTES;
-    const int xo = opa ^ (32 * s);
-    if (idx < TM) {
-      a[idx] = lds_read16(SA + (wm * C::WM + 32 * idx) * 64 + xo);
-      return;
-    }
-    const int j = idx - TM;
-    const int brow = (j / TN) * BN + wn * C::WN + 32 * (j % TN);  // panel j / TN
-    b[j] = lds_read16(SB + brow * 64 + xo);
-  };
-  constexpr int R = TM + TNB;         // operand fragments per substep
-  constexpr int MF = TM * TNB;        // MFMAs per substep
-  constexpr int FIRST = TNB;          // substep-1 MFMAs before the barrier
-  constexpr int ITEMS = R + C::LOADS; // reads and loads spread over the other MFMAs
-  constexpr int SLOTS = MF - FIRST;
-
-  const int nk = P.K / BKS;  // >= 2 (K is a multiple of 64)
-  // Stage k goes to slot k mod STAGES.  Stage indices past the last re-load the last
-  // stage into slots nothing reads again, so that every step has the same number of
-  // loads in flight (one fixed wait count).
-#pragma unroll
-  for (int st = 0; st < STAGES; ++st) {
-    const Src src = stage_src(min(st, nk - 1));
-#pragma unroll
-    for (int i = 0; i < C::LOADS; ++i) dma_piece(st, src, i);
-  }
-  wait_dma<C::LOADS * (STAGES - 1)>();
-  __syncthreads();
-  u32x4 a0[TM], b0[TNB], a1[TM], b1[TNB];
-#pragma unroll
-  for (int i = 0; i < R; ++i) read_one(0, 0, i, a0, b0);
-
-  auto step = [&](const int kt, auto last) {
-    const int slot = kt % STAGES;
-    // substep 0: MFMAs on (a0, b0), the reads of substep 1 spread over the first of them
-#pragma unroll
-    for (int i = 0; i < R; ++i) read_one(slot, 1, i, a1, b1);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TNB; ++j) acc[i][j] = mfma32(a0[i], b0[j], acc[i][j]);
-#pragma unroll
-    for (int i = 0; i < MF; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      if (2 * i + 1 < R) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      else if (2 * i < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    // substep 1: its first MFMAs (after which every read of stage kt has returned) ...
-#pragma unroll
-    for (int q = 0; q < FIRST; ++q)
-      acc[q / TNB][q % TNB] = mfma32(a1[q / TNB], b1[q % TNB], acc[q / TNB][q % TNB]);
-    if constexpr (!decltype(last)::value) {
-      const Src src = stage_src(min(kt + STAGES, nk - 1));
-      __builtin_amdgcn_sched_barrier(0);
-      // ... stage kt+1 resident (own loads waited for, everyone's through the barrier,
-      // which also ends every wavefront's reads of stage kt), then the rest of the
-      // MFMAs, with stage kt+1's first operand reads and the loads of stage kt+STAGES
-      // into slot kt spread between them.
-      wait_dma<C::LOADS * (STAGES - 2)>();
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      __syncthreads();
-      const int next = (kt + 1) % STAGES;
-#pragma unroll
-      for (int q = 0; q < SLOTS; ++q) {
-        const int qq = FIRST + q;
-        acc[qq / TNB][qq % TNB] = mfma32(a1[qq / TNB], b1[qq % TNB], acc[qq / TNB][qq % TNB]);
-#pragma unroll
-        for (int it = q * ITEMS / SLOTS; it < (q + 1) * ITEMS / SLOTS; ++it) {
-          if (it < R) read_one(next, 0, it, a0, b0);
-          else dma_piece(slot, src, it - R);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    } else {
-#pragma unroll
-      for (int q = FIRST; q < MF; ++q)
-        acc[q / TNB][q % TNB] = mfma32(a1[q / TNB], b1[q % TNB], acc[q / TNB][q % TNB]);
-    }
-  };
-  for (int kt = 0; kt + 1 < nk; ++kt) step(kt, std::false_type{});
-  step(nk - 1, std::true_type{});
-  wait_dma<0>();   // the re-loads of the last stages
-  __syncthreads();  // operand slots are free for the epilogue
-  gemm_epilogue<C, EPI>(P, acc, L, wave, lane, m0, n0, wm, wn);
-}
-
-template <int BM, int BN, int EPI, int STAGES>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
-    DrCfg<BM, BN, EPI, STAGES>::WAVES_PER_EU))) void gemm_dr_kernel(const GemmParams P) {
-  const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
-  gemm_tile_dr<BM, BN, EPI, STAGES>(P, xcd_work_index(blockIdx.x, tiles));
-}
-
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
 __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_kernel(const GemmParams P) {
   const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
@@ -823,54 +605,6 @@ hipError_t launch(const GemmParams& p, hipStream_t s) {
                          dim3((unsigned)tiles), dim3(C::THREADS), args, 0, s);
 }
 
-template <int BM, int BN, int EPI, int STAGES>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
-    DrCfg<BM, BN, EPI, STAGES>::WAVES_PER_EU))) void gemm_dr_group_kernel(const GemmGroup G) {
-  int tiles[kGemmGroupMax], total = 0;
-#pragma unroll
-  for (int i = 0; i < kGemmGroupMax; ++i) {
-    tiles[i] = i < G.n ? ((G.p[i].M + BM - 1) / BM) * ((G.p[i].N + BN - 1) / BN) : 0;
-    total += tiles[i];
-  }
-  int w = xcd_work_index(blockIdx.x, total), i = 0;
-  while (i + 1 < G.n && w >= tiles[i]) w -= tiles[i++];  // uniform per workgroup
-  gemm_tile_dr<BM, BN, EPI, STAGES>(G.p[i], w);
-}
-
-template <int BM, int BN, int EPI, int STAGES>
-hipError_t launch_dr(const GemmParams& p, hipStream_t s) {
-  if (p.M <= 0 || p.N <= 0) return hipSuccess;
-  if (p.k_splits > 1) return hipErrorInvalidValue;
-  const hipError_t e = check_params<BM, BN, 2, 2, false, EPI, STAGES>(p);
-  if (e != hipSuccess) return e;
-  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-  void* args[] = {const_cast<GemmParams*>(&p)};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&gemm_dr_kernel<BM, BN, EPI, STAGES>),
-                         dim3(tiles), dim3(256), args, 0, s);
-}
-
-template <int BM, int BN, int EPI, int STAGES>
-hipError_t launch_dr_group(const GemmParams* ps, int n, hipStream_t s) {
-  if (n == 1) return launch_dr<BM, BN, EPI, STAGES>(ps[0], s);
-  if (n < 1 || n > kGemmGroupMax) return hipErrorInvalidValue;
-  GemmGroup g = {};
-  long long total = 0;
-  for (int i = 0; i < n; ++i) {
-    const GemmParams& p = ps[i];
-    if (p.M <= 0 || p.N <= 0) return hipErrorInvalidValue;
-    const hipError_t e = check_params<BM, BN, 2, 2, false, EPI, STAGES>(p);
-    if (e != hipSuccess) return e;
-    g.p[i] = p;
-    total += (long long)((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-  }
-  g.n = n;
-  if (total > INT32_MAX) return hipErrorInvalidValue;
-  void* args[] = {&g};
-  return hipLaunchKernel(
-      reinterpret_cast<const void*>(&gemm_dr_group_kernel<BM, BN, EPI, STAGES>),
-      dim3((unsigned)total), dim3(256), args, 0, s);
-}
-
 long long tiles_of(const GemmParams* ps, int n, int bm, int bn) {
   long long t = 0;
   for (int i = 0; i < n && i < kGemmGroupMax; ++i)
@@ -882,8 +616,9 @@ long long tiles_of(const GemmParams* ps, int n, int bm, int bn) {
 
 // Tile shapes are chosen for the grouped shard products of the 7B-class layer on 256
 // CUs (one workgroup per CU).  Gate+up (M = S_loc, N = F/D = 1376 per shard, 8 shards
-// per launch) takes the deep-ring 256 x 128 tiles when they make at least 4 rounds
-// (S_loc = 8192: 2816 tiles), else 128 x 128 two-wavefront tiles with a 3-slot ring;
+// per launch) takes 256 x 128 tiles (256 x 256 accumulators: gate and up) with a 2-slot
+// ring when they make at least 4 rounds (S_loc = 8192: 2816 tiles), else 128 x 128 tiles
+// with a 3-slot ring;
 // Q/K/V (N = 3 d H_s = 1536 per shard) 256 x 256 tiles when they make two rounds or more
 // (S_loc = 8192: 1536 tiles), else 256 x 192 (S_loc = 1024: 256 tiles, one per CU) or,
 // below one tile per CU, 128 x 128; down / O-proj (N = h = 4096)
@@ -896,7 +631,10 @@ hipError_t launch_gemm_swiglu(const GemmParams& p, hipStream_t s) {
 }
 
 hipError_t launch_gemm_swiglu_group(const GemmParams* ps, int n, hipStream_t s) {
-  if (tiles_of(ps, n, 256, 128) >= 4 * kCus) return launch_dr_group<256, 128, EPI_SWIGLU, 4>(ps, n, s);
+  if (tiles_of(ps, n, 256, 128) >= 4 * kCus) {
+    if (n == 1) return launch<256, 128, 2, 4, false, EPI_SWIGLU, 2>(ps[0], s);
+    return launch_group<256, 128, 2, 4, false, EPI_SWIGLU, 2>(ps, n, s);
+  }
   if (n == 1) return launch<128, 128, 2, 4, false, EPI_SWIGLU, 3>(ps[0], s);
   return launch_group<128, 128, 2, 4, false, EPI_SWIGLU, 3>(ps, n, s);
 }

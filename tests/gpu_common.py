@@ -30,6 +30,9 @@ DEG16 = Workload("degree-d16", 1, 1024, 1024, 2048, 16, 16, 64, 16, 13, w_std=0.
 # launch plan pairs query tiles (5 tiles: pairs (0, 4), (1, 3) and tile 2 alone; in the
 # zigzag layout 6 tiles, pairs across the two segments); GQA g = 2.
 SUBL = Workload("sub-launch-b10", 10, 5120, 512, 1024, 8, 4, 64, 4, 2, w_std=0.05)
+# the gate+up product of a group of 8 shards in 256 x 128 tiles (at least 4 rounds on 256
+# CUs: 16 x 8 x 8 = 1024 tiles) with a ragged F/D = 1000
+MLP_BIG = Workload("mlp-big-fd1000", 1, 32768, 512, 8000, 8, 8, 64, 8, 7, w_std=0.04)
 
 
 def metrics(got, ref):

@@ -12,7 +12,7 @@ from paper_2604_26294_amd import inputs as I  # noqa: E402
 from paper_2604_26294_amd import tsp as T  # noqa: E402
 from paper_2604_26294_amd.harness import RankProblem  # noqa: E402
 from paper_2604_26294_amd.workloads import TINY  # noqa: E402
-from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, ODD3, SINGLE,  # noqa: E402
+from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, MLP_BIG, ODD3, SINGLE,  # noqa: E402
                               assert_close, f64, gen, oracle_blocks)
 
 CASES = [(TINY, 0), (TINY, 1), (MID_GQA64, 0), (MID_GQA64, 2), (MID_GQA64, 3),
@@ -183,6 +183,20 @@ def test_workspace_contents_do_not_matter(wl, p):
         got = run().clone()
         torch.cuda.synchronize()
         assert torch.equal(got, ref[name]), name
+
+
+def test_mlp_block_on_large_gate_up_tiles():
+    """The MLP block at a shape whose grouped gate+up product takes the 256 x 128 tiles
+    (1024 tiles, F/D = 1000: ragged column tiles and the zero padding of Hs to 1024),
+    every element against the oracle."""
+    wl = MLP_BIG
+    print(f"[mlp big tiles] {wl.name}", flush=True)
+    x_bits, w_bits = _inputs(wl)
+    prob = RankProblem(wl, x_bits, w_bits, wl.rank)
+    got = prob.mlp().double().cpu().numpy()
+    torch.cuda.synchronize()
+    ref = oracle_blocks(wl, x_bits, w_bits, wl.rank, blocks=("mlp",))["mlp"]
+    assert_close(got, ref, f"{wl.name} MLP")
 
 
 def test_accumulate_flag_adds_to_existing_output():
