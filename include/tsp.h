@@ -337,6 +337,16 @@ enum {
 tsp_status tsp_profile_enable(int enable);
 tsp_status tsp_profile_read(int kernel, double* total_ms, int64_t* launches);
 
+/* Test hook for the failure path of the attention forward (tsp_attn_rank_fwd and every
+ * entry point that runs it): its workgroups hand their K/V tiles over through counters
+ * in LDS, and each wait polls its counter at most a bounded number of times, so that a
+ * broken hand-over cannot hang the GPU; a query tile in which a wait gave up is written
+ * as NaN (and its log-sum-exp too).  polls > 0 caps every such wait at that many polls
+ * for launches enqueued after the call (a cap of 1 makes the waits give up and the
+ * outputs NaN, which is what the test checks); 0 restores the default of 4096.
+ * Process-wide.  TSP_ERR_SHAPE for polls < 0. */
+tsp_status tsp_test_set_attn_poll_limit(int32_t polls);
+
 /* Static, human-readable name of a status code. */
 const char* tsp_status_str(tsp_status status);
 

@@ -51,6 +51,8 @@
 // LDS read address is (per-lane base XOR a constant) + an immediate offset.
 #include <math.h>
 
+#include <atomic>
+
 #include <functional>
 #include <mutex>
 #include <queue>
@@ -122,8 +124,9 @@ __device__ __forceinline__ float sum_with_partner(float x) {
 // workgroup barrier per step).  The counters only grow within a query tile: slot s's
 // "full" count gains one per loader wavefront whose share of the slot's tile has landed,
 // its "empty" count one per wavefront done reading the slot.  A wait spins on the count
-// with s_sleep and gives up after kSpinMax polls, so an error in the protocol shows as
-// a wrong result, never as a hang.
+// with s_sleep and gives up after kSpinMax polls, so an error in the protocol can never
+// hang the kernel; a wait that gave up raises a flag, and the query tile's results are
+// then written as NaN (a loud wrong result rather than a quiet one).
 typedef __attribute__((address_space(3))) int lds_int;
 constexpr int kSpinMax = 4096;
 constexpr int kLoaders = kWaves / 2;  // the older wavefront of each SIMD loads the tiles
@@ -131,14 +134,19 @@ __device__ __forceinline__ void lds_signal(lds_int* p) {
   if ((threadIdx.x & 63) == 0)
     asm volatile("ds_add_u32 %0, %1" ::"v"((uint32_t)(uintptr_t)p), "v"(1u) : "memory");
 }
-__device__ __forceinline__ void lds_wait_ge(lds_int* p, int target) {
-  for (int i = 0; i < kSpinMax; ++i) {
-    int v;
-    asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-                 : "=v"(v) : "v"((uint32_t)(uintptr_t)p) : "memory");
-    if (__builtin_amdgcn_readfirstlane(v) >= target) return;
+__device__ __forceinline__ int lds_read_count(lds_int* p) {
+  int v;
+  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+               : "=v"(v) : "v"((uint32_t)(uintptr_t)p) : "memory");
+  return __builtin_amdgcn_readfirstlane(v);
+}
+__device__ __forceinline__ void lds_wait_ge(lds_int* p, int target, lds_int* flag,
+                                            int polls) {
+  for (int i = 0; i < polls; ++i) {
+    if (lds_read_count(p) >= target) return;
     __builtin_amdgcn_s_sleep(1);
   }
+  lds_signal(flag);
 }
 
 // One query tile of the kernel: tile `order` in the kernel's tile order (see
@@ -245,6 +253,8 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   };
   lds_int* const ctr_full = reinterpret_cast<lds_int*>(Ls + 4 * TB);
   lds_int* const ctr_empty = ctr_full + 2;
+  lds_int* const ctr_gave_up = ctr_full + 4;
+  const int polls = P.poll_limit > 0 ? P.poll_limit : kSpinMax;
   const bool loader = wave < kLoaders;
 
   // LDS read addresses.  Slot offsets and block strides are compile-time immediates;
@@ -565,7 +575,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
       wait_dma();
       lds_signal(ctr_full + S);
     }
-    lds_wait_ge(ctr_full + S, kLoaders * (use + 1));  // K and V tile j resident
+    lds_wait_ge(ctr_full + S, kLoaders * (use + 1), ctr_gave_up, polls);  // tile j resident
     // A half past every query of the wavefront (only in its last tile) is fully masked
     // and leaves the softmax state unchanged, so one code path serves every tile.
     const bool active = half_active(j, 0);
@@ -574,7 +584,8 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
       else both_halves_fast_a(slot, j);
     }
     if (loader && j + 1 < j0 + n_steps) {
-      if (j > j0) lds_wait_ge(ctr_empty + (1 - S), kWaves * (((j - 1 - j0) >> 1) + 1));
+      if (j > j0)
+        lds_wait_ge(ctr_empty + (1 - S), kWaves * (((j - 1 - j0) >> 1) + 1), ctr_gave_up, polls);
       load_tile(j + 1, 1 - S);
     }
     if (active) {
@@ -584,7 +595,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     lds_signal(ctr_empty + S);  // done with slot S (LDS operations complete in order)
   };
 
-  if (tid < 4) ctr_full[tid] = 0;  // full[0..1], empty[0..1]
+  if (tid < 5) ctr_full[tid] = 0;  // full[0..1], empty[0..1], gave-up flag
   __syncthreads();
   if (n_steps > 0 && loader) load_tile(j0, 0);
   if (n_steps > 0) step(IC<0>{}, j0);
@@ -593,6 +604,11 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     if (t + 1 < n_steps) step(IC<0>{}, j0 + t + 1);
   }
 
+  __syncthreads();  // every wavefront is past its last wait
+  if (lds_read_count(ctr_gave_up) != 0) {
+    l_run = __builtin_nanf("");
+    mref = __builtin_nanf("");
+  }
   l_run = sum_with_partner(l_run);
   if (!qvalid) return;
   const size_t trow = (size_t)b * P.s_loc + row0 + qloc;  // token row
@@ -849,7 +865,12 @@ double attn_launch_seconds(const AttnParams& p, bool pair) {
   return pair ? plan.sec_pair : plan.sec_split;
 }
 
-hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
+static std::atomic<int> g_attn_poll_limit{0};
+void set_attn_poll_limit(int polls) { g_attn_poll_limit.store(polls); }
+
+hipError_t launch_flash_attn(const AttnParams& p_in, hipStream_t s) {
+  AttnParams p = p_in;
+  p.poll_limit = g_attn_poll_limit.load();
   if (p.batch <= 0 || p.s_loc <= 0 || p.heads <= 0) return hipSuccess;
   if (p.n_seg < 1 || p.n_seg > 2) return hipErrorInvalidValue;
   int n_qt = 0, rows = 0;
@@ -885,7 +906,7 @@ hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s) {
     return hipErrorInvalidValue;
   }
   // hipLaunchKernel returns the status of this launch only (not an earlier error).
-  void* args[] = {const_cast<AttnParams*>(&p)};
+  void* args[] = {&p};
   const hipError_t e = hipLaunchKernel(fn, grid, dim3(kThreads), args, 0, s);
   if (e != hipSuccess || p.n_split == 1) return e;
   const long long threads = p.part_rows * (long long)(p.head_dim / 4);

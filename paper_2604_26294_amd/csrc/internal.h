@@ -152,6 +152,9 @@ struct AttnParams {
   // With n_split = 1: each workgroup takes two query tiles of one head, the i-th most
   // and the i-th fewest keys (equal work per workgroup).
   int pair_tiles;
+  // Polls after which a wait of the forward's slot hand-over gives up (its query tile is
+  // then written as NaN); set by launch_flash_attn from the process-wide test limit.
+  int poll_limit;
   long long part_rows;
   float* part_o;
   float* part_ml;
@@ -180,6 +183,9 @@ int attn_split_count(const AttnParams& p, int* split_len);
 // attn_split_count chooses (pair = false), or with paired query tiles and no split.
 double attn_launch_seconds(const AttnParams& p, bool pair);
 
+// Process-wide cap on the polls of the forward attention's slot waits (0: the default);
+// a test hook for that protocol's failure path.
+void set_attn_poll_limit(int polls);
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s);
 
 // Backward of launch_flash_attn for one shard's heads (same segments and buffers).

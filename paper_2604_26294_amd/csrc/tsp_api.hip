@@ -1145,6 +1145,12 @@ tsp_status tsp_layer_rank_fwd_noalloc(const tsp_shape* shape, const uint16_t* x_
                    static_cast<char*>(ws), stream);
 }
 
+tsp_status tsp_test_set_attn_poll_limit(int32_t polls) {
+  if (polls < 0) return TSP_ERR_SHAPE;
+  tsp::set_attn_poll_limit(polls);
+  return TSP_OK;
+}
+
 tsp_status tsp_profile_enable(int enable) {
   std::lock_guard<std::mutex> lock(g_timer.mu);
   g_timer.on = enable != 0;

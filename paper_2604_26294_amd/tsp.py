@@ -75,6 +75,7 @@ def _load() -> ctypes.CDLL:
         "tsp_last_hip_error": [],
         "tsp_hip_error_string": [I],
         "tsp_profile_enable": [I],
+        "tsp_test_set_attn_poll_limit": [I],
         "tsp_profile_read": [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
     }
     for name, args in sig.items():
@@ -236,6 +237,11 @@ def tsp_layer_rank_fwd_noalloc(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf
     _check(lib.tsp_layer_rank_fwd_noalloc(ctypes.byref(shape), _ptr(x_loc), a, g, u, d,
                                           _ptr(k_buf), _ptr(v_buf), _ptr(y_loc),
                                           _stream(stream)), "tsp_layer_rank_fwd_noalloc")
+
+
+def tsp_test_set_attn_poll_limit(polls: int):
+    """Test hook: cap the attention forward's slot waits at ``polls`` (0: default)."""
+    _check(lib.tsp_test_set_attn_poll_limit(int(polls)), "tsp_test_set_attn_poll_limit")
 
 
 def tsp_profile_enable(enable: bool = True):

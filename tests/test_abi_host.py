@@ -288,3 +288,12 @@ def test_training_pair_rejects_bad_arguments():
     a = list(bwd)
     a[0] = ctypes.byref(bad)
     assert L.tsp_attn_rank_bwd_saved(*a) == 3
+
+
+def test_attention_poll_limit_hook_validates():
+    """The attention forward's poll-limit test hook takes 0 (the default) and positive
+    caps, and rejects negative ones through the C ABI (no GPU work)."""
+    from paper_2604_26294_amd import tsp as T
+    assert T.STATUS_NAMES[T.lib.tsp_test_set_attn_poll_limit(-1)] == "TSP_ERR_SHAPE"
+    assert T.lib.tsp_test_set_attn_poll_limit(3) == T.TSP_OK
+    assert T.lib.tsp_test_set_attn_poll_limit(0) == T.TSP_OK

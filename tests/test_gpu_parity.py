@@ -12,7 +12,7 @@ from paper_2604_26294_amd import inputs as I  # noqa: E402
 from paper_2604_26294_amd import tsp as T  # noqa: E402
 from paper_2604_26294_amd.harness import RankProblem  # noqa: E402
 from paper_2604_26294_amd.workloads import TINY  # noqa: E402
-from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, MLP_BIG, ODD3, SINGLE,  # noqa: E402
+from tests.gpu_common import (MID_GQA64, MID_GQA8, MID_MHA128, MLP_BIG, ODD3, SINGLE, SUBL,  # noqa: E402
                               assert_close, f64, gen, oracle_blocks)
 
 CASES = [(TINY, 0), (TINY, 1), (MID_GQA64, 0), (MID_GQA64, 2), (MID_GQA64, 3),
@@ -197,6 +197,29 @@ def test_mlp_block_on_large_gate_up_tiles():
     torch.cuda.synchronize()
     ref = oracle_blocks(wl, x_bits, w_bits, wl.rank, blocks=("mlp",))["mlp"]
     assert_close(got, ref, f"{wl.name} MLP")
+
+
+@pytest.mark.parametrize("wl,p", [(MID_MHA128, 1), (SUBL.with_layout(1), 1)],
+                         ids=["key-range-split", "paired-tiles"])
+def test_attention_slot_wait_that_gives_up_is_loud(wl, p):
+    """The attention forward hands its K/V slots over through bounded waits on LDS
+    counters.  With every wait capped at one poll (the C ABI's test hook) the waits give
+    up, and every output of the attention block must come back NaN, not a quiet wrong
+    value; with the default restored the next call reproduces the first bit for bit."""
+    print(f"[poll limit] {wl.name} {wl.layout_name} rank {p}", flush=True)
+    prob = RankProblem(wl, *_inputs(wl), p)
+    prob.prefill_kv()
+    good = prob.attn_fwd().clone()
+    try:
+        T.tsp_test_set_attn_poll_limit(1)
+        bad = prob.attn_fwd().clone()
+        torch.cuda.synchronize()
+    finally:
+        T.tsp_test_set_attn_poll_limit(0)
+    again = prob.attn_fwd().clone()
+    torch.cuda.synchronize()
+    assert bool(torch.isnan(bad).all())
+    assert torch.equal(again, good)
 
 
 def test_accumulate_flag_adds_to_existing_output():
