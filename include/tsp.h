@@ -337,14 +337,15 @@ enum {
 tsp_status tsp_profile_enable(int enable);
 tsp_status tsp_profile_read(int kernel, double* total_ms, int64_t* launches);
 
-/* Test hook for the failure path of the attention forward (tsp_attn_rank_fwd and every
- * entry point that runs it): its workgroups hand their K/V tiles over through counters
+/* Test hook for the failure path of the attention kernels' tile hand-over (the forward
+ * of tsp_attn_rank_fwd and every entry point that runs it, and the dK/dV kernel of the
+ * attention backward): their workgroups hand K/V (or query) tiles over through counters
  * in LDS, and each wait polls its counter at most a bounded number of times, so that a
- * broken hand-over cannot hang the GPU; a query tile in which a wait gave up is written
- * as NaN (and its log-sum-exp too).  polls > 0 caps every such wait at that many polls
- * for launches enqueued after the call (a cap of 1 makes the waits give up and the
- * outputs NaN, which is what the test checks); 0 restores the default of 4096.
- * Process-wide.  TSP_ERR_SHAPE for polls < 0. */
+ * broken hand-over cannot hang the GPU; a workgroup in which a wait gave up writes its
+ * outputs as NaN (attention output and log-sum-exp, or dK / dV contributions).
+ * polls > 0 caps every such wait at that many polls for launches enqueued after the
+ * call (a cap of 1 makes the waits give up and the outputs NaN, which is what the tests
+ * check); 0 restores the default of 4096.  Process-wide.  TSP_ERR_SHAPE for polls < 0. */
 tsp_status tsp_test_set_attn_poll_limit(int32_t polls);
 
 /* Static, human-readable name of a status code. */

@@ -867,6 +867,7 @@ double attn_launch_seconds(const AttnParams& p, bool pair) {
 
 static std::atomic<int> g_attn_poll_limit{0};
 void set_attn_poll_limit(int polls) { g_attn_poll_limit.store(polls); }
+int attn_poll_limit() { return g_attn_poll_limit.load(); }
 
 hipError_t launch_flash_attn(const AttnParams& p_in, hipStream_t s) {
   AttnParams p = p_in;

@@ -145,6 +145,32 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const AttnBwdParams 
   }
 }
 
+// Slot hand-over of the dK/dV kernel's query ring through counters in LDS (as in the
+// forward kernel): "full" gains one per loader wavefront whose share of the slot's tile
+// (and its lse / delta rows) is in LDS, "empty" one per wavefront done reading the slot.
+// Waits poll with s_sleep and give up after a bounded number of polls; a wait that gave
+// up flags the workgroup, whose dK / dV are then written as NaN.
+typedef __attribute__((address_space(3))) int lds_int;
+constexpr int kKvLoaders = kKvWaves / 2;  // the older wavefront of each SIMD loads
+constexpr int kBwdSpinMax = 4096;
+__device__ __forceinline__ void bwd_signal(lds_int* p) {
+  if ((threadIdx.x & 63) == 0)
+    asm volatile("ds_add_u32 %0, %1" ::"v"((uint32_t)(uintptr_t)p), "v"(1u) : "memory");
+}
+__device__ __forceinline__ int bwd_count(lds_int* p) {
+  int v;
+  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+               : "=v"(v) : "v"((uint32_t)(uintptr_t)p) : "memory");
+  return __builtin_amdgcn_readfirstlane(v);
+}
+__device__ __forceinline__ void bwd_wait_ge(lds_int* p, int target, lds_int* flag, int polls) {
+  for (int i = 0; i < polls; ++i) {
+    if (bwd_count(p) >= target) return;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  bwd_signal(flag);
+}
+
 // ---------------------------------------------------------------------------------
 // Key-stationary kernel: dK, dV of 256 keys of one kv head.
 //
@@ -152,10 +178,10 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const AttnBwdParams 
 // and LDS phases overlap the other's matrix work; wave w owns keys 32 w .. 32 w + 31 of
 // the tile.  Its K fragments stay in registers; the V rows (B operand of dP) are read
 // from the workgroup's V tile, loaded into LDS once.  Query tiles of 64 rows of Qs and
-// dO stream through a two-slot ring, unrolled by slot so that LDS addresses are
-// registers plus immediates; each wave takes a tile in two 32-query blocks: S and dP
-// (row reads), the probabilities and dS (vector ops), then dV^T and dK^T (transpose
-// reads).
+// dO stream through a two-slot ring (handed over through the counters above, not a
+// barrier per tile), unrolled by slot so that LDS addresses are registers plus
+// immediates; each wave takes a tile in two 32-query blocks: S and dP (row reads), the
+// probabilities and dS (vector ops), then dV^T and dK^T (transpose reads).
 template <int D>
 __global__ __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
@@ -163,9 +189,10 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   constexpr int T64 = C::T64;
   constexpr int VT = kKvTile * C::RB;  // the V tile
   constexpr int VO = 4 * T64 + 2 * 2 * kQStage * 4;  // its offset
-  // [Qs slot 0][Qs slot 1][dO slot 0][dO slot 1][lse, delta slot 0][slot 1][V tile]: the
-  // ring first, so that its offsets fit the 16-bit immediate of the LDS reads.
-  __shared__ __attribute__((aligned(1024))) char L[VO + VT];
+  // [Qs slot 0][Qs slot 1][dO slot 0][dO slot 1][lse, delta slot 0][slot 1][V tile]
+  // [slot counters]: the ring first, so that its offsets fit the 16-bit immediate of the
+  // LDS reads.
+  __shared__ __attribute__((aligned(1024))) char L[VO + VT + 64];
   lds_char* Ls = (lds_char*)L;
   float* Lf = reinterpret_cast<float*>(L + 4 * T64);
 
@@ -255,7 +282,8 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   // first 16 lanes of each wave, lse / delta of rows 8 w .. 8 w + 7 into registers.
   // They are written to LDS negated; rows past the segment are clamped on load and get
   // -lse = -inf, -delta = 0 there (P = 0).
-  const int pr = 8 * wave + (lane & 7), pwhich = (lane >> 3) & 1;
+  // (loader wavefronts only: 16 rows each, lanes 0-15 lse, 16-31 delta)
+  const int pr = 16 * wave + (lane & 15), pwhich = (lane >> 4) & 1;
   // (the array base is chosen from two scalar values, not by indexing the parameter
   // block per lane, which would load the pointer from memory)
   const float* const pbase = pwhich ? P.delta : P.lse;
@@ -285,8 +313,13 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     adv(c_next);
     const size_t e0 = (((size_t)b * P.s_loc + P.seg_row0[T.seg] + T.r0) * P.heads + T.head) * D;
     const int last = P.seg_rows[T.seg] - 1 - T.r0;
-    load_tile64<D, kKvWaves>(P.Qs + e0, q_row_bytes, last, Ls + S * T64, wave, lane);
-    load_tile64<D, kKvWaves>(P.dO + e0, q_row_bytes, last, Ls + (2 + S) * T64, wave, lane);
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {  // the loader's two shares
+      load_tile64<D, kKvWaves>(P.Qs + e0, q_row_bytes, last, Ls + S * T64, wave + v * kKvLoaders,
+                               lane);
+      load_tile64<D, kKvWaves>(P.dO + e0, q_row_bytes, last, Ls + (2 + S) * T64,
+                               wave + v * kKvLoaders, lane);
+    }
   };
 
   // Per-lane LDS offsets (the swizzle of a row depends only on its index mod 16, which
@@ -376,26 +409,47 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
     (void)rows_left;
   };
 
-  // One tile in slot S: make it resident (its lse / delta into LDS, every wave's loads
-  // landed, every wave done with the previous tile), start the next one into the other
-  // slot, then its two blocks.
+  // One tile in slot S: the loaders put its lse / delta into LDS once their shares of
+  // its rows have landed and count themselves in; every wavefront waits for all four.
+  // Between its two blocks a loader starts the next tile into the other slot (once every
+  // wavefront is done with the tile before in that slot) and the lse / delta two tiles
+  // on; the older wavefront of a SIMD can so run up to about half a tile ahead of the
+  // younger one instead of waiting for it every tile.
+  lds_int* const ctr_full = reinterpret_cast<lds_int*>(Ls + VO + VT);
+  lds_int* const ctr_empty = ctr_full + 2;
+  lds_int* const ctr_gave_up = ctr_full + 4;
+  const int polls = P.poll_limit > 0 ? P.poll_limit : kBwdSpinMax;
+  const bool loader = wave < kKvLoaders;
   Cursor c_pos{0, 0};
   auto tile = [&](auto slot, int t) __attribute__((always_inline)) {
     constexpr int S = decltype(slot)::value;
-    if (lane < 16)
-      Lf[S * 2 * kQStage + pwhich * kQStage + pr] =
-          pr <= pend_last[S] ? -pend[S] : (pwhich ? 0.f : -INFINITY);
-    asm volatile("s_waitcnt vmcnt(1)" ::: "memory");  // all but tile t + 1's lse / delta
-    __syncthreads();
-    if (t + 1 < n_tiles) issue(IC<1 - S>{});
-    pend_load(IC<S>{});  // tile t + 2
+    if (loader) {
+      asm volatile("s_waitcnt vmcnt(1)" ::: "memory");  // all but tile t + 1's lse / delta
+      if (lane < 32)
+        Lf[S * 2 * kQStage + pwhich * kQStage + pr] =
+            pr <= pend_last[S] ? -pend[S] : (pwhich ? 0.f : -INFINITY);
+      bwd_signal(ctr_full + S);  // (LDS operations complete in order)
+    }
+    bwd_wait_ge(ctr_full + S, kKvLoaders * ((t >> 1) + 1), ctr_gave_up, polls);
     const Tile T = tile_at(c_pos);
     adv(c_pos);
     const int tpos = P.seg_pos0[T.seg] + T.r0;
     block(slot, IC<0>{}, tpos, 0);
+    if (loader) {
+      if (t + 1 < n_tiles) {
+        if (t > 0)
+          bwd_wait_ge(ctr_empty + (1 - S), kKvWaves * (((t - 1) >> 1) + 1), ctr_gave_up, polls);
+        issue(IC<1 - S>{});
+      }
+      pend_load(IC<S>{});  // tile t + 2
+    }
     if (T.r0 + 32 < P.seg_rows[T.seg]) block(slot, IC<1>{}, tpos, 0);
+    bwd_signal(ctr_empty + S);
   };
-  if (n_tiles > 0) {
+  if (tid < 5) ctr_full[tid] = 0;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wavefront's V rows
+  __syncthreads();  // every V row in LDS; counters zero
+  if (n_tiles > 0 && loader) {
     pend_load(IC<0>{});
     issue(IC<0>{});
     pend_load(IC<1>{});
@@ -403,6 +457,13 @@ void attn_bwd_dkdv_kernel(const AttnBwdParams P) {
   for (int t = 0; t < n_tiles; t += 2) {
     tile(IC<0>{}, t);
     if (t + 1 < n_tiles) tile(IC<1>{}, t + 1);
+  }
+  __syncthreads();  // every wavefront is past its last wait
+  if (bwd_count(ctr_gave_up) != 0) {
+#pragma unroll
+    for (int eb = 0; eb < C::EB; ++eb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) dkT[eb][e] = dvT[eb][e] = __builtin_nanf("");
   }
 
   // Accumulator element 4 g + r of block eb: d = 32 eb + 8 g + 4 hh + r, key = `key`.
@@ -707,11 +768,13 @@ hipError_t launch_attn_bwd_prep(const AttnBwdParams& p, hipStream_t s) {
   return hipLaunchKernel(fn, dim3((unsigned)((threads + 255) / 256)), dim3(256), args, 0, s);
 }
 
-hipError_t launch_attn_bwd_dkdv(const AttnBwdParams& p, hipStream_t s) {
-  if (bwd_empty(p)) return hipSuccess;
-  const hipError_t e = check_bwd(p);
+hipError_t launch_attn_bwd_dkdv(const AttnBwdParams& p_in, hipStream_t s) {
+  if (bwd_empty(p_in)) return hipSuccess;
+  const hipError_t e = check_bwd(p_in);
   if (e != hipSuccess) return e;
-  void* args[] = {const_cast<AttnBwdParams*>(&p)};
+  AttnBwdParams p = p_in;
+  p.poll_limit = attn_poll_limit();
+  void* args[] = {&p};
   const int n_kt = (int)((p.seq + kKvTile - 1) / kKvTile);
   const void* fn = p.head_dim == 128 ? reinterpret_cast<const void*>(&attn_bwd_dkdv_kernel<128>)
                                      : reinterpret_cast<const void*>(&attn_bwd_dkdv_kernel<64>);

@@ -186,6 +186,7 @@ double attn_launch_seconds(const AttnParams& p, bool pair);
 // Process-wide cap on the polls of the forward attention's slot waits (0: the default);
 // a test hook for that protocol's failure path.
 void set_attn_poll_limit(int polls);
+int attn_poll_limit();
 hipError_t launch_flash_attn(const AttnParams& p, hipStream_t s);
 
 // Backward of launch_flash_attn for one shard's heads (same segments and buffers).
@@ -236,6 +237,9 @@ struct AttnBwdParams {
   long long o_ld;
   int lse_head0;
   int lse_heads;
+  // Polls after which a wait of the dK/dV kernel's slot hand-over gives up (its dK / dV
+  // are then written as NaN); set by the launcher from the process-wide test limit.
+  int poll_limit;
 };
 
 // Number of key ranges for the dQ kernel (and their length, a multiple of the key

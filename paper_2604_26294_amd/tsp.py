@@ -240,7 +240,7 @@ def tsp_layer_rank_fwd_noalloc(shape, x_loc, w_attn, w_gate, w_up, w_down, k_buf
 
 
 def tsp_test_set_attn_poll_limit(polls: int):
-    """Test hook: cap the attention forward's slot waits at ``polls`` (0: default)."""
+    """Test hook: cap the attention kernels' slot waits at ``polls`` (0: default)."""
     _check(lib.tsp_test_set_attn_poll_limit(int(polls)), "tsp_test_set_attn_poll_limit")
 
 

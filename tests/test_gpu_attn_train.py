@@ -23,6 +23,7 @@ torch = pytest.importorskip("torch")
 
 from oracle import tsp_oracle as O  # noqa: E402
 from paper_2604_26294_amd import inputs as I  # noqa: E402
+from paper_2604_26294_amd import tsp as T  # noqa: E402
 from paper_2604_26294_amd.harness import (RankProblem, local_positions, local_rows,  # noqa: E402
                                           to_device_bf16)
 from paper_2604_26294_amd.workloads import TINY  # noqa: E402
@@ -131,3 +132,32 @@ def test_backward_from_kept_activations(wl, p):
         assert_close(dv_all[:, :, cols], ref["dv"][r], f"{wl.name} r{p} dV-hat[{r}]")
     assert_close(dk_all, dk_r.double().cpu().numpy(), "dK-hat vs recomputing")
     assert_close(dv_all, dv_r.double().cpu().numpy(), "dV-hat vs recomputing")
+
+
+def test_dkdv_slot_wait_that_gives_up_is_loud():
+    """The dK/dV kernel hands its query tiles over through bounded waits on LDS counters.
+    With every wait capped at one poll (the C ABI's test hook) the waits give up and the
+    dK-hat / dV-hat contributions must come back NaN, while dX (the query path, from the
+    dQ kernel, which has no such waits) stays finite; with the default restored the next
+    call reproduces the first bit for bit.  The kept-activation path is used so that no
+    forward attention runs under the cap."""
+    wl, p = MID_MHA128, 1
+    print(f"[bwd poll limit] {wl.name} rank {p}", flush=True)
+    x_bits, w_bits, dy_bits = _inputs(wl)
+    prob = RankProblem(wl, x_bits, w_bits, p)
+    prob.prefill_kv(include_self=True)
+    dy = to_device_bf16(local_rows(dy_bits, wl, p))
+    prob.attn_fwd_train()
+    first = [t.clone() for t in prob.attn_bwd_saved(dy) if torch.is_tensor(t)]
+    try:
+        T.tsp_test_set_attn_poll_limit(1)
+        dx, _, dk, dv = (t.clone() if torch.is_tensor(t) else t for t in prob.attn_bwd_saved(dy))
+        torch.cuda.synchronize()
+    finally:
+        T.tsp_test_set_attn_poll_limit(0)
+    assert bool(torch.isnan(dk).all()) and bool(torch.isnan(dv).all())
+    assert bool(torch.isfinite(dx).all())
+    again = [t.clone() for t in prob.attn_bwd_saved(dy) if torch.is_tensor(t)]
+    torch.cuda.synchronize()
+    for a, b in zip(again, first):
+        assert torch.equal(a, b)
