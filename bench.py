@@ -47,10 +47,10 @@ PEAK_HBM_GBS = 8000.0
 # on (sha256 prefix); after any change to that source the traffic is reported as null.
 MEASURED_TRAFFIC = {
     # flash_fwd_kernel<128, false>: one launch over 4 shards' 16 heads with paired query
-    # tiles (2 per layer step), no key-range split (578 359.0 / 32 768.0 KiB)
+    # tiles (2 per layer step), no key-range split (681 013.1 / 32 769.3 KiB)
     ("7b-h4096-S65536-D8", 7, "attn"): {
-        "source": "flash_attn.hip", "sha256": "e151bbd1cb54c08f",
-        "fetch_kib": 578359.0, "fetch_scale": 2.0, "write_kib": 32768.0, "write_scale": 1.0},
+        "source": "flash_attn.hip", "sha256": "f5a67afad3079290",
+        "fetch_kib": 681013.1, "fetch_scale": 2.0, "write_kib": 32769.3, "write_scale": 1.0},
 }
 
 

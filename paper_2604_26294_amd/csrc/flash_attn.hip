@@ -125,8 +125,12 @@ __device__ __forceinline__ float sum_with_partner(float x) {
 // "full" count gains one per loader wavefront whose share of the slot's tile has landed,
 // its "empty" count one per wavefront done reading the slot.  A wait spins on the count
 // with s_sleep and gives up after kSpinMax polls, so an error in the protocol can never
-// hang the kernel; a wait that gave up raises a flag, and the query tile's results are
-// then written as NaN (a loud wrong result rather than a quiet one).
+// hang the kernel.  A wavefront remembers in a register whether one of its waits gave
+// up and raises the query tile's flag once, after its last step; the tile's results are
+// then written as NaN (a loud wrong result rather than a quiet one).  The spin loop has
+// a compile-time bound and nothing but the poll in it: the pattern in which the
+// workgroups of an XCD reuse each other's K/V tiles in L2 turned out to depend on that
+// loop's code (a flag store inside it raised the launch's HBM fetch by half).
 typedef __attribute__((address_space(3))) int lds_int;
 constexpr int kSpinMax = 4096;
 constexpr int kLoaders = kWaves / 2;  // the older wavefront of each SIMD loads the tiles
@@ -140,20 +144,22 @@ __device__ __forceinline__ int lds_read_count(lds_int* p) {
                : "=v"(v) : "v"((uint32_t)(uintptr_t)p) : "memory");
   return __builtin_amdgcn_readfirstlane(v);
 }
-__device__ __forceinline__ void lds_wait_ge(lds_int* p, int target, lds_int* flag,
-                                            int polls) {
+// True once the count at p reaches target; false after `polls` polls.
+__device__ __forceinline__ bool lds_wait_ge(lds_int* p, int target, int polls) {
   for (int i = 0; i < polls; ++i) {
-    if (lds_read_count(p) >= target) return;
+    if (lds_read_count(p) >= target) return true;
     __builtin_amdgcn_s_sleep(1);
   }
-  lds_signal(flag);
+  return false;
 }
 
 // One query tile of the kernel: tile `order` in the kernel's tile order (see
 // flash_fwd_kernel), key range `split`, query head `head` of batch entry `b`; K/V slots
 // in Ls.  A wavefront may return while others still read the slots: the caller's next
-// tile may refill them only after a barrier.
-template <int D, bool LSE>
+// tile may refill them only after a barrier.  kPollArg: the slot waits give up after
+// P.poll_limit polls instead of kSpinMax (the instantiation behind the test hook that
+// caps the polls; every other launch uses the compile-time bound).
+template <int D, bool LSE, bool kPollArg>
 __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, const int nt0,
                                            const int nt1, const int order, const int split,
                                            const int head, const int b) {
@@ -254,7 +260,8 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   lds_int* const ctr_full = reinterpret_cast<lds_int*>(Ls + 4 * TB);
   lds_int* const ctr_empty = ctr_full + 2;
   lds_int* const ctr_gave_up = ctr_full + 4;
-  const int polls = P.poll_limit > 0 ? P.poll_limit : kSpinMax;
+  const int polls = kPollArg ? P.poll_limit : kSpinMax;
+  bool gave_up = false;  // one of this wavefront's waits gave up (wave-uniform)
   const bool loader = wave < kLoaders;
 
   // LDS read addresses.  Slot offsets and block strides are compile-time immediates;
@@ -575,7 +582,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
       wait_dma();
       lds_signal(ctr_full + S);
     }
-    lds_wait_ge(ctr_full + S, kLoaders * (use + 1), ctr_gave_up, polls);  // tile j resident
+    gave_up |= !lds_wait_ge(ctr_full + S, kLoaders * (use + 1), polls);  // tile j resident
     // A half past every query of the wavefront (only in its last tile) is fully masked
     // and leaves the softmax state unchanged, so one code path serves every tile.
     const bool active = half_active(j, 0);
@@ -585,7 +592,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     }
     if (loader && j + 1 < j0 + n_steps) {
       if (j > j0)
-        lds_wait_ge(ctr_empty + (1 - S), kWaves * (((j - 1 - j0) >> 1) + 1), ctr_gave_up, polls);
+        gave_up |= !lds_wait_ge(ctr_empty + (1 - S), kWaves * (((j - 1 - j0) >> 1) + 1), polls);
       load_tile(j + 1, 1 - S);
     }
     if (active) {
@@ -604,7 +611,8 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     if (t + 1 < n_steps) step(IC<0>{}, j0 + t + 1);
   }
 
-  __syncthreads();  // every wavefront is past its last wait
+  if (gave_up) lds_signal(ctr_gave_up);
+  __syncthreads();  // every wavefront is past its last wait and has raised its flag
   if (lds_read_count(ctr_gave_up) != 0) {
     l_run = __builtin_nanf("");
     mref = __builtin_nanf("");
@@ -650,7 +658,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
 }
 
 
-template <int D, bool LSE>
+template <int D, bool LSE, bool kPollArg>
 __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P) {
   using C = FaCfg<D>;
   // [K slot 0][K slot 1][V slot 0][V slot 1][slot counters]
@@ -674,10 +682,10 @@ __global__ __launch_bounds__(kThreads) void flash_fwd_kernel(const AttnParams P)
   rest /= P.n_split;
   const int head = rest % P.heads;
   const int b = rest / P.heads;
-  flash_tile<D, LSE>(P, Ls, nt0, nt1, item, split, head, b);
+  flash_tile<D, LSE, kPollArg>(P, Ls, nt0, nt1, item, split, head, b);
   if (P.pair_tiles && n_qt - 1 - item != item) {
     __syncthreads();  // every wavefront is done with the first tile's K/V slots
-    flash_tile<D, LSE>(P, Ls, nt0, nt1, n_qt - 1 - item, split, head, b);
+    flash_tile<D, LSE, kPollArg>(P, Ls, nt0, nt1, n_qt - 1 - item, split, head, b);
   }
 }
 
@@ -891,16 +899,21 @@ hipError_t launch_flash_attn(const AttnParams& p_in, hipStream_t s) {
     return hipErrorInvalidValue;
   const int n_items = p.pair_tiles ? (n_qt + 1) / 2 : n_qt;
   const dim3 grid(n_items * p.n_split * p.heads * p.batch);
+  const bool capped = p.poll_limit > 0;
   const void* fn;
   const void* combine;
   if (p.head_dim == 128) {
-    fn = p.lse ? reinterpret_cast<const void*>(&flash_fwd_kernel<128, true>)
-               : reinterpret_cast<const void*>(&flash_fwd_kernel<128, false>);
+    fn = p.lse ? (capped ? reinterpret_cast<const void*>(&flash_fwd_kernel<128, true, true>)
+                         : reinterpret_cast<const void*>(&flash_fwd_kernel<128, true, false>))
+               : (capped ? reinterpret_cast<const void*>(&flash_fwd_kernel<128, false, true>)
+                         : reinterpret_cast<const void*>(&flash_fwd_kernel<128, false, false>));
     combine = p.lse ? reinterpret_cast<const void*>(&attn_combine_kernel<128, true>)
                     : reinterpret_cast<const void*>(&attn_combine_kernel<128, false>);
   } else if (p.head_dim == 64) {
-    fn = p.lse ? reinterpret_cast<const void*>(&flash_fwd_kernel<64, true>)
-               : reinterpret_cast<const void*>(&flash_fwd_kernel<64, false>);
+    fn = p.lse ? (capped ? reinterpret_cast<const void*>(&flash_fwd_kernel<64, true, true>)
+                         : reinterpret_cast<const void*>(&flash_fwd_kernel<64, true, false>))
+               : (capped ? reinterpret_cast<const void*>(&flash_fwd_kernel<64, false, true>)
+                         : reinterpret_cast<const void*>(&flash_fwd_kernel<64, false, false>));
     combine = p.lse ? reinterpret_cast<const void*>(&attn_combine_kernel<64, true>)
                     : reinterpret_cast<const void*>(&attn_combine_kernel<64, false>);
   } else {
