@@ -321,14 +321,26 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   u32x4 pf[2][2][2];  // bf16 probabilities of the halves (B operands of P V)
 
   // S^T - mref of half H of the tile in slot SLOT: 2 blocks of 32 keys x 32 queries.
+  // The K fragments are read two contraction steps ahead of their MFMAs, in the source
+  // order itself: at this register count the compiler keeps the order it is given, and
+  // an MFMA whose operand read was issued just before it waits out the LDS latency.
   auto scores = [&](auto slot, auto half) __attribute__((always_inline)) {
     constexpr int S = decltype(slot)::value, H = decltype(half)::value;
+    auto kread = [&](int ks, int bb) __attribute__((always_inline)) {
+      return lds_read16(Ls + kad[ks] + (S * TB + (kHalfKeys * H + 32 * bb) * RB));
+    };
+    u32x4 kf[2][2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb) kf[ks][bb] = kread(ks, bb);
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
-      for (int bb = 0; bb < 2; ++bb)
-        sc[H][bb] = mfma32(lds_read16(Ls + kad[ks] + (S * TB + (kHalfKeys * H + 32 * bb) * RB)),
-                           qf[ks], ks == 0 ? negm : sc[H][bb]);
+      for (int bb = 0; bb < 2; ++bb) {
+        sc[H][bb] = mfma32(kf[ks & 1][bb], qf[ks], ks == 0 ? negm : sc[H][bb]);
+        if (ks + 2 < C::KS) kf[ks & 1][bb] = kread(ks + 2, bb);
+      }
   };
   // Issue order for a block holding only score MFMAs: K fragments two contraction steps
   // ahead of their MFMAs, so the LDS latency hides behind the matrix work.
@@ -420,20 +432,28 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   // 32 bb + 16 s2 + [0, 16) of the half tile; lane half hh feeds keys 4 hh + 0..3
   // (elements 0-3) and 8 + 4 hh + 0..3 (4-7), matching the accumulator layout of the
   // scores.
+  // MFMA i takes k-step i / EB (bb, s2) and column block i % EB; its V^T fragment is read
+  // kPvAhead MFMAs ahead, in the source order (as for the scores).
+  constexpr int kPvAhead = 3;
   auto pv = [&](auto slot, auto half) __attribute__((always_inline)) {
     constexpr int S = decltype(slot)::value, H = decltype(half)::value;
+    constexpr int N = 4 * C::EB;
+    auto vread = [&](int i) __attribute__((always_inline)) {
+      const int kx = i / C::EB, eb = i % C::EB;
+      const int imm = S * TB + (kHalfKeys * H + 32 * (kx >> 1) + 16 * (kx & 1)) * RB;
+      const u32x2 lo = lds_read_tr(Ls + va[eb] + imm);
+      const u32x2 hi = lds_read_tr(Ls + vb[eb] + imm);
+      return u32x4{lo[0], lo[1], hi[0], hi[1]};
+    };
+    u32x4 vf[kPvAhead];
 #pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
+    for (int i = 0; i < kPvAhead; ++i) vf[i] = vread(i);
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-#pragma unroll
-        for (int eb = 0; eb < C::EB; ++eb) {
-          const int imm = S * TB + (kHalfKeys * H + 32 * bb + 16 * s2) * RB;
-          const u32x2 lo = lds_read_tr(Ls + va[eb] + imm);
-          const u32x2 hi = lds_read_tr(Ls + vb[eb] + imm);
-          o[eb] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pf[H][bb][s2], o[eb]);
-        }
-      }
+    for (int i = 0; i < N; ++i) {
+      const int kx = i / C::EB, eb = i % C::EB;
+      o[eb] = mfma32(vf[i % kPvAhead], pf[H][kx >> 1][kx & 1], o[eb]);
+      if (i + kPvAhead < N) vf[i % kPvAhead] = vread(i + kPvAhead);
+    }
   };
   // Issue order for a block holding the probabilities of a half and its P V product:
   // the V^T reads of k-step k+1 and the 16 vector ops that produce its probabilities
@@ -512,13 +532,19 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
   };
   // The half's probabilities are final while the row sum stays below kSumLimit (then so
   // does every probability since the reference last moved, and none overflowed).
-  // Otherwise the sum goes back to its value before the half, the reference moves as in
-  // the first tile and the half is formed again.  Half 0 settles after half 1's scores
-  // were formed: those move with the reference.
-  auto settle = [&](auto half) __attribute__((always_inline)) {
+  // Otherwise the sum goes back to its value before the half, the half's scores are
+  // formed again from the K tile (still in its slot), the reference moves as in the
+  // first tile and the probabilities are formed again.  Recomputing the scores on this
+  // rare path lets them die as soon as their probabilities exist: keeping them for it
+  // would hold 32 more registers through the step, which is what the schedule of the
+  // steady-state step has no room for.  Half 0 settles after half 1's scores were
+  // formed: those move with the reference.
+  auto settle = [&](auto slot, auto half, int kt) __attribute__((always_inline)) {
     constexpr int H = decltype(half)::value;
     if (__any(!(l_run < kSumLimit))) {
       l_run = l_prev;
+      scores(slot, half);
+      mask(half, kt);
       rescale(half, rowmax(half), H == 0);
       probs(half);
     }
@@ -542,10 +568,10 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
       if (i + 2 < C::KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 2);
       __builtin_amdgcn_sched_group_barrier(0x002, 64 / C::KS, 2);
     }
-    settle(h0);
+    settle(slot, h0, kt0);
     mask(h1, kt1);
   };
-  auto both_halves_fast_b = [&](auto slot) __attribute__((always_inline)) {
+  auto both_halves_fast_b = [&](auto slot, int j) __attribute__((always_inline)) {
     constexpr IC<0> h0{};
     constexpr IC<1> h1{};
     pv(slot, h0);
@@ -559,7 +585,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
         if (k < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 3);
         __builtin_amdgcn_sched_group_barrier(0x002, 64 / (4 * C::EB), 3);
       }
-    settle(h1);
+    settle(slot, h1, j * kStepKeys + kHalfKeys);
     pv(slot, h1);
     __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::EB, 4);
 #pragma unroll
@@ -597,7 +623,7 @@ __device__ __forceinline__ void flash_tile(const AttnParams& P, lds_char* Ls, co
     }
     if (active) {
       if (j == j0) both_halves_b(slot);
-      else both_halves_fast_b(slot);
+      else both_halves_fast_b(slot, j);
     }
     lds_signal(ctr_empty + S);  // done with slot S (LDS operations complete in order)
   };
