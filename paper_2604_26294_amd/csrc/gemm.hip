@@ -40,6 +40,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "lds_dma.h"
 
 namespace tsp {
 namespace {
@@ -47,38 +48,12 @@ namespace {
 constexpr int BK = 64;
 enum { EPI_SWIGLU = 0, EPI_ACC = 1, EPI_QKV = 2, EPI_SWIGLU_BWD = 3 };
 
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) char lds_char;
-
 // Wait until at most N of this wavefront's operand loads are still in flight (loads
 // complete in issue order).
 template <int N>
 __device__ __forceinline__ void wait_dma() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane (M0 holds
-// the wave's LDS destination).  Issued from inline assembly: the compiler cannot tell
-// which LDS bytes such a load writes and would otherwise wait for ALL of them (vmcnt(0))
-// before the first transpose read of the NN panels, i.e. for the next stage's loads at
-// the start of every K step.  The loads are ordered by the ring's own counted waits and
-// barriers instead; loads complete in issue order, so the compiler's own waits remain
-// correct.  No other code in this kernel uses M0 (a reserved register the compiler
-// does not track through asm).
-__device__ __forceinline__ void dma16(const void* src, lds_char* lds) {
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(m0) : "memory", "m0");
-}
-
-__device__ __forceinline__ u32x4 lds_read16(const lds_char* p) {
-  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p);
-}
-
-__device__ __forceinline__ u32x2 lds_read_tr(const lds_char* p) {
-  return __builtin_bit_cast(
-      u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p));
 }
 
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
@@ -122,37 +97,72 @@ __device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int
 __device__ __forceinline__ int nt_swz(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ int nn_swz(int row) { return 4 * (row & 3); }
 
+// Operand panels go HBM -> LDS through buffer loads with an LDS destination (lds_dma.h):
+// address = resource base (the matrix) + scalar offset (the stage's K position) + a
+// per-lane offset.  The per-lane offsets only depend on the tile and the lane, so they
+// are formed once per tile and a stage is issued without vector arithmetic.  The byte
+// extent of every operand must stay below 4 GiB (checked at launch).
+//
 // NT panel rows [row0, row0 + ROWS) x k [k0, k0 + 64) of a row-major [nrows, ld] matrix
-// into LDS (128-byte rows).  Instruction i of wave w fills rows 8 (i W + w) .. +7.
+// (128-byte LDS rows): instruction i of wave w fills rows 8 (i W + w) .. +7, lane l row
+// 8 (i W + w) + l / 8, physical chunk l % 8 (logical chunk XOR nt_swz(row)); rows past
+// nrows are clamped to the last one.  Stage offset: 2 k0 bytes.
 template <int ROWS, int WAVES>
-__device__ __forceinline__ void dma_nt(lds_char* dst, const uint16_t* base, int ld, int row0,
-                                       int nrows, int k0, int wave, int lane) {
-  const int rsub = lane >> 3, pc = lane & 7;
+struct NtRows {
+  static constexpr int NI = ROWS / 8 / WAVES;
+  uint32_t off[NI];
+  __device__ __forceinline__ void init(int ld, int row0, int nrows, int wave, int lane) {
+    const int rsub = lane >> 3, pc = lane & 7;
 #pragma unroll
-  for (int i = 0; i < ROWS / 8 / WAVES; ++i) {
-    const int blk = i * WAVES + wave;
-    const int r = 8 * blk + rsub;
-    const int grow = min(row0 + r, nrows - 1);
-    dma16(base + (size_t)grow * ld + k0 + 8 * (pc ^ nt_swz(r)), dst + blk * 1024);
+    for (int i = 0; i < NI; ++i) {
+      const int r = 8 * (i * WAVES + wave) + rsub;
+      const uint32_t grow = (uint32_t)min(row0 + r, nrows - 1);
+      off[i] = 2u * (grow * (uint32_t)ld + 8u * (uint32_t)(pc ^ nt_swz(r)));
+    }
   }
-}
+  __device__ __forceinline__ void issue(lds_char* dst, const rsrc_t& rs, uint32_t k0,
+                                        int wave) const {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) dma16(rs, off[i], 2u * k0, dst + (i * WAVES + wave) * 1024);
+  }
+};
 
-// NN panel: k rows [k0, k0 + 64) x n [n0, n0 + BN) of a row-major [K, N] matrix into LDS
-// (natural layout, BN * 2-byte rows).  Rows past krows and columns past ncols are clamped.
+// NN panel: k rows [k0, k0 + 64) x n [n0, n0 + BN) of a row-major [krows, ld] matrix
+// (natural layout, BN * 2-byte LDS rows, chunk XOR nn_swz(row)); instruction i of wave w
+// fills rows RPI (i W + w) .. +RPI-1.  Columns past ncols are clamped (in the per-lane
+// offsets) and rows past krows too (only in a stage that reaches past them).
 template <int BN, int WAVES>
-__device__ __forceinline__ void dma_nn(lds_char* dst, const uint16_t* base, int ld, int k0,
-                                       int krows, int n0, int ncols, int wave, int lane) {
-  constexpr int CH = BN / 8, RPI = kWave / CH;  // chunks per row, rows per instruction
-  const int rsub = lane / CH, pc = lane % CH;
+struct NnRows {
+  static constexpr int CH = BN / 8, RPI = kWave / CH, NI = BK / RPI / WAVES;
+  uint32_t off[NI];  // 2 (r ld + gn): row r of the stage, column gn
+  int r0;            // this lane's row in instruction 0 (instruction i: r0 + i RPI W)
+  __device__ __forceinline__ void init(int ld, int n0, int ncols, int wave, int lane) {
+    const int rsub = lane / CH, pc = lane % CH;
+    r0 = RPI * wave + rsub;
 #pragma unroll
-  for (int i = 0; i < BK / RPI / WAVES; ++i) {
-    const int blk = i * WAVES + wave;
-    const int r = RPI * blk + rsub;
-    const int gk = min(k0 + r, krows - 1);
-    const int gn = min(n0 + 8 * (pc ^ nn_swz(r)), ncols - 8);
-    dma16(base + (size_t)gk * ld + gn, dst + blk * 1024);
+    for (int i = 0; i < NI; ++i) {
+      const int r = r0 + i * RPI * WAVES;
+      const uint32_t gn = (uint32_t)min(n0 + 8 * (pc ^ nn_swz(r)), ncols - 8);
+      off[i] = 2u * ((uint32_t)r * (uint32_t)ld + gn);
+    }
   }
-}
+  __device__ __forceinline__ void issue(lds_char* dst, const rsrc_t& rs, int k0, int krows,
+                                        int ld, int wave) const {
+    if (k0 + BK <= krows) {
+      const uint32_t soff = 2u * (uint32_t)k0 * (uint32_t)ld;
+#pragma unroll
+      for (int i = 0; i < NI; ++i) dma16(rs, off[i], soff, dst + (i * WAVES + wave) * 1024);
+    } else {
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int r = r0 + i * RPI * WAVES;
+        const int gk = min(k0 + r, krows - 1);
+        const uint32_t voff = off[i] + 2u * (uint32_t)(gk - r) * (uint32_t)ld;
+        dma16(rs, voff, 0u, dst + (i * WAVES + wave) * 1024);
+      }
+    }
+  }
+};
 
 // Epilogue of one C tile (configuration C: WAVES, WM, WN, TM, TN, TNB, LDS_BYTES, BWD)
 // from the accumulators of each wavefront, staged through the workgroup's LDS (free:
@@ -372,7 +382,20 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
     if (multi) k_part = P.k_part;
     asm volatile("" : "+s"(k_part));
   }
-  auto dma_stage = [&](int stage, int k0) {
+  // Per-lane DMA offsets of this tile (A and A2 share rows and stride, as do the NT B
+  // panels), and the operands' buffer resources.
+  NtRows<BM, C::WAVES> rows_a;
+  rows_a.init(P.lda, m0, P.M, wave, lane);
+  NtRows<NN ? 8 * C::WAVES : BN, C::WAVES> rows_b;  // (unused for NN)
+  NnRows<BN, C::WAVES> rows_nn;                     // (unused for NT)
+  if constexpr (NN) rows_nn.init(P.ldb, n0, P.N, wave, lane);
+  else rows_b.init(P.ldb, n0, P.N, wave, lane);
+  const rsrc_t rs_a = make_rsrc(P.A);
+  const rsrc_t rs_a2 = make_rsrc(C::BWD ? P.A2 : P.A);
+  const rsrc_t rs_b = make_rsrc(P.B);
+  const rsrc_t rs_b2 = make_rsrc(EPI == EPI_SWIGLU || C::BWD ? P.B2 : P.B);
+  const rsrc_t rs_b3 = make_rsrc(C::BWD ? P.B3 : P.B);
+  auto dma_stage = [&](int stage, int k0) __attribute__((always_inline)) {
     lds_char* S = Ls + stage * C::STAGE;
     if constexpr (NN) {
       // (k0 is uniform: the part is chosen per stage, from scalar values)
@@ -384,21 +407,16 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
         a = part == i ? ap[i] : a;
         b = part == i ? bp[i] : b;
       }
-      dma_nt<BM, C::WAVES>(S, a, P.lda, m0, P.M, kk, wave, lane);
-      dma_nn<BN, C::WAVES>(S + C::A_BYTES, b, P.ldb, kk, P.Kb_rows, n0, P.N, wave, lane);
+      rows_a.issue(S, make_rsrc(a), (uint32_t)kk, wave);
+      rows_nn.issue(S + C::A_BYTES, make_rsrc(b), kk, P.Kb_rows, P.ldb, wave);
       return;
     }
-    dma_nt<BM, C::WAVES>(S, P.A, P.lda, m0, P.M, k0, wave, lane);
-    if constexpr (C::BWD) dma_nt<BM, C::WAVES>(S + BM * BK * 2, P.A2, P.lda, m0, P.M, k0, wave, lane);
-    if constexpr (EPI == EPI_SWIGLU || C::BWD) {
-      dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
-      dma_nt<BN, C::WAVES>(S + C::A_BYTES + BN * BK * 2, P.B2, P.ldb, n0, P.N, k0, wave, lane);
-      if constexpr (C::BWD)
-        dma_nt<BN, C::WAVES>(S + C::A_BYTES + 2 * BN * BK * 2, P.B3, P.ldb, n0, P.N, k0, wave,
-                             lane);
-    } else {
-      dma_nt<BN, C::WAVES>(S + C::A_BYTES, P.B, P.ldb, n0, P.N, k0, wave, lane);
-    }
+    rows_a.issue(S, rs_a, (uint32_t)k0, wave);
+    if constexpr (C::BWD) rows_a.issue(S + BM * BK * 2, rs_a2, (uint32_t)k0, wave);
+    rows_b.issue(S + C::A_BYTES, rs_b, (uint32_t)k0, wave);
+    if constexpr (EPI == EPI_SWIGLU || C::BWD)
+      rows_b.issue(S + C::A_BYTES + BN * BK * 2, rs_b2, (uint32_t)k0, wave);
+    if constexpr (C::BWD) rows_b.issue(S + C::A_BYTES + 2 * BN * BK * 2, rs_b3, (uint32_t)k0, wave);
   };
 
   // Operand addressing (see the header): A / NT-B row R, chunk 2 s + hh ->
@@ -442,20 +460,18 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
       wait_dma<0>();
     }
     __syncthreads();  // stage kt resident; every wave is past step kt-1
-    if (kt + STAGES - 1 < nk)
-      dma_stage((kt + STAGES - 1) % STAGES, (kb + kt + STAGES - 1) * BK);
     const lds_char* SA = Ls + (kt % STAGES) * C::STAGE;
     const lds_char* SB = SA + C::A_BYTES;
+    // Operands of substep s into set s % 2.
+    u32x4 a[2][TM], a2[2][TM], b[2][TNB];
+    auto read_sub = [&](int s) __attribute__((always_inline)) {
+      const int xo = opa ^ (32 * s), q = s & 1;
 #pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      u32x4 a[TM], a2[TM], b[TNB];
-      const int xo = opa ^ (32 * s);
-#pragma unroll
-      for (int i = 0; i < TM; ++i) a[i] = lds_read16(SA + (wm * C::WM + 32 * i) * 128 + xo);
+      for (int i = 0; i < TM; ++i) a[q][i] = lds_read16(SA + (wm * C::WM + 32 * i) * 128 + xo);
       if constexpr (C::BWD) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
-          a2[i] = lds_read16(SA + BM * BK * 2 + (wm * C::WM + 32 * i) * 128 + xo);
+          a2[q][i] = lds_read16(SA + BM * BK * 2 + (wm * C::WM + 32 * i) * 128 + xo);
       }
 #pragma unroll
       for (int j = 0; j < TNB; ++j) {
@@ -463,17 +479,27 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
           const int cx = 2 * (wn * C::WN + 32 * j);
           const u32x2 lo = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_lo ^ cx));
           const u32x2 hi = lds_read_tr(SB + 16 * s * C::NN_RB + (nb_hi ^ cx));
-          b[j] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+          b[q][j] = u32x4{lo[0], lo[1], hi[0], hi[1]};
         } else {
           const int brow = (j / TN) * BN + wn * C::WN + 32 * (j % TN);  // panel j / TN
-          b[j] = lds_read16(SB + brow * 128 + xo);
+          b[q][j] = lds_read16(SB + brow * 128 + xo);
         }
       }
+    };
+    // The first substep's operand reads go out before the refill, so their LDS latency
+    // overlaps the issue of the next stage's loads.
+    read_sub(0);
+    if (kt + STAGES - 1 < nk)
+      dma_stage((kt + STAGES - 1) % STAGES, (kb + kt + STAGES - 1) * BK);
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      if (s + 1 < BK / 16) read_sub(s + 1);
+      const int q = s & 1;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TNB; ++j)
-          acc[i][j] = mfma32(C::BWD && j >= 2 * TN ? a2[i] : a[i], b[j], acc[i][j]);
+          acc[i][j] = mfma32(C::BWD && j >= 2 * TN ? a2[q][i] : a[q][i], b[q][j], acc[i][j]);
     }
     // Issue order: the operand reads of k-substep s+1 are spread between the MFMAs of
     // substep s (R / M per MFMA, one more for the first R mod M), so LDS latency hides
@@ -556,6 +582,11 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_group_kernel(const Gem
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
 hipError_t check_params(const GemmParams& p) {
   if (p.K <= 0 || p.K % BK != 0) return hipErrorInvalidValue;
+  // The operand loads address each operand with 32-bit byte offsets from its base.
+  constexpr long long kMaxBytes = 1LL << 32;
+  const long long b_rows = NN ? (long long)p.Kb_rows : (long long)p.N;
+  if ((long long)p.M * p.lda * 2 >= kMaxBytes || b_rows * p.ldb * 2 >= kMaxBytes)
+    return hipErrorInvalidValue;
   if (p.k_splits > 1 && (EPI != EPI_ACC || !p.part || p.N % 4 != 0 || p.k_splits > p.K / BK))
     return hipErrorInvalidValue;
   if (p.n_parts > 1) {
