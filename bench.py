@@ -47,10 +47,10 @@ PEAK_HBM_GBS = 8000.0
 # on (sha256 prefix); after any change to that source the traffic is reported as null.
 MEASURED_TRAFFIC = {
     # flash_fwd_kernel<128, false>: one launch over 4 shards' 16 heads with paired query
-    # tiles (2 per layer step), no key-range split (681 013.1 / 32 769.3 KiB)
+    # tiles (2 per layer step), no key-range split (641 107.5 / 32 768.5 KiB)
     ("7b-h4096-S65536-D8", 7, "attn"): {
-        "source": "flash_attn.hip", "sha256": "f5a67afad3079290",
-        "fetch_kib": 681013.1, "fetch_scale": 2.0, "write_kib": 32769.3, "write_scale": 1.0},
+        "source": "flash_attn.hip", "sha256": "e059f25e8c899e28",
+        "fetch_kib": 641107.5, "fetch_scale": 2.0, "write_kib": 32768.5, "write_scale": 1.0},
 }
 
 
@@ -215,7 +215,7 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--forward-only", action="store_true",
                     help="skip the backward blocks (for short profiling runs)")
-    ap.add_argument("--cpu-rows", type=int, default=128)
+    ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--rank-sweep", action="store_true",
                     help="also time the layer of every rank of the group")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
