@@ -80,7 +80,10 @@ typedef enum tsp_status {
 /* Problem statement of one rank (paper notation, Section 4 notation table).
  * Shape rules (TSP_ERR_SHAPE otherwise): batch >= 0, seq >= 0, every other size >= 1;
  * seq % degree == 0; hidden == n_heads * head_dim; n_heads % n_kv_heads == 0;
- * n_heads % degree == 0; n_kv_heads % degree == 0; ffn % degree == 0. */
+ * n_heads % degree == 0; n_kv_heads % degree == 0; ffn % degree == 0.
+ * Size limit (TSP_ERR_UNSUPPORTED otherwise): the rank's widest per-token operand,
+ * batch * seq / degree rows of max(hidden, ffn, G * (ffn / degree rounded up to 64))
+ * bf16 values (G the forward grouping below), is smaller than 4 GiB. */
 typedef struct tsp_shape {
   int32_t batch;        /* B: micro-batch */
   int32_t seq;          /* S: full sequence length; each rank holds S_loc = S / D tokens */

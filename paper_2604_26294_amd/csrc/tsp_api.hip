@@ -1,6 +1,7 @@
 // Host side of the libtsp C ABI: argument validation, workspace planning and the
 // per-rank shard loops of the paper's two schedules.  Every check runs before the
 // first launch, so a call that returns an error has enqueued nothing.
+#include <algorithm>
 #include <math.h>
 #include <stdint.h>
 
@@ -78,6 +79,11 @@ tsp_status check_shape(const tsp_shape* s, Dims* o) {
   o->s_c = o->s_loc / 2;
   o->G = s->group_steps > 0 ? s->group_steps : kGroupMax;
   if (o->G > o->D) o->G = o->D;
+  // The GEMM operand loads address each operand with 32-bit byte offsets: the widest
+  // per-token rows (x and Y [M, h]; the group's gated products [M, G (F/D rounded up to
+  // 64)]; the backward's [M, F/D] and transposed [F/D, M] operands) must stay below 4 GiB.
+  const long long width = std::max({(long long)o->h, (long long)o->G * o->fs_pad, (long long)o->F});
+  if (o->M * width * 2 >= (1LL << 32)) return TSP_ERR_UNSUPPORTED;
   return TSP_OK;
 }
 

@@ -91,6 +91,11 @@ def _shape(**kw):
     (dict(layout=1), 0), (dict(head_dim=32, n_heads=8), 6), (dict(ffn=680), 6),
     (dict(group_steps=-1), 2), (dict(group_steps=T.GROUP_STEPS_MAX + 1), 6),
     (dict(group_steps=T.GROUP_STEPS_MAX), 0), (dict(group_steps=1), 0),
+    # a 4 GiB per-rank operand (M h bf16 = 2^18 x 8192 x 2 bytes) and just below it
+    (dict(hidden=8192, n_heads=64, n_kv_heads=64, head_dim=128, ffn=1024, seq=2 ** 19,
+          degree=2, rank=0), 6),
+    (dict(hidden=8192, n_heads=64, n_kv_heads=64, head_dim=128, ffn=1024, seq=2 ** 19 - 2,
+          degree=2, rank=0), 0),
 ])
 def test_shape_validation(kw, code):
     out = ctypes.c_size_t(0)
