@@ -12,9 +12,9 @@
 //
 // One workgroup = WGM x WGN wavefronts (8 by default: two per SIMD); each wavefront owns
 // a (BM/WGM) x (BN/WGN) block of C as 32 x 32 MFMA tiles.  K advances in steps of 64.
-// Operand panels go from HBM straight into LDS (global_load_lds, no register staging),
-// in a ring of STAGES slots: while the MFMAs consume step k the DMA fills the steps
-// up to k + STAGES - 1.
+// Operand panels go from HBM straight into LDS (buffer loads with an LDS destination, no
+// register staging), in a ring of STAGES slots: while the MFMAs consume step k the loads
+// fill the steps up to k + STAGES - 1.
 //
 // LDS layouts.  LDS has 64 banks of 4 bytes, so a byte address maps to bank window
 // position (address mod 256).  A [M, K] and "NT" B [N, K] panels are rows of 64 bf16
