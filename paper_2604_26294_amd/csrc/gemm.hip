@@ -71,7 +71,12 @@ struct Cfg {
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int LDS_BYTES = STAGES * STAGE;
   // Operand load instructions one wavefront issues per stage.
-  static constexpr int LOADS = NAP * BM / 8 / WAVES + (NN ? BK * (BN * 2) / 1024 / WAVES : NB / 8 / WAVES);
+  // [N, K]-operand tiles: only the first half of the wavefronts (one per SIMD) load, each
+  // its own share of a stage and that of the other wavefront of its SIMD; [K, N] tiles:
+  // every wavefront loads its share.
+  static constexpr bool HALF_LOADERS = !NN;
+  static constexpr int LOADS = (HALF_LOADERS ? 2 : 1) *
+      (NAP * BM / 8 / WAVES + (NN ? BK * (BN * 2) / 1024 / WAVES : NB / 8 / WAVES));
   static_assert(STAGES >= 2 && LDS_BYTES <= 160 * 1024, "LDS ring");
   static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
   static constexpr int NN_RB = BN * 2;                         // NN panel row bytes
@@ -384,18 +389,34 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
   }
   // Per-lane DMA offsets of this tile (A and A2 share rows and stride, as do the NT B
   // panels), and the operands' buffer resources.
-  NtRows<BM, C::WAVES> rows_a;
+  // With HALF_LOADERS only the first half of the wavefronts (one per SIMD: wavefronts are
+  // placed on the SIMDs round-robin) issue loads, each its own share and that of
+  // wavefront wave + W/2 (the other wavefront of its SIMD): a CU's load path takes a
+  // stage's 64 KB at about 60 bytes per cycle, so a wavefront that issues loads stalls
+  // for hundreds of cycles, and this way one wavefront of every SIMD never does and keeps
+  // the matrix pipe fed meanwhile.
+  constexpr int HW = C::WAVES / 2;
+  const bool loader = !C::HALF_LOADERS || wave < HW;
+  const int wave2 = wave + HW;
+  NtRows<BM, C::WAVES> rows_a, rows_a_hi;
   rows_a.init(P.lda, m0, P.M, wave, lane);
-  NtRows<NN ? 8 * C::WAVES : BN, C::WAVES> rows_b;  // (unused for NN)
-  NnRows<BN, C::WAVES> rows_nn;                     // (unused for NT)
-  if constexpr (NN) rows_nn.init(P.ldb, n0, P.N, wave, lane);
-  else rows_b.init(P.ldb, n0, P.N, wave, lane);
+  if constexpr (C::HALF_LOADERS) rows_a_hi.init(P.lda, m0, P.M, wave2, lane);
+  NtRows<NN ? 8 * C::WAVES : BN, C::WAVES> rows_b, rows_b_hi;  // (unused for NN)
+  NnRows<BN, C::WAVES> rows_nn, rows_nn_hi;                     // (unused for NT)
+  if constexpr (NN) {
+    rows_nn.init(P.ldb, n0, P.N, wave, lane);
+    if constexpr (C::HALF_LOADERS) rows_nn_hi.init(P.ldb, n0, P.N, wave2, lane);
+  } else {
+    rows_b.init(P.ldb, n0, P.N, wave, lane);
+    if constexpr (C::HALF_LOADERS) rows_b_hi.init(P.ldb, n0, P.N, wave2, lane);
+  }
   const rsrc_t rs_a = make_rsrc(P.A);
   const rsrc_t rs_a2 = make_rsrc(C::BWD ? P.A2 : P.A);
   const rsrc_t rs_b = make_rsrc(P.B);
   const rsrc_t rs_b2 = make_rsrc(EPI == EPI_SWIGLU || C::BWD ? P.B2 : P.B);
   const rsrc_t rs_b3 = make_rsrc(C::BWD ? P.B3 : P.B);
   auto dma_stage = [&](int stage, int k0) __attribute__((always_inline)) {
+    if (!loader) return;
     lds_char* S = Ls + stage * C::STAGE;
     if constexpr (NN) {
       // (k0 is uniform: the part is chosen per stage, from scalar values)
@@ -407,16 +428,32 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& P, const int w) {
         a = part == i ? ap[i] : a;
         b = part == i ? bp[i] : b;
       }
-      rows_a.issue(S, make_rsrc(a), (uint32_t)kk, wave);
-      rows_nn.issue(S + C::A_BYTES, make_rsrc(b), kk, P.Kb_rows, P.ldb, wave);
+      const rsrc_t ra = make_rsrc(a), rb = make_rsrc(b);
+      rows_a.issue(S, ra, (uint32_t)kk, wave);
+      if constexpr (C::HALF_LOADERS) rows_a_hi.issue(S, ra, (uint32_t)kk, wave2);
+      rows_nn.issue(S + C::A_BYTES, rb, kk, P.Kb_rows, P.ldb, wave);
+      if constexpr (C::HALF_LOADERS)
+        rows_nn_hi.issue(S + C::A_BYTES, rb, kk, P.Kb_rows, P.ldb, wave2);
       return;
     }
     rows_a.issue(S, rs_a, (uint32_t)k0, wave);
-    if constexpr (C::BWD) rows_a.issue(S + BM * BK * 2, rs_a2, (uint32_t)k0, wave);
+    if constexpr (C::HALF_LOADERS) rows_a_hi.issue(S, rs_a, (uint32_t)k0, wave2);
+    if constexpr (C::BWD) {
+      rows_a.issue(S + BM * BK * 2, rs_a2, (uint32_t)k0, wave);
+      if constexpr (C::HALF_LOADERS) rows_a_hi.issue(S + BM * BK * 2, rs_a2, (uint32_t)k0, wave2);
+    }
     rows_b.issue(S + C::A_BYTES, rs_b, (uint32_t)k0, wave);
-    if constexpr (EPI == EPI_SWIGLU || C::BWD)
+    if constexpr (C::HALF_LOADERS) rows_b_hi.issue(S + C::A_BYTES, rs_b, (uint32_t)k0, wave2);
+    if constexpr (EPI == EPI_SWIGLU || C::BWD) {
       rows_b.issue(S + C::A_BYTES + BN * BK * 2, rs_b2, (uint32_t)k0, wave);
-    if constexpr (C::BWD) rows_b.issue(S + C::A_BYTES + 2 * BN * BK * 2, rs_b3, (uint32_t)k0, wave);
+      if constexpr (C::HALF_LOADERS)
+        rows_b_hi.issue(S + C::A_BYTES + BN * BK * 2, rs_b2, (uint32_t)k0, wave2);
+    }
+    if constexpr (C::BWD) {
+      rows_b.issue(S + C::A_BYTES + 2 * BN * BK * 2, rs_b3, (uint32_t)k0, wave);
+      if constexpr (C::HALF_LOADERS)
+        rows_b_hi.issue(S + C::A_BYTES + 2 * BN * BK * 2, rs_b3, (uint32_t)k0, wave2);
+    }
   };
 
   // Operand addressing (see the header): A / NT-B row R, chunk 2 s + hh ->
