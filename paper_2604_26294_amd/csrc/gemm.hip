@@ -613,7 +613,11 @@ __global__ __launch_bounds__(kWave * WGM * WGN) void gemm_group_kernel(const Gem
   }
   int w = xcd_work_index(blockIdx.x, total), i = 0;
   while (i + 1 < G.n && w >= tiles[i]) w -= tiles[i++];  // uniform per workgroup
-  gemm_tile<BM, BN, WGM, WGN, NN, EPI, STAGES>(G.p[i], w);
+  // A copy of the product's parameters: read through G.p[i] (an index into the kernel
+  // arguments), the compiler reloads every field after each global store of the epilogue
+  // (it cannot rule out aliasing), hundreds of serialized scalar loads per tile.
+  const GemmParams P = G.p[i];
+  gemm_tile<BM, BN, WGM, WGN, NN, EPI, STAGES>(P, w);
 }
 
 template <int BM, int BN, int WGM, int WGN, bool NN, int EPI, int STAGES>
