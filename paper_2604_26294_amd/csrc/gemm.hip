@@ -169,6 +169,15 @@ struct NnRows {
   }
 };
 
+// Orders this wavefront's LDS writes before its later LDS reads (and those reads before
+// its next writes) without a workgroup barrier: every wavefront stages its blocks in an
+// LDS region of its own, and LDS operations of one wavefront complete in issue order, so
+// only the compiler must be kept from moving them across each other.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
 // Epilogue of one C tile (configuration C: WAVES, WM, WN, TM, TN, TNB, LDS_BYTES, BWD)
 // from the accumulators of each wavefront, staged through the workgroup's LDS (free:
 // every operand read has completed).
@@ -201,7 +210,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const float g = acc[i][j][e], u = acc[i][j + TN][e], dh = acc[i][j + 2 * TN][e];
-          const float sg = 1.f / (1.f + __expf(-g));
+          const float sg = __builtin_amdgcn_rcpf(1.f + __expf(-g));
           const float sl = g * sg;
           acc[i][j][e] = dh * u * (sg * (1.f + g * (1.f - sg)));  // dG
           acc[i][j + TN][e] = dh * sl;                           // dU
@@ -215,7 +224,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
 #pragma unroll
           for (int e = 0; e < 16; ++e)
             E[(8 * (e >> 2) + 4 * hh + (e & 3)) * EST + 32 * j + l32] = acc[i][q * TN + j][e];
-        __syncthreads();
+        wave_lds_sync();
         if (q < 2) {
           uint16_t* H = q == 0 ? P.H : P.H2;
 #pragma unroll
@@ -243,7 +252,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
           }
           *reinterpret_cast<u32x4*>(T + (size_t)nn * P.ldt + mm) = u32x4{w[0], w[1], w[2], w[3]};
         }
-        __syncthreads();
+        wave_lds_sync();
       }
     }
     return;
@@ -255,10 +264,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         float v = acc[i][j][e];
-        if constexpr (EPI == EPI_SWIGLU) v = v / (1.f + __expf(-v)) * acc[i][j + TN][e];
+        if constexpr (EPI == EPI_SWIGLU)
+          v = v * __builtin_amdgcn_rcpf(1.f + __expf(-v)) * acc[i][j + TN][e];
         E[(8 * (e >> 2) + 4 * hh + (e & 3)) * EST + 32 * j + l32] = v;
       }
-    __syncthreads();
+    wave_lds_sync();
     const int mrow0 = m0 + wm * C::WM + 32 * i;
     f32x4 v[PER_LANE];
     int mm[PER_LANE], nn[PER_LANE];
@@ -277,7 +287,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
 #pragma unroll
         for (int q = 0; q < PER_LANE; ++q)
           if (ok[q]) *reinterpret_cast<f32x4*>(dst + (size_t)mm[q] * P.N + nn[q]) = v[q];
-        __syncthreads();
+        wave_lds_sync();
         continue;
       }
       f32x4 base[PER_LANE];
@@ -333,7 +343,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
         }
       }
     }
-    __syncthreads();
+    wave_lds_sync();
   }
 }
 
