@@ -270,6 +270,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
       }
     wave_lds_sync();
     const int mrow0 = m0 + wm * C::WM + 32 * i;
+    // Q/K/V scatter: batch entry and token of the block's first row, once per block (a row
+    // r of the block is then token t0 + r of entry b0, or of the next entry past its end).
+    int b0 = 0, t0 = 0;
+    if constexpr (EPI == EPI_QKV) {
+      b0 = mrow0 / P.rows_per_batch;
+      t0 = mrow0 - b0 * P.rows_per_batch;
+    }
     f32x4 v[PER_LANE];
     int mm[PER_LANE], nn[PER_LANE];
     bool ok[PER_LANE];
@@ -333,7 +340,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
           if (n < P.nq) {
             dst = P.Q + (size_t)m * P.ldq + n;
           } else {
-            const int b = m / P.rows_per_batch, t = m - b * P.rows_per_batch;
+            int b = b0, t = t0 + (m - mrow0);
+            while (t >= P.rows_per_batch) {  // once at most when entries hold >= 32 rows
+              t -= P.rows_per_batch;
+              ++b;
+            }
             const long long pos = t < P.kv_seg ? P.kv_pos0 + t : P.kv_pos1 + (t - P.kv_seg);
             const size_t row = (size_t)b * P.kv_batch_stride +
                                (size_t)pos * P.kv_row_stride + P.kv_col0;
