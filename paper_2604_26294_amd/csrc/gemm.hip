@@ -297,19 +297,28 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& P, f32x16 (&acc)
         wave_lds_sync();
         continue;
       }
+      // The base values of the block: every lane loads (chunks outside the product read
+      // an in-range element instead and are not stored), so that all loads of the block
+      // are issued before the first wait rather than one load and one wait per chunk.
       f32x4 base[PER_LANE];
+      if (P.R) {
+        u32x2 r[PER_LANE];
 #pragma unroll
-      for (int q = 0; q < PER_LANE; ++q) {
-        base[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (ok[q]) {
-          if (P.R) {
-            const u32x2 r = *reinterpret_cast<const u32x2*>(P.R + (size_t)mm[q] * P.ldr + nn[q]);
-            base[q] = f32x4{bf16_bits_to_f32(r[0] & 0xffffu), bf16_bits_to_f32(r[0] >> 16),
-                            bf16_bits_to_f32(r[1] & 0xffffu), bf16_bits_to_f32(r[1] >> 16)};
-          } else if (P.accumulate) {
-            base[q] = *reinterpret_cast<const f32x4*>(P.Y + (size_t)mm[q] * P.ldy + nn[q]);
-          }
-        }
+        for (int q = 0; q < PER_LANE; ++q)
+          r[q] = *reinterpret_cast<const u32x2*>(P.R + (size_t)min(mm[q], P.M - 1) * P.ldr +
+                                                 min(nn[q], P.N - 4));
+#pragma unroll
+        for (int q = 0; q < PER_LANE; ++q)
+          base[q] = f32x4{bf16_bits_to_f32(r[q][0] & 0xffffu), bf16_bits_to_f32(r[q][0] >> 16),
+                          bf16_bits_to_f32(r[q][1] & 0xffffu), bf16_bits_to_f32(r[q][1] >> 16)};
+      } else if (P.accumulate) {
+#pragma unroll
+        for (int q = 0; q < PER_LANE; ++q)
+          base[q] = *reinterpret_cast<const f32x4*>(P.Y + (size_t)min(mm[q], P.M - 1) * P.ldy +
+                                                    min(nn[q], P.N - 4));
+      } else {
+#pragma unroll
+        for (int q = 0; q < PER_LANE; ++q) base[q] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
 #pragma unroll
       for (int q = 0; q < PER_LANE; ++q) {
