@@ -47,10 +47,10 @@ PEAK_HBM_GBS = 8000.0
 # on (sha256 prefix); after any change to that source the traffic is reported as null.
 MEASURED_TRAFFIC = {
     # flash_fwd_kernel<128, false>: one launch over 4 shards' 16 heads with paired query
-    # tiles (2 per layer step), no key-range split (650 889.7 / 32 768.4 KiB)
+    # tiles (2 per layer step), no key-range split (668 450.8 / 32 768.3 KiB)
     ("7b-h4096-S65536-D8", 7, "attn"): {
-        "source": "flash_attn.hip", "sha256": "e059f25e8c899e28",
-        "fetch_kib": 650889.7, "fetch_scale": 2.0, "write_kib": 32768.4, "write_scale": 1.0},
+        "source": "flash_attn.hip", "sha256": "7938e38808f946ca",
+        "fetch_kib": 668450.8, "fetch_scale": 2.0, "write_kib": 32768.3, "write_scale": 1.0},
 }
 
 

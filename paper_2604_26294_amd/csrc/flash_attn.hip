@@ -813,11 +813,11 @@ AttnPlan attn_plan_uncached(const AttnParams& p) {
   AttnPlan plan = {1, len_of(1), 0.0, 0.0};
   if (bh <= 0 || n_qt > kMaxTiles) return plan;
   // Time per key of a workgroup: 4 kQTile d FLOPs (its Q K^T and P V rows) at the
-  // fraction of one CU's bf16 MFMA peak (2516.6 / 256 TFLOP/s) this kernel reaches (0.44
-  // measured at 7B, S = 65536: ~30 ns per key at d = 128).  Key-range partials move at
-  // about half the HBM peak (8 TB/s).  Only the ratio of the two matters, so the
-  // constants need refitting only when that fraction moves a lot.
-  constexpr double kCuPeak = 2516.6e12 / 256, kPeakFraction = 0.44, kPartialBw = 4e12;
+  // fraction of one CU's bf16 MFMA peak (2516.6 / 256 TFLOP/s) this kernel reaches (0.50
+  // measured at 7B, S = 65536: ~27 ns per key at d = 128).  Key-range partials move at
+  // about half the HBM peak (8 TB/s).  Only the ratio of the two matters; the fraction is
+  // refitted to the measured one whenever the kernel's speed changes.
+  constexpr double kCuPeak = 2516.6e12 / 256, kPeakFraction = 0.50, kPartialBw = 4e12;
   const double t_key = 4.0 * kQTile * p.head_dim / (kPeakFraction * kCuPeak);
   const double rows = (double)bh * p.s_loc;
   // Key ranges: candidate counts 1..8, at least 4 key tiles per range; estimated time =
